@@ -1,0 +1,388 @@
+"""CPU oracle for the PASK decode hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  It shares no code with
+the HIP library and never imports it.
+
+What it computes, each piece following the passage named in its docstring:
+  * the per-token, per-layer-group action: a = max(a0[z][c], a-[z][c]) under
+    the order DROP < RETAIN-LOW < RETAIN-HIGH (Section 3.1; Eq. 10, the max step
+    of the online lookup, Alg. 2);
+  * persistence of each entry (the Persist step of Alg. 2): DROP entries are
+    released from future attention (Section 3.1), LOW / HIGH entries are kept
+    in two compacted stores in position order;
+  * RETAIN-LOW storage: symmetric int4 with one fp16 scale per 32 elements.  The
+    paper names no low-bit format; this is the format chosen for the build,
+    computed here in exact integer arithmetic on bf16 bit patterns;
+  * decode attention over the persisted history, by the textbook definition
+    softmax(q k^T * scale) v, in fp64;
+  * the normalised KV cost C_KV of Eq. 1.
+
+Everything is plain numpy.  The attention is the definition written out
+(exact, up to fp64 rounding order); the decisions, compaction and codes are
+exact integer results.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+DROP, LOW, HIGH = 0, 1, 2        # R < L < H (Section 3.1)
+QGROUP = 32                      # elements per fp16 scale of a RETAIN-LOW entry
+QMAX = 7                         # symmetric int4 code range [-7, 7]
+FP16_MAX_BITS = 0x7BFF           # 65504
+
+
+# --------------------------------------------------------------------------
+# Decisions (Eq. 10; Alg. 2, lookup and max steps)
+# --------------------------------------------------------------------------
+
+def decide(tags, positions, group: int, action, floor, n_sink: int, keep_all: bool):
+    """Actions for a run of tokens of one sequence in layer group `group`.
+
+    The table gives the selected action a0 = action[z][c] and the floor
+    a- = floor[z][c]; the online action is their maximum under R < L < H.
+    Overrides: the first n_sink positions of a sequence and tokens appended
+    in keep-all mode (prompt tokens not governed by the table) are HIGH; a tag
+    outside the table is HIGH and reported (fail-safe).
+
+    Returns (actions uint8 [n], forced bool [n], bad_tag bool [n])."""
+    tags = np.asarray(tags, dtype=np.int64)
+    positions = np.asarray(positions, dtype=np.int64)
+    action = np.asarray(action)
+    floor = np.asarray(floor)
+    n_tags = action.shape[0]
+    out = np.empty(tags.shape, dtype=np.uint8)
+    forced = np.zeros(tags.shape, dtype=bool)
+    bad = tags >= n_tags
+    for i in range(tags.size):
+        z = int(tags[i])
+        if keep_all or positions[i] < n_sink or z >= n_tags:
+            out[i] = HIGH
+            forced[i] = True
+        else:
+            out[i] = max(int(action[z, group]), int(floor[z, group]))
+    return out, forced, bad
+
+
+def compact(actions, positions):
+    """The two persisted stores of one (sequence, layer): the positions whose
+    action is HIGH and those whose action is LOW, each in increasing position
+    order.  A DROP position appears in neither (release, Section 3.1).  The
+    slot of an entry is its rank in its store."""
+    actions = np.asarray(actions)
+    positions = np.asarray(positions, dtype=np.int64)
+    order = np.argsort(positions, kind="stable")
+    a, p = actions[order], positions[order]
+    return p[a == HIGH].copy(), p[a == LOW].copy()
+
+
+# --------------------------------------------------------------------------
+# RETAIN-LOW format: int4, symmetric absmax / 7, fp16 scale per 32 elements.
+# Exact integer arithmetic on bit patterns.
+# --------------------------------------------------------------------------
+
+def bf16_mag(bits):
+    """Split bf16 bit patterns into sign and an exact magnitude M * 2**E.
+    Normal: M = 128 + mantissa, E = exponent - 134.  Subnormal: M = mantissa,
+    E = -133.  Inputs must be finite."""
+    bits = np.asarray(bits, dtype=np.int64) & 0xFFFF
+    sign = bits >> 15
+    ex = (bits >> 7) & 0xFF
+    man = bits & 0x7F
+    if np.any(ex == 0xFF):
+        raise ValueError("non-finite bf16 input")
+    m = np.where(ex == 0, man, man | 0x80)
+    e = np.where(ex == 0, -133, ex - 134)
+    return sign, m, e
+
+
+def _rne_div(num, den):
+    """Round-half-to-even of num/den for non-negative int64 arrays, den > 0."""
+    q, r = np.divmod(num, den)
+    up = (2 * r > den) | ((2 * r == den) & ((q & 1) == 1))
+    return q + up.astype(np.int64)
+
+
+def _floor_log2_ratio(m, e, d: int):
+    """floor(log2(m * 2**e / d)) for integer m >= 1 and small odd d, exactly."""
+    m = np.asarray(m, dtype=np.int64)
+    f = np.zeros(m.shape, dtype=np.int64)
+    # Largest f with d * 2**f <= m, searched over the small range m allows.
+    for cand in range(-4, 9):
+        ok = (m >= d * (1 << cand)) if cand >= 0 else (m * (1 << -cand) >= d)
+        f = np.where(ok, cand, f)
+    return f + e
+
+
+def fp16_scale_bits(absmax_bits):
+    """fp16 bit pattern of the group scale s = RNE_fp16(absmax / 7), saturated
+    at 65504.  absmax_bits are non-negative finite bf16 patterns."""
+    _, m, e = bf16_mag(absmax_bits)
+    m = np.asarray(m, dtype=np.int64)
+    e = np.asarray(e, dtype=np.int64)
+    zero = m == 0
+    m1 = np.where(zero, 1, m)
+    # Exponent k such that the significand S = a/7 / 2**k lies in [1024, 2048);
+    # fp16 normal numbers are S * 2**k with k in [-24, 5]; below, k = -24 and
+    # S < 1024 (subnormals).
+    k = _floor_log2_ratio(m1, e, QMAX) - 10
+    k = np.maximum(k, -24)
+    sh = e - k                                 # S = m * 2**sh / 7
+    sh_c = np.clip(sh, -62, 40)
+    num = np.where(sh_c >= 0, m1 << np.maximum(sh_c, 0), m1)
+    den = np.where(sh_c >= 0, QMAX, QMAX << np.maximum(-sh_c, 0))
+    tiny = sh < -40                            # quotient far below 1/2
+    s = np.where(tiny, 0, _rne_div(np.where(tiny, 0, num), np.where(tiny, 1, den)))
+    carry = s == 2048                          # rounding reached the next binade
+    s = np.where(carry, 1024, s)
+    k = np.where(carry, k + 1, k)
+    over = k > 5                               # beyond 65504: saturate
+    bits = np.where(s >= 1024, ((k + 25) << 10) | (s - 1024), s)
+    bits = np.where(over, FP16_MAX_BITS, bits)
+    bits = np.where(zero, 0, bits)
+    return bits.astype(np.uint16)
+
+
+def fp16_mag(bits):
+    """fp16 pattern -> (S, k) with value S * 2**k (finite, non-negative)."""
+    bits = np.asarray(bits, dtype=np.int64)
+    ex = (bits >> 10) & 0x1F
+    man = bits & 0x3FF
+    s = np.where(ex == 0, man, man | 0x400)
+    k = np.where(ex == 0, -24, ex - 25)
+    return s, k
+
+
+def quantize_groups(x_bits):
+    """Quantise bf16 vectors group-wise along the last axis (length a multiple
+    of 32).  Returns (codes int8 [..., n], scale_bits uint16 [..., n/32]).
+
+    Per group: absmax a = max |x_i|; s = RNE_fp16(a / 7) saturated at 65504;
+    q_i = clamp(RNE(x_i / s), -7, 7), and q = 0 for the whole group when s = 0.
+    RNE of the quotient is symmetric, so q_i = sign(x_i) * RNE(|x_i| / s)."""
+    x = np.asarray(x_bits, dtype=np.int64) & 0xFFFF
+    shape = x.shape
+    n = shape[-1]
+    assert n % QGROUP == 0
+    g = x.reshape(-1, n // QGROUP, QGROUP)
+    absmax = (g & 0x7FFF).max(axis=-1)          # order of finite magnitudes = order of bits
+    sbits = fp16_scale_bits(absmax)
+    S, k = fp16_mag(sbits)
+    sign, m, e = bf16_mag(g)
+    S_ = S[..., None]
+    sh = e - k[..., None]                       # |x| / s = m * 2**sh / S
+    big = sh > 15                               # quotient >= 2**15 / 2047 > 7.5
+    tiny = sh < -40                             # quotient < 2**-29
+    sh_c = np.clip(sh, -40, 15)
+    num = np.where(sh_c >= 0, m << np.maximum(sh_c, 0), m)
+    den = np.where(sh_c >= 0, S_, S_ << np.maximum(-sh_c, 0))
+    safe_den = np.where(den == 0, 1, den)
+    q = _rne_div(num, safe_den)
+    q = np.where(big, QMAX, np.where(tiny, 0, q))
+    q = np.minimum(q, QMAX)
+    q = np.where(S_ == 0, 0, q)
+    q = np.where(sign == 1, -q, q)
+    return q.reshape(shape).astype(np.int8), sbits.reshape(shape[:-1] + (n // QGROUP,))
+
+
+def pack_nibbles(codes):
+    """Two's-complement nibbles, element 2j in the low nibble of byte j."""
+    c = np.asarray(codes, dtype=np.int64) & 0xF
+    return (c[..., 0::2] | (c[..., 1::2] << 4)).astype(np.uint8)
+
+
+def unpack_nibbles(packed):
+    p = np.asarray(packed, dtype=np.int64)
+    lo, hi = p & 0xF, (p >> 4) & 0xF
+    out = np.empty(p.shape[:-1] + (2 * p.shape[-1],), dtype=np.int64)
+    out[..., 0::2], out[..., 1::2] = lo, hi
+    return np.where(out >= 8, out - 16, out).astype(np.int8)
+
+
+def fp16_to_f64(bits):
+    s, k = fp16_mag(np.asarray(bits, dtype=np.int64) & 0x7FFF)
+    v = s.astype(np.float64) * np.exp2(k.astype(np.float64))
+    return np.where((np.asarray(bits, dtype=np.int64) >> 15) == 1, -v, v)
+
+
+def bf16_to_f64(bits):
+    sign, m, e = bf16_mag(bits)
+    v = m.astype(np.float64) * np.exp2(e.astype(np.float64))
+    return np.where(sign == 1, -v, v)
+
+
+def dequant(codes, scale_bits):
+    """x_hat = q * s (exact in fp64)."""
+    c = np.asarray(codes, dtype=np.float64)
+    s = fp16_to_f64(scale_bits)
+    n = c.shape[-1]
+    return (c.reshape(c.shape[:-1] + (n // QGROUP, QGROUP)) * s[..., None]).reshape(c.shape)
+
+
+# --------------------------------------------------------------------------
+# Attention over the persisted history (textbook definition, fp64)
+# --------------------------------------------------------------------------
+
+def attention(q, k, v, scale: float):
+    """o_h = sum_j softmax_j(scale * q_h . k_j) v_j for every query head h,
+    with grouped-query sharing: query head h reads KV head h // G.
+
+    q [Hq, D], k and v [n, Hkv, D] (fp64).  Returns (o [Hq, D], lse [Hq]) with
+    lse = m + ln(sum_j exp(s_j - m)).  An empty history gives o = 0, lse = -inf."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    hq, d = q.shape
+    n, hkv, _ = k.shape
+    g = hq // hkv
+    o = np.zeros((hq, d))
+    lse = np.full(hq, -np.inf)
+    if n == 0:
+        return o, lse
+    for h in range(hq):
+        kv = h // g
+        s = (k[:, kv, :] @ q[h]) * scale
+        m = s.max()
+        w = np.exp(s - m)
+        tot = w.sum()
+        o[h] = (w / tot) @ v[:, kv, :]
+        lse[h] = m + math.log(tot)
+    return o, lse
+
+
+# --------------------------------------------------------------------------
+# Persisted-history model of one cache (Alg. 2 Persist step, replayed)
+# --------------------------------------------------------------------------
+
+@dataclass
+class _SeqLayer:
+    n_pos: int = 0
+    hi_pos: list = field(default_factory=list)
+    lo_pos: list = field(default_factory=list)
+    hi_k: list = field(default_factory=list)     # bf16 bits [Hkv, D] per entry
+    hi_v: list = field(default_factory=list)
+    lo_kc: list = field(default_factory=list)    # int8 codes [Hkv, D]
+    lo_ks: list = field(default_factory=list)    # fp16 scale bits [Hkv, D/32]
+    lo_vc: list = field(default_factory=list)
+    lo_vs: list = field(default_factory=list)
+    n_forced: int = 0
+    n_drop: int = 0
+
+
+class OracleCache:
+    """The persisted history of a set of sequences, replayed append by append.
+
+    policy: dict with action [T][C], floor [T][C], group_of_layer [L], n_sink."""
+
+    def __init__(self, policy: dict, n_kv_heads: int, head_dim: int):
+        self.action = np.asarray(policy["action"])
+        self.floor = np.asarray(policy["floor"])
+        self.group_of_layer = np.asarray(policy["group_of_layer"])
+        self.n_sink = int(policy.get("n_sink", 0))
+        self.hkv = n_kv_heads
+        self.d = head_dim
+        self.state: dict = {}
+        self.bad_tag = False
+
+    def sl(self, seq: int, layer: int) -> _SeqLayer:
+        return self.state.setdefault((seq, layer), _SeqLayer())
+
+    def append(self, layer: int, seq: int, tags, k_bits, v_bits, keep_all: bool = False):
+        """Persist n new tokens of one sequence in one layer.
+        k_bits, v_bits: bf16 bit patterns [n, Hkv, D]."""
+        st = self.sl(seq, layer)
+        tags = np.asarray(tags).reshape(-1)
+        n = tags.size
+        k_bits = np.asarray(k_bits, dtype=np.int64).reshape(n, self.hkv, self.d)
+        v_bits = np.asarray(v_bits, dtype=np.int64).reshape(n, self.hkv, self.d)
+        pos = st.n_pos + np.arange(n)
+        c = int(self.group_of_layer[layer])
+        acts, forced, bad = decide(tags, pos, c, self.action, self.floor, self.n_sink, keep_all)
+        self.bad_tag |= bool(bad.any())
+        st.n_forced += int(forced.sum())
+        lo_idx = np.nonzero(acts == LOW)[0]
+        if lo_idx.size:
+            kc, ks = quantize_groups(k_bits[lo_idx])
+            vc, vs = quantize_groups(v_bits[lo_idx])
+        j = 0
+        for i in range(n):
+            a = acts[i]
+            if a == HIGH:
+                st.hi_pos.append(int(pos[i]))
+                st.hi_k.append(k_bits[i])
+                st.hi_v.append(v_bits[i])
+            elif a == LOW:
+                st.lo_pos.append(int(pos[i]))
+                st.lo_kc.append(kc[j])
+                st.lo_ks.append(ks[j])
+                st.lo_vc.append(vc[j])
+                st.lo_vs.append(vs[j])
+                j += 1
+            else:
+                st.n_drop += 1
+        st.n_pos += n
+        return acts
+
+    def lists(self, seq: int, layer: int):
+        st = self.sl(seq, layer)
+        return np.asarray(st.hi_pos, dtype=np.int64), np.asarray(st.lo_pos, dtype=np.int64)
+
+    def lo_entries(self, seq: int, layer: int):
+        """(k codes, k scale bits, v codes, v scale bits) of the LOW store, by slot."""
+        st = self.sl(seq, layer)
+        shp_c = (0, self.hkv, self.d)
+        shp_s = (0, self.hkv, self.d // QGROUP)
+        f = lambda xs, shp, dt: (np.stack(xs).astype(dt) if xs else np.zeros(shp, dt))
+        return (f(st.lo_kc, shp_c, np.int8), f(st.lo_ks, shp_s, np.uint16),
+                f(st.lo_vc, shp_c, np.int8), f(st.lo_vs, shp_s, np.uint16))
+
+    def visible_kv(self, seq: int, layer: int):
+        """K and V of every persisted entry in position order, in fp64."""
+        st = self.sl(seq, layer)
+        entries = []
+        for i, p in enumerate(st.hi_pos):
+            entries.append((p, bf16_to_f64(st.hi_k[i]), bf16_to_f64(st.hi_v[i])))
+        for i, p in enumerate(st.lo_pos):
+            entries.append((p, dequant(st.lo_kc[i], st.lo_ks[i]), dequant(st.lo_vc[i], st.lo_vs[i])))
+        entries.sort(key=lambda t: t[0])
+        if not entries:
+            z = np.zeros((0, self.hkv, self.d))
+            return z, z.copy()
+        return np.stack([e[1] for e in entries]), np.stack([e[2] for e in entries])
+
+    def attend(self, layer: int, seq: int, q_bits, scale: float):
+        """Decode attention of one sequence's query (bf16 bits [Hq, D]) over the
+        history persisted so far in `layer`.  `scale` is the fp32 softmax scale
+        widened to fp64."""
+        k, v = self.visible_kv(seq, layer)
+        return attention(bf16_to_f64(q_bits), k, v, scale)
+
+    def counts(self, seq: int, layer: int):
+        st = self.sl(seq, layer)
+        return dict(hi=len(st.hi_pos), lo=len(st.lo_pos), pos=st.n_pos, drop=st.n_drop,
+                    forced=st.n_forced)
+
+
+# --------------------------------------------------------------------------
+# Normalised KV cost (Eq. 1)
+# --------------------------------------------------------------------------
+
+def entry_bytes(n_kv_heads: int, head_dim: int):
+    """Stored bytes of one (token, layer) entry per action: K and V of every KV
+    head; bf16 for HIGH; int4 codes plus fp16 scales per 32 elements for LOW."""
+    hi = 2 * n_kv_heads * head_dim * 2
+    lo = 2 * n_kv_heads * (head_dim // 2 + 2 * (head_dim // QGROUP))
+    return {DROP: 0, LOW: lo, HIGH: hi}
+
+
+def c_kv(n_high: int, n_low: int, n_drop: int, n_kv_heads: int, head_dim: int) -> float:
+    """C_KV = sum of m(a) over (token, layer) entries / the same with every a = H."""
+    m = entry_bytes(n_kv_heads, head_dim)
+    tot = n_high + n_low + n_drop
+    if tot == 0:
+        return float("nan")
+    return (n_high * m[HIGH] + n_low * m[LOW]) / (tot * m[HIGH])

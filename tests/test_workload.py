@@ -1,0 +1,50 @@
+"""The seeded input generators: determinism, shapes and the tag mix."""
+
+import struct
+
+import numpy as np
+
+from workload import CONFIGS, make_policy, pack_blob, prompt_lengths, tag_mix, walk_function_calls
+from workload.policy import fnv1a32
+from workload.tags import schema_prompt_tags
+from workload.tensors import bf16_normal
+
+
+def test_walker_deterministic_and_mix():
+    a = walk_function_calls(50000, 17)
+    assert (a == walk_function_calls(50000, 17)).all()
+    m = tag_mix(a, 6)
+    # ~35% scaffold+boundary, 25% keys, 30% argument values, 10% free text.
+    assert abs(m[3] + m[4] - 0.35) < 0.07
+    assert abs(m[0] - 0.25) < 0.05
+    assert abs(m[1] + m[2] - 0.30) < 0.05
+    assert abs(m[5] - 0.10) < 0.04
+
+
+def test_schema_prompt_labels_in_range():
+    t = schema_prompt_tags(20000, 3)
+    assert t.min() >= 6 and t.max() <= 11 and t.size == 20000
+
+
+def test_policy_budget_and_blob_layout():
+    for cfg in CONFIGS:
+        pol = make_policy(cfg.n_tags, cfg.n_groups, cfg.n_layers, 0.33, cfg.seed)
+        assert abs(pol.expected_cost - 0.33) < 0.02 or pol.expected_cost < 0.33
+        blob = pack_blob(pol)
+        magic, ver, hdr, T, C, L, sink, win, body = struct.unpack_from("<4sHHIIIIII", blob)
+        assert magic == b"PASK" and ver == 1 and hdr == 32 and (T, C, L) == (cfg.n_tags, cfg.n_groups, cfg.n_layers)
+        assert len(blob) == 32 + body + 4
+        assert struct.unpack_from("<I", blob, len(blob) - 4)[0] == fnv1a32(blob[:-4])
+
+
+def test_prompt_lengths_ranges():
+    for cfg in CONFIGS:
+        p = prompt_lengths(cfg)
+        assert p.shape == (cfg.batch,)
+        assert p.min() >= cfg.prompt_min and p.max() <= cfg.prompt_max
+
+
+def test_bf16_normal_seeded():
+    a = bf16_normal((4, 8), 5)
+    b = bf16_normal((4, 8), 5)
+    assert (a == b).all() and a.shape == (4, 8)
