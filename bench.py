@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Decode-attention throughput of the PASK hot path on one MI355X.
+
+One step = one decode step of every sequence through every layer: per layer
+one pask_decode_attn call that persists the step's token (table lookup,
+compaction, quantise-and-pack or bf16 copy) and runs grouped-query attention
+over the layer's mixed bf16 / int4 cache.  Prints one JSON line.
+
+Workload (default): Qwen3-4B attention geometry (36 layers in 4 groups,
+32 query / 8 KV heads, head_dim 128), batch 64, prompts U{1024..8192} kept
+RETAIN-HIGH, function-call tag streams from the seeded grammar walker, a
+6 x 4 policy table at budget 0.33.  512 generated tokens are persisted
+before timing; the timed steps continue the same streams.  Synthetic data,
+random values; inputs are resident in HBM before the timed region.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+METRIC = "decode-attn tokens/s at KV budget 0.33; achieved HBM GB/s vs MI355X peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_workload(cfg_idx: int):
+    from workload import CONFIGS, make_policy, prompt_lengths, tag_mix, walk_function_calls
+    from workload.tags import iid_tags
+    from workload.tensors import sub_seed
+    cfg = CONFIGS[cfg_idx]
+    P = prompt_lengths(cfg)
+    if cfg.tag_source == "walker":
+        tags = np.stack([walk_function_calls(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b))
+                         for b in range(cfg.batch)])
+        probs = tag_mix(walk_function_calls(200000, sub_seed(cfg.seed, "tags", 1 << 20)), 6)
+    else:
+        tags = np.stack([iid_tags(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)])
+        probs = None
+    beta = cfg.budgets[0] if len(cfg.budgets) == 1 else 0.33
+    pol = make_policy(6, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs)
+    return cfg, P, tags.astype(np.uint8), pol
+
+
+def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
+    import torch
+
+    from paper_2608_28276_amd import pask
+    from paper_2608_28276_amd.session import PaskSession
+    from workload.policy import pack_blob
+
+    dev = torch.device("cuda:0")
+    B, L, Hq, Hkv, D = cfg.batch, cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    T = cfg.gen_tokens
+    assert t_start + warmup + steps <= T, "not enough generated tokens for the requested steps"
+    pages = lambda n: int(np.sum((np.asarray(n) + 15) // 16))
+    hi_pages = L * pages(P + T)
+    lo_pages = L * pages(np.full(B, T))
+    max_tok = int(P.max()) + T
+    sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=cfg.n_layers, n_q_heads=Hq, n_kv_heads=Hkv,
+                       head_dim=D, max_tokens_per_seq=max_tok, hi_pages=hi_pages, lo_pages=lo_pages,
+                       max_ctx_hint=max_tok)
+    log(f"cache {sess.nbytes / 2**30:.1f} GiB, workspace {sess.ws_bytes / 2**20:.1f} MiB")
+    g = torch.Generator(device=dev)
+    g.manual_seed(cfg.seed)
+    n_new = torch.as_tensor(P, dtype=torch.int32, device=dev)
+    tags_dev = torch.as_tensor(tags, device=dev)
+    t0 = time.time()
+    for layer in range(L):
+        k = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        v = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        sess.append(layer, None, k, v, n_new=n_new, keep_all=True)
+        del k, v
+        if t_start:
+            k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+            v = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+            sess.append(layer, tags_dev[:, :t_start].contiguous(), k, v)
+            del k, v
+    torch.cuda.synchronize()
+    log(f"prompt + {t_start} generated tokens persisted in {time.time() - t0:.1f} s")
+
+    q = torch.randn((L, B, Hq, D), generator=g, device=dev, dtype=torch.bfloat16)
+    kn = torch.randn((L, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+    vn = torch.randn((L, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+    out = torch.empty((L, B, Hq, D), dtype=torch.bfloat16, device=dev)
+    tags_t = tags_dev.t().contiguous()                   # [T, B]
+    stream = torch.cuda.current_stream(dev)
+    sptr = stream.cuda_stream
+    pol_c, cache_c = sess.policy, sess.cache
+    ws, ws_bytes, hint, scale = sess.ws.data_ptr(), sess.ws_bytes, sess.max_ctx_hint, sess.softmax_scale
+    qp = [q[i].data_ptr() for i in range(L)]
+    op = [out[i].data_ptr() for i in range(L)]
+    kp = [kn[i].data_ptr() for i in range(L)]
+    vp = [vn[i].data_ptr() for i in range(L)]
+    lib = pask.library()
+    import ctypes as C
+    pol_ref, cache_ref = C.byref(pol_c), C.byref(cache_c)
+
+    def step(t, events=None):
+        tp = tags_t[t].data_ptr()
+        for layer in range(L):
+            if events is not None:
+                events[layer][0].record(stream)
+            st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, tp, kp[layer],
+                                      vp[layer], C.c_float(scale), hint, ws, ws_bytes, sptr)
+            if st != 0:
+                raise pask.PaskError(st, "pask_decode_attn")
+            if events is not None:
+                events[layer][1].record(stream)
+
+    for i in range(warmup):
+        step(t_start + i)
+    torch.cuda.synchronize()
+    cnt0 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
+    events = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(L)]
+              for _ in range(steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(steps):
+        step(t_start + warmup + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    cnt1 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
+    call_ms = np.array([[e[0].elapsed_time(e[1]) for e in ev] for ev in events])   # [steps, L]
+    st, status, _ = sess.stats(batch=B)
+    if status != 0:
+        raise RuntimeError(f"device flags set: {st.device_flags:#x}")
+
+    mH = 2 * Hkv * D * 2
+    mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
+    # Algorithmic bytes of one layer call, averaged over the timed calls: every
+    # persisted entry read once (counts grow linearly over the region), q read,
+    # o written, the step's token stored in its persisted form, one list entry.
+    kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL
+    read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)          # per layer, summed over seqs
+    new_tok = (kv_bytes(cnt1) - kv_bytes(cnt0)).sum(axis=0) / steps      # per layer per step
+    stored = ((cnt1[..., 0] + cnt1[..., 1]) - (cnt0[..., 0] + cnt0[..., 1])).sum(axis=0) / steps
+    per_call = read + new_tok + 4 * stored + 2 * 2 * B * Hq * D         # [L]
+    bytes_per_step = float(per_call.sum())
+    avg_call_s = float(call_ms.mean()) / 1e3
+    achieved = float(per_call.mean()) / avg_call_s / 1e9
+    tokens_per_s = B * steps / wall
+    res = dict(
+        tokens_per_s=tokens_per_s, ms_per_step=wall / steps * 1e3, achieved=achieved,
+        avg_call_us=avg_call_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(per_call.mean()),
+        c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
+        step_gbs=bytes_per_step / (wall / steps) / 1e9,
+        mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()),
+    )
+    return res
+
+
+def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
+    """The oracle as it stands, on a bounded sample: n_seq sequences of the
+    same workload (their prompt lengths and tag streams, seeded CPU inputs),
+    history built untimed, then one timed decode step through all layers."""
+    import threadpoolctl
+    import torch
+
+    import oracle
+    from workload.tensors import bf16_normal, sub_seed
+    L, Hq, Hkv, D = cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    oc = oracle.OracleCache(dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer,
+                                 n_sink=pol.n_sink), Hkv, D)
+    bits = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+    seqs = list(range(n_seq))
+    for b in seqs:
+        for layer in range(L):
+            p = int(P[b])
+            k = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_k", layer, b))
+            v = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_v", layer, b))
+            oc.append(layer, b, np.zeros(p, np.uint8), bits(k[:p]), bits(v[:p]), keep_all=True)
+            oc.append(layer, b, tags[b, :t_start], bits(k[p:]), bits(v[p:]))
+    q = bf16_normal((L, Hq, D), sub_seed(cfg.seed, "q", 0))
+    kn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_k", 0))
+    vn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_v", 0))
+    scale = float(np.float32(1.0 / math.sqrt(D)))
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    t0 = time.perf_counter()
+    for b in seqs:
+        for layer in range(L):
+            oc.append(layer, b, tags[b, t_start:t_start + 1], bits(kn[layer][None]), bits(vn[layer][None]))
+            oc.attend(layer, b, bits(q[layer]), scale)
+    el = time.perf_counter() - t0
+    return dict(value=n_seq / el, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{n_seq} sequences (prompts {', '.join(str(int(P[b])) for b in seqs)} + {t_start} "
+                       f"generated tokens) x 1 decode step x {L} layers, fp64 numpy, {el:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload index (default: the B=64 serving batch)")
+    ap.add_argument("--t-start", type=int, default=512, help="generated tokens persisted before timing")
+    ap.add_argument("--cpu-seqs", type=int, default=1, help="sequences in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the PASK hot path here has no cross-GPU part "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+    cfg, P, tags, pol = build_workload(args.config)
+    log(f"workload {cfg.name}: B={cfg.batch} L={cfg.n_layers} prompts {int(P.min())}..{int(P.max())}, "
+        f"policy expected cost {pol.expected_cost:.3f}")
+    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start)
+    log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
+        f"{g['achieved']:.0f} GB/s algorithmic")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs)
+        log(f"cpu oracle: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
+    line = {
+        "metric": METRIC,
+        "value": round(g["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(g["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name, "batch": cfg.batch, "layers": cfg.n_layers, "layer_groups": cfg.n_groups,
+            "q_heads": cfg.n_q_heads, "kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
+            "prompt_tokens": f"U{{{cfg.prompt_min}..{cfg.prompt_max}}}", "generated_before_timing": args.t_start,
+            "budget": 0.33, "realised_c_kv_generated": round(g["c_kv_governed"], 4),
+            "realised_c_kv_all": round(g["c_kv_all"], 4), "page_tokens": 16,
+            "mean_persisted_entries": round(g["mean_entries"], 1),
+            "hbm_gb_per_step": round(g["bytes_per_step"] / 1e9, 3),
+            "step_gbs": round(g["step_gbs"], 1),
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "pask_decode_attn call (append_step + attn_split + attn_combine)",
+            "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,246 @@
+/*
+ * pask.h - C ABI of the PASK decode hot path on MI355X (gfx950).
+ *
+ * PASK (parser-aware structural KV persistence) gives every generated token a
+ * structural tag z_t from the accepted parser transition (Section 3.2, Eq. 3).
+ * The pair (z_t, layer group c) indexes a frozen table Lambda that stores, per
+ * bucket, a selected action a0, a protection floor a- and adjacent upgrade
+ * scores (Section 3.3, end of the offline calibration).  Online, the action
+ * is max(a0, a-) under the order DROP < RETAIN-LOW < RETAIN-HIGH (Eq. 10; the
+ * lookup and max steps of Alg. 2), and the token's KV in that group's layers
+ * is persisted accordingly (the Persist step of Alg. 2): DROP releases it from
+ * future attention, RETAIN-LOW keeps it at low precision, RETAIN-HIGH keeps it
+ * at full precision (Section 3.1).  Decode attention then reads only the
+ * persisted history.  The normalised KV cost C_KV is that of Eq. 1.
+ *
+ * Formats chosen here where the paper is silent:
+ *   RETAIN-HIGH  bf16 K and V.
+ *   RETAIN-LOW   int4, symmetric: per 32 consecutive head_dim elements of one
+ *                (token, layer, KV head, K or V) vector, s = RNE_fp16(absmax/7)
+ *                saturated at 65504; q_i = clamp(RNE(x_i / s), -7, 7), all 0
+ *                when s == 0; two's-complement nibbles, element 2j in the low
+ *                nibble of byte j.  Dequantised value q * s.
+ *   Protected recent window: 0 (a window > 0 is rejected as unsupported).
+ *
+ * Conventions for every entry point:
+ *   - Return an int status: PASK_OK (0) or a negative PASK_E_* code.  No
+ *     exception crosses the ABI.
+ *   - Host-side validation happens before any HIP call; a call that fails it
+ *     returns an error and touches neither the cache nor the stream.
+ *   - Device pointers are HIP device memory owned by the caller; the library
+ *     never allocates or frees device memory and keeps no pointer after a call
+ *     returns.  Work is enqueued on the caller's stream and is asynchronous
+ *     except where stated (pask_cache_stats synchronises its stream).
+ *   - Calls on one cache must be ordered on one stream (append before the
+ *     attention that must see it).  Distinct caches may run concurrently.
+ *   - Device-side anomalies do not fail a launch: they set sticky bits in the
+ *     cache's status word (PASK_FLAG_*), reported by pask_cache_stats.
+ */
+#ifndef PASK_H
+#define PASK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+  PASK_OK = 0,
+  PASK_E_ARG = -1,          /* null pointer, misaligned pointer, bad scalar  */
+  PASK_E_POLICY = -2,       /* malformed or inconsistent policy blob         */
+  PASK_E_SHAPE = -3,        /* geometry / shape not supported or mismatched  */
+  PASK_E_CAPACITY = -4,     /* buffer smaller than required                  */
+  PASK_E_HIP = -5,          /* a HIP runtime call or launch failed           */
+  PASK_E_DEVICE_FLAG = -6,  /* stats read fine, device status word non-zero  */
+  PASK_E_UNSUPPORTED = -7   /* valid per the paper, not supported here       */
+};
+
+/* ---- actions, ordered R < L < H (Section 3.1) --------------------------- */
+enum { PASK_DROP = 0, PASK_RETAIN_LOW = 1, PASK_RETAIN_HIGH = 2 };
+
+/* ---- device status-word bits (sticky until pask_cache_reset) ----------- */
+enum {
+  PASK_FLAG_BAD_TAG = 1u << 0,          /* tag >= n_tags: token kept HIGH      */
+  PASK_FLAG_HI_POOL_EXHAUSTED = 1u << 1,/* no HIGH page: token not stored      */
+  PASK_FLAG_LO_POOL_EXHAUSTED = 1u << 2,/* no LOW page: token not stored       */
+  PASK_FLAG_SEQ_CAPACITY = 1u << 3,     /* position >= max_tokens_per_seq      */
+  PASK_FLAG_BAD_COUNT = 1u << 4         /* n_new[b] outside [0, max_new]       */
+};
+
+/* ---- append flags -------------------------------------------------------- */
+enum {
+  /* Every appended token is RETAIN-HIGH regardless of its tag (prompt KV that
+   * the table does not govern).  Counted as "forced". */
+  PASK_APPEND_KEEP_ALL = 1u << 0
+};
+
+#define PASK_MAX_TAGS 64
+#define PASK_MAX_GROUPS 16
+#define PASK_MAX_LAYERS 128
+#define PASK_PAGE_TOKENS 16
+#define PASK_QGROUP 32
+
+/* Cache geometry.  Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in
+ * {1, 2, 4, 8}; page_tokens 16. */
+typedef struct pask_geom {
+  int32_t max_batch;           /* sequences the cache holds                      */
+  int32_t n_layers;            /* layers the cache holds (== policy n_layers)    */
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t page_tokens;         /* 16                                             */
+  int32_t max_tokens_per_seq;  /* positions per (sequence, layer)                */
+  int32_t hi_pages;            /* pages in the RETAIN-HIGH pool (all layers)     */
+  int32_t lo_pages;            /* pages in the RETAIN-LOW pool (all layers)      */
+} pask_geom;
+
+/* The frozen table Lambda after parsing (caller-owned plain data). */
+typedef struct pask_policy {
+  uint32_t n_tags, n_groups, n_layers, n_sink, recent_window;
+  uint8_t group_of_layer[PASK_MAX_LAYERS];
+  uint8_t action[PASK_MAX_TAGS][PASK_MAX_GROUPS];   /* selected action a0     */
+  uint8_t floor_[PASK_MAX_TAGS][PASK_MAX_GROUPS];   /* protection floor a-    */
+  float rho_up[PASK_MAX_TAGS][PASK_MAX_GROUPS][2];  /* Eq. 7: R->L, L->H      */
+  uint64_t entry_bytes[3];  /* m(a) per (token, layer): DROP, LOW, HIGH       */
+} pask_policy;
+
+/* A cache: geometry plus one caller-owned device buffer of
+ * pask_cache_bytes(&geom) bytes, 256-byte aligned. */
+typedef struct pask_cache {
+  pask_geom geom;
+  void* base;
+  uint64_t bytes;
+} pask_cache;
+
+/* Byte offsets of the regions inside a cache buffer (for inspection). */
+typedef struct pask_cache_layout {
+  uint64_t status_off;       /* u32 status word; u32 HI and LO page cursors at +8, +12 */
+  uint64_t counters_off;     /* i32 [max_batch][n_layers][8]: n_hi, n_lo, n_pos,
+                                n_drop, n_forced, n_lost, 0, 0                      */
+  uint64_t block_table_off;  /* i32 [max_batch][n_layers][2][max_pages]: page ids,
+                                store 0 = HIGH, 1 = LOW                            */
+  uint64_t index_list_off;   /* i32 [max_batch][n_layers][2][max_tokens_per_seq]:
+                                position of each slot of each store               */
+  uint64_t staging_off;      /* i32 [max_batch][max_tokens_per_seq]: append plan   */
+  uint64_t hi_pool_off;      /* hi_pages pages of hi_page_bytes                    */
+  uint64_t lo_pool_off;      /* lo_pages pages of lo_page_bytes                    */
+  uint64_t total_bytes;
+  uint64_t hi_page_bytes;    /* per KV head h at h * (2*16*D*2): K [16][D] bf16,
+                                then V [16][D] bf16                               */
+  uint64_t lo_page_bytes;    /* per KV head h at h * 2*(16*D/2 + 16*D/32*2):
+                                K codes [16][D/2] u8, K scales [16][D/32] fp16,
+                                V codes [16][D/2] u8, V scales [16][D/32] fp16   */
+  int32_t max_pages;         /* ceil(max_tokens_per_seq / 16)                      */
+  int32_t counter_stride;    /* 8                                                  */
+} pask_cache_layout;
+
+/* Accounting of what a cache holds (Eq. 1).  Entry = one (token, layer). */
+typedef struct pask_stats {
+  int64_t n_entries;       /* positions appended, summed over sequences, layers */
+  int64_t n_high, n_low, n_drop, n_lost;
+  int64_t n_forced_high;   /* HIGH entries not governed by the table           */
+  int64_t bytes_high, bytes_low;
+  int64_t hi_pages_used, lo_pages_used;
+  double c_kv_governed;    /* Eq. 1 over table-governed entries                */
+  double c_kv_all;         /* stored bytes / bf16 bytes over all entries       */
+  uint32_t device_flags;
+  uint32_t reserved;
+} pask_stats;
+
+/* Parse and validate a policy blob (the frozen table of the offline
+ * calibration, Section 3.3; format version 1, see below) against a geometry.
+ *
+ * Blob, little-endian: "PASK", u16 version = 1, u16 header bytes = 32,
+ * u32 n_tags, n_groups, n_layers, n_sink, recent_window, payload bytes;
+ * payload: u8 group_of_layer[n_layers], u8 action[n_tags][n_groups],
+ * u8 floor[n_tags][n_groups], zero pad to 4, f32 rho_up[n_tags][n_groups][2];
+ * then u32 FNV-1a hash of all preceding bytes.
+ *
+ * Errors: PASK_E_ARG (null pointers), PASK_E_POLICY (bad magic, version,
+ * sizes, hash, action or floor > 2, group id >= n_groups, rho not finite or
+ * negative, n_tags/n_groups/n_layers out of range), PASK_E_SHAPE (n_layers !=
+ * geometry's, or the geometry itself invalid), PASK_E_UNSUPPORTED
+ * (recent_window != 0).  Host only: no HIP call. */
+int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pask_policy* out);
+
+/* Region offsets of a cache of this geometry.  PASK_E_SHAPE if unsupported. */
+int pask_cache_layout_query(const pask_geom* geom, pask_cache_layout* out);
+
+/* Bytes a cache of this geometry needs; 0 if the geometry is unsupported. */
+size_t pask_cache_bytes(const pask_geom* geom);
+
+/* Bind a caller-owned device buffer (>= pask_cache_bytes, 256-byte aligned) to
+ * a cache and reset it.  Errors: PASK_E_ARG, PASK_E_SHAPE, PASK_E_CAPACITY,
+ * PASK_E_HIP. */
+int pask_cache_init(pask_cache* cache, const pask_geom* geom, void* base, size_t bytes,
+                    hipStream_t stream);
+
+/* Empty every sequence: zero counters, page cursors and the status word (page
+ * contents are left as they are). */
+int pask_cache_reset(pask_cache* cache, hipStream_t stream);
+
+/* Persist new tokens (the Persist step of Alg. 2) for one layer.
+ *
+ * For sequence b < batch, the next n_new[b] tokens (n_new_dev may be NULL:
+ * every sequence appends max_new) with tags tags_dev[b][0..n_new[b]) and
+ * bf16 K, V at k_dev / v_dev [batch][max_new][n_kv_heads][head_dim] get the
+ * action max(action[z][c], floor[z][c]) of the layer's group c (Eq. 10);
+ * positions below n_sink, tokens of a KEEP_ALL call (tags_dev may be NULL) and
+ * tags >= n_tags get RETAIN-HIGH.  Surviving tokens receive the next slots of
+ * their store in position order; DROP tokens get none (release, Section 3.1).
+ *
+ * Errors: PASK_E_ARG (null or misaligned pointers, flags), PASK_E_SHAPE
+ * (layer, batch or max_new out of range, policy / geometry mismatch),
+ * PASK_E_HIP. */
+int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
+                   const int32_t* n_new_dev, int32_t max_new, const uint8_t* tags_dev,
+                   const void* k_dev, const void* v_dev, uint32_t flags, hipStream_t stream);
+
+/* Workspace bytes pask_decode_attn needs for `batch` sequences when no
+ * sequence holds more than max_ctx_hint persisted entries (a larger count is
+ * still correct, only less parallel). */
+size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint);
+
+/* One decode step of one layer: optionally persist one new token per sequence
+ * (when tags_new_dev != NULL: tags [batch], k_new / v_new bf16
+ * [batch][n_kv_heads][head_dim]; the same rules as pask_kv_append), then
+ * grouped-query attention of q_dev bf16 [batch][n_q_heads][head_dim] over the
+ * persisted history of the layer (HIGH entries as stored, LOW entries
+ * dequantised), query head h reading KV head h / (n_q_heads / n_kv_heads):
+ *   out[b][h] = sum_j softmax_j(softmax_scale * q . k_j) v_j   (bf16)
+ *   lse_dev[b][h] = natural-log sum-exp of the scaled scores (fp32; nullable)
+ * A sequence with no persisted entry gives out = 0 and lse = -inf.
+ * ws_dev: device workspace of at least pask_workspace_bytes(geom, batch,
+ * max_ctx_hint) bytes, 256-byte aligned.
+ *
+ * Errors: PASK_E_ARG, PASK_E_SHAPE, PASK_E_CAPACITY (workspace too small),
+ * PASK_E_HIP. */
+int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
+                     const void* q_dev, void* out_dev, float* lse_dev,
+                     const uint8_t* tags_new_dev, const void* k_new_dev, const void* v_new_dev,
+                     float softmax_scale, int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes,
+                     hipStream_t stream);
+
+/* Read the cache's counters (synchronises `stream`) and fill `out`: entry
+ * counts per action, stored bytes, realised C_KV (Eq. 1) and the device
+ * status word.  per_seq_group_head (nullable, host) receives int64
+ * [batch][n_groups][n_kv_heads][3] counts of DROP, LOW, HIGH entries summed
+ * over the layers of each group (identical across KV heads: the table has no
+ * head axis).  Returns PASK_E_DEVICE_FLAG when the status word is non-zero
+ * (after filling `out`). */
+int pask_cache_stats(const pask_policy* policy, const pask_cache* cache, int32_t batch,
+                     pask_stats* out, int64_t* per_seq_group_head, hipStream_t stream);
+
+/* Static text for a status code. */
+const char* pask_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PASK_H */

@@ -263,10 +263,10 @@ class _SeqLayer:
     n_pos: int = 0
     hi_pos: list = field(default_factory=list)
     lo_pos: list = field(default_factory=list)
-    hi_k: list = field(default_factory=list)     # bf16 bits [Hkv, D] per entry
+    hi_k: list = field(default_factory=list)     # bf16 bits [n, Hkv, D] per append
     hi_v: list = field(default_factory=list)
-    lo_kc: list = field(default_factory=list)    # int8 codes [Hkv, D]
-    lo_ks: list = field(default_factory=list)    # fp16 scale bits [Hkv, D/32]
+    lo_kc: list = field(default_factory=list)    # int8 codes [n, Hkv, D] per append
+    lo_ks: list = field(default_factory=list)    # fp16 scale bits [n, Hkv, D/32] per append
     lo_vc: list = field(default_factory=list)
     lo_vs: list = field(default_factory=list)
     n_forced: int = 0
@@ -297,33 +297,27 @@ class OracleCache:
         st = self.sl(seq, layer)
         tags = np.asarray(tags).reshape(-1)
         n = tags.size
-        k_bits = np.asarray(k_bits, dtype=np.int64).reshape(n, self.hkv, self.d)
-        v_bits = np.asarray(v_bits, dtype=np.int64).reshape(n, self.hkv, self.d)
+        k_bits = (np.asarray(k_bits).astype(np.int64) & 0xFFFF).astype(np.uint16).reshape(n, self.hkv, self.d)
+        v_bits = (np.asarray(v_bits).astype(np.int64) & 0xFFFF).astype(np.uint16).reshape(n, self.hkv, self.d)
         pos = st.n_pos + np.arange(n)
         c = int(self.group_of_layer[layer])
         acts, forced, bad = decide(tags, pos, c, self.action, self.floor, self.n_sink, keep_all)
         self.bad_tag |= bool(bad.any())
         st.n_forced += int(forced.sum())
-        lo_idx = np.nonzero(acts == LOW)[0]
-        if lo_idx.size:
-            kc, ks = quantize_groups(k_bits[lo_idx])
-            vc, vs = quantize_groups(v_bits[lo_idx])
-        j = 0
-        for i in range(n):
-            a = acts[i]
-            if a == HIGH:
-                st.hi_pos.append(int(pos[i]))
-                st.hi_k.append(k_bits[i])
-                st.hi_v.append(v_bits[i])
-            elif a == LOW:
-                st.lo_pos.append(int(pos[i]))
-                st.lo_kc.append(kc[j])
-                st.lo_ks.append(ks[j])
-                st.lo_vc.append(vc[j])
-                st.lo_vs.append(vs[j])
-                j += 1
-            else:
-                st.n_drop += 1
+        hi = acts == HIGH
+        lo = acts == LOW
+        st.hi_pos.extend(pos[hi].tolist())
+        st.hi_k.append(k_bits[hi])
+        st.hi_v.append(v_bits[hi])
+        if lo.any():
+            kc, ks = quantize_groups(k_bits[lo])
+            vc, vs = quantize_groups(v_bits[lo])
+            st.lo_pos.extend(pos[lo].tolist())
+            st.lo_kc.append(kc)
+            st.lo_ks.append(ks)
+            st.lo_vc.append(vc)
+            st.lo_vs.append(vs)
+        st.n_drop += int((acts == DROP).sum())
         st.n_pos += n
         return acts
 
@@ -336,23 +330,27 @@ class OracleCache:
         st = self.sl(seq, layer)
         shp_c = (0, self.hkv, self.d)
         shp_s = (0, self.hkv, self.d // QGROUP)
-        f = lambda xs, shp, dt: (np.stack(xs).astype(dt) if xs else np.zeros(shp, dt))
+        f = lambda xs, shp, dt: (np.concatenate(xs).astype(dt) if xs else np.zeros(shp, dt))
         return (f(st.lo_kc, shp_c, np.int8), f(st.lo_ks, shp_s, np.uint16),
                 f(st.lo_vc, shp_c, np.int8), f(st.lo_vs, shp_s, np.uint16))
 
+    def hi_entries(self, seq: int, layer: int):
+        """(k bits, v bits) of the HIGH store, by slot (uint16 bf16 patterns)."""
+        st = self.sl(seq, layer)
+        shp = (0, self.hkv, self.d)
+        f = lambda xs: np.concatenate(xs) if xs else np.zeros(shp, np.uint16)
+        return f(st.hi_k), f(st.hi_v)
+
     def visible_kv(self, seq: int, layer: int):
         """K and V of every persisted entry in position order, in fp64."""
-        st = self.sl(seq, layer)
-        entries = []
-        for i, p in enumerate(st.hi_pos):
-            entries.append((p, bf16_to_f64(st.hi_k[i]), bf16_to_f64(st.hi_v[i])))
-        for i, p in enumerate(st.lo_pos):
-            entries.append((p, dequant(st.lo_kc[i], st.lo_ks[i]), dequant(st.lo_vc[i], st.lo_vs[i])))
-        entries.sort(key=lambda t: t[0])
-        if not entries:
-            z = np.zeros((0, self.hkv, self.d))
-            return z, z.copy()
-        return np.stack([e[1] for e in entries]), np.stack([e[2] for e in entries])
+        hk, hv = self.hi_entries(seq, layer)
+        kc, ks, vc, vs = self.lo_entries(seq, layer)
+        hi_pos, lo_pos = self.lists(seq, layer)
+        pos = np.concatenate([hi_pos, lo_pos])
+        k = np.concatenate([bf16_to_f64(hk), dequant(kc, ks)])
+        v = np.concatenate([bf16_to_f64(hv), dequant(vc, vs)])
+        order = np.argsort(pos, kind="stable")
+        return k[order], v[order]
 
     def attend(self, layer: int, seq: int, q_bits, scale: float):
         """Decode attention of one sequence's query (bf16 bits [Hq, D]) over the

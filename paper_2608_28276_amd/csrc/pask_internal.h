@@ -1,0 +1,71 @@
+// Internal declarations shared by the C ABI (pask_api.cpp) and the gfx950
+// kernels (pask_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "pask.h"
+
+namespace pask {
+
+enum Store { kHi = 0, kLo = 1 };
+enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4, kCntLost = 5 };
+constexpr int kCounterStride = 8;
+constexpr int kPage = 16;          // tokens per page
+constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW vector
+constexpr int kUnitTokens = 256;   // slots per attention work unit (16 pages)
+constexpr uint32_t kKeepAll = 1u;
+
+// Device-side view of one cache buffer.
+struct CacheView {
+  uint32_t* status;       // [0] status word, [2] HI cursor, [3] LO cursor
+  int32_t* counters;      // [max_batch][n_layers][8]
+  int32_t* block_table;   // [max_batch][n_layers][2][max_pages]
+  int32_t* index_list;    // [max_batch][n_layers][2][max_tokens]
+  int32_t* staging;       // [max_batch][max_tokens]
+  uint8_t* hi_pool;
+  uint8_t* lo_pool;
+  int32_t n_layers, n_kv_heads, head_dim, max_tokens, max_pages, hi_pages, lo_pages;
+  uint32_t hi_page_bytes, lo_page_bytes;
+};
+
+// Lambda's column for one layer group: selected action a0 and floor a- per tag.
+struct TableColumn {
+  uint8_t a0[64];
+  uint8_t amin[64];
+  uint32_t n_tags;
+  uint32_t n_sink;
+};
+
+struct AppendArgs {
+  CacheView cv;
+  TableColumn tab;
+  const int32_t* n_new;     // [batch] or null (all max_new)
+  const uint8_t* tags;      // [batch][max_new] or null (KEEP_ALL)
+  const uint16_t* k;        // bf16 bits [batch][max_new][Hkv][D]
+  const uint16_t* v;
+  int32_t layer, batch, max_new;
+  uint32_t flags;
+};
+
+struct AttnArgs {
+  CacheView cv;
+  const uint16_t* q;        // bf16 bits [batch][Hq][D]
+  uint16_t* out;            // bf16 bits [batch][Hq][D]
+  float* lse;               // [batch][Hq] or null
+  float* ws_o;              // [batch][Hq][splits][D]
+  float* ws_ml;             // [batch][Hq][splits][2]  (max, sum) in log2 units
+  float scale_log2;         // softmax_scale * log2(e)
+  int32_t layer, batch, n_q_heads, splits;
+};
+
+// Launchers (pask_kernels.hip).  Return hipSuccess or the launch error.
+hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+hipError_t launch_append_step(const AppendArgs& a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s);
+
+}  // namespace pask

@@ -1,0 +1,137 @@
+"""A cache, its workspace and the calls of one decode loop, with torch
+providing device memory and the stream.  Every computation runs in
+libpask.so's kernels through the C ABI binding.
+"""
+
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import pask
+
+
+class PaskSession:
+    """One cache of `max_batch` sequences x `n_layers` layers on one GPU."""
+
+    def __init__(self, policy_blob: bytes, *, max_batch: int, n_layers: int, n_q_heads: int, n_kv_heads: int,
+                 head_dim: int, max_tokens_per_seq: int, hi_pages: int, lo_pages: int,
+                 max_ctx_hint: int | None = None, device: str = "cuda:0", extra_bytes: int = 0):
+        self.device = torch.device(device)
+        self.geom = pask.make_geom(max_batch=max_batch, n_layers=n_layers, n_q_heads=n_q_heads,
+                                   n_kv_heads=n_kv_heads, head_dim=head_dim,
+                                   max_tokens_per_seq=max_tokens_per_seq, hi_pages=hi_pages, lo_pages=lo_pages)
+        self.policy = pask.pask_policy_load(policy_blob, self.geom)
+        self.nbytes = pask.pask_cache_bytes(self.geom)
+        if self.nbytes == 0:
+            raise pask.PaskError(pask.PASK_E_SHAPE, "pask_cache_bytes")
+        self.layout = pask.pask_cache_layout_query(self.geom)
+        # extra_bytes: room after the cache for out-of-bounds canaries in tests.
+        self.buf = torch.empty(self.nbytes + extra_bytes, dtype=torch.uint8, device=self.device)
+        self.cache = pask.pask_cache()
+        pask.pask_cache_init(self.cache, self.geom, self.buf, self.nbytes, self.stream)
+        self.max_ctx_hint = max_ctx_hint or max_tokens_per_seq
+        self.ws_bytes = pask.pask_workspace_bytes(self.geom, max_batch, self.max_ctx_hint)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.softmax_scale = float(torch.tensor(1.0 / math.sqrt(head_dim), dtype=torch.float32))
+
+    @property
+    def stream(self) -> int:
+        return torch.cuda.current_stream(self.device).cuda_stream
+
+    # -- the hot path ------------------------------------------------------
+    def append(self, layer: int, tags, k, v, n_new=None, keep_all: bool = False, batch: int | None = None):
+        """k, v: bf16 [batch, max_new, Hkv, D]; tags: uint8 [batch, max_new]."""
+        b = batch or k.shape[0]
+        pask.pask_kv_append(self.policy, self.cache, layer, b, n_new, k.shape[1], tags, k, v,
+                            pask.PASK_APPEND_KEEP_ALL if keep_all else 0, self.stream)
+
+    def decode(self, layer: int, q, out, lse=None, tags_new=None, k_new=None, v_new=None,
+               batch: int | None = None, max_ctx_hint: int | None = None):
+        """q, out: bf16 [batch, Hq, D]; optional fused append of one token per
+        sequence (tags_new uint8 [batch], k_new / v_new bf16 [batch, Hkv, D])."""
+        b = batch or q.shape[0]
+        hint = max_ctx_hint or self.max_ctx_hint
+        pask.pask_decode_attn(self.policy, self.cache, layer, b, q, out, lse, tags_new, k_new, v_new,
+                              self.softmax_scale, hint, self.ws, self.ws_bytes, self.stream)
+
+    def stats(self, batch: int | None = None, per_seq: bool = False):
+        import numpy as np
+        b = batch or self.geom.max_batch
+        arr = None
+        if per_seq:
+            arr = np.zeros(b * self.policy.n_groups * self.geom.n_kv_heads * 3, dtype=np.int64)
+        st, status = pask.pask_cache_stats(self.policy, self.cache, b, arr, self.stream)
+        if arr is not None:
+            arr = arr.reshape(b, self.policy.n_groups, self.geom.n_kv_heads, 3)
+        return st, status, arr
+
+    def reset(self):
+        pask.pask_cache_reset(self.cache, self.stream)
+
+    # -- views of the cache buffer (inspection) ----------------------------
+    def _i32(self, off: int, shape):
+        n = 1
+        for s in shape:
+            n *= s
+        return self.buf[off:off + 4 * n].view(torch.int32).view(*shape)
+
+    def status_words(self):
+        return self._i32(self.layout.status_off, (4,))
+
+    def counters(self):
+        g = self.geom
+        return self._i32(self.layout.counters_off, (g.max_batch, g.n_layers, self.layout.counter_stride))
+
+    def block_tables(self):
+        g = self.geom
+        return self._i32(self.layout.block_table_off, (g.max_batch, g.n_layers, 2, self.layout.max_pages))
+
+    def index_lists(self):
+        g = self.geom
+        return self._i32(self.layout.index_list_off, (g.max_batch, g.n_layers, 2, g.max_tokens_per_seq))
+
+    def hi_pool(self):
+        L = self.layout
+        return self.buf[L.hi_pool_off:L.hi_pool_off + self.geom.hi_pages * L.hi_page_bytes].view(
+            self.geom.hi_pages, L.hi_page_bytes)
+
+    def lo_pool(self):
+        L = self.layout
+        return self.buf[L.lo_pool_off:L.lo_pool_off + self.geom.lo_pages * L.lo_page_bytes].view(
+            self.geom.lo_pages, L.lo_page_bytes)
+
+    def gather_store(self, b: int, layer: int, store: int):
+        """Host copies of one store's entries, by slot, read through the block
+        table.  HIGH: (k bits [n, Hkv, D], v bits) as int64.  LOW: (k codes
+        packed [n, Hkv, D/2] u8, k scale bits [n, Hkv, D/32], v codes, v scales)."""
+        import numpy as np
+        g = self.geom
+        D, H = g.head_dim, g.n_kv_heads
+        cnt = self.counters()[b, layer].cpu().numpy()
+        n = int(cnt[store])
+        bt = self.block_tables()[b, layer, store].cpu().numpy()
+        pages = bt[: (n + 15) // 16]
+        if store == 0:
+            pool = self.hi_pool()
+            raw = pool[torch.as_tensor(pages, dtype=torch.long, device=self.device)].cpu().numpy() if n else \
+                np.zeros((0, self.layout.hi_page_bytes), np.uint8)
+            x = raw.view(np.uint16).reshape(-1, H, 2, 16, D).astype(np.int64)
+            k = x[:, :, 0].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+            v = x[:, :, 1].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+            return k, v
+        pool = self.lo_pool()
+        raw = pool[torch.as_tensor(pages, dtype=torch.long, device=self.device)].cpu().numpy() if n else \
+            np.zeros((0, self.layout.lo_page_bytes), np.uint8)
+        per_head = 2 * (16 * D // 2 + 16 * (D // 32) * 2)
+        half = per_head // 2
+        r = raw.reshape(-1, H, per_head)
+        out = []
+        for kv in range(2):
+            seg = r[:, :, kv * half:(kv + 1) * half]
+            codes = seg[:, :, :16 * D // 2].reshape(-1, H, 16, D // 2).transpose(0, 2, 1, 3).reshape(-1, H, D // 2)
+            sc = seg[:, :, 16 * D // 2:].copy().view(np.uint16).reshape(-1, H, 16, D // 32)
+            sc = sc.transpose(0, 2, 1, 3).reshape(-1, H, D // 32)
+            out += [codes[:n], sc[:n].astype(np.int64)]
+        return tuple(out)

@@ -1,0 +1,207 @@
+"""The C ABI on the host (no GPU): the library loads, exports every entry
+point include/pask.h declares, parses and validates policy blobs, lays out
+caches and rejects bad arguments before any HIP call."""
+
+import os
+import re
+import struct
+
+import numpy as np
+import pytest
+
+from workload.policy import fnv1a32, make_policy, pack_blob
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+pask = pytest.importorskip("paper_2608_28276_amd.pask", reason="libpask.so not built")
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "pask.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(pask_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) == 10
+    lib = pask.library()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(pask.EXPORTS)
+
+
+def geom(**kw):
+    d = dict(max_batch=4, n_layers=2, n_q_heads=8, n_kv_heads=2, head_dim=64, max_tokens_per_seq=512,
+             hi_pages=64, lo_pages=64)
+    d.update(kw)
+    return pask.make_geom(**d)
+
+
+def blob_for(T=6, C=2, L=2, beta=0.33, seed=1, **over):
+    pol = make_policy(T, C, L, beta, seed)
+    for k, v in over.items():
+        setattr(pol, k, v)
+    return pol, pack_blob(pol)
+
+
+def test_policy_load_roundtrip():
+    pol, blob = blob_for()
+    p = pask.pask_policy_load(blob, geom())
+    assert (p.n_tags, p.n_groups, p.n_layers, p.n_sink, p.recent_window) == (6, 2, 2, 0, 0)
+    got_a = np.array([[p.action[z][c] for c in range(2)] for z in range(6)])
+    got_f = np.array([[p.floor_[z][c] for c in range(2)] for z in range(6)])
+    got_r = np.array([[[p.rho_up[z][c][i] for i in range(2)] for c in range(2)] for z in range(6)], np.float32)
+    assert (got_a == pol.action).all() and (got_f == pol.floor).all() and (got_r == pol.rho_up).all()
+    assert list(p.group_of_layer[:2]) == pol.group_of_layer.tolist()
+    assert list(p.entry_bytes) == [0, 144, 512]
+
+
+def _rehash(b: bytes) -> bytes:
+    return b[:-4] + struct.pack("<I", fnv1a32(b[:-4]))
+
+
+def _patch(blob: bytes, off: int, fmt: str, val) -> bytes:
+    b = bytearray(blob)
+    struct.pack_into(fmt, b, off, val)
+    return _rehash(bytes(b))
+
+
+@pytest.mark.parametrize("case,code", [
+    ("magic", pask.PASK_E_POLICY), ("version", pask.PASK_E_POLICY), ("hash", pask.PASK_E_POLICY),
+    ("truncated", pask.PASK_E_POLICY), ("action3", pask.PASK_E_POLICY), ("group_oob", pask.PASK_E_POLICY),
+    ("rho_nan", pask.PASK_E_POLICY), ("rho_neg", pask.PASK_E_POLICY), ("n_tags0", pask.PASK_E_POLICY),
+    ("window", pask.PASK_E_UNSUPPORTED), ("layers_mismatch", pask.PASK_E_SHAPE), ("pad", pask.PASK_E_POLICY),
+])
+def test_policy_load_rejects(case, code):
+    pol, blob = blob_for()
+    L, T, C = 2, 6, 2
+    rho_off = 32 + ((L + 2 * T * C + 3) // 4) * 4
+    if case == "magic":
+        bad = b"XASK" + blob[4:]
+    elif case == "version":
+        bad = _patch(blob, 4, "<H", 2)
+    elif case == "hash":
+        bad = blob[:-1] + bytes([blob[-1] ^ 1])
+    elif case == "truncated":
+        bad = blob[:-8]
+    elif case == "action3":
+        bad = _patch(blob, 32 + L + 3, "<B", 3)
+    elif case == "group_oob":
+        bad = _patch(blob, 32, "<B", 2)
+    elif case == "rho_nan":
+        bad = _patch(blob, rho_off, "<f", float("nan"))
+    elif case == "rho_neg":
+        bad = _patch(blob, rho_off + 4, "<f", -1.0)
+    elif case == "n_tags0":
+        bad = _patch(blob, 8, "<I", 0)
+    elif case == "window":
+        bad = _patch(blob, 24, "<I", 4)
+    elif case == "layers_mismatch":
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_policy_load(blob, geom(n_layers=4))
+        assert e.value.status == code
+        return
+    else:  # non-zero padding byte between the u8 tables and rho
+        pad_at = 32 + L + 2 * T * C
+        assert pad_at < rho_off
+        bad = _patch(blob, pad_at, "<B", 1)
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_policy_load(bad, geom())
+    assert e.value.status == code
+
+
+def test_layout_and_sizes():
+    g = geom()
+    L = pask.pask_cache_layout_query(g)
+    assert L.hi_page_bytes == 2 * 2 * 16 * 64 * 2
+    assert L.lo_page_bytes == 2 * 2 * (16 * 32 + 16 * 2 * 2)
+    assert L.max_pages == 32 and L.counter_stride == 8
+    offs = [L.status_off, L.counters_off, L.block_table_off, L.index_list_off, L.staging_off, L.hi_pool_off,
+            L.lo_pool_off, L.total_bytes]
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
+    assert L.counters_off - L.status_off >= 16
+    assert L.block_table_off - L.counters_off >= 4 * 2 * 8 * 4
+    assert L.index_list_off - L.block_table_off >= 4 * 2 * 2 * 32 * 4
+    assert L.lo_pool_off - L.hi_pool_off >= 64 * L.hi_page_bytes
+    assert L.total_bytes - L.lo_pool_off >= 64 * L.lo_page_bytes
+    assert pask.pask_cache_bytes(g) == L.total_bytes
+    g4 = geom(n_q_heads=64, n_kv_heads=8, head_dim=128)
+    L4 = pask.pask_cache_layout_query(g4)
+    assert L4.hi_page_bytes == 65536 and L4.lo_page_bytes == 8 * 2 * (16 * 64 + 16 * 4 * 2)
+
+
+@pytest.mark.parametrize("bad", [dict(head_dim=96), dict(n_q_heads=6), dict(n_q_heads=32, n_kv_heads=2),
+                                 dict(page_tokens=32), dict(max_batch=0), dict(n_layers=200),
+                                 dict(hi_pages=-1), dict(max_tokens_per_seq=0)])
+def test_unsupported_geometry(bad):
+    g = geom(**bad)
+    assert pask.pask_cache_bytes(g) == 0
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_cache_layout_query(g)
+    assert e.value.status == pask.PASK_E_SHAPE
+
+
+def test_workspace_bytes():
+    g = geom()
+    # splits = ceil(hint / 256) + 1; rows = batch * Hq * splits; o: rows*D*4, ml: rows*2*4 (256-aligned)
+    ws = pask.pask_workspace_bytes(g, 4, 512)
+    rows = 4 * 8 * 3
+    want = ((rows * 64 * 4 + 255) // 256) * 256
+    want = ((want + rows * 8 + 255) // 256) * 256
+    assert ws == want
+
+
+def _fake_cache(g):
+    c = pask.pask_cache()
+    c.geom = g
+    c.base = 1 << 40       # never dereferenced: every call below fails validation first
+    c.bytes = pask.pask_cache_bytes(g)
+    return c
+
+
+def test_append_and_attn_validation_before_any_hip_call():
+    g = geom()
+    _, blob = blob_for()
+    p = pask.pask_policy_load(blob, g)
+    c = _fake_cache(g)
+    A = 1 << 41
+    cases = [
+        (dict(layer=2), pask.PASK_E_SHAPE), (dict(layer=-1), pask.PASK_E_SHAPE),
+        (dict(batch=0), pask.PASK_E_SHAPE), (dict(batch=5), pask.PASK_E_SHAPE),
+        (dict(max_new=513), pask.PASK_E_SHAPE), (dict(k=A + 2), pask.PASK_E_ARG),
+        (dict(k=0), pask.PASK_E_ARG), (dict(tags=0), pask.PASK_E_ARG), (dict(flags=2), pask.PASK_E_ARG),
+    ]
+    for over, code in cases:
+        kw = dict(layer=0, batch=1, n_new=None, max_new=4, tags=A, k=A, v=A, flags=0)
+        kw.update(over)
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_kv_append(p, c, kw["layer"], kw["batch"], kw["n_new"], kw["max_new"], kw["tags"], kw["k"],
+                                kw["v"], kw["flags"], 0)
+        assert e.value.status == code, over
+    small = _fake_cache(g)
+    small.bytes = c.bytes - 1
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_kv_append(p, small, 0, 1, None, 4, A, A, A, 0, 0)
+    assert e.value.status == pask.PASK_E_CAPACITY
+    ws_need = pask.pask_workspace_bytes(g, 1, 512)
+    acases = [
+        (dict(q=A + 8), pask.PASK_E_ARG), (dict(out=0), pask.PASK_E_ARG), (dict(ws=A + 128), pask.PASK_E_ARG),
+        (dict(ws_bytes=ws_need - 1), pask.PASK_E_CAPACITY), (dict(scale=float("inf")), pask.PASK_E_ARG),
+        (dict(tags=A, k=0), pask.PASK_E_ARG), (dict(layer=9), pask.PASK_E_SHAPE),
+    ]
+    for over, code in acases:
+        kw = dict(layer=0, q=A, out=A, tags=None, k=None, ws=A, ws_bytes=ws_need, scale=0.125)
+        kw.update(over)
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_decode_attn(p, c, kw["layer"], 1, kw["q"], kw["out"], None, kw["tags"], kw["k"], kw["k"],
+                                  kw["scale"], 512, kw["ws"], kw["ws_bytes"], 0)
+        assert e.value.status == code, over
+    other = pask.pask_policy_load(blob_for(L=4, C=2)[1], geom(n_layers=4))
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_kv_append(other, c, 0, 1, None, 4, A, A, A, 0, 0)
+    assert e.value.status == pask.PASK_E_SHAPE
+
+
+def test_status_strings():
+    assert pask.pask_status_string(0) == "ok"
+    assert "policy" in pask.pask_status_string(pask.PASK_E_POLICY)
+    assert pask.pask_status_string(-99) == "unknown status"
