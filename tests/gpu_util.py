@@ -58,11 +58,11 @@ class Scenario:
         self.prompt_tags = prompt_tags
         self.seed = seed
         self.max_tok = int(self.P.max()) + self.T
-        pages = lambda n: int(np.sum((n + 15) // 16))
+        pages = lambda n: int(np.sum((np.asarray(n, dtype=np.int64) + 15) // 16))
         if hi_pages is None:
             hi_pages = L * pages(self.P + self.T)
         if lo_pages is None:
-            lo_pages = L * pages((self.P if prompt_tags is not None else 0) + self.T)
+            lo_pages = L * pages((self.P if prompt_tags is not None else np.zeros(B, np.int64)) + self.T)
         self.sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=L, n_q_heads=Hq, n_kv_heads=Hkv,
                                 head_dim=D, max_tokens_per_seq=self.max_tok, hi_pages=hi_pages,
                                 lo_pages=lo_pages, max_ctx_hint=max_ctx_hint, extra_bytes=extra_bytes)
@@ -132,6 +132,7 @@ class Scenario:
                 self.oc.append(layer, b, self.gen_tags[b, t:t + 1], bits16(k[b]), bits16(v[b]))
             if not check:
                 continue
+            self.check_state(layers=[layer], seqs=seqs)
             o_gpu = bf16_f64(out)
             l_gpu = lse.cpu().double().numpy()
             for b in (range(self.B) if seqs is None else seqs):
@@ -165,4 +166,7 @@ class Scenario:
                 assert (vc == oracle.pack_nibbles(ovc)).all(), ("LOW V codes", layer, b)
                 assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
         st, status, _ = self.sess.stats(batch=self.B)
-        assert status == 0 and st.device_flags == 0
+        sw = self.sess.status_words().cpu().numpy()
+        assert status == 0 and st.device_flags == 0, (
+            f"device flags {st.device_flags:#x}; cursors {sw[2]}, {sw[3]} of pools "
+            f"{self.sess.geom.hi_pages}, {self.sess.geom.lo_pages}; lost {st.n_lost}")
