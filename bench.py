@@ -201,6 +201,20 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
                        f"generated tokens) x 1 decode step x {L} layers, fp64 numpy, {el:.1f} s")
 
 
+def copy_probe(gib: float):
+    """A plain copy kernel of known size: reads and writes n bytes, 3 times.
+    rocprofv3 counter readings of it calibrate FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = int(gib * 2**30)
+    x = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "repeats": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -210,7 +224,12 @@ def main():
     ap.add_argument("--t-start", type=int, default=512, help="generated tokens persisted before timing")
     ap.add_argument("--cpu-seqs", type=int, default=1, help="sequences in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
+                    help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the PASK hot path here has no cross-GPU part "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
