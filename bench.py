@@ -2,9 +2,9 @@
 """Decode-attention throughput of the PASK hot path on one MI355X.
 
 One step = one decode step of every sequence through every layer: per layer
-one pask_decode_attn call that persists the step's token (table lookup,
-compaction, quantise-and-pack or bf16 copy) and runs grouped-query attention
-over the layer's mixed bf16 / int4 cache.  Prints one JSON line.
+pask_kv_append persists the step's token (table lookup, compaction,
+quantise-and-pack or bf16 copy) and pask_decode_attn runs grouped-query
+attention over the layer's mixed bf16 / int4 cache.  Prints one JSON line.
 
 Workload (default): Qwen3-4B attention geometry (36 layers in 4 groups,
 32 query / 8 KV heads, head_dim 128), batch 64, prompts U{1024..8192} kept
@@ -110,12 +110,17 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
     pol_ref, cache_ref = C.byref(pol_c), C.byref(cache_c)
 
     def step(t, events=None):
+        # One decode step: per layer, persist the step's token (one-token append
+        # kernel), then the attention kernel over the layer's persisted history.
         tp = tags_t[t].data_ptr()
         for layer in range(L):
+            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, kp[layer], vp[layer], 0, sptr)
+            if st != 0:
+                raise pask.PaskError(st, "pask_kv_append")
             if events is not None:
                 events[layer][0].record(stream)
-            st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, tp, kp[layer],
-                                      vp[layer], C.c_float(scale), hint, ws, ws_bytes, sptr)
+            st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, None, None, None,
+                                      C.c_float(scale), hint, ws, ws_bytes, sptr)
             if st != 0:
                 raise pask.PaskError(st, "pask_decode_attn")
             if events is not None:
@@ -141,21 +146,24 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
 
     mH = 2 * Hkv * D * 2
     mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
-    # Algorithmic bytes of one layer call, averaged over the timed calls: every
-    # persisted entry read once (counts grow linearly over the region), q read,
-    # o written, the step's token stored in its persisted form, one list entry.
+    # Algorithmic bytes of one attention launch, averaged over the timed ones:
+    # every persisted entry read once (counts grow linearly over the region,
+    # each launch sees its step's token), q read, o written.  The one-token
+    # append adds the step's token in its stored form and one list entry.
     kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL
     read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)          # per layer, summed over seqs
+    qo = 2 * 2 * B * Hq * D
+    attn_bytes = read + qo                                                 # [L]
     new_tok = (kv_bytes(cnt1) - kv_bytes(cnt0)).sum(axis=0) / steps      # per layer per step
     stored = ((cnt1[..., 0] + cnt1[..., 1]) - (cnt0[..., 0] + cnt0[..., 1])).sum(axis=0) / steps
-    per_call = read + new_tok + 4 * stored + 2 * 2 * B * Hq * D         # [L]
-    bytes_per_step = float(per_call.sum())
-    avg_call_s = float(call_ms.mean()) / 1e3
-    achieved = float(per_call.mean()) / avg_call_s / 1e9
+    append_bytes = new_tok + 4 * stored + 2 * B * Hkv * D * 2             # stored form + lists + k/v read
+    bytes_per_step = float((attn_bytes + append_bytes).sum())
+    avg_attn_s = float(call_ms.mean()) / 1e3
+    achieved = float(attn_bytes.mean()) / avg_attn_s / 1e9
     tokens_per_s = B * steps / wall
     res = dict(
         tokens_per_s=tokens_per_s, ms_per_step=wall / steps * 1e3, achieved=achieved,
-        avg_call_us=avg_call_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(per_call.mean()),
+        avg_call_us=avg_attn_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(attn_bytes.mean()),
         c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
         step_gbs=bytes_per_step / (wall / steps) / 1e9,
         mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()),
@@ -201,18 +209,55 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
                        f"generated tokens) x 1 decode step x {L} layers, fp64 numpy, {el:.1f} s")
 
 
+def kernel_source_digest() -> str:
+    import hashlib
+    path = os.path.join(ROOT, "paper_2608_28276_amd", "csrc", "pask_kernels.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def traffic_record(cfg):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary of this workload, or None when the kernel source has changed since
+    the counters were taken (or no summary exists)."""
+    path = os.path.join(ROOT, "profiles", f"attn_kernel_{cfg.name}.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.startswith("<!-- traffic "):
+            rec = json.loads(line[len("<!-- traffic "):line.rindex("-->")])
+            if rec.get("source_digest") == kernel_source_digest():
+                return rec["bytes_per_launch"]
+    return None
+
+
 def copy_probe(gib: float):
     """A plain copy kernel of known size: reads and writes n bytes, 3 times.
-    rocprofv3 counter readings of it calibrate FETCH_SIZE / WRITE_SIZE."""
+    rocprofv3 counter readings of it calibrate FETCH_SIZE / WRITE_SIZE.  Also
+    reports the copy's and a read-only reduction's bandwidth (HIP events), an
+    on-box reference for what a streaming kernel reaches."""
     import torch
     n = int(gib * 2**30)
     x = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
     y = torch.empty_like(x)
     torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     for _ in range(3):
         y.copy_(x)
+    ev[0].record()
+    for _ in range(5):
+        y.copy_(x)
+    ev[1].record()
+    xf = x.view(torch.bfloat16)
+    xf.float().sum() if False else xf.sum(dtype=torch.float32)
+    ev[2].record()
+    for _ in range(5):
+        xf.sum(dtype=torch.float32)
+    ev[3].record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_probe_bytes": n, "repeats": 3}), flush=True)
+    copy_gbs = 2 * n * 5 / (ev[0].elapsed_time(ev[1]) / 1e3) / 1e9
+    read_gbs = n * 5 / (ev[2].elapsed_time(ev[3]) / 1e3) / 1e9
+    print(json.dumps({"copy_probe_bytes": n, "copy_gbs": round(copy_gbs, 1),
+                      "sum_read_gbs": round(read_gbs, 1)}), flush=True)
 
 
 def main():
@@ -269,8 +314,8 @@ def main():
         },
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": None,
-            "kernel": "pask_decode_attn call (append_step + attn_split + attn_combine)",
+            "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(cfg),
+            "kernel": f"attn_kernel<{cfg.head_dim}, {cfg.group_size}>",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
         },
         "cpu_baseline": cpu,

@@ -85,8 +85,8 @@ enum {
 #define PASK_PAGE_TOKENS 16
 #define PASK_QGROUP 32
 
-/* Cache geometry.  Supported: head_dim 64 or 128; n_q_heads / n_kv_heads in
- * {1, 2, 4, 8}; page_tokens 16. */
+/* Cache geometry.  Supported: head_dim 64 or 128; n_kv_heads 1..8;
+ * n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_tokens 16. */
 typedef struct pask_geom {
   int32_t max_batch;           /* sequences the cache holds                      */
   int32_t n_layers;            /* layers the cache holds (== policy n_layers)    */

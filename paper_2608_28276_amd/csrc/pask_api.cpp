@@ -25,7 +25,7 @@ bool valid_geom(const pask_geom* g) {
   if (!g) return false;
   if (g->max_batch < 1 || g->max_batch > 65535) return false;
   if (g->n_layers < 1 || g->n_layers > PASK_MAX_LAYERS) return false;
-  if (g->n_kv_heads < 1 || g->n_q_heads < g->n_kv_heads) return false;
+  if (g->n_kv_heads < 1 || g->n_kv_heads > 8 || g->n_q_heads < g->n_kv_heads) return false;
   if (g->n_q_heads % g->n_kv_heads != 0) return false;
   const int gs = g->n_q_heads / g->n_kv_heads;
   if (gs != 1 && gs != 2 && gs != 4 && gs != 8) return false;

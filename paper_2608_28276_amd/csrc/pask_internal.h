@@ -16,7 +16,10 @@ enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4
 constexpr int kCounterStride = 8;
 constexpr int kPage = 16;          // tokens per page
 constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW vector
-constexpr int kUnitTokens = 256;   // slots per attention work unit (16 pages)
+#ifndef PASK_UNIT_TOKENS
+#define PASK_UNIT_TOKENS 256
+#endif
+constexpr int kUnitTokens = PASK_UNIT_TOKENS;   // slots per attention work unit (multiple of 16)
 constexpr uint32_t kKeepAll = 1u;
 
 // Device-side view of one cache buffer.

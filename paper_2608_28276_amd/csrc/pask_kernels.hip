@@ -11,14 +11,17 @@
 //   append_pack  copy RETAIN-HIGH K/V (bf16) or quantise-and-pack RETAIN-LOW
 //                K/V (int4, one fp16 scale per 32 elements) into the pages.
 //   append_step  both of the above for one token per sequence (decode).
-//   attn_split   grouped-query flash-decode over one (sequence, KV head) and a
+//   attn         grouped-query flash-decode over one (sequence, KV head) and a
 //                set of 256-slot work units of the HIGH and LOW stores: query
 //                slice in registers, bf16 dot2 for q.k, int4 codes widened
-//                exactly in registers, online softmax in base 2.
-//   attn_combine merge the split partials (max, sum, weighted values).
+//                exactly in registers, online softmax in base 2, next page
+//                prefetched into registers.
+//   attn_merge   merge the split partials (max, sum, weighted values).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
+
+#include <type_traits>
 
 #include "pask_internal.h"
 
@@ -379,58 +382,93 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
 // decode attention
 // ---------------------------------------------------------------------------
 //
-// One wavefront per (split, KV head g, sequence b).  Two lane mappings of a
-// 16-slot page:
-//   K mapping  lane = 4t + s: slot t, head_dim slice s (D/4 contiguous dims);
-//              q . k is reduced over the 4 lanes of a quad.
-//   V mapping  lane = (D/8) r + c: slots r, r + 64/(D/8), ...; dims 8c..8c+7;
-//              every lane accumulates 8 dims of the G heads' outputs.
-// Probabilities move from the K to the V mapping through LDS.
+// One wavefront per (split, KV head g, sequence b).  A split walks 256-slot
+// work units, HIGH units first, then LOW units; within a unit it streams
+// 16-slot pages and loads page p+1 while it computes page p.  Two lane maps
+// of a page:
+//   K map  lane = 4t + s: slot t, head_dim slice s (D/4 contiguous dims);
+//          q . k over the slice, then summed over the 4 lanes of a quad.
+//   V map  lane = (D/8) r + c: slots r + (64/(D/8)) i, dims 8c..8c+7; every
+//          lane accumulates 8 dims of the G heads' outputs.
+// Probabilities move from the K map to the V map through LDS.  Each split
+// leaves a partial (max, sum, unnormalised o); attn_merge combines them.
 
 template <int D, int G>
 struct Tile {
-  static constexpr int KS = D / 4;       // dims per lane, K mapping
+  static constexpr int KS = D / 4;       // dims per lane, K map
   static constexpr int KP = KS / 2;      // bf16 pairs per lane
-  static constexpr int VL = D / 8;       // lanes per slot, V mapping
+  static constexpr int KQ = KS / 8;      // 16-byte K chunks per lane (HIGH)
+  static constexpr int VL = D / 8;       // lanes per slot, V map
   static constexpr int VT = 64 / VL;     // slots per V load
   static constexpr int VI = kPage / VT;  // V loads per page
+  static constexpr int KW = KS / 8;      // 32-bit words of K codes per lane (LOW)
 };
 
-// Scores (log2 units) and V values of one HIGH page.
 template <int D, int G>
-__device__ __forceinline__ void tile_hi(const uint8_t* head, int nvalid, int t, int s, int r, int c,
-                                        const uint32_t (&qp)[G][Tile<D, G>::KP], float scale_log2,
-                                        float (&sc)[G], float (&vf)[Tile<D, G>::VI][8]) {
+struct RawHi {
+  uint4 k[Tile<D, G>::KQ];
+  uint4 v[Tile<D, G>::VI];
+};
+
+template <int D, int G>
+struct RawLo {
+  uint32_t k[Tile<D, G>::KW];
+  uint32_t ks;
+  uint32_t v[Tile<D, G>::VI];
+  uint32_t vs[Tile<D, G>::VI];
+};
+
+template <int D, int G>
+__device__ __forceinline__ RawHi<D, G> load_hi(const uint8_t* head, int t, int s, int r, int c) {
   using T = Tile<D, G>;
-  uint32_t kw[T::KP];
+  RawHi<D, G> x;
   const uint4* kp = reinterpret_cast<const uint4*>(head + t * (D * 2) + s * (T::KS * 2));
 #pragma unroll
-  for (int i = 0; i < T::KP / 4; ++i) {
-    const uint4 w = kp[i];
-    kw[4 * i] = w.x; kw[4 * i + 1] = w.y; kw[4 * i + 2] = w.z; kw[4 * i + 3] = w.w;
-  }
+  for (int i = 0; i < T::KQ; ++i) x.k[i] = kp[i];
   const uint8_t* vb = head + kPage * D * 2;
+#pragma unroll
+  for (int i = 0; i < T::VI; ++i)
+    x.v[i] = *reinterpret_cast<const uint4*>(vb + (i * T::VT + r) * (D * 2) + c * 16);
+  return x;
+}
+
+template <int D, int G>
+__device__ __forceinline__ RawLo<D, G> load_lo(const uint8_t* head, int t, int s, int r, int c) {
+  using T = Tile<D, G>;
+  constexpr int kGpr = D / kQGroup;
+  const uint8_t* kcodes = head;
+  const uint8_t* kscales = head + kPage * (D / 2);
+  const uint8_t* vcodes = kscales + kPage * kGpr * 2;
+  const uint8_t* vscales = vcodes + kPage * (D / 2);
+  RawLo<D, G> x;
+  if constexpr (T::KW == 4) {
+    const uint4 w = *reinterpret_cast<const uint4*>(kcodes + t * (D / 2) + s * (T::KS / 2));
+    x.k[0] = w.x; x.k[1] = w.y; x.k[2] = w.z; x.k[3] = w.w;
+  } else {
+    const uint2 w = *reinterpret_cast<const uint2*>(kcodes + t * (D / 2) + s * (T::KS / 2));
+    x.k[0] = w.x; x.k[1] = w.y;
+  }
+  x.ks = *reinterpret_cast<const uint16_t*>(kscales + (t * kGpr + (s * T::KS) / kQGroup) * 2);
 #pragma unroll
   for (int i = 0; i < T::VI; ++i) {
     const int tv = i * T::VT + r;
-    const uint4 w = *reinterpret_cast<const uint4*>(vb + tv * (D * 2) + c * 16);
-    const bool ok = tv < nvalid;
-    const uint32_t x[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      vf[i][2 * e] = ok ? bf16_lo(x[e]) : 0.0f;
-      vf[i][2 * e + 1] = ok ? bf16_hi(x[e]) : 0.0f;
-    }
+    x.v[i] = *reinterpret_cast<const uint32_t*>(vcodes + tv * (D / 2) + c * 4);
+    x.vs[i] = *reinterpret_cast<const uint16_t*>(vscales + (tv * kGpr + c / 4) * 2);
   }
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float d = 0.0f;
-#pragma unroll
-    for (int p = 0; p < T::KP; ++p) d = dot2_bf16(qp[h][p], kw[p], d);
-    d += __shfl_xor(d, 1);
-    d += __shfl_xor(d, 2);
-    sc[h] = t < nvalid ? d * scale_log2 : -INFINITY;
-  }
+  return x;
+}
+
+// Order LDS traffic between the lanes of this (single-wave) workgroup without
+// waiting for outstanding global loads: wavefront-scope fences around a wave
+// barrier.  __syncthreads() would also drain the prefetch of the next page.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
 }
 
 // int4 codes of 8 elements (one 32-bit word) as 4 exact bf16 pairs.
@@ -443,77 +481,195 @@ __device__ __forceinline__ void codes_to_bf16_pairs(uint32_t w, uint32_t (&out)[
   }
 }
 
-// Scores (log2 units) and dequantised V values of one LOW page.
+// Scores of this lane's slot for the G heads, in log2 units (-inf if invalid).
 template <int D, int G>
-__device__ __forceinline__ void tile_lo(const uint8_t* head, int nvalid, int t, int s, int r, int c,
-                                        const uint32_t (&qp)[G][Tile<D, G>::KP], float scale_log2,
-                                        float (&sc)[G], float (&vf)[Tile<D, G>::VI][8]) {
+__device__ __forceinline__ void scores_hi(const RawHi<D, G>& x, const uint32_t (&qp)[G][Tile<D, G>::KP],
+                                          bool valid, float scale_log2, float (&sc)[G]) {
   using T = Tile<D, G>;
-  constexpr int kGpr = D / kQGroup;
-  const uint8_t* kcodes = head;
-  const uint8_t* kscales = head + kPage * (D / 2);
-  const uint8_t* vcodes = kscales + kPage * kGpr * 2;
-  const uint8_t* vscales = vcodes + kPage * (D / 2);
-  // K: this lane's KS dims are KS/2 bytes of codes inside one scale group.
-  uint32_t kwords[T::KS / 8];
-  if constexpr (T::KS / 8 == 4) {
-    const uint4 w = *reinterpret_cast<const uint4*>(kcodes + t * (D / 2) + s * (T::KS / 2));
-    kwords[0] = w.x; kwords[1] = w.y; kwords[2] = w.z; kwords[3] = w.w;
-  } else {
-    const uint2 w = *reinterpret_cast<const uint2*>(kcodes + t * (D / 2) + s * (T::KS / 2));
-    kwords[0] = w.x; kwords[1] = w.y;
-  }
-  const int kgrp = (s * T::KS) / kQGroup;
-  const float ks = (float)__builtin_bit_cast(_Float16,
-      *reinterpret_cast<const uint16_t*>(kscales + (t * kGpr + kgrp) * 2));
+  uint32_t kw[T::KP];
 #pragma unroll
-  for (int i = 0; i < T::VI; ++i) {
-    const int tv = i * T::VT + r;
-    const uint32_t w = *reinterpret_cast<const uint32_t*>(vcodes + tv * (D / 2) + c * 4);
-    const float vs = (float)__builtin_bit_cast(_Float16,
-        *reinterpret_cast<const uint16_t*>(vscales + (tv * kGpr + c / 4) * 2));
-    const bool ok = tv < nvalid;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int q = ((int)(w << (28 - 4 * e))) >> 28;
-      vf[i][e] = ok ? (float)q * vs : 0.0f;
-    }
+  for (int i = 0; i < T::KQ; ++i) {
+    kw[4 * i] = x.k[i].x; kw[4 * i + 1] = x.k[i].y; kw[4 * i + 2] = x.k[i].z; kw[4 * i + 3] = x.k[i].w;
   }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     float d = 0.0f;
 #pragma unroll
-    for (int wi = 0; wi < T::KS / 8; ++wi) {
-      uint32_t pairs[4];
-      codes_to_bf16_pairs(kwords[wi], pairs);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) d = dot2_bf16(qp[h][4 * wi + e], pairs[e], d);
-    }
-    d *= ks;
+    for (int p = 0; p < T::KP; ++p) d = dot2_bf16(qp[h][p], kw[p], d);
     d += __shfl_xor(d, 1);
     d += __shfl_xor(d, 2);
-    sc[h] = t < nvalid ? d * scale_log2 : -INFINITY;
+    sc[h] = valid ? d * scale_log2 : -INFINITY;
   }
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(64) void attn_split_kernel(AttnArgs a) {
+__device__ __forceinline__ void scores_lo(const RawLo<D, G>& x, const uint32_t (&qp)[G][Tile<D, G>::KP],
+                                          bool valid, float scale_log2, float (&sc)[G]) {
+  using T = Tile<D, G>;
+  uint32_t pairs[T::KP];
+#pragma unroll
+  for (int wi = 0; wi < T::KW; ++wi) {
+    uint32_t p4[4];
+    codes_to_bf16_pairs(x.k[wi], p4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pairs[4 * wi + e] = p4[e];
+  }
+  const float ks = half_bits_to_float(x.ks);
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float d = 0.0f;
+#pragma unroll
+    for (int p = 0; p < T::KP; ++p) d = dot2_bf16(qp[h][p], pairs[p], d);
+    d *= ks;
+    d += __shfl_xor(d, 1);
+    d += __shfl_xor(d, 2);
+    sc[h] = valid ? d * scale_log2 : -INFINITY;
+  }
+}
+
+// Online-softmax update for one page; leaves this page's probabilities in s_p.
+template <int G>
+__device__ __forceinline__ void softmax_page(const float (&sc)[G], float (&m)[G], float (&l)[G],
+                                             float (&acc)[G][8], float (*s_p)[G], int t, int s) {
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float mx = sc[h];
+    mx = fmaxf(mx, __shfl_xor(mx, 4));
+    mx = fmaxf(mx, __shfl_xor(mx, 8));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mn = fmaxf(m[h], mx);
+    const float p = exp2f(sc[h] - mn);
+    if (mn > m[h]) {
+      const float alpha = exp2f(m[h] - mn);
+      l[h] *= alpha;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] *= alpha;
+      m[h] = mn;
+    }
+    l[h] += p;
+    if ((h & 3) == s) s_p[t][h] = p;
+  }
+}
+
+template <int D, int G>
+__device__ __forceinline__ void pv_hi(const RawHi<D, G>& x, int r, int nvalid, float (*s_p)[G],
+                                      float (&acc)[G][8]) {
+  using T = Tile<D, G>;
+#pragma unroll
+  for (int i = 0; i < T::VI; ++i) {
+    const int tv = i * T::VT + r;
+    const bool ok = tv < nvalid;
+    const uint32_t w[4] = {x.v[i].x, x.v[i].y, x.v[i].z, x.v[i].w};
+    float vf[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vf[2 * e] = ok ? bf16_lo(w[e]) : 0.0f;
+      vf[2 * e + 1] = ok ? bf16_hi(w[e]) : 0.0f;
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float ph = s_p[tv][h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, vf[e], acc[h][e]);
+    }
+  }
+}
+
+template <int D, int G>
+__device__ __forceinline__ void pv_lo(const RawLo<D, G>& x, int r, int nvalid, float (*s_p)[G],
+                                      float (&acc)[G][8]) {
+  using T = Tile<D, G>;
+#pragma unroll
+  for (int i = 0; i < T::VI; ++i) {
+    const int tv = i * T::VT + r;
+    const bool ok = tv < nvalid;
+    const float vs = half_bits_to_float(x.vs[i]);
+    float vf[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int q = ((int)(x.v[i] << (28 - 4 * e))) >> 28;
+      vf[e] = ok ? (float)q * vs : 0.0f;
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float ph = s_p[tv][h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, vf[e], acc[h][e]);
+    }
+  }
+}
+
+// Stream the pages of one unit, loading page p+1 while computing page p.
+template <int D, int G, bool kIsHi>
+__device__ __forceinline__ void run_unit(const uint8_t* pool, size_t page_bytes, size_t head_off,
+                                         const int32_t* bt, int slot0, int slot_end,
+                                         const uint32_t (&qp)[G][Tile<D, G>::KP], float scale_log2,
+                                         float (&m)[G], float (&l)[G], float (&acc)[G][8],
+                                         float (*s_p)[G], int t, int s, int r, int c) {
+  using Raw = typename std::conditional<kIsHi, RawHi<D, G>, RawLo<D, G>>::type;
+  auto load = [&](int p) -> Raw {
+    const uint8_t* head = pool + (size_t)bt[p / kPage] * page_bytes + head_off;
+    if constexpr (kIsHi) return load_hi<D, G>(head, t, s, r, c);
+    else return load_lo<D, G>(head, t, s, r, c);
+  };
+  // The prefetch is unconditional (the last page of the unit is loaded again,
+  // an L2 hit) so that the loop body is straight-line code and the compiler
+  // waits only for the current page's loads, not for the prefetch.
+  const int last = slot_end - 1;
+  Raw cur = load(slot0);
+  for (int p = slot0; p < slot_end; p += kPage) {
+    const Raw nxt = load(min(p + kPage, last));
+    const int nvalid = min(kPage, slot_end - p);
+    float sc[G];
+    if constexpr (kIsHi) scores_hi<D, G>(cur, qp, t < nvalid, scale_log2, sc);
+    else scores_lo<D, G>(cur, qp, t < nvalid, scale_log2, sc);
+    softmax_page<G>(sc, m, l, acc, s_p, t, s);
+    wave_lds_sync();
+    if constexpr (kIsHi) pv_hi<D, G>(cur, r, nvalid, s_p, acc);
+    else pv_lo<D, G>(cur, r, nvalid, s_p, acc);
+    wave_lds_sync();
+    cur = nxt;
+  }
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
   using T = Tile<D, G>;
   __shared__ float s_p[kPage][G];
   const CacheView& cv = a.cv;
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int S = gridDim.x;
   const int lane = threadIdx.x;
   const int32_t* cnt = counters_of(cv, b, a.layer);
   const int n_hi = cnt[kCntHi], n_lo = cnt[kCntLo];
   const int u_hi = (n_hi + kUnitTokens - 1) / kUnitTokens;
   const int u_all = u_hi + (n_lo + kUnitTokens - 1) / kUnitTokens;
+  const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head of this group
+  constexpr int E = D / 64;                                       // output dims per lane in the merge
+  if (u_all == 0) {                                               // nothing persisted: o = 0, lse = -inf
+    if (split == 0) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) a.out[(bh0 + h) * D + lane * E + e] = 0;
+        if (a.lse && lane == 0) a.lse[bh0 + h] = -INFINITY;
+      }
+    }
+    return;
+  }
   if (split >= u_all) return;
+  const int nparts = min(u_all, S);
 
   const int t = lane >> 2, s = lane & 3;
   const int r = lane / T::VL, c = lane % T::VL;
-
   uint32_t qp[G][T::KP];
-  const uint16_t* qb = a.q + ((size_t)b * a.n_q_heads + (size_t)g * G) * D + s * T::KS;
+  const uint16_t* qb = a.q + bh0 * D + s * T::KS;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
 #pragma unroll
@@ -532,59 +688,22 @@ __global__ __launch_bounds__(64) void attn_split_kernel(AttnArgs a) {
   }
   const size_t hi_head = (size_t)g * (2 * kPage * D * 2);
   const size_t lo_head = (size_t)g * 2 * (kPage * (D / 2) + kPage * (D / kQGroup) * 2);
+  const int32_t* bt_hi = block_table_of(cv, b, a.layer, kHi);
+  const int32_t* bt_lo = block_table_of(cv, b, a.layer, kLo);
 
-  for (int u = split; u < u_all; u += gridDim.x) {
-    const bool hi = u < u_hi;
-    const int n = hi ? n_hi : n_lo;
-    const int slot0 = (hi ? u : u - u_hi) * kUnitTokens;
-    const int slot_end = min(n, slot0 + kUnitTokens);
-    const int32_t* bt = block_table_of(cv, b, a.layer, hi ? kHi : kLo);
-    for (int p0 = slot0; p0 < slot_end; p0 += kPage) {
-      const int page = bt[p0 / kPage];
-      const int nvalid = min(kPage, slot_end - p0);
-      float sc[G], vf[T::VI][8];
-      if (hi)
-        tile_hi<D, G>(cv.hi_pool + (size_t)page * cv.hi_page_bytes + hi_head, nvalid, t, s, r, c, qp,
-                      a.scale_log2, sc, vf);
-      else
-        tile_lo<D, G>(cv.lo_pool + (size_t)page * cv.lo_page_bytes + lo_head, nvalid, t, s, r, c, qp,
-                      a.scale_log2, sc, vf);
-      // Online softmax over the page, per head (base 2).
-      float pv[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float mx = sc[h];
-        mx = fmaxf(mx, __shfl_xor(mx, 4));
-        mx = fmaxf(mx, __shfl_xor(mx, 8));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mn = fmaxf(m[h], mx);
-        const float alpha = exp2f(m[h] - mn);
-        pv[h] = exp2f(sc[h] - mn);
-        l[h] = l[h] * alpha + pv[h];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] *= alpha;
-        m[h] = mn;
-      }
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-        if ((h & 3) == s) s_p[t][h] = pv[h];
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < T::VI; ++i) {
-        const int tv = i * T::VT + r;
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float ph = s_p[tv][h];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, vf[i][e], acc[h][e]);
-        }
-      }
-      __syncthreads();
+  for (int u = split; u < u_all; u += S) {
+    if (u < u_hi) {
+      const int slot0 = u * kUnitTokens;
+      run_unit<D, G, true>(cv.hi_pool, cv.hi_page_bytes, hi_head, bt_hi, slot0,
+                           min(n_hi, slot0 + kUnitTokens), qp, a.scale_log2, m, l, acc, s_p, t, s, r, c);
+    } else {
+      const int slot0 = (u - u_hi) * kUnitTokens;
+      run_unit<D, G, false>(cv.lo_pool, cv.lo_page_bytes, lo_head, bt_lo, slot0,
+                            min(n_lo, slot0 + kUnitTokens), qp, a.scale_log2, m, l, acc, s_p, t, s, r, c);
     }
   }
 
-  // Reduce l over slots (lanes with equal s) and acc over V-mapping rows.
+  // Sum l over slots (lanes with equal s) and acc over V-map rows.
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     float lh = l[h];
@@ -601,11 +720,35 @@ __global__ __launch_bounds__(64) void attn_split_kernel(AttnArgs a) {
       acc[h][e] = v;
     }
   }
-  const size_t S = gridDim.x;
+
+  if (nparts == 1) {                       // the only split: write the output directly
+    if (r == 0) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float inv = 1.0f / l[h];
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = (uint32_t)f32_to_bf16_rne(acc[h][2 * e] * inv) |
+                 ((uint32_t)f32_to_bf16_rne(acc[h][2 * e + 1] * inv) << 16);
+        *reinterpret_cast<uint4*>(a.out + (bh0 + h) * D + c * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+    }
+    if (a.lse && lane < G) {
+      float mh = m[0], lh = l[0];
+#pragma unroll
+      for (int h = 1; h < G; ++h)
+        if (lane == h) { mh = m[h]; lh = l[h]; }
+      a.lse[bh0 + lane] = (mh + log2f(lh)) * 0.69314718055994530942f;
+    }
+    return;
+  }
+
+  // Publish this split's partial: o (unnormalised), running max, sum.
   if (r == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      float* o = a.ws_o + (((size_t)b * a.n_q_heads + g * G + h) * S + split) * D + c * 8;
+      float* o = a.ws_o + ((bh0 + h) * S + split) * D + c * 8;
       reinterpret_cast<float4*>(o)[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
       reinterpret_cast<float4*>(o)[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
     }
@@ -615,53 +758,67 @@ __global__ __launch_bounds__(64) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
     for (int h = 1; h < G; ++h)
       if (lane == h) { mh = m[h]; lh = l[h]; }
-    float* ml = a.ws_ml + (((size_t)b * a.n_q_heads + g * G + lane) * S + split) * 2;
-    ml[0] = mh;
-    ml[1] = lh;
+    *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + lane) * S + split) * 2) = make_float2(mh, lh);
   }
 }
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
+// Merge the split partials of one (sequence, query head) when there are two or
+// more: lane p holds split p's (max, sum) for the global max and the weights;
+// the weighted values are summed with all loads of a batch of splits in
+// flight at once.  (One split writes its output itself.)
 template <int D>
-__global__ __launch_bounds__(64) void attn_combine_kernel(AttnArgs a, int G) {
+__global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
+  constexpr int E = D / 64;           // dims per lane
+  constexpr int kBatch = 8;           // splits whose loads are issued together
   const CacheView& cv = a.cv;
-  const int b = blockIdx.x / a.n_q_heads, h = blockIdx.x % a.n_q_heads;
-  const int g = h / G;
+  const int b = blockIdx.x / a.n_q_heads;
+  const size_t bh = blockIdx.x;
   const int32_t* cnt = counters_of(cv, b, a.layer);
-  const int units = (cnt[kCntHi] + kUnitTokens - 1) / kUnitTokens + (cnt[kCntLo] + kUnitTokens - 1) / kUnitTokens;
+  const int u_all = (cnt[kCntHi] + kUnitTokens - 1) / kUnitTokens + (cnt[kCntLo] + kUnitTokens - 1) / kUnitTokens;
   const int S = a.splits;
-  const int nparts = min(units, S);
-  (void)g;
-  const size_t bh = (size_t)b * a.n_q_heads + h;
-  uint16_t* out = a.out + bh * D;
+  const int nparts = min(u_all, S);
+  if (nparts <= 1) return;
   const int lane = threadIdx.x;
-  constexpr int kPer = D / 64;
-  if (nparts == 0) {
+  const float2* ml = reinterpret_cast<const float2*>(a.ws_ml + bh * S * 2);
+  const float* o = a.ws_o + bh * S * D + lane * E;
+  float M = -INFINITY, L = 0.0f, acc[E];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) out[lane + 64 * i] = 0;
-    if (a.lse && lane == 0) a.lse[bh] = -INFINITY;
-    return;
-  }
-  const float* ml = a.ws_ml + bh * S * 2;
-  const float* o = a.ws_o + bh * S * D;
-  float M = -INFINITY;
-  for (int p = 0; p < nparts; ++p) M = fmaxf(M, ml[2 * p]);
-  float L = 0.0f, acc[kPer];
+  for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+  for (int p0 = 0; p0 < nparts; p0 += 64) {           // nparts <= 64 in every supported shape but one pass each
+    const int p = p0 + lane;
+    const float2 x = p < nparts ? ml[p] : make_float2(-INFINITY, 0.0f);
+    float mx = x.x;
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) acc[i] = 0.0f;
-  for (int p = 0; p < nparts; ++p) {
-    const float w = exp2f(ml[2 * p] - M);
-    L += w * ml[2 * p + 1];
+    for (int off = 1; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    const float Mn = fmaxf(M, mx);
+    const float alpha = exp2f(M - Mn);                   // rescale what earlier passes summed
+    const float w = p < nparts ? exp2f(x.x - Mn) : 0.0f;
+    float lw = w * x.y;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) acc[i] += w * o[(size_t)p * D + lane + 64 * i];
+    for (int off = 1; off < 64; off <<= 1) lw += __shfl_xor(lw, off);
+    L = L * alpha + lw;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] *= alpha;
+    M = Mn;
+    const int n = min(64, nparts - p0);
+    for (int q0 = 0; q0 < n; q0 += kBatch) {
+      float v[kBatch][E], wq[kBatch];
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int q = min(q0 + k, n - 1);
+        wq[k] = q0 + k < n ? __shfl(w, q) : 0.0f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[k][e] = o[(size_t)(p0 + q) * D + e];
+      }
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k)
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = fmaf(wq[k], v[k][e], acc[e]);
+    }
   }
   const float inv = 1.0f / L;
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) out[lane + 64 * i] = f32_to_bf16_rne(acc[i] * inv);
+  for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = f32_to_bf16_rne(acc[e] * inv);
   if (a.lse && lane == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
 }
 
@@ -675,6 +832,7 @@ hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s) {
 }
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
+  if (a.max_new == 1 && a.n_new == nullptr) return launch_append_step(a, s);
   append_plan_kernel<<<dim3(a.batch), dim3(256), 0, s>>>(a);
   const dim3 grid((a.max_new + kPackTokens - 1) / kPackTokens, a.batch);
   if (a.cv.head_dim == 64) append_pack_kernel<64><<<grid, dim3(256), 0, s>>>(a);
@@ -688,16 +846,16 @@ hipError_t launch_append_step(const AppendArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D, int G>
-static void launch_attn_dg(const AttnArgs& a, hipStream_t s) {
-  attn_split_kernel<D, G><<<dim3(a.splits, a.cv.n_kv_heads, a.batch), dim3(64), 0, s>>>(a);
-  attn_combine_kernel<D><<<dim3(a.batch * a.n_q_heads), dim3(64), 0, s>>>(a, G);
-}
-
 hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s) {
   const int D = a.cv.head_dim;
-#define PASK_CASE(DD, GG) \
-  if (D == DD && group_size == GG) { launch_attn_dg<DD, GG>(a, s); return hipGetLastError(); }
+  const dim3 grid(a.splits, a.cv.n_kv_heads, a.batch);
+  const dim3 block(64);
+#define PASK_CASE(DD, GG)                                                        \
+  if (D == DD && group_size == GG) {                                             \
+    attn_kernel<DD, GG><<<grid, block, 0, s>>>(a);                               \
+    attn_merge_kernel<DD><<<dim3(a.batch * a.n_q_heads), dim3(64), 0, s>>>(a);   \
+    return hipGetLastError();                                                    \
+  }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
   PASK_CASE(128, 1) PASK_CASE(128, 2) PASK_CASE(128, 4) PASK_CASE(128, 8)
 #undef PASK_CASE

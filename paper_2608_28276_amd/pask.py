@@ -13,7 +13,8 @@ import ctypes as C
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpask.so")
+# The in-tree build; PASK_LIB names another build of the same sources to load.
+LIB_PATH = os.environ.get("PASK_LIB") or os.path.join(_HERE, "libpask.so")
 
 PASK_OK = 0
 PASK_E_ARG = -1
