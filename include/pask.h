@@ -130,11 +130,20 @@ typedef struct pask_cache_layout {
   uint64_t hi_pool_off;      /* hi_pages pages of hi_page_bytes                    */
   uint64_t lo_pool_off;      /* lo_pages pages of lo_page_bytes                    */
   uint64_t total_bytes;
-  uint64_t hi_page_bytes;    /* per KV head h at h * (2*16*D*2): K [16][D] bf16,
-                                then V [16][D] bf16                               */
-  uint64_t lo_page_bytes;    /* per KV head h at h * 2*(16*D/2 + 16*D/32*2):
-                                K codes [16][D/2] u8, K scales [16][D/32] fp16,
-                                V codes [16][D/2] u8, V scales [16][D/32] fp16   */
+  /* In both pools KV head g of page P sits in head slot h = (g + P) mod
+     n_kv_heads; the offsets below are those of head slot h. */
+  uint64_t hi_page_bytes;    /* head slot h at h * 64*D: K tile then V tile, 16*D bf16
+                                each; K element (t, d), d = 32i + 8q + j, at
+                                (i*64 + q*16 + t)*8 + j; V element (t, d),
+                                d = 16m + e, at (((m/2)*64 + t/4*16 + e)*2 + m%2)*4
+                                + t%4 (the bf16 MFMA operand order)              */
+  uint64_t lo_page_bytes;    /* head slot h at h * (16*D + 64*D/32): K codes (8*D
+                                bytes: element (t, d), d = 32i + 8q + j, is nibble
+                                ((q*16 + t)*D/32 + i)*8 + j, low nibble first),
+                                K scales [16][D/32] fp16, V codes (8*D bytes:
+                                byte ((t/4*16 + e)*D/32 + i)*4 + t%4 holds dims
+                                32i + e (low nibble) and 32i + 16 + e (high) of
+                                slot t, e < 16), V scales [16][D/32] fp16       */
   int32_t max_pages;         /* ceil(max_tokens_per_seq / 16)                      */
   int32_t counter_stride;    /* 8                                                  */
 } pask_cache_layout;

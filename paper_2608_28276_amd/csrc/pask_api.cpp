@@ -141,10 +141,14 @@ T rd(const uint8_t* p) {
   return v;
 }
 
+// Partials one (sequence, KV head) may be cut into: the attention kernel picks
+// its pages-per-block so that this bound holds for any counts; the hint only
+// sizes the workspace.
 int splits_for(int32_t max_ctx_hint) {
   const int units = (max_ctx_hint + pask::kUnitTokens - 1) / pask::kUnitTokens;
-  return units + 1;
+  return units + 2;
 }
+
 
 struct WsLayout {
   uint64_t o_off, ml_off, total;
@@ -348,6 +352,7 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
   a.batch = batch;
   a.n_q_heads = g.n_q_heads;
   a.splits = splits;
+  a.group_size = g.n_q_heads / g.n_kv_heads;
   return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
 }
 

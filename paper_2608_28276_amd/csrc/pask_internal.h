@@ -16,6 +16,21 @@ enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4
 constexpr int kCounterStride = 8;
 constexpr int kPage = 16;          // tokens per page
 constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW vector
+// Units a LOW page weighs in the attention kernel's work split; a HIGH page
+// weighs 32.  Bytes alone would give 9, but with the memory system saturated
+// a page iteration costs about the same time whatever its size, and equal
+// weights measure fastest.
+#ifndef PASK_WEIGHT_LO
+#define PASK_WEIGHT_LO 32
+#endif
+// Pages the attention kernel loads ahead of the one it computes (1 or 2).
+#ifndef PASK_PREFETCH_PAGES
+#define PASK_PREFETCH_PAGES 1
+#endif
+// One-wave attention blocks per compute unit (0: the kernel's occupancy).
+#ifndef PASK_ATTN_BLOCKS_PER_CU
+#define PASK_ATTN_BLOCKS_PER_CU 0
+#endif
 #ifndef PASK_UNIT_TOKENS
 #define PASK_UNIT_TOKENS 256
 #endif
@@ -62,7 +77,9 @@ struct AttnArgs {
   float* ws_o;              // [batch][Hq][splits][D]
   float* ws_ml;             // [batch][Hq][splits][2]  (max, sum) in log2 units
   float scale_log2;         // softmax_scale * log2(e)
-  int32_t layer, batch, n_q_heads, splits;
+  int32_t layer, batch, n_q_heads, splits;   // splits: partials per (b, g) the workspace holds
+  int32_t group_size;       // n_q_heads / n_kv_heads
+  int32_t attn_blocks;      // grid of the attention kernel (stream-K blocks), set at launch
 };
 
 // Launchers (pask_kernels.hip).  Return hipSuccess or the launch error.

@@ -12,13 +12,15 @@
 //                K/V (int4, one fp16 scale per 32 elements) into the pages.
 //   append_step  both of the above for one token per sequence (decode).
 //   attn         grouped-query flash-decode over one (sequence, KV head) and a
-//                set of 256-slot work units of the HIGH and LOW stores: query
-//                slice in registers, bf16 dot2 for q.k, int4 codes widened
-//                exactly in registers, online softmax in base 2, next page
-//                prefetched into registers.
+//                set of 256-slot work units of the HIGH and LOW stores: q.k and
+//                p.v on bf16 MFMA (query heads as rows), int4 codes widened
+//                exactly to bf16 in registers with the K scale applied per
+//                32-dim group and the V scale folded into p, online softmax in
+//                base 2, next page prefetched into registers.
 //   attn_merge   merge the split partials (max, sum, weighted values).
 #include <hip/hip_runtime.h>
 
+#include <limits.h>
 #include <math.h>
 
 #include <type_traits>
@@ -47,12 +49,12 @@ __device__ __forceinline__ int32_t* index_list_of(const CacheView& cv, int b, in
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-// acc + a.lo * b.lo + a.hi * b.hi over packed bf16 pairs (v_dot2c_f32_bf16).
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                         __builtin_bit_cast(bf16x2_t, b), acc, false);
+// fp32 -> bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
+
 
 // ---------------------------------------------------------------------------
 // reset
@@ -246,41 +248,82 @@ __device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& pac
   packed = p;
 }
 
+// Page layout, per KV head, chosen so that the MFMA operands of the attention
+// kernel arrive by fully coalesced loads: load instruction i of lane l = 16q + n
+// reads bytes 1024 i + 16 l of a HIGH tile, so each instruction of the wave
+// covers 1 KiB contiguously.
+//   HIGH  K tile: element (t, d), d = 32i + 8q + j  at ((i*64 + q*16 + t)*8 + j)   (bf16)
+//         V tile: element (t, d), d = 16m + dd      at (((m/2)*64 + t/4*16 + dd)*2 + m%2)*4 + t%4
+//   LOW   K codes: nibble ((q*16 + t)*NG + i)*8 + j (element j of the 8 at byte j/2,
+//                  low nibble for even j); K scales [t][NG] fp16;
+//         V codes: byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i+dd (low
+//                  nibble) and 32i+16+dd (high nibble) of slot t; V scales [t][NG].
+// NG = D/32 scale groups, NM = D/16.  Every byte belongs to a single slot, so
+// appends of different slots never share a byte.  KV head g of page P is kept
+// in head slot (g + P) mod n_kv_heads of the page.
 template <int D>
-__device__ __forceinline__ void write_hi(const CacheView& cv, int page, int s16, const uint16_t* kin,
+struct PageLayout {
+  static constexpr int NG = D / 32, NM = D / 16;
+  static constexpr int kHiHead = 64 * D, kHiV = 32 * D;
+  static constexpr int kLoKS = 8 * D, kLoVC = 8 * D + 32 * NG, kLoVS = 16 * D + 32 * NG;
+  static constexpr int kLoHead = 16 * D + 64 * NG;
+};
+
+template <int D>
+__device__ __forceinline__ void write_hi(const CacheView& cv, int page, int t, const uint16_t* kin,
                                          const uint16_t* vin) {
-  constexpr int kChunks = D / 8;  // 16-byte chunks per row
-  const int n = cv.n_kv_heads * 2 * kChunks;
+  using PL = PageLayout<D>;
   uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const int row = i / kChunks, col = i % kChunks;
-    const int g = row >> 1, kv = row & 1;
-    const uint16_t* src = (kv ? vin : kin) + g * D + col * 8;
-    uint8_t* dst = pg + (size_t)g * (2 * kPage * D * 2) + kv * (kPage * D * 2) + s16 * (D * 2) + col * 16;
-    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+  const int nk = cv.n_kv_heads * (D / 8);          // 16-byte K chunks of the token
+  for (int x = threadIdx.x; x < nk; x += blockDim.x) {
+    const int g = x / (D / 8), c = x % (D / 8);      // dims 8c..8c+7 = 32i + 8q + 0..7
+    const int i = c / 4, q = c % 4;
+    uint8_t* dst = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + (i * 64 + q * 16 + t) * 16;
+    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(kin + g * D + c * 8);
+  }
+  const int nv = cv.n_kv_heads * D;
+  const int qq = t / 4, jj = t % 4;
+  for (int x = threadIdx.x; x < nv; x += blockDim.x) {
+    const int g = x / D, d = x % D;
+    const int m = d / 16, dd = d % 16;
+    uint16_t* dst = reinterpret_cast<uint16_t*>(pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + PL::kHiV);
+    dst[(((m >> 1) * 64 + qq * 16 + dd) * 2 + (m & 1)) * 4 + jj] = vin[g * D + d];
   }
 }
 
 template <int D>
-__device__ __forceinline__ void write_lo(const CacheView& cv, int page, int s16, const uint16_t* kin,
+__device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, const uint16_t* kin,
                                          const uint16_t* vin) {
-  constexpr int kGpr = D / kQGroup;                                 // groups per row
-  constexpr int kHalf = kPage * (D / 2) + kPage * kGpr * 2;         // K (or V) bytes per head
-  const int n_tasks = cv.n_kv_heads * 2 * kGpr * 8;                 // 8 lanes per group
+  using PL = PageLayout<D>;
+  const int n_tasks = cv.n_kv_heads * 2 * PL::NG * 8;               // 8 lanes per 32-element group
   uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
+  const int qq = t / 4, jj = t % 4;
   for (int base = 0; base < n_tasks; base += blockDim.x) {
     const int task = base + (int)threadIdx.x;
     if (task < n_tasks) {  // whole 8-lane groups are active together
       const int gi = task >> 3, lig = task & 7;
-      const int grp = gi % kGpr, row = gi / kGpr, g = row >> 1, kv = row & 1;
-      const uint16_t* src = (kv ? vin : kin) + g * D + grp * kQGroup + lig * 4;
+      const int i = gi % PL::NG, row = gi / PL::NG, g = row >> 1, kv = row & 1;
+      const uint16_t* src = (kv ? vin : kin) + g * D + i * kQGroup + lig * 4;   // dims 32i + 4lig + e
       const uint2 raw = *reinterpret_cast<const uint2*>(src);
       uint32_t packed, sbits;
       quant4(raw.x, raw.y, packed, sbits);
-      uint8_t* codes = pg + (size_t)g * (2 * kHalf) + kv * kHalf;
-      uint8_t* scales = codes + kPage * (D / 2);
-      *reinterpret_cast<uint16_t*>(codes + s16 * (D / 2) + grp * 16 + lig * 2) = (uint16_t)packed;
-      if (lig == 0) *reinterpret_cast<uint16_t*>(scales + (s16 * kGpr + grp) * 2) = (uint16_t)sbits;
+      uint8_t* hb = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kLoHead;
+      if (kv == 0) {
+        const int q = lig / 2, half = lig % 2;                        // j = 4*half + e
+        *reinterpret_cast<uint16_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4 + 2 * half) = (uint16_t)packed;
+        if (lig == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      } else {
+        const uint32_t partner = __shfl_xor(packed, 4, 8);           // dims 16 higher
+        if (lig < 4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int dd = 4 * lig + e;
+            const uint32_t b = ((packed >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4);
+            hb[PL::kLoVC + ((qq * 16 + dd) * (PL::NM / 2) + i) * 4 + jj] = (uint8_t)b;
+          }
+        }
+        if (lig == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      }
     }
   }
 }
@@ -393,69 +436,104 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
 // Probabilities move from the K map to the V map through LDS.  Each split
 // leaves a partial (max, sum, unnormalised o); attn_merge combines them.
 
-template <int D, int G>
-struct Tile {
-  static constexpr int KS = D / 4;       // dims per lane, K map
-  static constexpr int KP = KS / 2;      // bf16 pairs per lane
-  static constexpr int KQ = KS / 8;      // 16-byte K chunks per lane (HIGH)
-  static constexpr int VL = D / 8;       // lanes per slot, V map
-  static constexpr int VT = 64 / VL;     // slots per V load
-  static constexpr int VI = kPage / VT;  // V loads per page
-  static constexpr int KW = KS / 8;      // 32-bit words of K codes per lane (LOW)
-};
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-template <int D, int G>
-struct RawHi {
-  uint4 k[Tile<D, G>::KQ];
-  uint4 v[Tile<D, G>::VI];
-};
+// D[16x16] += A[16x32] B[32x16], bf16 operands: lane l holds A[l%16][8(l/16)..+8],
+// B[8(l/16)..+8][l%16], D[4(l/16)..+4][l%16].
+__device__ __forceinline__ f32x4_t mfma_k32(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 c, 0, 0, 0);
+}
+// D[16x16] += A[16x16] B[16x16]: lane l holds A[l%16][4(l/16)..+4], B[4(l/16)..+4][l%16].
+__device__ __forceinline__ f32x4_t mfma_k16(uint2 a, uint2 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, a), __builtin_bit_cast(short4_t, b),
+                                                   c, 0, 0, 0);
+}
 
-template <int D, int G>
-struct RawLo {
-  uint32_t k[Tile<D, G>::KW];
-  uint32_t ks;
-  uint32_t v[Tile<D, G>::VI];
-  uint32_t vs[Tile<D, G>::VI];
-};
-
-template <int D, int G>
-__device__ __forceinline__ RawHi<D, G> load_hi(const uint8_t* head, int t, int s, int r, int c) {
-  using T = Tile<D, G>;
-  RawHi<D, G> x;
-  const uint4* kp = reinterpret_cast<const uint4*>(head + t * (D * 2) + s * (T::KS * 2));
+template <int N>
+__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t (&w)[N]) {
+  if constexpr (N % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < T::KQ; ++i) x.k[i] = kp[i];
-  const uint8_t* vb = head + kPage * D * 2;
+    for (int k = 0; k < N / 4; ++k) {
+      const uint4 x = reinterpret_cast<const uint4*>(p)[k];
+      w[4 * k] = x.x; w[4 * k + 1] = x.y; w[4 * k + 2] = x.z; w[4 * k + 3] = x.w;
+    }
+  } else if constexpr (N % 2 == 0) {
 #pragma unroll
-  for (int i = 0; i < T::VI; ++i)
-    x.v[i] = *reinterpret_cast<const uint4*>(vb + (i * T::VT + r) * (D * 2) + c * 16);
+    for (int k = 0; k < N / 2; ++k) {
+      const uint2 x = reinterpret_cast<const uint2*>(p)[k];
+      w[2 * k] = x.x; w[2 * k + 1] = x.y;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = reinterpret_cast<const uint32_t*>(p)[k];
+  }
+}
+
+// Raw operands of one page for one lane.
+template <int D>
+struct HiRaw {
+  uint32_t k[4 * PageLayout<D>::NG];   // QK B operands: NG x 8 bf16
+  uint32_t v[2 * PageLayout<D>::NM];   // PV B operands: NM x 4 bf16
+};
+template <int D>
+struct LoRaw {
+  uint32_t kc[PageLayout<D>::NG];      // NG x 8 int4 codes
+  uint32_t ks[PageLayout<D>::NG / 2];  // K scales of this lane's slot (fp16)
+  uint32_t vc[PageLayout<D>::NM / 2];  // 4 slots x NM/2 bytes of V code pairs
+  uint32_t vs[2 * PageLayout<D>::NG];  // V scales of this lane's 4 slots (fp16)
+};
+
+template <int D>
+__device__ __forceinline__ HiRaw<D> load_hi(const uint8_t* head, int q, int n) {
+  using PL = PageLayout<D>;
+  HiRaw<D> x;
+  const int l = q * 16 + n;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {
+    const uint4 w = *reinterpret_cast<const uint4*>(head + (i * 64 + l) * 16);
+    x.k[4 * i] = w.x; x.k[4 * i + 1] = w.y; x.k[4 * i + 2] = w.z; x.k[4 * i + 3] = w.w;
+  }
+#pragma unroll
+  for (int i = 0; i < PL::NM / 2; ++i) {
+    const uint4 w = *reinterpret_cast<const uint4*>(head + PL::kHiV + (i * 64 + l) * 16);
+    x.v[4 * i] = w.x; x.v[4 * i + 1] = w.y; x.v[4 * i + 2] = w.z; x.v[4 * i + 3] = w.w;
+  }
   return x;
 }
 
-template <int D, int G>
-__device__ __forceinline__ RawLo<D, G> load_lo(const uint8_t* head, int t, int s, int r, int c) {
-  using T = Tile<D, G>;
-  constexpr int kGpr = D / kQGroup;
-  const uint8_t* kcodes = head;
-  const uint8_t* kscales = head + kPage * (D / 2);
-  const uint8_t* vcodes = kscales + kPage * kGpr * 2;
-  const uint8_t* vscales = vcodes + kPage * (D / 2);
-  RawLo<D, G> x;
-  if constexpr (T::KW == 4) {
-    const uint4 w = *reinterpret_cast<const uint4*>(kcodes + t * (D / 2) + s * (T::KS / 2));
-    x.k[0] = w.x; x.k[1] = w.y; x.k[2] = w.z; x.k[3] = w.w;
-  } else {
-    const uint2 w = *reinterpret_cast<const uint2*>(kcodes + t * (D / 2) + s * (T::KS / 2));
-    x.k[0] = w.x; x.k[1] = w.y;
-  }
-  x.ks = *reinterpret_cast<const uint16_t*>(kscales + (t * kGpr + (s * T::KS) / kQGroup) * 2);
-#pragma unroll
-  for (int i = 0; i < T::VI; ++i) {
-    const int tv = i * T::VT + r;
-    x.v[i] = *reinterpret_cast<const uint32_t*>(vcodes + tv * (D / 2) + c * 4);
-    x.vs[i] = *reinterpret_cast<const uint16_t*>(vscales + (tv * kGpr + c / 4) * 2);
-  }
+template <int D>
+__device__ __forceinline__ LoRaw<D> load_lo(const uint8_t* head, int q, int n) {
+  using PL = PageLayout<D>;
+  LoRaw<D> x;
+  load_words(head + (q * 16 + n) * PL::NG * 4, x.kc);
+  load_words(head + PL::kLoKS + n * PL::NG * 2, x.ks);
+  load_words(head + PL::kLoVC + (q * 16 + n) * (PL::NM / 2) * 4, x.vc);
+  load_words(head + PL::kLoVS + 4 * q * PL::NG * 2, x.vs);
   return x;
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16_rne_dev(lo) | ((uint32_t)f32_to_bf16_rne_dev(hi) << 16);
+}
+// x = hi + lo with hi = bf16(x) and lo = bf16(x - hi): 16 significant bits,
+// so the weights of the p.v MFMA carry fp32-like precision (two products).
+__device__ __forceinline__ void split_bf16x4(const float (&x)[4], uint2& hi, uint2& lo) {
+  float r[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) r[k] = x[k] - __uint_as_float((uint32_t)f32_to_bf16_rne_dev(x[k]) << 16);
+  hi = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+  lo = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+}
+// int4 code c (two's complement nibble) as an exact bf16 bit pattern.
+__device__ __forceinline__ uint32_t code_bf16(uint32_t nib) {
+  const int c = ((int)(nib << 28)) >> 28;
+  return __float_as_uint((float)c) >> 16;
 }
 
 // Order LDS traffic between the lanes of this (single-wave) workgroup without
@@ -467,324 +545,402 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
-}
-
-// int4 codes of 8 elements (one 32-bit word) as 4 exact bf16 pairs.
-__device__ __forceinline__ void codes_to_bf16_pairs(uint32_t w, uint32_t (&out)[4]) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int lo = ((int)(w << (28 - 8 * e))) >> 28;
-    const int hi = ((int)(w << (24 - 8 * e))) >> 28;
-    out[e] = (__float_as_uint((float)lo) >> 16) | (__float_as_uint((float)hi) & 0xFFFF0000u);
-  }
-}
-
-// Scores of this lane's slot for the G heads, in log2 units (-inf if invalid).
+// Per-wave attention state.  Score and output tiles share the MFMA row = query
+// head (4q + r) and column = slot (scores) or dim 16m + n (outputs).
 template <int D, int G>
-__device__ __forceinline__ void scores_hi(const RawHi<D, G>& x, const uint32_t (&qp)[G][Tile<D, G>::KP],
-                                          bool valid, float scale_log2, float (&sc)[G]) {
-  using T = Tile<D, G>;
-  uint32_t kw[T::KP];
-#pragma unroll
-  for (int i = 0; i < T::KQ; ++i) {
-    kw[4 * i] = x.k[i].x; kw[4 * i + 1] = x.k[i].y; kw[4 * i + 2] = x.k[i].z; kw[4 * i + 3] = x.k[i].w;
-  }
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float d = 0.0f;
-#pragma unroll
-    for (int p = 0; p < T::KP; ++p) d = dot2_bf16(qp[h][p], kw[p], d);
-    d += __shfl_xor(d, 1);
-    d += __shfl_xor(d, 2);
-    sc[h] = valid ? d * scale_log2 : -INFINITY;
-  }
-}
+struct AttnState {
+  uint32_t qa[4 * PageLayout<D>::NG];   // QK A operands: q of head n, dims 32i + 8q + 0..7
+  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs
+  float m[4], l[4];                      // running max (log2 units), lane-partial sums
+};
 
-template <int D, int G>
-__device__ __forceinline__ void scores_lo(const RawLo<D, G>& x, const uint32_t (&qp)[G][Tile<D, G>::KP],
-                                          bool valid, float scale_log2, float (&sc)[G]) {
-  using T = Tile<D, G>;
-  uint32_t pairs[T::KP];
-#pragma unroll
-  for (int wi = 0; wi < T::KW; ++wi) {
-    uint32_t p4[4];
-    codes_to_bf16_pairs(x.k[wi], p4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) pairs[4 * wi + e] = p4[e];
-  }
-  const float ks = half_bits_to_float(x.ks);
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float d = 0.0f;
-#pragma unroll
-    for (int p = 0; p < T::KP; ++p) d = dot2_bf16(qp[h][p], pairs[p], d);
-    d *= ks;
-    d += __shfl_xor(d, 1);
-    d += __shfl_xor(d, 2);
-    sc[h] = valid ? d * scale_log2 : -INFINITY;
-  }
-}
-
-// Online-softmax update for one page; leaves this page's probabilities in s_p.
+// Online-softmax update for one page's scores; leaves p in LDS s_p[head][slot].
 template <int G>
-__device__ __forceinline__ void softmax_page(const float (&sc)[G], float (&m)[G], float (&l)[G],
-                                             float (&acc)[G][8], float (*s_p)[G], int t, int s) {
+__device__ __forceinline__ void softmax_page(f32x4_t sc, float* m, float* l, f32x4_t* acc, int n_acc,
+                                             float (*s_p)[20], int q, int n) {
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float mx = sc[h];
-    mx = fmaxf(mx, __shfl_xor(mx, 4));
-    mx = fmaxf(mx, __shfl_xor(mx, 8));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mn = fmaxf(m[h], mx);
-    const float p = exp2f(sc[h] - mn);
-    if (mn > m[h]) {
-      const float alpha = exp2f(m[h] - mn);
-      l[h] *= alpha;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] *= alpha;
-      m[h] = mn;
+  for (int r = 0; r < 4; ++r) {
+    float mx = sc[r];
+    mx = fmaxf(mx, __shfl_xor(mx, 1, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 4, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 8, 16));
+    const float mn = fmaxf(m[r], mx);
+    if (mn > m[r]) {
+      const float alpha = exp2f(m[r] - mn);
+      l[r] *= alpha;
+      for (int k = 0; k < n_acc; ++k) acc[k][r] *= alpha;
+      m[r] = mn;
     }
-    l[h] += p;
-    if ((h & 3) == s) s_p[t][h] = p;
+    const float p = exp2f(sc[r] - m[r]);
+    l[r] += p;
+    if (4 * q + r < G) s_p[4 * q + r][n] = p;
   }
 }
 
-template <int D, int G>
-__device__ __forceinline__ void pv_hi(const RawHi<D, G>& x, int r, int nvalid, float (*s_p)[G],
-                                      float (&acc)[G][8]) {
-  using T = Tile<D, G>;
+// One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
+template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
+__device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2,
+                                            float (*s_p)[20], int q, int n) {
+  using PL = PageLayout<D>;
+  f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+  if constexpr (kIsHi) {
 #pragma unroll
-  for (int i = 0; i < T::VI; ++i) {
-    const int tv = i * T::VT + r;
-    const bool ok = tv < nvalid;
-    const uint32_t w[4] = {x.v[i].x, x.v[i].y, x.v[i].z, x.v[i].w};
-    float vf[8];
+    for (int i = 0; i < PL::NG; ++i)
+      sc = mfma_k32(make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]),
+                    make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]), sc);
+  } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      vf[2 * e] = ok ? bf16_lo(w[e]) : 0.0f;
-      vf[2 * e + 1] = ok ? bf16_hi(w[e]) : 0.0f;
+    for (int i = 0; i < PL::NG; ++i) {
+      uint32_t b[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        b[e] = code_bf16(x.kc[i] >> (8 * e)) | (code_bf16(x.kc[i] >> (8 * e + 4)) << 16);
+      const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
+      const f32x4_t c = mfma_k32(make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]),
+                                 make_uint4(b[0], b[1], b[2], b[3]), zero);
+      const float ks = half_bits_to_float(x.ks[i / 2] >> (16 * (i % 2)));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sc[r] = fmaf(ks, c[r], sc[r]);
     }
+  }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float ph = s_p[tv][h];
+  for (int r = 0; r < 4; ++r) sc[r] = (!kMasked || n < nvalid) ? sc[r] * scale_log2 : -INFINITY;
+  softmax_page<G>(sc, st.m, st.l, st.acc, PL::NM, s_p, q, n);
+  wave_lds_sync();
+  // PV A operand: p of head n for slots 4q..4q+3.
+  float pr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (n < G) {
+    const float4 v4 = *reinterpret_cast<const float4*>(&s_p[n][4 * q]);
+    pr[0] = v4.x; pr[1] = v4.y; pr[2] = v4.z; pr[3] = v4.w;
+  }
+  if constexpr (kIsHi) {
+    uint2 pa_hi, pa_lo;
+    split_bf16x4(pr, pa_hi, pa_lo);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, vf[e], acc[h][e]);
+    for (int mm = 0; mm < PL::NM; ++mm) {
+      uint32_t v0 = x.v[2 * mm], v1 = x.v[2 * mm + 1];
+      if constexpr (kMasked) {   // zero V of slots past the end (their memory is not written)
+        const int t0 = 4 * q;
+        v0 = (t0 + 1 < nvalid) ? v0 : (t0 < nvalid ? (v0 & 0xFFFFu) : 0u);
+        v1 = (t0 + 3 < nvalid) ? v1 : (t0 + 2 < nvalid ? (v1 & 0xFFFFu) : 0u);
+      }
+      st.acc[mm] = mfma_k16(pa_hi, make_uint2(v0, v1), st.acc[mm]);
+      st.acc[mm] = mfma_k16(pa_lo, make_uint2(v0, v1), st.acc[mm]);
     }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {
+      float w[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int hidx = jj * PL::NG + i;
+        const float vs = half_bits_to_float(x.vs[hidx / 2] >> (16 * (hidx % 2)));
+        w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vs : 0.0f;
+      }
+      uint2 pa_hi, pa_lo;
+      split_bf16x4(w, pa_hi, pa_lo);
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const uint32_t bytes = x.vc[i];     // slots 4q..4q+3, dims 32i + 16hh + n
+        const uint32_t sh = 4 * hh;
+        const uint32_t b0 = code_bf16(bytes >> sh) | (code_bf16(bytes >> (8 + sh)) << 16);
+        const uint32_t b1 = code_bf16(bytes >> (16 + sh)) | (code_bf16(bytes >> (24 + sh)) << 16);
+        st.acc[2 * i + hh] = mfma_k16(pa_hi, make_uint2(b0, b1), st.acc[2 * i + hh]);
+        st.acc[2 * i + hh] = mfma_k16(pa_lo, make_uint2(b0, b1), st.acc[2 * i + hh]);
+      }
+    }
+  }
+  wave_lds_sync();
+}
+
+__device__ __forceinline__ int cdiv(int x, int y) { return (x + y - 1) / y; }
+
+__device__ __forceinline__ int wave_sum(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+__device__ __forceinline__ int wave_max(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = max(x, __shfl_xor(x, off));
+  return x;
+}
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+// Pages of the HIGH and LOW stores of sequence b in the layer, and their
+// length in work units: the stream-K decomposition weighs a HIGH page
+// kWeightHi units and a LOW page kWeightLo (PASK_WEIGHT_LO).
+constexpr int kWeightHi = 32;
+constexpr int kWeightLo = PASK_WEIGHT_LO;
+static_assert(kWeightLo >= 1 && kWeightLo <= kWeightHi, "LOW page weight out of range");
+struct SeqPages {
+  int n_hi, n_lo, np_hi, np, len;
+};
+__device__ __forceinline__ SeqPages seq_pages(const CacheView& cv, int layer, int b) {
+  const int32_t* c = counters_of(cv, b, layer);
+  SeqPages s;
+  s.n_hi = c[kCntHi];
+  s.n_lo = c[kCntLo];
+  s.np_hi = cdiv(s.n_hi, kPage);
+  const int np_lo = cdiv(s.n_lo, kPage);
+  s.np = s.np_hi + np_lo;
+  s.len = kWeightHi * s.np_hi + kWeightLo * np_lo;
+  return s;
+}
+// Unit offset of page j (HIGH pages first, then LOW) inside its segment.
+__device__ __forceinline__ int page_start(const SeqPages& s, int j) {
+  return j < s.np_hi ? kWeightHi * j : kWeightHi * s.np_hi + kWeightLo * (j - s.np_hi);
+}
+// First page whose unit offset is >= u (s.np when there is none).
+__device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
+  if (u <= kWeightHi * s.np_hi) return cdiv(u, kWeightHi);
+  return s.np_hi + min(s.np - s.np_hi, cdiv(u - kWeightHi * s.np_hi, kWeightLo));
+}
+
+// Stream-K decomposition of one attention call, computed identically by every
+// block of the attention and merge kernels.  The work list is the segments
+// (sequence b, KV head g) in that nesting order, each the pages of (b, g) laid
+// out in units; segment (b, g) starts at unit excl(b) * Hkv + g * len(b), where
+// excl(b) sums len over the sequences before b.  Block w takes the pages that
+// start in units [w*U, (w+1)*U): contiguous ranges of equal weight.  U is at
+// least one HIGH page and kWeightLo <= kWeightHi, so every block between the
+// first and the last one of a segment holds a page of it; U is also large
+// enough that no segment is cut into more than `splits` pieces (the workspace
+// bound).
+struct StreamPlan {
+  long long total;   // units
+  int U;             // units per block
+};
+constexpr int kMinPagesPerBlock = 16;
+
+__device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, int n_blocks) {
+  const int lane = threadIdx.x & 63;
+  int total = 0, mx = 0;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int b = c0 + lane;
+    const int len = b < a.batch ? seq_pages(a.cv, a.layer, b).len : 0;
+    total += wave_sum(len);
+    mx = max(mx, wave_max(len));
+  }
+  StreamPlan pl;
+  pl.total = (long long)total * a.cv.n_kv_heads;
+  const long long even = (pl.total + n_blocks - 1) / n_blocks;
+  pl.U = max(kWeightHi * kMinPagesPerBlock, (int)min(even, (long long)INT_MAX));
+  pl.U = max(pl.U, cdiv(mx, a.splits - 1));
+  return pl;
+}
+
+// Sequence whose segments hold unit P, and the units of the sequences before it.
+__device__ __forceinline__ void locate(const AttnArgs& a, long long P, int& b_out, int& excl_out) {
+  const int lane = threadIdx.x & 63;
+  const long long H = a.cv.n_kv_heads;
+  int base = 0;
+  b_out = -1;
+  excl_out = 0;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int b = c0 + lane;
+    const int len = b < a.batch ? seq_pages(a.cv, a.layer, b).len : 0;
+    const int incl = wave_inclusive_scan(len) + base;
+    const int excl = incl - len;
+    const bool hit = len > 0 && (long long)excl * H <= P && P < (long long)incl * H;
+    const unsigned long long m = __ballot(hit);
+    if (m) {
+      const int src = __ffsll((long long)m) - 1;
+      b_out = c0 + src;
+      excl_out = __shfl(excl, src);
+      return;
+    }
+    base = __shfl(incl, 63);
   }
 }
 
-template <int D, int G>
-__device__ __forceinline__ void pv_lo(const RawLo<D, G>& x, int r, int nvalid, float (*s_p)[G],
-                                      float (&acc)[G][8]) {
-  using T = Tile<D, G>;
-#pragma unroll
-  for (int i = 0; i < T::VI; ++i) {
-    const int tv = i * T::VT + r;
-    const bool ok = tv < nvalid;
-    const float vs = half_bits_to_float(x.vs[i]);
-    float vf[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int q = ((int)(x.v[i] << (28 - 4 * e))) >> 28;
-      vf[e] = ok ? (float)q * vs : 0.0f;
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float ph = s_p[tv][h];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(ph, vf[e], acc[h][e]);
-    }
-  }
-}
-
-// Stream the pages of one unit, loading page p+1 while computing page p.
+// Stream pages [p0, p1) of one store of (b, g), loading ahead while computing
+// page p.  The prefetches are unconditional (past the end the last page is
+// loaded again, an L2 hit) so the loop body is straight-line code and the
+// compiler waits only for the current page's loads.  KV head g of a page sits
+// in head slot (g + page) mod n_kv_heads, which spreads one head's data over
+// DRAM channels.
 template <int D, int G, bool kIsHi>
-__device__ __forceinline__ void run_unit(const uint8_t* pool, size_t page_bytes, size_t head_off,
-                                         const int32_t* bt, int slot0, int slot_end,
-                                         const uint32_t (&qp)[G][Tile<D, G>::KP], float scale_log2,
-                                         float (&m)[G], float (&l)[G], float (&acc)[G][8],
-                                         float (*s_p)[G], int t, int s, int r, int c) {
-  using Raw = typename std::conditional<kIsHi, RawHi<D, G>, RawLo<D, G>>::type;
+__device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes, int head_bytes, int n_heads,
+                                          const int32_t* bt, int p0, int p1, int n_slots, int g,
+                                          AttnState<D, G>& st, float scale_log2, float (*s_p)[20], int q, int n) {
+  using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
   auto load = [&](int p) -> Raw {
-    const uint8_t* head = pool + (size_t)bt[p / kPage] * page_bytes + head_off;
-    if constexpr (kIsHi) return load_hi<D, G>(head, t, s, r, c);
-    else return load_lo<D, G>(head, t, s, r, c);
+    const int page = bt[p];
+    const uint8_t* head = pool + (size_t)page * page_bytes + (size_t)((g + page) % n_heads) * head_bytes;
+    if constexpr (kIsHi) return load_hi<D>(head, q, n);
+    else return load_lo<D>(head, q, n);
   };
-  // The prefetch is unconditional (the last page of the unit is loaded again,
-  // an L2 hit) so that the loop body is straight-line code and the compiler
-  // waits only for the current page's loads, not for the prefetch.
-  const int last = slot_end - 1;
-  Raw cur = load(slot0);
-  for (int p = slot0; p < slot_end; p += kPage) {
-    const Raw nxt = load(min(p + kPage, last));
-    const int nvalid = min(kPage, slot_end - p);
-    float sc[G];
-    if constexpr (kIsHi) scores_hi<D, G>(cur, qp, t < nvalid, scale_log2, sc);
-    else scores_lo<D, G>(cur, qp, t < nvalid, scale_log2, sc);
-    softmax_page<G>(sc, m, l, acc, s_p, t, s);
-    wave_lds_sync();
-    if constexpr (kIsHi) pv_hi<D, G>(cur, r, nvalid, s_p, acc);
-    else pv_lo<D, G>(cur, r, nvalid, s_p, acc);
-    wave_lds_sync();
+  auto attend = [&](const Raw& r, int p) {
+    const int nvalid = min(kPage, n_slots - p * kPage);
+    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, s_p, q, n);
+    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, s_p, q, n);
+  };
+#if PASK_PREFETCH_PAGES == 2
+  Raw cur = load(p0);
+  Raw nx1 = load(min(p0 + 1, p1 - 1));
+  for (int p = p0; p < p1; ++p) {
+    const Raw nx2 = load(min(p + 2, p1 - 1));
+    attend(cur, p);
+    cur = nx1;
+    nx1 = nx2;
+  }
+#else
+  Raw cur = load(p0);
+  for (int p = p0; p < p1; ++p) {
+    const Raw nxt = load(min(p + 1, p1 - 1));
+    attend(cur, p);
     cur = nxt;
   }
+#endif
 }
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+// Pages [j0, j1) of (b, g) (HIGH pages, then LOW pages).  Writes the output
+// when this block holds all pages of (b, g), else a partial.
+template <int D, int G>
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, int b, int g, int j0, int j1, const SeqPages& sp,
+                                               long long seg0, int U, float (*s_p)[20], int q, int n) {
+  using PL = PageLayout<D>;
+  const CacheView& cv = a.cv;
+  const int H = cv.n_kv_heads;
+  const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;
+  AttnState<D, G> st;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {
+    uint4 w = make_uint4(0u, 0u, 0u, 0u);
+    if (n < G) w = *reinterpret_cast<const uint4*>(a.q + (bh0 + n) * D + 32 * i + 8 * q);
+    st.qa[4 * i] = w.x; st.qa[4 * i + 1] = w.y; st.qa[4 * i + 2] = w.z; st.qa[4 * i + 3] = w.w;
+  }
+#pragma unroll
+  for (int k = 0; k < PL::NM; ++k) st.acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    st.m[r] = -INFINITY;
+    st.l[r] = 0.0f;
+  }
+  if (j0 < sp.np_hi)
+    run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), j0,
+                          min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, s_p, q, n);
+  if (j1 > sp.np_hi)
+    run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo),
+                           max(j0, sp.np_hi) - sp.np_hi, j1 - sp.np_hi, sp.n_lo, g, st, a.scale_log2, s_p, q, n);
+  // Sum l over the slots of each row (the 16 lanes with equal q).
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float lh = st.l[r];
+    lh += __shfl_xor(lh, 1, 16);
+    lh += __shfl_xor(lh, 2, 16);
+    lh += __shfl_xor(lh, 4, 16);
+    lh += __shfl_xor(lh, 8, 16);
+    st.l[r] = lh;
+  }
+  const long long first = seg0 / U, last = (seg0 + page_start(sp, sp.np - 1)) / U;
+  if (first == last) {                       // this block holds all of (b, g): final output
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * q + r;
+      if (h < G) {
+        const float inv = 1.0f / st.l[r];
+#pragma unroll
+        for (int k = 0; k < PL::NM; ++k) a.out[(bh0 + h) * D + 16 * k + n] = f32_to_bf16_rne_dev(st.acc[k][r] * inv);
+        if (a.lse && n == 0) a.lse[bh0 + h] = (st.m[r] + log2f(st.l[r])) * 0.69314718055994530942f;
+      }
+    }
+    return;
+  }
+  const int slot = (int)(blockIdx.x - first);   // < a.splits by the choice of U
+  const size_t S = a.splits;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * q + r;
+    if (h < G) {
+      float* o = a.ws_o + ((bh0 + h) * S + slot) * D;
+#pragma unroll
+      for (int k = 0; k < PL::NM; ++k) o[16 * k + n] = st.acc[k][r];
+      if (n == 0) *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + h) * S + slot) * 2) = make_float2(st.m[r], st.l[r]);
+    }
+  }
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
-  using T = Tile<D, G>;
-  __shared__ float s_p[kPage][G];
-  const CacheView& cv = a.cv;
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int S = gridDim.x;
+__global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
+  __shared__ float s_p[16][20];   // row stride 80 B: 16-byte aligned rows
   const int lane = threadIdx.x;
-  const int32_t* cnt = counters_of(cv, b, a.layer);
-  const int n_hi = cnt[kCntHi], n_lo = cnt[kCntLo];
-  const int u_hi = (n_hi + kUnitTokens - 1) / kUnitTokens;
-  const int u_all = u_hi + (n_lo + kUnitTokens - 1) / kUnitTokens;
-  const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head of this group
-  constexpr int E = D / 64;                                       // output dims per lane in the merge
-  if (u_all == 0) {                                               // nothing persisted: o = 0, lse = -inf
-    if (split == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-#pragma unroll
-        for (int e = 0; e < E; ++e) a.out[(bh0 + h) * D + lane * E + e] = 0;
-        if (a.lse && lane == 0) a.lse[bh0 + h] = -INFINITY;
-      }
+  const int q = lane >> 4, n = lane & 15;
+  const int H = a.cv.n_kv_heads;
+  const StreamPlan plan = stream_plan(a, gridDim.x);
+  const long long start = (long long)blockIdx.x * plan.U;
+  if (start >= plan.total) return;
+  const long long end = min(plan.total, start + plan.U);
+  int b, excl;
+  locate(a, start, b, excl);
+  if (b < 0) return;
+  SeqPages sp = seq_pages(a.cv, a.layer, b);
+  const long long rel = start - (long long)excl * H;
+  int g = (int)(rel / sp.len);
+  int j0 = first_page_at(sp, (int)(rel % sp.len));
+  while (true) {
+    const long long seg0 = (long long)excl * H + (long long)g * sp.len;
+    if (seg0 >= end) return;
+    const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
+    if (j0 < j1) attend_segment<D, G>(a, b, g, j0, j1, sp, seg0, plan.U, s_p, q, n);
+    if (j1 < sp.np) return;
+    j0 = 0;
+    if (++g == H) {                              // next sequence that holds any page
+      g = 0;
+      excl += sp.len;
+      do {
+        if (++b >= a.batch) return;
+        sp = seq_pages(a.cv, a.layer, b);
+      } while (sp.len == 0);
     }
-    return;
-  }
-  if (split >= u_all) return;
-  const int nparts = min(u_all, S);
-
-  const int t = lane >> 2, s = lane & 3;
-  const int r = lane / T::VL, c = lane % T::VL;
-  uint32_t qp[G][T::KP];
-  const uint16_t* qb = a.q + bh0 * D + s * T::KS;
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-#pragma unroll
-    for (int i = 0; i < T::KP / 4; ++i) {
-      const uint4 w = *reinterpret_cast<const uint4*>(qb + h * D + i * 8);
-      qp[h][4 * i] = w.x; qp[h][4 * i + 1] = w.y; qp[h][4 * i + 2] = w.z; qp[h][4 * i + 3] = w.w;
-    }
-  }
-  float m[G], l[G], acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m[h] = -INFINITY;
-    l[h] = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[h][e] = 0.0f;
-  }
-  const size_t hi_head = (size_t)g * (2 * kPage * D * 2);
-  const size_t lo_head = (size_t)g * 2 * (kPage * (D / 2) + kPage * (D / kQGroup) * 2);
-  const int32_t* bt_hi = block_table_of(cv, b, a.layer, kHi);
-  const int32_t* bt_lo = block_table_of(cv, b, a.layer, kLo);
-
-  for (int u = split; u < u_all; u += S) {
-    if (u < u_hi) {
-      const int slot0 = u * kUnitTokens;
-      run_unit<D, G, true>(cv.hi_pool, cv.hi_page_bytes, hi_head, bt_hi, slot0,
-                           min(n_hi, slot0 + kUnitTokens), qp, a.scale_log2, m, l, acc, s_p, t, s, r, c);
-    } else {
-      const int slot0 = (u - u_hi) * kUnitTokens;
-      run_unit<D, G, false>(cv.lo_pool, cv.lo_page_bytes, lo_head, bt_lo, slot0,
-                            min(n_lo, slot0 + kUnitTokens), qp, a.scale_log2, m, l, acc, s_p, t, s, r, c);
-    }
-  }
-
-  // Sum l over slots (lanes with equal s) and acc over V-map rows.
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    float lh = l[h];
-    lh += __shfl_xor(lh, 4);
-    lh += __shfl_xor(lh, 8);
-    lh += __shfl_xor(lh, 16);
-    lh += __shfl_xor(lh, 32);
-    l[h] = lh;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = acc[h][e];
-#pragma unroll
-      for (int off = T::VL; off < 64; off <<= 1) v += __shfl_xor(v, off);
-      acc[h][e] = v;
-    }
-  }
-
-  if (nparts == 1) {                       // the only split: write the output directly
-    if (r == 0) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float inv = 1.0f / l[h];
-        uint32_t w[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          w[e] = (uint32_t)f32_to_bf16_rne(acc[h][2 * e] * inv) |
-                 ((uint32_t)f32_to_bf16_rne(acc[h][2 * e + 1] * inv) << 16);
-        *reinterpret_cast<uint4*>(a.out + (bh0 + h) * D + c * 8) = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-    }
-    if (a.lse && lane < G) {
-      float mh = m[0], lh = l[0];
-#pragma unroll
-      for (int h = 1; h < G; ++h)
-        if (lane == h) { mh = m[h]; lh = l[h]; }
-      a.lse[bh0 + lane] = (mh + log2f(lh)) * 0.69314718055994530942f;
-    }
-    return;
-  }
-
-  // Publish this split's partial: o (unnormalised), running max, sum.
-  if (r == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float* o = a.ws_o + ((bh0 + h) * S + split) * D + c * 8;
-      reinterpret_cast<float4*>(o)[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
-      reinterpret_cast<float4*>(o)[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
-    }
-  }
-  if (lane < G) {
-    float mh = m[0], lh = l[0];
-#pragma unroll
-    for (int h = 1; h < G; ++h)
-      if (lane == h) { mh = m[h]; lh = l[h]; }
-    *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + lane) * S + split) * 2) = make_float2(mh, lh);
   }
 }
 
-// Merge the split partials of one (sequence, query head) when there are two or
-// more: lane p holds split p's (max, sum) for the global max and the weights;
-// the weighted values are summed with all loads of a batch of splits in
-// flight at once.  (One split writes its output itself.)
+// One (sequence, query head): zero output for an empty history; otherwise
+// merge the partials when (b, g) was split over several blocks.  Lane p holds
+// partial p's (max, sum) for the global max and the weights; the weighted
+// values are summed with the loads of a batch of partials in flight at once.
 template <int D>
 __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
   constexpr int E = D / 64;           // dims per lane
-  constexpr int kBatch = 8;           // splits whose loads are issued together
-  const CacheView& cv = a.cv;
+  constexpr int kBatch = 8;           // partials whose loads are issued together
+  const int lane = threadIdx.x;
   const int b = blockIdx.x / a.n_q_heads;
   const size_t bh = blockIdx.x;
-  const int32_t* cnt = counters_of(cv, b, a.layer);
-  const int u_all = (cnt[kCntHi] + kUnitTokens - 1) / kUnitTokens + (cnt[kCntLo] + kUnitTokens - 1) / kUnitTokens;
+  const int g = (blockIdx.x % a.n_q_heads) / a.group_size;
+  const SeqPages sp = seq_pages(a.cv, a.layer, b);
+  if (sp.np == 0) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = 0;
+    if (a.lse && lane == 0) a.lse[bh] = -INFINITY;
+    return;
+  }
+  const StreamPlan plan = stream_plan(a, a.attn_blocks);
+  int excl = 0;                                   // units of the sequences before b
+  for (int c0 = 0; c0 < b; c0 += 64) {
+    const int bb = c0 + lane;
+    excl += wave_sum(bb < b ? seq_pages(a.cv, a.layer, bb).len : 0);
+  }
+  const long long seg0 = (long long)excl * a.cv.n_kv_heads + (long long)g * sp.len;
+  const int nparts = (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
+  if (nparts <= 1) return;                        // written by the attention kernel
   const int S = a.splits;
-  const int nparts = min(u_all, S);
-  if (nparts <= 1) return;
-  const int lane = threadIdx.x;
   const float2* ml = reinterpret_cast<const float2*>(a.ws_ml + bh * S * 2);
   const float* o = a.ws_o + bh * S * D + lane * E;
   float M = -INFINITY, L = 0.0f, acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.0f;
-  for (int p0 = 0; p0 < nparts; p0 += 64) {           // nparts <= 64 in every supported shape but one pass each
+  for (int p0 = 0; p0 < nparts; p0 += 64) {
     const int p = p0 + lane;
     const float2 x = p < nparts ? ml[p] : make_float2(-INFINITY, 0.0f);
     float mx = x.x;
@@ -800,15 +956,15 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] *= alpha;
     M = Mn;
-    const int n = min(64, nparts - p0);
-    for (int q0 = 0; q0 < n; q0 += kBatch) {
+    const int nn = min(64, nparts - p0);
+    for (int q0 = 0; q0 < nn; q0 += kBatch) {
       float v[kBatch][E], wq[kBatch];
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) {
-        const int q = min(q0 + k, n - 1);
-        wq[k] = q0 + k < n ? __shfl(w, q) : 0.0f;
+        const int qq = min(q0 + k, nn - 1);
+        wq[k] = q0 + k < nn ? __shfl(w, qq) : 0.0f;
 #pragma unroll
-        for (int e = 0; e < E; ++e) v[k][e] = o[(size_t)(p0 + q) * D + e];
+        for (int e = 0; e < E; ++e) v[k][e] = o[(size_t)(p0 + qq) * D + e];
       }
 #pragma unroll
       for (int k = 0; k < kBatch; ++k)
@@ -818,7 +974,7 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
   }
   const float inv = 1.0f / L;
 #pragma unroll
-  for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = f32_to_bf16_rne(acc[e] * inv);
+  for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = f32_to_bf16_rne_dev(acc[e] * inv);
   if (a.lse && lane == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
 }
 
@@ -846,14 +1002,36 @@ hipError_t launch_append_step(const AppendArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s) {
-  const int D = a.cv.head_dim;
-  const dim3 grid(a.splits, a.cv.n_kv_heads, a.batch);
+// Stream-K grid of attn_kernel<D, G> on the current device: as many one-wave
+// blocks as can be resident at once (occupancy x compute units), so every
+// block starts at launch.  Queried once per device and instance.
+template <int D, int G>
+int attn_grid() {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  if (cached[dev] == 0) {
+    int per_cu = PASK_ATTN_BLOCKS_PER_CU, cus = 0;
+    if (per_cu == 0 &&
+        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64, 0) != hipSuccess || per_cu <= 0))
+      return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
+    cached[dev] = per_cu * cus;
+  }
+  return cached[dev];
+}
+
+hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s) {
+  const int D = args.cv.head_dim;
+  AttnArgs a = args;
   const dim3 block(64);
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
-    attn_kernel<DD, GG><<<grid, block, 0, s>>>(a);                               \
-    attn_merge_kernel<DD><<<dim3(a.batch * a.n_q_heads), dim3(64), 0, s>>>(a);   \
+    a.attn_blocks = attn_grid<DD, GG>();                                         \
+    if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
+    attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
+    attn_merge_kernel<DD><<<dim3(a.batch * a.n_q_heads), block, 0, s>>>(a);      \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)

@@ -104,34 +104,44 @@ class PaskSession:
 
     def gather_store(self, b: int, layer: int, store: int):
         """Host copies of one store's entries, by slot, read through the block
-        table.  HIGH: (k bits [n, Hkv, D], v bits) as int64.  LOW: (k codes
-        packed [n, Hkv, D/2] u8, k scale bits [n, Hkv, D/32], v codes, v scales)."""
+        table and decoded from the page layout (KV head g of page P sits in
+        head slot (g + P) mod Hkv).  HIGH: (k bits, v bits) int64
+        [n, Hkv, D].  LOW: (k codes int8 [n, Hkv, D], k scale bits [n, Hkv, D/32],
+        v codes, v scale bits)."""
         import numpy as np
         g = self.geom
         D, H = g.head_dim, g.n_kv_heads
+        NG, NM = D // 32, D // 16
         cnt = self.counters()[b, layer].cpu().numpy()
         n = int(cnt[store])
         bt = self.block_tables()[b, layer, store].cpu().numpy()
         pages = bt[: (n + 15) // 16]
-        if store == 0:
-            pool = self.hi_pool()
-            raw = pool[torch.as_tensor(pages, dtype=torch.long, device=self.device)].cpu().numpy() if n else \
-                np.zeros((0, self.layout.hi_page_bytes), np.uint8)
-            x = raw.view(np.uint16).reshape(-1, H, 2, 16, D).astype(np.int64)
-            k = x[:, :, 0].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
-            v = x[:, :, 1].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
-            return k, v
-        pool = self.lo_pool()
+        pool = self.hi_pool() if store == 0 else self.lo_pool()
+        nbytes = self.layout.hi_page_bytes if store == 0 else self.layout.lo_page_bytes
         raw = pool[torch.as_tensor(pages, dtype=torch.long, device=self.device)].cpu().numpy() if n else \
-            np.zeros((0, self.layout.lo_page_bytes), np.uint8)
-        per_head = 2 * (16 * D // 2 + 16 * (D // 32) * 2)
-        half = per_head // 2
-        r = raw.reshape(-1, H, per_head)
-        out = []
-        for kv in range(2):
-            seg = r[:, :, kv * half:(kv + 1) * half]
-            codes = seg[:, :, :16 * D // 2].reshape(-1, H, 16, D // 2).transpose(0, 2, 1, 3).reshape(-1, H, D // 2)
-            sc = seg[:, :, 16 * D // 2:].copy().view(np.uint16).reshape(-1, H, 16, D // 32)
-            sc = sc.transpose(0, 2, 1, 3).reshape(-1, H, D // 32)
-            out += [codes[:n], sc[:n].astype(np.int64)]
-        return tuple(out)
+            np.zeros((0, nbytes), np.uint8)
+        t = np.arange(16)[:, None]
+        d = np.arange(D)[None, :]
+        kidx = (((d % 32) // 8 * 16 + t) * NG + d // 32) * 8 + d % 8                      # [16, D], LOW K
+        if store == 0:
+            x = raw.view(np.uint16).reshape(-1, H, 2, 16 * D).astype(np.int64)
+            kidx = ((d // 32 * 64 + (d % 32) // 8 * 16 + t) * 8 + d % 8)
+            vidx = ((((d // 16) // 2) * 64 + t // 4 * 16 + d % 16) * 2 + (d // 16) % 2) * 4 + t % 4
+            x = x[np.arange(x.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]   # head slots
+            k = x[:, :, 0][:, :, kidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+            v = x[:, :, 1][:, :, vidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+            return k, v
+        head = 16 * D + 64 * NG
+        r = raw.reshape(-1, H, head)
+        r = r[np.arange(r.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]       # head slots
+        nib = lambda by, idx: ((by[..., idx // 2] >> (4 * (idx % 2))) & 0xF).astype(np.int8)
+        sext = lambda c: np.where(c >= 8, c - 16, c).astype(np.int8)
+        kc = sext(nib(r[:, :, :8 * D], kidx))                                            # [P, H, 16, D]
+        ks = r[:, :, 8 * D:8 * D + 32 * NG].copy().view(np.uint16).reshape(-1, H, 16, NG)
+        vbyte = ((t // 4 * 16 + d % 16) * (NM // 2) + d // 32) * 4 + t % 4
+        vhalf = (d % 32) // 16
+        vb = r[:, :, 8 * D + 32 * NG:16 * D + 32 * NG]
+        vc = sext(((vb[..., vbyte] >> (4 * vhalf)) & 0xF).astype(np.int8))
+        vs = r[:, :, 16 * D + 32 * NG:].copy().view(np.uint16).reshape(-1, H, 16, NG)
+        fix = lambda a: a.transpose(0, 2, 1, 3).reshape(-1, H, a.shape[-1])[:n]
+        return fix(kc), fix(ks).astype(np.int64), fix(vc), fix(vs).astype(np.int64)

@@ -142,9 +142,9 @@ def test_unsupported_geometry(bad):
 
 def test_workspace_bytes():
     g = geom()
-    # splits = ceil(hint / 256) + 1; rows = batch * Hq * splits; o: rows*D*4, ml: rows*2*4 (256-aligned)
+    # splits = ceil(hint / 256) + 2; rows = batch * Hq * splits; o: rows*D*4, ml: rows*2*4 (256-aligned)
     ws = pask.pask_workspace_bytes(g, 4, 512)
-    rows = 4 * 8 * 3
+    rows = 4 * 8 * 4
     want = ((rows * 64 * 4 + 255) // 256) * 256
     want = ((want + rows * 8 + 255) // 256) * 256
     assert ws == want
