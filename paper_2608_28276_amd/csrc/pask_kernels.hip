@@ -11,13 +11,15 @@
 //   append_pack  copy RETAIN-HIGH K/V (bf16) or quantise-and-pack RETAIN-LOW
 //                K/V (int4, one fp16 scale per 32 elements) into the pages.
 //   append_step  both of the above for one token per sequence (decode).
-//   attn         grouped-query flash-decode over one (sequence, KV head) and a
-//                set of 256-slot work units of the HIGH and LOW stores: q.k and
-//                p.v on bf16 MFMA (query heads as rows), int4 codes widened
-//                exactly to bf16 in registers with the K scale applied per
-//                32-dim group and the V scale folded into p, online softmax in
-//                base 2, next page prefetched into registers.
-//   attn_merge   merge the split partials (max, sum, weighted values).
+//   attn         grouped-query flash-decode, stream-K: one single-wave block
+//                per resident wave slot, each streaming an equal contiguous
+//                range of the (sequence, KV head, page) list over the HIGH and
+//                LOW stores; q.k and p.v on bf16 MFMA (query heads as rows),
+//                int4 codes widened exactly to bf16 in registers with the K
+//                scale applied per 32-dim group and the V scale folded into p,
+//                online softmax in base 2, next page prefetched into registers.
+//   attn_merge   zero output for empty histories; merge the partials of each
+//                (sequence, KV head) split over blocks (max, sum, values).
 #include <hip/hip_runtime.h>
 
 #include <limits.h>
