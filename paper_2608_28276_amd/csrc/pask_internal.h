@@ -23,13 +23,13 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #ifndef PASK_WEIGHT_LO
 #define PASK_WEIGHT_LO 32
 #endif
-// Pages the attention kernel loads ahead of the one it computes (1 or 2).
-#ifndef PASK_PREFETCH_PAGES
-#define PASK_PREFETCH_PAGES 1
+// Waves per attention workgroup (each an independent worker).
+#ifndef PASK_ATTN_WAVES
+#define PASK_ATTN_WAVES 1
 #endif
-// One-wave attention blocks per compute unit (0: the kernel's occupancy).
-#ifndef PASK_ATTN_BLOCKS_PER_CU
-#define PASK_ATTN_BLOCKS_PER_CU 0
+// Attention workers (waves) per compute unit (0: the kernel's occupancy).
+#ifndef PASK_ATTN_WAVES_PER_CU
+#define PASK_ATTN_WAVES_PER_CU 0
 #endif
 #ifndef PASK_UNIT_TOKENS
 #define PASK_UNIT_TOKENS 256
@@ -79,7 +79,7 @@ struct AttnArgs {
   float scale_log2;         // softmax_scale * log2(e)
   int32_t layer, batch, n_q_heads, splits;   // splits: partials per (b, g) the workspace holds
   int32_t group_size;       // n_q_heads / n_kv_heads
-  int32_t attn_blocks;      // grid of the attention kernel (stream-K blocks), set at launch
+  int32_t attn_blocks;      // stream-K workers (waves) of the attention kernel, set at launch
 };
 
 // Launchers (pask_kernels.hip).  Return hipSuccess or the launch error.

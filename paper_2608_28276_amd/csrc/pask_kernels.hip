@@ -477,13 +477,13 @@ __device__ __forceinline__ void load_words(const uint8_t* p, uint32_t (&w)[N]) {
 // Raw operands of one page for one lane.
 template <int D>
 struct HiRaw {
-  uint32_t k[4 * PageLayout<D>::NG];   // QK B operands: NG x 8 bf16
+  uint32_t k[4 * PageLayout<D>::NG];   // QK A operands: NG x 8 bf16
   uint32_t v[2 * PageLayout<D>::NM];   // PV B operands: NM x 4 bf16
 };
 template <int D>
 struct LoRaw {
   uint32_t kc[PageLayout<D>::NG];      // NG x 8 int4 codes
-  uint32_t ks[PageLayout<D>::NG / 2];  // K scales of this lane's slot (fp16)
+  uint32_t ks[2 * PageLayout<D>::NG];  // K scales of this lane's 4 slots (fp16)
   uint32_t vc[PageLayout<D>::NM / 2];  // 4 slots x NM/2 bytes of V code pairs
   uint32_t vs[2 * PageLayout<D>::NG];  // V scales of this lane's 4 slots (fp16)
 };
@@ -511,7 +511,7 @@ __device__ __forceinline__ LoRaw<D> load_lo(const uint8_t* head, int q, int n) {
   using PL = PageLayout<D>;
   LoRaw<D> x;
   load_words(head + (q * 16 + n) * PL::NG * 4, x.kc);
-  load_words(head + PL::kLoKS + n * PL::NG * 2, x.ks);
+  load_words(head + PL::kLoKS + 4 * q * PL::NG * 2, x.ks);
   load_words(head + PL::kLoVC + (q * 16 + n) * (PL::NM / 2) * 4, x.vc);
   load_words(head + PL::kLoVS + 4 * q * PL::NG * 2, x.vs);
   return x;
@@ -538,83 +538,79 @@ __device__ __forceinline__ uint32_t code_bf16(uint32_t nib) {
   return __float_as_uint((float)c) >> 16;
 }
 
-// Order LDS traffic between the lanes of this (single-wave) workgroup without
-// waiting for outstanding global loads: wavefront-scope fences around a wave
-// barrier.  __syncthreads() would also drain the prefetch of the next page.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Per-wave attention state.  Score and output tiles share the MFMA row = query
-// head (4q + r) and column = slot (scores) or dim 16m + n (outputs).
+// Per-wave attention state.  The score tile is S^T (MFMA row = slot 4q + r,
+// column = query head n), so lane (q, n) holds p of head n for slots
+// 4q..4q+3: the A operand of the p.v MFMA as it stands, with no transpose.
+// The output tile has row = query head 4q + r and column = dim 16m + n.
 template <int D, int G>
 struct AttnState {
-  uint32_t qa[4 * PageLayout<D>::NG];   // QK A operands: q of head n, dims 32i + 8q + 0..7
+  uint32_t qa[4 * PageLayout<D>::NG];   // QK B operands: q of head n, dims 32i + 8q + 0..7
   f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs
-  float m[4], l[4];                      // running max (log2 units), lane-partial sums
+  float m, l;                            // head n: running max (log2 units), lane-partial sum
 };
 
-// Online-softmax update for one page's scores; leaves p in LDS s_p[head][slot].
-template <int G>
-__device__ __forceinline__ void softmax_page(f32x4_t sc, float* m, float* l, f32x4_t* acc, int n_acc,
-                                             float (*s_p)[20], int q, int n) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float mx = sc[r];
-    mx = fmaxf(mx, __shfl_xor(mx, 1, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 2, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 4, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 8, 16));
-    const float mn = fmaxf(m[r], mx);
-    if (mn > m[r]) {
-      const float alpha = exp2f(m[r] - mn);
-      l[r] *= alpha;
-      for (int k = 0; k < n_acc; ++k) acc[k][r] *= alpha;
-      m[r] = mn;
-    }
-    const float p = exp2f(sc[r] - m[r]);
-    l[r] += p;
-    if (4 * q + r < G) s_p[4 * q + r][n] = p;
-  }
+// Max over the 64 lanes' copies of one head (lanes n, n+16, n+32, n+48).
+__device__ __forceinline__ float head_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float head_sum(float x) {
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
 }
 
 // One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
 template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
 __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2,
-                                            float (*s_p)[20], int q, int n) {
+                                            int q, int n) {
   using PL = PageLayout<D>;
   f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
   if constexpr (kIsHi) {
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i)
-      sc = mfma_k32(make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]),
-                    make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]), sc);
+      sc = mfma_k32(make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]),
+                    make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), sc);
   } else {
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
-      uint32_t b[4];
+      uint32_t a[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        b[e] = code_bf16(x.kc[i] >> (8 * e)) | (code_bf16(x.kc[i] >> (8 * e + 4)) << 16);
+        a[e] = code_bf16(x.kc[i] >> (8 * e)) | (code_bf16(x.kc[i] >> (8 * e + 4)) << 16);
       const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
-      const f32x4_t c = mfma_k32(make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]),
-                                 make_uint4(b[0], b[1], b[2], b[3]), zero);
-      const float ks = half_bits_to_float(x.ks[i / 2] >> (16 * (i % 2)));
+      const f32x4_t c = mfma_k32(make_uint4(a[0], a[1], a[2], a[3]),
+                                 make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), zero);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sc[r] = fmaf(ks, c[r], sc[r]);
+      for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
+        const int hidx = r * PL::NG + i;
+        sc[r] = fmaf(half_bits_to_float(x.ks[hidx / 2] >> (16 * (hidx % 2))), c[r], sc[r]);
+      }
     }
   }
+  float mx = -INFINITY;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) sc[r] = (!kMasked || n < nvalid) ? sc[r] * scale_log2 : -INFINITY;
-  softmax_page<G>(sc, st.m, st.l, st.acc, PL::NM, s_p, q, n);
-  wave_lds_sync();
-  // PV A operand: p of head n for slots 4q..4q+3.
-  float pr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (n < G) {
-    const float4 v4 = *reinterpret_cast<const float4*>(&s_p[n][4 * q]);
-    pr[0] = v4.x; pr[1] = v4.y; pr[2] = v4.z; pr[3] = v4.w;
+  for (int r = 0; r < 4; ++r) {
+    sc[r] = (!kMasked || 4 * q + r < nvalid) ? sc[r] * scale_log2 : -INFINITY;
+    mx = fmaxf(mx, sc[r]);
+  }
+  // Online softmax for head n: rescale only when some head's max grew.
+  const float mn = fmaxf(st.m, head_max(mx));
+  if (__ballot(mn > st.m)) {
+    const float alpha = exp2f(st.m - mn);
+    st.l *= alpha;
+    st.m = mn;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {                   // output row 4q + r takes head 4q + r's factor
+      const float ar = __shfl(alpha, 4 * q + r);
+#pragma unroll
+      for (int k = 0; k < PL::NM; ++k) st.acc[k][r] *= ar;
+    }
+  }
+  float pr[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    pr[r] = exp2f(sc[r] - st.m);
+    st.l += pr[r];
   }
   if constexpr (kIsHi) {
     uint2 pa_hi, pa_lo;
@@ -653,10 +649,12 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
       }
     }
   }
-  wave_lds_sync();
 }
 
 __device__ __forceinline__ int cdiv(int x, int y) { return (x + y - 1) / y; }
+// A value the whole wave holds alike, moved to a scalar register so the
+// compiler treats what depends on it as uniform.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ int wave_sum(int x) {
 #pragma unroll
@@ -687,16 +685,47 @@ static_assert(kWeightLo >= 1 && kWeightLo <= kWeightHi, "LOW page weight out of 
 struct SeqPages {
   int n_hi, n_lo, np_hi, np, len;
 };
-__device__ __forceinline__ SeqPages seq_pages(const CacheView& cv, int layer, int b) {
-  const int32_t* c = counters_of(cv, b, layer);
+__device__ __forceinline__ int len_of(int n_hi, int n_lo) {
+  return kWeightHi * cdiv(n_hi, kPage) + kWeightLo * cdiv(n_lo, kPage);
+}
+__device__ __forceinline__ SeqPages make_pages(int n_hi, int n_lo) {
   SeqPages s;
-  s.n_hi = c[kCntHi];
-  s.n_lo = c[kCntLo];
-  s.np_hi = cdiv(s.n_hi, kPage);
-  const int np_lo = cdiv(s.n_lo, kPage);
-  s.np = s.np_hi + np_lo;
-  s.len = kWeightHi * s.np_hi + kWeightLo * np_lo;
+  s.n_hi = n_hi;
+  s.n_lo = n_lo;
+  s.np_hi = cdiv(n_hi, kPage);
+  s.np = s.np_hi + cdiv(n_lo, kPage);
+  s.len = len_of(n_hi, n_lo);
   return s;
+}
+
+// Store counts of sequence `lane` for the first 64 sequences, read once per
+// block: the plan, the search for a block's first sequence and the walk to
+// the next sequence take them from registers instead of memory.
+struct FirstCounts {
+  int n_hi, n_lo;   // 0 past the batch
+};
+__device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
+  const int lane = threadIdx.x & 63;
+  const int32_t* c = counters_of(a.cv, lane < a.batch ? lane : 0, a.layer);
+  const int hi = c[kCntHi], lo = c[kCntLo];
+  FirstCounts f;
+  f.n_hi = lane < a.batch ? hi : 0;
+  f.n_lo = lane < a.batch ? lo : 0;
+  return f;
+}
+// Pages of sequence b (wave-uniform, < batch).
+__device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const FirstCounts& f, int b) {
+  if (b < 64) return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_lo, b));
+  const int32_t* c = counters_of(a.cv, b, a.layer);
+  return make_pages(uni(c[kCntHi]), uni(c[kCntLo]));
+}
+// Length in units of sequence c0 + lane (c0 wave-uniform; 0 past `limit`).
+__device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f, int c0, int limit) {
+  const int b = c0 + (int)(threadIdx.x & 63);
+  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_lo) : 0;
+  const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
+  const int len = len_of(c[kCntHi], c[kCntLo]);
+  return b < limit ? len : 0;
 }
 // Unit offset of page j (HIGH pages first, then LOW) inside its segment.
 __device__ __forceinline__ int page_start(const SeqPages& s, int j) {
@@ -724,14 +753,12 @@ struct StreamPlan {
 };
 constexpr int kMinPagesPerBlock = 16;
 
-__device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, int n_blocks) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
   int total = 0, mx = 0;
   for (int c0 = 0; c0 < a.batch; c0 += 64) {
-    const int b = c0 + lane;
-    const int len = b < a.batch ? seq_pages(a.cv, a.layer, b).len : 0;
-    total += wave_sum(len);
-    mx = max(mx, wave_max(len));
+    const int len = lane_len(a, f, c0, a.batch);
+    total += uni(wave_sum(len));
+    mx = max(mx, uni(wave_max(len)));
   }
   StreamPlan pl;
   pl.total = (long long)total * a.cv.n_kv_heads;
@@ -742,124 +769,118 @@ __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, int n_block
 }
 
 // Sequence whose segments hold unit P, and the units of the sequences before it.
-__device__ __forceinline__ void locate(const AttnArgs& a, long long P, int& b_out, int& excl_out) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void locate(const AttnArgs& a, const FirstCounts& f, long long P, int& b_out,
+                                       int& excl_out) {
   const long long H = a.cv.n_kv_heads;
   int base = 0;
   b_out = -1;
   excl_out = 0;
   for (int c0 = 0; c0 < a.batch; c0 += 64) {
-    const int b = c0 + lane;
-    const int len = b < a.batch ? seq_pages(a.cv, a.layer, b).len : 0;
+    const int len = lane_len(a, f, c0, a.batch);
     const int incl = wave_inclusive_scan(len) + base;
     const int excl = incl - len;
     const bool hit = len > 0 && (long long)excl * H <= P && P < (long long)incl * H;
     const unsigned long long m = __ballot(hit);
     if (m) {
       const int src = __ffsll((long long)m) - 1;
-      b_out = c0 + src;
-      excl_out = __shfl(excl, src);
+      b_out = uni(c0 + src);
+      excl_out = uni(__shfl(excl, src));
       return;
     }
-    base = __shfl(incl, 63);
+    base = uni(__shfl(incl, 63));
   }
 }
 
-// Stream pages [p0, p1) of one store of (b, g), loading ahead while computing
-// page p.  The prefetches are unconditional (past the end the last page is
-// loaded again, an L2 hit) so the loop body is straight-line code and the
-// compiler waits only for the current page's loads.  KV head g of a page sits
-// in head slot (g + page) mod n_kv_heads, which spreads one head's data over
-// DRAM channels.
+// Stream pages [p0, p1) of one store of (b, g), loading page p+1 while
+// computing page p.  The page ids come from the block table kIdChunk at a time, one per
+// lane, and are read with readlane, so a page's loads depend on no other
+// memory access.  The prefetches are unconditional (past the end the last
+// page is loaded again, an L2 hit): the loop body is straight-line code and
+// the compiler waits only for the current page's loads.  KV head g of a page
+// sits in head slot (g + page) mod n_kv_heads, which spreads one head's data
+// over DRAM channels.
+constexpr int kIdChunk = 128;
+
 template <int D, int G, bool kIsHi>
 __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes, int head_bytes, int n_heads,
                                           const int32_t* bt, int p0, int p1, int n_slots, int g,
-                                          AttnState<D, G>& st, float scale_log2, float (*s_p)[20], int q, int n) {
+                                          AttnState<D, G>& st, float scale_log2, int q, int n) {
   using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
-  auto load = [&](int p) -> Raw {
-    const int page = bt[p];
+  const int lane = threadIdx.x & 63;
+  auto load = [&](int page) -> Raw {
     const uint8_t* head = pool + (size_t)page * page_bytes + (size_t)((g + page) % n_heads) * head_bytes;
     if constexpr (kIsHi) return load_hi<D>(head, q, n);
     else return load_lo<D>(head, q, n);
   };
   auto attend = [&](const Raw& r, int p) {
     const int nvalid = min(kPage, n_slots - p * kPage);
-    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, s_p, q, n);
-    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, s_p, q, n);
+    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, q, n);
+    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, q, n);
   };
-#if PASK_PREFETCH_PAGES == 2
-  Raw cur = load(p0);
-  Raw nx1 = load(min(p0 + 1, p1 - 1));
-  for (int p = p0; p < p1; ++p) {
-    const Raw nx2 = load(min(p + 2, p1 - 1));
-    attend(cur, p);
-    cur = nx1;
-    nx1 = nx2;
+  for (int c = p0; c < p1; c += kIdChunk) {
+    const int cn = min(kIdChunk, p1 - c);
+    const int ids0 = bt[c + min(lane, cn - 1)];
+    const int ids1 = bt[c + min(64 + lane, cn - 1)];
+    auto id = [&](int i) -> int {   // i: wave-uniform, < cn
+      return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
+    };
+    auto ld = [&](int i) -> Raw { return load(id(min(i, cn - 1))); };
+    // Two page buffers used in turn (unrolled by two), so no buffer is
+    // copied while its loads are in flight.
+    Raw x0 = ld(0);
+    for (int i = 0; i < cn; i += 2) {
+      const Raw x1 = ld(i + 1);
+      attend(x0, c + i);
+      x0 = ld(i + 2);
+      if (i + 1 < cn) attend(x1, c + i + 1);
+    }
   }
-#else
-  Raw cur = load(p0);
-  for (int p = p0; p < p1; ++p) {
-    const Raw nxt = load(min(p + 1, p1 - 1));
-    attend(cur, p);
-    cur = nxt;
-  }
-#endif
 }
 
 // Pages [j0, j1) of (b, g) (HIGH pages, then LOW pages).  Writes the output
 // when this block holds all pages of (b, g), else a partial.
 template <int D, int G>
-__device__ __forceinline__ void attend_segment(const AttnArgs& a, int b, int g, int j0, int j1, const SeqPages& sp,
-                                               long long seg0, int U, float (*s_p)[20], int q, int n) {
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
+                                               long long seg0, int U, int q, int n) {
   using PL = PageLayout<D>;
   const CacheView& cv = a.cv;
   const int H = cv.n_kv_heads;
   const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;
   AttnState<D, G> st;
+  // Columns n >= G repeat head G-1 (finite scores; their results are unused).
+  const uint16_t* qh = a.q + (bh0 + min(n, G - 1)) * D + 8 * q;
 #pragma unroll
   for (int i = 0; i < PL::NG; ++i) {
-    uint4 w = make_uint4(0u, 0u, 0u, 0u);
-    if (n < G) w = *reinterpret_cast<const uint4*>(a.q + (bh0 + n) * D + 32 * i + 8 * q);
+    const uint4 w = *reinterpret_cast<const uint4*>(qh + 32 * i);
     st.qa[4 * i] = w.x; st.qa[4 * i + 1] = w.y; st.qa[4 * i + 2] = w.z; st.qa[4 * i + 3] = w.w;
   }
 #pragma unroll
   for (int k = 0; k < PL::NM; ++k) st.acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    st.m[r] = -INFINITY;
-    st.l[r] = 0.0f;
-  }
+  st.m = -INFINITY;
+  st.l = 0.0f;
   if (j0 < sp.np_hi)
     run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), j0,
-                          min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, s_p, q, n);
+                          min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, q, n);
   if (j1 > sp.np_hi)
     run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo),
-                           max(j0, sp.np_hi) - sp.np_hi, j1 - sp.np_hi, sp.n_lo, g, st, a.scale_log2, s_p, q, n);
-  // Sum l over the slots of each row (the 16 lanes with equal q).
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float lh = st.l[r];
-    lh += __shfl_xor(lh, 1, 16);
-    lh += __shfl_xor(lh, 2, 16);
-    lh += __shfl_xor(lh, 4, 16);
-    lh += __shfl_xor(lh, 8, 16);
-    st.l[r] = lh;
-  }
+                           max(j0, sp.np_hi) - sp.np_hi, j1 - sp.np_hi, sp.n_lo, g, st, a.scale_log2, q, n);
+  const float l_n = head_sum(st.l);              // head n, over all slots
   const long long first = seg0 / U, last = (seg0 + page_start(sp, sp.np - 1)) / U;
   if (first == last) {                       // this block holds all of (b, g): final output
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int h = 4 * q + r;
+      const float lr = __shfl(l_n, h);
       if (h < G) {
-        const float inv = 1.0f / st.l[r];
+        const float inv = 1.0f / lr;
 #pragma unroll
         for (int k = 0; k < PL::NM; ++k) a.out[(bh0 + h) * D + 16 * k + n] = f32_to_bf16_rne_dev(st.acc[k][r] * inv);
-        if (a.lse && n == 0) a.lse[bh0 + h] = (st.m[r] + log2f(st.l[r])) * 0.69314718055994530942f;
       }
     }
+    if (a.lse && q == 0 && n < G) a.lse[bh0 + n] = (st.m + log2f(l_n)) * 0.69314718055994530942f;
     return;
   }
-  const int slot = (int)(blockIdx.x - first);   // < a.splits by the choice of U
+  const int slot = (int)(w - first);           // < a.splits by the choice of U
   const size_t S = a.splits;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -868,25 +889,30 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int b, int g, 
       float* o = a.ws_o + ((bh0 + h) * S + slot) * D;
 #pragma unroll
       for (int k = 0; k < PL::NM; ++k) o[16 * k + n] = st.acc[k][r];
-      if (n == 0) *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + h) * S + slot) * 2) = make_float2(st.m[r], st.l[r]);
     }
   }
+  if (q == 0 && n < G) *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + n) * S + slot) * 2) = make_float2(st.m, l_n);
 }
 
+// Each wave of a workgroup is an independent stream-K worker w (kAttnWaves
+// waves per workgroup only cut the number of workgroup dispatches).
+constexpr int kAttnWaves = PASK_ATTN_WAVES;
+
 template <int D, int G>
-__global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
-  __shared__ float s_p[16][20];   // row stride 80 B: 16-byte aligned rows
-  const int lane = threadIdx.x;
+__global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int w = uni(blockIdx.x * kAttnWaves + (threadIdx.x >> 6));
   const int q = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
-  const StreamPlan plan = stream_plan(a, gridDim.x);
-  const long long start = (long long)blockIdx.x * plan.U;
+  const FirstCounts f = first_counts(a);
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const long long start = (long long)w * plan.U;
   if (start >= plan.total) return;
   const long long end = min(plan.total, start + plan.U);
   int b, excl;
-  locate(a, start, b, excl);
+  locate(a, f, start, b, excl);
   if (b < 0) return;
-  SeqPages sp = seq_pages(a.cv, a.layer, b);
+  SeqPages sp = seq_pages(a, f, b);
   const long long rel = start - (long long)excl * H;
   int g = (int)(rel / sp.len);
   int j0 = first_page_at(sp, (int)(rel % sp.len));
@@ -894,7 +920,7 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
     const long long seg0 = (long long)excl * H + (long long)g * sp.len;
     if (seg0 >= end) return;
     const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
-    if (j0 < j1) attend_segment<D, G>(a, b, g, j0, j1, sp, seg0, plan.U, s_p, q, n);
+    if (j0 < j1) attend_segment<D, G>(a, w, b, g, j0, j1, sp, seg0, plan.U, q, n);
     if (j1 < sp.np) return;
     j0 = 0;
     if (++g == H) {                              // next sequence that holds any page
@@ -902,7 +928,7 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
       excl += sp.len;
       do {
         if (++b >= a.batch) return;
-        sp = seq_pages(a.cv, a.layer, b);
+        sp = seq_pages(a, f, b);
       } while (sp.len == 0);
     }
   }
@@ -920,19 +946,17 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
   const int b = blockIdx.x / a.n_q_heads;
   const size_t bh = blockIdx.x;
   const int g = (blockIdx.x % a.n_q_heads) / a.group_size;
-  const SeqPages sp = seq_pages(a.cv, a.layer, b);
+  const FirstCounts f = first_counts(a);
+  const SeqPages sp = seq_pages(a, f, uni(b));
   if (sp.np == 0) {
 #pragma unroll
     for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = 0;
     if (a.lse && lane == 0) a.lse[bh] = -INFINITY;
     return;
   }
-  const StreamPlan plan = stream_plan(a, a.attn_blocks);
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
   int excl = 0;                                   // units of the sequences before b
-  for (int c0 = 0; c0 < b; c0 += 64) {
-    const int bb = c0 + lane;
-    excl += wave_sum(bb < b ? seq_pages(a.cv, a.layer, bb).len : 0);
-  }
+  for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
   const long long seg0 = (long long)excl * a.cv.n_kv_heads + (long long)g * sp.len;
   const int nparts = (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
   if (nparts <= 1) return;                        // written by the attention kernel
@@ -1004,9 +1028,9 @@ hipError_t launch_append_step(const AppendArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Stream-K grid of attn_kernel<D, G> on the current device: as many one-wave
-// blocks as can be resident at once (occupancy x compute units), so every
-// block starts at launch.  Queried once per device and instance.
+// Stream-K workers of attn_kernel<D, G> on the current device: as many waves
+// as can be resident at once (occupancy x compute units), so every worker
+// starts at launch.  Queried once per device and instance.
 template <int D, int G>
 int attn_grid() {
   constexpr int kMaxDevices = 64;
@@ -1014,12 +1038,15 @@ int attn_grid() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
   if (cached[dev] == 0) {
-    int per_cu = PASK_ATTN_BLOCKS_PER_CU, cus = 0;
-    if (per_cu == 0 &&
-        (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64, 0) != hipSuccess || per_cu <= 0))
-      return 0;
+    int per_cu = PASK_ATTN_WAVES_PER_CU, cus = 0;
+    if (per_cu == 0) {
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64 * kAttnWaves, 0) !=
+              hipSuccess || per_cu <= 0)
+        return 0;
+      per_cu *= kAttnWaves;
+    }
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
-    cached[dev] = per_cu * cus;
+    cached[dev] = (per_cu * cus) / kAttnWaves * kAttnWaves;   // whole workgroups
   }
   return cached[dev];
 }
@@ -1032,7 +1059,7 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
   if (D == DD && group_size == GG) {                                             \
     a.attn_blocks = attn_grid<DD, GG>();                                         \
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
-    attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
+    attn_kernel<DD, GG><<<dim3(a.attn_blocks / kAttnWaves), dim3(64 * kAttnWaves), 0, s>>>(a); \
     attn_merge_kernel<DD><<<dim3(a.batch * a.n_q_heads), block, 0, s>>>(a);      \
     return hipGetLastError();                                                    \
   }

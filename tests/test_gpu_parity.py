@@ -154,8 +154,9 @@ def test_prompt_side_persistence_tagged_prompt():
 
 
 def test_small_ctx_hint_grid_stride():
-    """A max_ctx_hint far below the real history: fewer splits than work
-    units, each split walks several units; results unchanged."""
+    """A max_ctx_hint far below the real history: a workspace with room for
+    few partials per (sequence, KV head) forces larger per-block page
+    ranges; results unchanged."""
     say("case: small ctx hint")
     pol = make_policy(6, 2, 2, 0.33, seed=14)
     tags = iid_tags(10, 5)[None].repeat(2, axis=0)
@@ -163,6 +164,28 @@ def test_small_ctx_hint_grid_stride():
                   max_ctx_hint=100)
     sc.fill_prompt()
     sc.decode_step(0)
+    sc.check_state()
+
+
+def test_batch_beyond_64_sequences():
+    """150 sequences (three 64-sequence chunks in the attention work plan, the
+    last ragged), about one in five with no prompt, short ragged prompts and
+    three long ones (at indices 5, 70 and 140, each split over several
+    blocks): the plan, the block search, the walk to the next sequence and the
+    merge read counts beyond the first 64 sequences."""
+    say("case: batch of 150")
+    rng = np.random.default_rng(21)
+    B = 150
+    P = rng.integers(1, 90, size=B)
+    P[rng.random(B) < 0.2] = 0
+    P[[5, 70, 140]] = [700, 1000, 913]
+    pol = make_policy(6, 2, 2, 0.33, seed=21)
+    tags = np.stack([walk_function_calls(12, 60 + b) for b in range(B)])
+    sc = Scenario(pol, B=B, L=2, Hq=8, Hkv=2, D=64, prompt_lens=P, gen_tags=tags, seed=21)
+    sc.fill_prompt()
+    sc.decode_step(0)
+    sc.append_steps(1, 11)
+    sc.decode_step(11)
     sc.check_state()
 
 
