@@ -154,12 +154,16 @@ struct WsLayout {
   uint64_t o_off, ml_off, total;
 };
 
+// Partials of the attention pieces: per (sequence, KV head, piece) a block of
+// G4 = max(G, 4) query-head rows of head_dim fp32 values, and G4 (max, sum)
+// pairs.
 WsLayout ws_layout(const pask_geom* g, int32_t batch, int splits) {
   WsLayout w;
-  const uint64_t rows = (uint64_t)batch * g->n_q_heads * splits;
+  const uint64_t group = (uint64_t)std::max(4, g->n_q_heads / g->n_kv_heads);
+  const uint64_t blocks = (uint64_t)batch * g->n_kv_heads * splits;
   w.o_off = 0;
-  w.ml_off = align_up(rows * g->head_dim * 4, kAlignSmall);
-  w.total = align_up(w.ml_off + rows * 2 * 4, kAlignSmall);
+  w.ml_off = align_up(blocks * group * g->head_dim * 4, kAlignSmall);
+  w.total = align_up(w.ml_off + blocks * group * 2 * 4, kAlignSmall);
   return w;
 }
 
@@ -352,7 +356,6 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
   a.batch = batch;
   a.n_q_heads = g.n_q_heads;
   a.splits = splits;
-  a.group_size = g.n_q_heads / g.n_kv_heads;
   return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
 }
 

@@ -23,14 +23,6 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #ifndef PASK_WEIGHT_LO
 #define PASK_WEIGHT_LO 32
 #endif
-// Waves per attention workgroup (each an independent worker).
-#ifndef PASK_ATTN_WAVES
-#define PASK_ATTN_WAVES 1
-#endif
-// Attention workers (waves) per compute unit (0: the kernel's occupancy).
-#ifndef PASK_ATTN_WAVES_PER_CU
-#define PASK_ATTN_WAVES_PER_CU 0
-#endif
 #ifndef PASK_UNIT_TOKENS
 #define PASK_UNIT_TOKENS 256
 #endif
@@ -74,11 +66,10 @@ struct AttnArgs {
   const uint16_t* q;        // bf16 bits [batch][Hq][D]
   uint16_t* out;            // bf16 bits [batch][Hq][D]
   float* lse;               // [batch][Hq] or null
-  float* ws_o;              // [batch][Hq][splits][D]
-  float* ws_ml;             // [batch][Hq][splits][2]  (max, sum) in log2 units
+  float* ws_o;              // [batch][Hkv][splits][G4 * D], G4 = max(G, 4) heads
+  float* ws_ml;             // [batch][Hkv][splits][G4][2]  (max, sum) in log2 units
   float scale_log2;         // softmax_scale * log2(e)
   int32_t layer, batch, n_q_heads, splits;   // splits: partials per (b, g) the workspace holds
-  int32_t group_size;       // n_q_heads / n_kv_heads
   int32_t attn_blocks;      // stream-K workers (waves) of the attention kernel, set at launch
 };
 

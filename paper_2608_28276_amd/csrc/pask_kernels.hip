@@ -18,8 +18,8 @@
 //                int4 codes widened exactly to bf16 in registers with the K
 //                scale applied per 32-dim group and the V scale folded into p,
 //                online softmax in base 2, next page prefetched into registers.
-//   attn_merge   zero output for empty histories; merge the partials of each
-//                (sequence, KV head) split over blocks (max, sum, values).
+//   attn_merge   per (sequence, KV head): combine the partials of its pieces
+//                (max, sum, values) into bf16 outputs; zero for empty histories.
 #include <hip/hip_runtime.h>
 
 #include <limits.h>
@@ -864,44 +864,30 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   if (j1 > sp.np_hi)
     run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo),
                            max(j0, sp.np_hi) - sp.np_hi, j1 - sp.np_hi, sp.n_lo, g, st, a.scale_log2, q, n);
+  // Partial of piece `slot` of (b, g): rows of G4 = max(G, 4) query heads,
+  // stored as float4s of 4 heads at one dim (index ((q*NM + k)*16 + n)*4 + r
+  // for head 4q + r, dim 16k + n): each store instruction writes 256
+  // contiguous bytes, and the (max, sum) pairs of the G4 heads sit together.
+  // Rows past G hold finite values that are never read into an output.
+  constexpr int G4 = G > 4 ? G : 4;
   const float l_n = head_sum(st.l);              // head n, over all slots
-  const long long first = seg0 / U, last = (seg0 + page_start(sp, sp.np - 1)) / U;
-  if (first == last) {                       // this block holds all of (b, g): final output
+  const int slot = (int)(w - seg0 / U);          // < a.splits by the choice of U
+  const size_t blk = ((size_t)b * H + g) * a.splits + slot;
+  if (4 * q < G4) {
+    float* o = a.ws_o + blk * (G4 * D);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int h = 4 * q + r;
-      const float lr = __shfl(l_n, h);
-      if (h < G) {
-        const float inv = 1.0f / lr;
-#pragma unroll
-        for (int k = 0; k < PL::NM; ++k) a.out[(bh0 + h) * D + 16 * k + n] = f32_to_bf16_rne_dev(st.acc[k][r] * inv);
-      }
-    }
-    if (a.lse && q == 0 && n < G) a.lse[bh0 + n] = (st.m + log2f(l_n)) * 0.69314718055994530942f;
-    return;
+    for (int k = 0; k < PL::NM; ++k)
+      *reinterpret_cast<float4*>(o + ((q * PL::NM + k) * 16 + n) * 4) =
+          make_float4(st.acc[k][0], st.acc[k][1], st.acc[k][2], st.acc[k][3]);
   }
-  const int slot = (int)(w - first);           // < a.splits by the choice of U
-  const size_t S = a.splits;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int h = 4 * q + r;
-    if (h < G) {
-      float* o = a.ws_o + ((bh0 + h) * S + slot) * D;
-#pragma unroll
-      for (int k = 0; k < PL::NM; ++k) o[16 * k + n] = st.acc[k][r];
-    }
-  }
-  if (q == 0 && n < G) *reinterpret_cast<float2*>(a.ws_ml + ((bh0 + n) * S + slot) * 2) = make_float2(st.m, l_n);
+  if (q == 0 && n < G4) *reinterpret_cast<float2*>(a.ws_ml + (blk * G4 + n) * 2) = make_float2(st.m, l_n);
 }
 
-// Each wave of a workgroup is an independent stream-K worker w (kAttnWaves
-// waves per workgroup only cut the number of workgroup dispatches).
-constexpr int kAttnWaves = PASK_ATTN_WAVES;
-
+// One single-wave workgroup per stream-K worker w.
 template <int D, int G>
-__global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63;
-  const int w = uni(blockIdx.x * kAttnWaves + (threadIdx.x >> 6));
+  const int w = uni(blockIdx.x);
   const int q = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
   const FirstCounts f = first_counts(a);
@@ -934,74 +920,82 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(AttnArgs a) {
   }
 }
 
-// One (sequence, query head): zero output for an empty history; otherwise
-// merge the partials when (b, g) was split over several blocks.  Lane p holds
-// partial p's (max, sum) for the global max and the weights; the weighted
-// values are summed with the loads of a batch of partials in flight at once.
-template <int D>
-__global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
-  constexpr int E = D / 64;           // dims per lane
-  constexpr int kBatch = 8;           // partials whose loads are issued together
-  const int lane = threadIdx.x;
-  const int b = blockIdx.x / a.n_q_heads;
-  const size_t bh = blockIdx.x;
-  const int g = (blockIdx.x % a.n_q_heads) / a.group_size;
+// One (sequence, KV head): combine the partials of its pieces (one or more)
+// into the bf16 outputs and log-sum-exps of its G query heads; zero output
+// and -inf for an empty history.  Thread t owns float4 position t of the
+// partial rows (4 heads at one dim) and merges it online over the pieces,
+// keeping the running (max, sum) of those 4 heads; the normalised rows are
+// staged in LDS and written as contiguous 16-byte pieces.
+template <int D, int G>
+constexpr int merge_threads() { return (G > 4 ? G : 4) * D / 4; }
+
+template <int D, int G>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merge_threads <= 256
+  constexpr int G4 = G > 4 ? G : 4;
+  constexpr int NM = D / 16;
+  constexpr int kBatch = 8;                      // pieces whose loads are issued together
+  static_assert(merge_threads<D, G>() % 64 == 0 && merge_threads<D, G>() <= 256, "merge block size");
+  __shared__ __align__(16) uint16_t s_out[G][D];
+  const int t = threadIdx.x;
+  const int H = a.cv.n_kv_heads;
+  const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
+  const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
   const FirstCounts f = first_counts(a);
-  const SeqPages sp = seq_pages(a, f, uni(b));
+  const SeqPages sp = seq_pages(a, f, b);
   if (sp.np == 0) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = 0;
-    if (a.lse && lane == 0) a.lse[bh] = -INFINITY;
+    for (int i = t; i < G * D; i += merge_threads<D, G>()) a.out[row0 * D + i] = 0;
+    if (a.lse && t < G) a.lse[row0 + t] = -INFINITY;
     return;
   }
   const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
   int excl = 0;                                   // units of the sequences before b
   for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
-  const long long seg0 = (long long)excl * a.cv.n_kv_heads + (long long)g * sp.len;
+  const long long seg0 = (long long)excl * H + (long long)g * sp.len;
   const int nparts = (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
-  if (nparts <= 1) return;                        // written by the attention kernel
-  const int S = a.splits;
-  const float2* ml = reinterpret_cast<const float2*>(a.ws_ml + bh * S * 2);
-  const float* o = a.ws_o + bh * S * D + lane * E;
-  float M = -INFINITY, L = 0.0f, acc[E];
+  const size_t blk0 = ((size_t)b * H + g) * a.splits;
+  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f}, M[4], L[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int e = 0; e < E; ++e) acc[e] = 0.0f;
-  for (int p0 = 0; p0 < nparts; p0 += 64) {
-    const int p = p0 + lane;
-    const float2 x = p < nparts ? ml[p] : make_float2(-INFINITY, 0.0f);
-    float mx = x.x;
+  for (int r = 0; r < 4; ++r) M[r] = -INFINITY;
+  for (int p0 = 0; p0 < nparts; p0 += kBatch) {
+    float4 v[kBatch], mla[kBatch], mlb[kBatch];
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-    const float Mn = fmaxf(M, mx);
-    const float alpha = exp2f(M - Mn);                   // rescale what earlier passes summed
-    const float w = p < nparts ? exp2f(x.x - Mn) : 0.0f;
-    float lw = w * x.y;
+    for (int u = 0; u < kBatch; ++u) {            // past the last piece: repeat it, skipped below
+      const size_t pb = blk0 + min(p0 + u, nparts - 1);
+      const float* ml = a.ws_ml + pb * G4 * 2 + 8 * q;
+      v[u] = *reinterpret_cast<const float4*>(a.ws_o + pb * (G4 * D) + t * 4);
+      mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
+      mlb[u] = *reinterpret_cast<const float4*>(ml + 4);   // (m, l) of heads 4q+2, 4q+3
+    }
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) lw += __shfl_xor(lw, off);
-    L = L * alpha + lw;
+    for (int u = 0; u < kBatch; ++u) {
+      if (p0 + u >= nparts) break;
+      const float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      const float mlv[8] = {mla[u].x, mla[u].y, mla[u].z, mla[u].w, mlb[u].x, mlb[u].y, mlb[u].z, mlb[u].w};
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] *= alpha;
-    M = Mn;
-    const int nn = min(64, nparts - p0);
-    for (int q0 = 0; q0 < nn; q0 += kBatch) {
-      float v[kBatch][E], wq[kBatch];
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int qq = min(q0 + k, nn - 1);
-        wq[k] = q0 + k < nn ? __shfl(w, qq) : 0.0f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) v[k][e] = o[(size_t)(p0 + qq) * D + e];
+      for (int r = 0; r < 4; ++r) {
+        const float mp = mlv[2 * r], lp = mlv[2 * r + 1];
+        const float mn = fmaxf(M[r], mp);
+        const float alpha = exp2f(M[r] - mn), wgt = exp2f(mp - mn);
+        L[r] = L[r] * alpha + wgt * lp;
+        acc[r] = acc[r] * alpha + wgt * vv[r];
+        M[r] = mn;
       }
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k)
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] = fmaf(wq[k], v[k][e], acc[e]);
     }
   }
-  const float inv = 1.0f / L;
 #pragma unroll
-  for (int e = 0; e < E; ++e) a.out[bh * D + lane * E + e] = f32_to_bf16_rne_dev(acc[e] * inv);
-  if (a.lse && lane == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * q + r;
+    if (h < G) {
+      s_out[h][16 * k + n] = f32_to_bf16_rne_dev(acc[r] / L[r]);
+      if (a.lse && k == 0 && n == 0) a.lse[row0 + h] = (M[r] + log2f(L[r])) * 0.69314718055994530942f;
+    }
+  }
+  __syncthreads();
+  // G rows of D bf16 are contiguous in the output: 16-byte pieces.
+  const uint4* src = reinterpret_cast<const uint4*>(&s_out[0][0]);
+  uint4* dst = reinterpret_cast<uint4*>(a.out + row0 * D);
+  for (int i = t; i < G * D / 8; i += merge_threads<D, G>()) dst[i] = src[i];
 }
 
 }  // namespace
@@ -1038,15 +1032,11 @@ int attn_grid() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
   if (cached[dev] == 0) {
-    int per_cu = PASK_ATTN_WAVES_PER_CU, cus = 0;
-    if (per_cu == 0) {
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64 * kAttnWaves, 0) !=
-              hipSuccess || per_cu <= 0)
-        return 0;
-      per_cu *= kAttnWaves;
-    }
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64, 0) != hipSuccess || per_cu <= 0)
+      return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
-    cached[dev] = (per_cu * cus) / kAttnWaves * kAttnWaves;   // whole workgroups
+    cached[dev] = per_cu * cus;
   }
   return cached[dev];
 }
@@ -1059,8 +1049,8 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
   if (D == DD && group_size == GG) {                                             \
     a.attn_blocks = attn_grid<DD, GG>();                                         \
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
-    attn_kernel<DD, GG><<<dim3(a.attn_blocks / kAttnWaves), dim3(64 * kAttnWaves), 0, s>>>(a); \
-    attn_merge_kernel<DD><<<dim3(a.batch * a.n_q_heads), block, 0, s>>>(a);      \
+    attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
+    attn_merge_kernel<DD, GG><<<dim3(a.batch * a.cv.n_kv_heads), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)

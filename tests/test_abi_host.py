@@ -142,11 +142,13 @@ def test_unsupported_geometry(bad):
 
 def test_workspace_bytes():
     g = geom()
-    # splits = ceil(hint / 256) + 2; rows = batch * Hq * splits; o: rows*D*4, ml: rows*2*4 (256-aligned)
+    # splits = ceil(hint / 256) + 2; per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
+    # o: blocks*G4*D*4, ml: blocks*G4*2*4 (each 256-aligned)
     ws = pask.pask_workspace_bytes(g, 4, 512)
-    rows = 4 * 8 * 4
-    want = ((rows * 64 * 4 + 255) // 256) * 256
-    want = ((want + rows * 8 + 255) // 256) * 256
+    G4 = max(4, g.n_q_heads // g.n_kv_heads)
+    blocks = 4 * g.n_kv_heads * 4
+    want = ((blocks * G4 * g.head_dim * 4 + 255) // 256) * 256
+    want = ((want + blocks * G4 * 8 + 255) // 256) * 256
     assert ws == want
 
 
