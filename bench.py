@@ -267,7 +267,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload index (default: the B=64 serving batch)")
     ap.add_argument("--t-start", type=int, default=512, help="generated tokens persisted before timing")
-    ap.add_argument("--cpu-seqs", type=int, default=1, help="sequences in the oracle's timed sample")
+    ap.add_argument("--cpu-seqs", type=int, default=3, help="sequences in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
@@ -315,7 +315,8 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(cfg),
-            "kernel": f"attn_kernel<{cfg.head_dim}, {cfg.group_size}>",
+            "kernel": f"attn_kernel<{cfg.head_dim}, {cfg.group_size}> + attn_merge_kernel<{cfg.head_dim}, "
+                      f"{cfg.group_size}> (one pask_decode_attn call)",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
         },
         "cpu_baseline": cpu,
