@@ -1,0 +1,181 @@
+"""Parity at the workloads' full sizes: the whole cache is built on the device
+(inputs from torch's device generator, in token chunks), the oracle replays
+sampled (sequence, layer) pairs from host copies of the same inputs, and the
+decisions of every sequence come from the oracle's decision and compaction
+steps.  Comparisons: counters and index lists of every driven (sequence,
+layer) and the stored bits / codes / scales of the sampled pairs bit-exactly;
+attention of the sampled pairs within |gpu - ref| <= 2e-3 + 1e-2 |ref|."""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from tests.gpu_util import assert_attn_close, bf16_f64, bits16, policy_dict, say
+from workload.policy import pack_blob
+from workload.tensors import sub_seed
+
+
+def _pages(n) -> int:
+    return int(np.sum((np.asarray(n, dtype=np.int64) + 15) // 16))
+
+
+class DeviceRun:
+    """One workload on one GPU.
+
+    layers: the layer indices driven (the geometry keeps all n_layers of the
+    policy); P: prompt lengths; prompt_tags [B, Pmax] or None (prompt kept
+    HIGH); gen_tags [B, T]; sample: (sequence, layer) pairs replayed by the
+    oracle.  Generated tokens 0..n_bulk-1 are bulk-appended, the following
+    ones go through one-token appends with attention (`step`)."""
+
+    def __init__(self, pol, *, n_layers, layers, Hq, Hkv, D, P, prompt_tags, gen_tags, sample, seed,
+                 n_bulk, n_steps, chunk=2048):
+        from paper_2608_28276_amd.session import PaskSession
+        self.pol, self.layers, self.Hq, self.Hkv, self.D = pol, list(layers), Hq, Hkv, D
+        self.P = np.asarray(P, dtype=np.int64)
+        self.B = self.P.size
+        self.prompt_tags = prompt_tags
+        self.gen_tags = np.asarray(gen_tags, dtype=np.uint8)
+        self.sample = list(sample)
+        self.seed, self.chunk = seed, chunk
+        self.n_bulk, self.n_steps = n_bulk, n_steps
+        self.dev = torch.device("cuda:0")
+        self.gol = np.asarray(pol.group_of_layer)
+        self.t = 0                                   # generated tokens appended so far
+        self._expected(n_bulk + n_steps)
+        hi_pages = sum(_pages(self.exp[(b, int(self.gol[l]))]["hi"].size) for b in range(self.B) for l in self.layers)
+        lo_pages = sum(_pages(self.exp[(b, int(self.gol[l]))]["lo"].size) for b in range(self.B) for l in self.layers)
+        self.max_tok = int(self.P.max()) + n_bulk + n_steps
+        self.sess = PaskSession(pack_blob(pol), max_batch=self.B, n_layers=n_layers, n_q_heads=Hq,
+                                n_kv_heads=Hkv, head_dim=D, max_tokens_per_seq=self.max_tok,
+                                hi_pages=hi_pages + 1, lo_pages=lo_pages + 1, max_ctx_hint=self.max_tok)
+        say(f"cache {self.sess.nbytes / 2**30:.1f} GiB: {hi_pages} HIGH + {lo_pages} LOW pages")
+        self.oc = oracle.OracleCache(policy_dict(pol), Hkv, D)
+        self.scale = self.sess.softmax_scale
+        self.gen = torch.Generator(device=self.dev)
+
+    # -- expected decisions of every (sequence, layer group) ---------------
+    def _expected(self, n_gen):
+        self.exp = {}
+        act, flo, ns = np.asarray(self.pol.action), np.asarray(self.pol.floor), int(self.pol.n_sink)
+        for c in sorted({int(self.gol[l]) for l in self.layers}):
+            for b in range(self.B):
+                p = int(self.P[b])
+                ptags = np.zeros(p, np.uint8) if self.prompt_tags is None else self.prompt_tags[b, :p]
+                a0, f0, _ = oracle.decide(ptags, np.arange(p), c, act, flo, ns, self.prompt_tags is None)
+                a1, f1, _ = oracle.decide(self.gen_tags[b, :n_gen], p + np.arange(n_gen), c, act, flo, ns, False)
+                acts = np.concatenate([a0, a1])
+                hi, lo = oracle.compact(acts, np.arange(p + n_gen))
+                self.exp[(b, c)] = dict(hi=hi, lo=lo, drop=int((acts == oracle.DROP).sum()),
+                                        forced=int(f0.sum() + f1.sum()), pos=p + n_gen)
+
+    # -- inputs ------------------------------------------------------------
+    def _randn(self, shape, *key):
+        self.gen.manual_seed(sub_seed(self.seed, "device_inputs", *key))
+        return torch.randn(shape, generator=self.gen, device=self.dev, dtype=torch.bfloat16)
+
+    def _feed_oracle(self, layer, k, v, n, tags, keep_all):
+        for (b, l) in self.sample:
+            if l == layer and n[b] > 0:
+                t = np.zeros(n[b], np.uint8) if tags is None else tags[b, :n[b]]
+                self.oc.append(layer, b, t, bits16(k[b, :n[b]]), bits16(v[b, :n[b]]), keep_all=keep_all)
+
+    def fill(self):
+        """Prompts, then generated tokens 0..n_bulk-1, in token chunks."""
+        Pmax, C = int(self.P.max()), self.chunk
+        for li, layer in enumerate(self.layers):
+            for c0 in range(0, Pmax, C):
+                n = np.clip(self.P - c0, 0, C)
+                w = int(n.max())
+                k = self._randn((self.B, w, self.Hkv, self.D), 1, layer, c0)
+                v = self._randn((self.B, w, self.Hkv, self.D), 2, layer, c0)
+                nd = torch.as_tensor(n.astype(np.int32), device=self.dev)
+                if self.prompt_tags is None:
+                    self.sess.append(layer, None, k, v, n_new=nd, keep_all=True)
+                    self._feed_oracle(layer, k, v, n, None, True)
+                else:
+                    tg = np.ascontiguousarray(self.prompt_tags[:, c0:c0 + w])
+                    self.sess.append(layer, torch.as_tensor(tg, device=self.dev), k, v, n_new=nd)
+                    self._feed_oracle(layer, k, v, n, tg, False)
+                del k, v
+            for t0 in range(0, self.n_bulk, C):
+                w = min(C, self.n_bulk - t0)
+                k = self._randn((self.B, w, self.Hkv, self.D), 3, layer, t0)
+                v = self._randn((self.B, w, self.Hkv, self.D), 4, layer, t0)
+                tg = np.ascontiguousarray(self.gen_tags[:, t0:t0 + w])
+                self.sess.append(layer, torch.as_tensor(tg, device=self.dev), k, v)
+                self._feed_oracle(layer, k, v, np.full(self.B, w), tg, False)
+                del k, v
+            if li == 0 or li == len(self.layers) - 1:
+                say(f"filled layer {layer}")
+        self.t = self.n_bulk
+        torch.cuda.synchronize()
+
+    def step(self, check: bool, fused: bool = False):
+        """One decode step on every driven layer: the step's token of every
+        sequence is appended (one-token append, or the fused call), then
+        attention; the sampled pairs are compared when `check`."""
+        t = self.t
+        tg = torch.as_tensor(np.ascontiguousarray(self.gen_tags[:, t]), device=self.dev)
+        worst = 0.0
+        for layer in self.layers:
+            q = self._randn((self.B, self.Hq, self.D), 5, layer, t)
+            k = self._randn((self.B, 1, self.Hkv, self.D), 6, layer, t)
+            v = self._randn((self.B, 1, self.Hkv, self.D), 7, layer, t)
+            out = torch.empty((self.B, self.Hq, self.D), dtype=torch.bfloat16, device=self.dev)
+            lse = torch.empty((self.B, self.Hq), dtype=torch.float32, device=self.dev)
+            if fused:
+                self.sess.decode(layer, q, out, lse, tg, k[:, 0].contiguous(), v[:, 0].contiguous())
+            else:
+                self.sess.append(layer, tg[:, None].contiguous(), k, v)
+                self.sess.decode(layer, q, out, lse)
+            self._feed_oracle(layer, k, v, np.ones(self.B, np.int64), self.gen_tags[:, t:t + 1], False)
+            if not check:
+                continue
+            o_gpu, l_gpu = bf16_f64(out), lse.cpu().double().numpy()
+            for (b, l) in self.sample:
+                if l != layer:
+                    continue
+                o_ref, lse_ref = self.oc.attend(layer, b, bits16(q[b]), self.scale)
+                assert_attn_close(o_gpu[b], o_ref, f"attention step {t} layer {layer} seq {b}")
+                assert np.abs(l_gpu[b] - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max()
+                worst = max(worst, float(np.abs(o_gpu[b] - o_ref).max()))
+        self.t += 1
+        if check:
+            say(f"step {t}: attention of {len(self.sample)} sampled pairs within tolerance (worst {worst:.2e})")
+        return worst
+
+    # -- state ---------------------------------------------------------------
+    def check_lists(self):
+        """Counters and index lists of every sequence in every driven layer."""
+        n_gen = self.t
+        if n_gen != self.n_bulk + self.n_steps:
+            self._expected(n_gen)
+        cnt = self.sess.counters().cpu().numpy()
+        for layer in self.layers:
+            il = self.sess.index_lists()[:, layer].cpu().numpy()
+            c = int(self.gol[layer])
+            for b in range(self.B):
+                e = self.exp[(b, c)]
+                got = cnt[b, layer]
+                assert (got[0], got[1], got[2], got[3], got[4], got[5]) == \
+                    (e["hi"].size, e["lo"].size, e["pos"], e["drop"], e["forced"], 0), (layer, b, got)
+                assert (il[b, 0, :e["hi"].size] == e["hi"]).all(), ("HIGH list", layer, b)
+                assert (il[b, 1, :e["lo"].size] == e["lo"]).all(), ("LOW list", layer, b)
+        st, status, _ = self.sess.stats(batch=self.B)
+        assert status == 0 and st.device_flags == 0, f"device flags {st.device_flags:#x}"
+        say(f"counters and lists of {self.B} sequences x {len(self.layers)} layers bit-exact")
+
+    def check_stores(self):
+        """Stored bits, codes and scales of the sampled pairs."""
+        for (b, layer) in self.sample:
+            gk, gv = self.sess.gather_store(b, layer, 0)
+            ok, ov = self.oc.hi_entries(b, layer)
+            assert (gk == ok).all() and (gv == ov).all(), ("HIGH bf16 copies", layer, b)
+            kc, ks, vc, vs = self.sess.gather_store(b, layer, 1)
+            okc, oks, ovc, ovs = self.oc.lo_entries(b, layer)
+            assert (kc == okc).all() and (vc == ovc).all(), ("LOW codes", layer, b)
+            assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
+        say(f"stores of {len(self.sample)} sampled pairs bit-exact")

@@ -12,7 +12,7 @@ import numpy as np
 import torch
 
 PURPOSE = {"prompt_k": 1, "prompt_v": 2, "gen_k": 3, "gen_v": 4, "q": 5,
-           "tags": 6, "lengths": 7, "policy": 8, "outlier": 9}
+           "tags": 6, "lengths": 7, "policy": 8, "outlier": 9, "prompt_tags": 10, "device_inputs": 11}
 
 
 def sub_seed(seed: int, purpose: str, *keys: int) -> int:
