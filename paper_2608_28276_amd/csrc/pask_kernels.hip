@@ -15,8 +15,9 @@
 //                per resident wave slot, each streaming an equal contiguous
 //                range of the (sequence, KV head, page) list over the HIGH and
 //                LOW stores; q.k and p.v on bf16 MFMA (query heads as rows),
-//                int4 codes widened exactly to bf16 in registers with the K
-//                scale applied per 32-dim group and the V scale folded into p,
+//                int4 codes widened to bf16 in registers with an exact offset
+//                removed after the products, the K scale applied per 32-dim
+//                group and the V scale folded into p,
 //                online softmax in base 2, next page prefetched into registers.
 //   attn_merge   per (sequence, KV head): combine the partials of its pieces
 //                (max, sum, values) into bf16 outputs; zero for empty histories.
@@ -51,10 +52,14 @@ __device__ __forceinline__ int32_t* index_list_of(const CacheView& cv, int b, in
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// fp32 -> bf16, round to nearest even (finite inputs).
+// fp32 -> bf16, round to nearest even: gfx950's v_cvt_pk_bf16_f32.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
 __device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+  return (uint16_t)pack_bf16x2(f, 0.0f);
 }
 
 
@@ -520,22 +525,35 @@ __device__ __forceinline__ LoRaw<D> load_lo(const uint8_t* head, int q, int n) {
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
 }
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16_rne_dev(lo) | ((uint32_t)f32_to_bf16_rne_dev(hi) << 16);
-}
 // x = hi + lo with hi = bf16(x) and lo = bf16(x - hi): 16 significant bits,
 // so the weights of the p.v MFMA carry fp32-like precision (two products).
 __device__ __forceinline__ void split_bf16x4(const float (&x)[4], uint2& hi, uint2& lo) {
   float r[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) r[k] = x[k] - __uint_as_float((uint32_t)f32_to_bf16_rne_dev(x[k]) << 16);
   hi = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+  r[0] = x[0] - bf16_lo(hi.x);
+  r[1] = x[1] - bf16_hi(hi.x);
+  r[2] = x[2] - bf16_lo(hi.y);
+  r[3] = x[3] - bf16_hi(hi.y);
   lo = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
 }
-// int4 code c (two's complement nibble) as an exact bf16 bit pattern.
-__device__ __forceinline__ uint32_t code_bf16(uint32_t nib) {
-  const int c = ((int)(nib << 28)) >> 28;
-  return __float_as_uint((float)c) >> 16;
+// int4 codes widened to bf16 with an offset: a nibble n (two's complement
+// code c) becomes the bf16 bit pattern 0x4300 | (n ^ 8), the exact value
+// 128 + (c + 8) = 136 + c (bf16 spacing is 1 on [128, 256)).  Two codes per
+// 32-bit word cost one byte permute and one xor; the offset 136 is removed
+// after the products (kOffset * sum of the other operand).
+constexpr float kCodeOffset = 136.0f;
+constexpr uint32_t kCodeBias = 0x43084308u;
+// Codes 2e (low nibble) and 2e+1 (high nibble) of byte e of w, as a bf16 pair.
+template <int e>
+__device__ __forceinline__ uint32_t codes_pair_in_byte(uint32_t lo4, uint32_t hi4) {
+  // v_perm_b32: selector bytes 0-3 pick bytes of the second source (lo4),
+  // 4-7 bytes of the first (hi4), 0x0C gives zero.
+  return __builtin_amdgcn_perm(hi4, lo4, 0x0C000C00u | ((4u + e) << 16) | e) ^ kCodeBias;
+}
+// Nibbles in bytes j0 and j1 of n4 (one nibble per byte) as a bf16 pair.
+template <int j0, int j1>
+__device__ __forceinline__ uint32_t codes_pair_from_bytes(uint32_t n4) {
+  return __builtin_amdgcn_perm(n4, n4, 0x0C000C00u | (j1 << 16) | j0) ^ kCodeBias;
 }
 
 // Per-wave attention state.  The score tile is S^T (MFMA row = slot 4q + r,
@@ -545,8 +563,10 @@ __device__ __forceinline__ uint32_t code_bf16(uint32_t nib) {
 template <int D, int G>
 struct AttnState {
   uint32_t qa[4 * PageLayout<D>::NG];   // QK B operands: q of head n, dims 32i + 8q + 0..7
-  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs
+  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs (LOW values carry the code offset)
   float m, l;                            // head n: running max (log2 units), lane-partial sum
+  float kq[PageLayout<D>::NG];           // head n: offset x sum of q over 32-dim group i
+  float vw[PageLayout<D>::NG];           // head n: lane-partial sum of p x (V scale of group i)
 };
 
 // Max over the 64 lanes' copies of one head (lanes n, n+16, n+32, n+48).
@@ -573,17 +593,15 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
   } else {
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
-      uint32_t a[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        a[e] = code_bf16(x.kc[i] >> (8 * e)) | (code_bf16(x.kc[i] >> (8 * e + 4)) << 16);
+      const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;
       const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
-      const f32x4_t c = mfma_k32(make_uint4(a[0], a[1], a[2], a[3]),
+      const f32x4_t c = mfma_k32(make_uint4(codes_pair_in_byte<0>(lo4, hi4), codes_pair_in_byte<1>(lo4, hi4),
+                                            codes_pair_in_byte<2>(lo4, hi4), codes_pair_in_byte<3>(lo4, hi4)),
                                  make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), zero);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
         const int hidx = r * PL::NG + i;
-        sc[r] = fmaf(half_bits_to_float(x.ks[hidx / 2] >> (16 * (hidx % 2))), c[r], sc[r]);
+        sc[r] = fmaf(half_bits_to_float(x.ks[hidx / 2] >> (16 * (hidx % 2))), c[r] - st.kq[i], sc[r]);
       }
     }
   }
@@ -599,6 +617,10 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
     const float alpha = exp2f(st.m - mn);
     st.l *= alpha;
     st.m = mn;
+    if constexpr (!kIsHi) {
+#pragma unroll
+      for (int i = 0; i < PL::NG; ++i) st.vw[i] *= alpha;
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {                   // output row 4q + r takes head 4q + r's factor
       const float ar = __shfl(alpha, 4 * q + r);
@@ -636,14 +658,14 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
         const float vs = half_bits_to_float(x.vs[hidx / 2] >> (16 * (hidx % 2)));
         w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vs : 0.0f;
       }
+      st.vw[i] += (w[0] + w[1]) + (w[2] + w[3]);
       uint2 pa_hi, pa_lo;
       split_bf16x4(w, pa_hi, pa_lo);
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const uint32_t bytes = x.vc[i];     // slots 4q..4q+3, dims 32i + 16hh + n
-        const uint32_t sh = 4 * hh;
-        const uint32_t b0 = code_bf16(bytes >> sh) | (code_bf16(bytes >> (8 + sh)) << 16);
-        const uint32_t b1 = code_bf16(bytes >> (16 + sh)) | (code_bf16(bytes >> (24 + sh)) << 16);
+        // byte jj of vc[i]: slot 4q + jj, dim 32i + n (low nibble) and 32i + 16 + n (high)
+        const uint32_t n4 = (hh ? x.vc[i] >> 4 : x.vc[i]) & 0x0F0F0F0Fu;
+        const uint32_t b0 = codes_pair_from_bytes<0, 1>(n4), b1 = codes_pair_from_bytes<2, 3>(n4);
         st.acc[2 * i + hh] = mfma_k16(pa_hi, make_uint2(b0, b1), st.acc[2 * i + hh]);
         st.acc[2 * i + hh] = mfma_k16(pa_lo, make_uint2(b0, b1), st.acc[2 * i + hh]);
       }
@@ -858,6 +880,14 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   for (int k = 0; k < PL::NM; ++k) st.acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   st.m = -INFINITY;
   st.l = 0.0f;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {            // offset x sum of q over group i (head n)
+    float part = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part += bf16_lo(st.qa[4 * i + e]) + bf16_hi(st.qa[4 * i + e]);
+    st.kq[i] = kCodeOffset * head_sum(part);
+    st.vw[i] = 0.0f;
+  }
   if (j0 < sp.np_hi)
     run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), j0,
                           min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, q, n);
@@ -870,6 +900,18 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   // contiguous bytes, and the (max, sum) pairs of the G4 heads sit together.
   // Rows past G hold finite values that are never read into an output.
   constexpr int G4 = G > 4 ? G : 4;
+  if (j1 > sp.np_hi) {                           // remove the code offset of the LOW values
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {
+      const float off = kCodeOffset * head_sum(st.vw[i]);   // head n
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float o = __shfl(off, 4 * q + r);            // output row 4q + r
+        st.acc[2 * i][r] -= o;
+        st.acc[2 * i + 1][r] -= o;
+      }
+    }
+  }
   const float l_n = head_sum(st.l);              // head n, over all slots
   const int slot = (int)(w - seg0 / U);          // < a.splits by the choice of U
   const size_t blk = ((size_t)b * H + g) * a.splits + slot;
