@@ -16,7 +16,11 @@ What it computes, each piece following the passage named in its docstring:
     computed here in exact integer arithmetic on bf16 bit patterns;
   * decode attention over the persisted history, by the textbook definition
     softmax(q k^T * scale) v, in fp64;
-  * the normalised KV cost C_KV of Eq. 1.
+  * the normalised KV cost C_KV of Eq. 1;
+  * the online budget controller of Alg. 2 (Eq. 8-10): the remaining budget
+    R_t, B_t = max(0, R_t - Gamma(s_t)), demotions above the floors in
+    ascending upgrade score, promotions in critical states in descending
+    score, R_{t+1} = R_t - sum_c m(a_c, c), all in integer bytes.
 
 Everything is plain numpy.  The attention is the definition written out
 (exact, up to fp64 rounding order); the decisions, compaction and codes are
@@ -271,6 +275,7 @@ class _SeqLayer:
     lo_vs: list = field(default_factory=list)
     n_forced: int = 0
     n_drop: int = 0
+    R: int = 0                                    # remaining budget (bytes) of the online controller
 
 
 class OracleCache:
@@ -287,13 +292,30 @@ class OracleCache:
         self.d = head_dim
         self.state: dict = {}
         self.bad_tag = False
+        self.bad_state = False
+        # online controller (Alg. 2), when the table carries it
+        self.rho_up = np.asarray(policy.get("rho_up", np.zeros(self.action.shape + (2,), np.float32)),
+                                 dtype=np.float32)
+        n_groups = self.action.shape[1]
+        self.m = group_costs(self.group_of_layer, n_groups, n_kv_heads, head_dim)
+        self.n_states = int(policy.get("n_states", 0))
+        self.beta_q = int(policy.get("beta_q", 0))
+        self.crit = np.asarray(policy.get("crit", np.zeros(0, np.uint8)))
+        self.gamma = reserve_bytes(policy.get("reserve_q", np.zeros(0, np.uint32)), self.m)
+
+    def budget_init(self, seq: int, layers, t_max: int):
+        """R_0 for one sequence in the given layers (each layer keeps its copy)."""
+        for layer in layers:
+            self.sl(seq, layer).R = initial_budget(self.beta_q, t_max, self.m)
 
     def sl(self, seq: int, layer: int) -> _SeqLayer:
         return self.state.setdefault((seq, layer), _SeqLayer())
 
-    def append(self, layer: int, seq: int, tags, k_bits, v_bits, keep_all: bool = False):
+    def append(self, layer: int, seq: int, tags, k_bits, v_bits, keep_all: bool = False, states=None):
         """Persist n new tokens of one sequence in one layer.
-        k_bits, v_bits: bf16 bit patterns [n, Hkv, D]."""
+        k_bits, v_bits: bf16 bit patterns [n, Hkv, D].  states: parser states
+        [n] (the online controller decides, token after token) or None (the
+        static lookup of Eq. 10).  Keep-all appends bypass the controller."""
         st = self.sl(seq, layer)
         tags = np.asarray(tags).reshape(-1)
         n = tags.size
@@ -302,6 +324,17 @@ class OracleCache:
         pos = st.n_pos + np.arange(n)
         c = int(self.group_of_layer[layer])
         acts, forced, bad = decide(tags, pos, c, self.action, self.floor, self.n_sink, keep_all)
+        if states is not None and not keep_all:
+            states = np.asarray(states).reshape(-1)
+            for i in range(n):
+                s = int(states[i])
+                known = s < self.n_states
+                self.bad_state |= not known
+                a, cost = online_actions(int(tags[i]), s, st.R, self.action, self.floor, self.rho_up, self.m,
+                                         self.gamma[s] if known else 0, bool(self.crit[s]) if known else False,
+                                         bool(forced[i]))
+                acts[i] = a[c]
+                st.R -= cost
         self.bad_tag |= bool(bad.any())
         st.n_forced += int(forced.sum())
         hi = acts == HIGH
@@ -362,7 +395,7 @@ class OracleCache:
     def counts(self, seq: int, layer: int):
         st = self.sl(seq, layer)
         return dict(hi=len(st.hi_pos), lo=len(st.lo_pos), pos=st.n_pos, drop=st.n_drop,
-                    forced=st.n_forced)
+                    forced=st.n_forced, R=st.R)
 
 
 # --------------------------------------------------------------------------
@@ -375,6 +408,84 @@ def entry_bytes(n_kv_heads: int, head_dim: int):
     hi = 2 * n_kv_heads * head_dim * 2
     lo = 2 * n_kv_heads * (head_dim // 2 + 2 * (head_dim // QGROUP))
     return {DROP: 0, LOW: lo, HIGH: hi}
+
+
+# --------------------------------------------------------------------------
+# Online budget controller (Eq. 8-10; Alg. 2)
+# --------------------------------------------------------------------------
+
+def group_costs(group_of_layer, n_groups: int, n_kv_heads: int, head_dim: int) -> np.ndarray:
+    """m(a, c): bytes one token persists in layer group c under action a, the
+    stored bytes of one (token, layer) entry times the layers of the group
+    (the cost accounting of Eq. 1).  int64 [n_groups][3]."""
+    layers = np.bincount(np.asarray(group_of_layer, dtype=np.int64), minlength=n_groups)
+    e = entry_bytes(n_kv_heads, head_dim)
+    return np.array([[layers[c] * e[a] for a in (DROP, LOW, HIGH)] for c in range(n_groups)], dtype=np.int64)
+
+
+def initial_budget(beta_q: int, t_max: int, m) -> int:
+    """R_0 = beta * T_max * sum_c m(H, c) bytes, beta = beta_q / 65536, rounded
+    down (the paper gives no R_0; this build's reading)."""
+    full = int(np.asarray(m)[:, HIGH].sum())
+    return (int(beta_q) * int(t_max) * full) // 65536
+
+
+def reserve_bytes(reserve_q, m) -> np.ndarray:
+    """Gamma(s) (Eq. 8) in bytes: reserve_q[s] sixteenths of sum_c m(H, c),
+    rounded down."""
+    full = int(np.asarray(m)[:, HIGH].sum())
+    return np.array([(int(r) * full) // 16 for r in np.asarray(reserve_q)], dtype=np.int64)
+
+
+def online_actions(z: int, s: int, R: int, action, floor, rho_up, m, gamma, crit, forced: bool):
+    """The actions of one accepted token in every layer group, and their bytes.
+
+    Follows Alg. 2 after the lookup: a_c = max(a0_c, a-_c) (Eq. 10); the budget
+    available now is B = max(0, R - Gamma(s)) (Eq. 10); while the actions cost
+    more than B, the group whose current action sits above its floor and whose
+    last upgrade has the smallest score rho_D (Eq. 7, distortion loss per saved
+    byte) is demoted one step, lower group first on ties, until the cost fits
+    or only floors remain (the floors take priority); then, in a critical or
+    lookahead-critical state, the eligible promotion (action below HIGH,
+    positive score, fits in B) with the largest score is applied, lower group
+    first on ties, until none fits.  A forced token (a sink, a tag outside the
+    table) is HIGH in every group and is neither demoted nor promoted.
+    Returns (actions uint8 [C], bytes)."""
+    C = len(m)
+    if forced:
+        a = [HIGH] * C
+    else:
+        a = [max(int(action[z][c]), int(floor[z][c])) for c in range(C)]
+    cost = sum(int(m[c][a[c]]) for c in range(C))
+    if forced:
+        return np.asarray(a, dtype=np.uint8), cost
+    B = max(0, int(R) - int(gamma))
+    while cost > B:                                                     # Demote
+        best = None
+        for c in range(C):
+            if a[c] > int(floor[z][c]):
+                loss = float(rho_up[z][c][a[c] - 1])
+                if best is None or loss < best[0]:
+                    best = (loss, c)
+        if best is None:
+            break
+        c = best[1]
+        cost -= int(m[c][a[c]]) - int(m[c][a[c] - 1])
+        a[c] -= 1
+    if crit:                                                            # Promote
+        while True:
+            best = None
+            for c in range(C):
+                if a[c] < HIGH:
+                    gain = float(rho_up[z][c][a[c]])
+                    extra = int(m[c][a[c] + 1]) - int(m[c][a[c]])
+                    if gain > 0.0 and cost + extra <= B and (best is None or gain > best[0]):
+                        best = (gain, c, extra)
+            if best is None:
+                break
+            cost += best[2]
+            a[best[1]] += 1
+    return np.asarray(a, dtype=np.uint8), cost
 
 
 def c_kv(n_high: int, n_low: int, n_drop: int, n_kv_heads: int, head_dim: int) -> float:

@@ -48,3 +48,32 @@ def test_bf16_normal_seeded():
     a = bf16_normal((4, 8), 5)
     b = bf16_normal((4, 8), 5)
     assert (a == b).all() and a.shape == (4, 8)
+
+
+def test_walker_states_align_with_tags_and_reserve_follows_eq8():
+    """Parser states come with the same tag stream; keys are produced in key
+    states and enum values in enum states; Gamma(s) is the median future floor
+    cost, so it shrinks toward the end of a trace and a state that never
+    occurs reserves nothing."""
+    from workload.tags import (walk_function_calls_with_states, ST_KEY, ST_ENUM, ST_TEXT, CRITICAL_STATES,
+                               PARSER_STATES, REQUIRED_KEY, ENUM_VALUE, FREE_TEXT)
+    from workload.policy import with_budget_controller, pack_blob, floor_cost
+    tags, states = walk_function_calls_with_states(5000, 17)
+    assert (tags == walk_function_calls(5000, 17)).all()
+    assert states.max() < len(PARSER_STATES)
+    assert (states[tags == REQUIRED_KEY] == ST_KEY).all()
+    assert (states[tags == ENUM_VALUE] == ST_ENUM).all()
+    assert (states[tags == FREE_TEXT] == ST_TEXT).all()
+    pol = make_policy(6, 2, 4, 0.33, seed=3)
+    trace = (tags[:200], states[:200])
+    bp = with_budget_controller(pol, [trace], len(PARSER_STATES) + 1, CRITICAL_STATES)
+    f = floor_cost(pol, trace[0])
+    future = np.array([f[u + 1:].sum() for u in range(200)])
+    for s in range(len(PARSER_STATES)):
+        sel = trace[1] == s
+        if sel.any():
+            assert bp.reserve_q[s] == int(round(16 * np.quantile(future[sel], 0.5)))
+    assert bp.reserve_q[len(PARSER_STATES)] == 0
+    assert bp.crit.tolist()[:len(PARSER_STATES)] == [int(s in CRITICAL_STATES) for s in range(len(PARSER_STATES))]
+    blob = pack_blob(bp)
+    assert blob[4:6] == (2).to_bytes(2, "little") and len(blob) > len(pack_blob(pol))

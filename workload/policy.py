@@ -28,6 +28,14 @@ Blob layout (little-endian), version 1:
      u8       zero padding to a multiple of 4
      f32      rho_up[n_tags][n_groups][2]  (R->L, L->H)
   end u32     FNV-1a 32-bit hash of all preceding bytes
+Version 2 appends, after rho_up, the state of the online budget controller
+(Eq. 8-10, Alg. 2):
+     u32      n_states        (parser states s)
+     u32      beta_q          target budget beta in units of 1/65536
+     u32      reserve_q[n_states]  Gamma(s) in units of 1/16 of the bytes one token
+                                  persists at RETAIN-HIGH in every layer
+     u8       crit[n_states]  Crit(s): critical or lookahead-critical state
+     u8       zero padding to a multiple of 4
 Actions: 0 = DROP (release), 1 = RETAIN-LOW, 2 = RETAIN-HIGH.
 """
 
@@ -66,6 +74,11 @@ class PolicyTable:
     beta: float = float("nan")
     expected_cost: float = float("nan")
     tag_probs: np.ndarray = field(default=None)
+    # Online budget controller (blob version 2); n_states == 0: static lookup only.
+    n_states: int = 0
+    beta_q: int = 0
+    reserve_q: np.ndarray = field(default=None)   # uint32 [n_states]
+    crit: np.ndarray = field(default=None)        # uint8 [n_states]
 
 
 def contiguous_groups(n_layers: int, n_groups: int) -> np.ndarray:
@@ -137,6 +150,45 @@ def make_policy(n_tags: int, n_groups: int, n_layers: int, beta: float, seed: in
     return pol
 
 
+def floor_cost(pol: PolicyTable, tags) -> np.ndarray:
+    """Bytes the floors alone persist for each token, in units of one token at
+    RETAIN-HIGH in every layer: sum over groups of (layers of the group) x
+    m(floor) / m(HIGH), with m(LOW) / m(HIGH) = 0.28125."""
+    w = np.bincount(np.asarray(pol.group_of_layer), minlength=pol.n_groups).astype(np.float64)
+    m = np.array([0.0, LOW_COST_RATIO, 1.0])
+    per_tag = (m[np.asarray(pol.floor)] * w[None, :]).sum(axis=1) / w.sum()
+    return per_tag[np.asarray(tags, dtype=np.int64)]
+
+
+def with_budget_controller(pol: PolicyTable, traces, n_states: int, critical, beta: float | None = None,
+                           quantile: float = 0.5) -> PolicyTable:
+    """Adds the online controller's state to a table.
+
+    traces: calibration (tags, states) pairs.  Gamma(s) follows Eq. 8: the
+    empirical quantile, over every position u of every trace whose state is s,
+    of the floor cost of the positions after u (the protected history still to
+    come); it is stored in sixteenths of a full-precision token.  A state that
+    never occurs reserves nothing."""
+    samples = [[] for _ in range(n_states)]
+    for tags, states in traces:
+        f = floor_cost(pol, tags)
+        future = np.concatenate([np.cumsum(f[::-1])[::-1][1:], [0.0]])   # floor cost after u
+        for st in range(n_states):
+            sel = np.asarray(states) == st
+            if sel.any():
+                samples[st].append(future[sel])
+    reserve = np.zeros(n_states, dtype=np.uint32)
+    for st in range(n_states):
+        if samples[st]:
+            reserve[st] = int(round(16.0 * float(np.quantile(np.concatenate(samples[st]), quantile))))
+    crit = np.zeros(n_states, dtype=np.uint8)
+    crit[list(critical)] = 1
+    b = pol.beta if beta is None else beta
+    out = PolicyTable(**{k: getattr(pol, k) for k in pol.__dataclass_fields__})
+    out.n_states, out.beta_q, out.reserve_q, out.crit = n_states, int(round(b * 65536)), reserve, crit
+    return out
+
+
 def uniform_policy(n_tags: int, n_groups: int, n_layers: int, a: int, n_sink: int = 0) -> PolicyTable:
     """Every bucket selects action a, with floor DROP (special-case tables for tests)."""
     return PolicyTable(
@@ -155,13 +207,21 @@ def fnv1a32(data: bytes) -> int:
     return h
 
 
-def pack_blob(pol: PolicyTable, version: int = 1) -> bytes:
+def pack_blob(pol: PolicyTable, version: int | None = None) -> bytes:
+    """Version 1 for a static table, 2 when the table carries the controller."""
+    if version is None:
+        version = 2 if pol.n_states else 1
     gol = np.asarray(pol.group_of_layer, dtype=np.uint8).tobytes()
     act = np.asarray(pol.action, dtype=np.uint8).tobytes()
     flo = np.asarray(pol.floor, dtype=np.uint8).tobytes()
     body = gol + act + flo
     body += b"\0" * ((-len(body)) % 4)
     body += np.asarray(pol.rho_up, dtype="<f4").tobytes()
+    if version == 2:
+        body += struct.pack("<II", pol.n_states, pol.beta_q)
+        body += np.asarray(pol.reserve_q, dtype="<u4").tobytes()
+        body += np.asarray(pol.crit, dtype=np.uint8).tobytes()
+        body += b"\0" * ((-len(body)) % 4)
     head = struct.pack("<4sHHIIIIII", b"PASK", version, 32, pol.n_tags, pol.n_groups,
                        pol.n_layers, pol.n_sink, pol.recent_window, len(body))
     data = head + body

@@ -21,6 +21,15 @@ REQUIRED_KEY, ENUM_VALUE, ARG_VALUE, BOUNDARY, SCAFFOLD, FREE_TEXT = range(6)
 PROTECTED, FUNC_NAME, PARAM_KEY, CONSTRAINT, SCHEMA_SCAFFOLD, INSTRUCTION = range(6, 12)
 
 
+# Parser states of the synthetic function-call grammar (the s_t of the online
+# lookup, Section 3.4): where the parser frontier is when a token is accepted.
+PARSER_STATES = ("text", "expect_key", "key", "expect_value", "enum", "argument", "close")
+ST_TEXT, ST_EXPECT_KEY, ST_KEY, ST_EXPECT_VALUE, ST_ENUM, ST_ARG, ST_CLOSE = range(7)
+# Critical or lookahead-critical states: a key or an enumerated value is being
+# produced, or the next token must be one.
+CRITICAL_STATES = (ST_EXPECT_KEY, ST_KEY, ST_EXPECT_VALUE, ST_ENUM)
+
+
 def iid_tags(n: int, seed: int, n_tags: int = 6) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return rng.integers(0, n_tags, size=n).astype(np.uint8)
@@ -37,53 +46,61 @@ class _Walker:
     def __init__(self, rng: np.random.Generator):
         self.rng = rng
         self.out: list[int] = []
+        self.states: list[int] = []
 
-    def emit(self, tag: int, n: int = 1):
+    def emit(self, tag: int, state: int, n: int = 1):
         self.out.extend([tag] * n)
+        self.states.extend([state] * n)
 
     def value(self, depth: int):
         r = self.rng.random()
         if depth < 3 and r < 0.10:
             self.obj(depth + 1, int(self.rng.integers(1, 4)))
         elif r < 0.40:                       # enum value, quoted
-            self.emit(SCAFFOLD)
-            self.emit(ENUM_VALUE, int(self.rng.integers(1, 3)))
+            self.emit(SCAFFOLD, ST_ENUM)
+            self.emit(ENUM_VALUE, ST_ENUM, int(self.rng.integers(1, 3)))
         elif r < 0.80:                       # string argument, quoted
-            self.emit(SCAFFOLD)
-            self.emit(ARG_VALUE, int(self.rng.integers(1, 11)))
+            self.emit(SCAFFOLD, ST_ARG)
+            self.emit(ARG_VALUE, ST_ARG, int(self.rng.integers(1, 11)))
         else:                                # number argument
-            self.emit(ARG_VALUE, int(self.rng.integers(1, 4)))
+            self.emit(ARG_VALUE, ST_ARG, int(self.rng.integers(1, 4)))
 
     def obj(self, depth: int, n_keys: int):
-        self.emit(BOUNDARY)                  # {
+        self.emit(BOUNDARY, ST_EXPECT_KEY)   # {
         for i in range(n_keys):
             if i:
-                self.emit(BOUNDARY)          # ,
+                self.emit(BOUNDARY, ST_EXPECT_KEY)   # ,
             if self.rng.random() < 0.5:
-                self.emit(SCAFFOLD)          # opening quote as its own token
-            self.emit(REQUIRED_KEY, int(self.rng.integers(1, 6)))
-            self.emit(BOUNDARY)              # ":
+                self.emit(SCAFFOLD, ST_KEY)  # opening quote as its own token
+            self.emit(REQUIRED_KEY, ST_KEY, int(self.rng.integers(1, 6)))
+            self.emit(BOUNDARY, ST_EXPECT_VALUE)     # ":
             self.value(depth)
-        self.emit(BOUNDARY)                  # }
+        self.emit(BOUNDARY, ST_CLOSE)        # }
 
     def call(self):
         if self.rng.random() < 0.7:
-            self.emit(FREE_TEXT, int(self.rng.integers(3, 16)))
-        self.emit(BOUNDARY)                  # {
-        self.emit(SCAFFOLD, 2)               # "name":
-        self.emit(ENUM_VALUE, int(self.rng.integers(1, 4)))
-        self.emit(BOUNDARY)                  # ,
-        self.emit(SCAFFOLD, 2)               # "arguments":
+            self.emit(FREE_TEXT, ST_TEXT, int(self.rng.integers(3, 16)))
+        self.emit(BOUNDARY, ST_EXPECT_KEY)   # {
+        self.emit(SCAFFOLD, ST_KEY, 2)       # "name":
+        self.emit(ENUM_VALUE, ST_ENUM, int(self.rng.integers(1, 4)))
+        self.emit(BOUNDARY, ST_EXPECT_KEY)   # ,
+        self.emit(SCAFFOLD, ST_KEY, 2)       # "arguments":
         self.obj(1, int(self.rng.integers(1, 7)))
-        self.emit(BOUNDARY)                  # }
+        self.emit(BOUNDARY, ST_CLOSE)        # }
 
 
 def walk_function_calls(n: int, seed: int) -> np.ndarray:
     """Tags of n generated tokens from back-to-back synthetic function calls."""
+    return walk_function_calls_with_states(n, seed)[0]
+
+
+def walk_function_calls_with_states(n: int, seed: int):
+    """(tags, parser states) of n generated tokens; the tags are those of
+    walk_function_calls with the same seed."""
     w = _Walker(np.random.default_rng(seed))
     while len(w.out) < n:
         w.call()
-    return np.asarray(w.out[:n], dtype=np.uint8)
+    return np.asarray(w.out[:n], dtype=np.uint8), np.asarray(w.states[:n], dtype=np.uint8)
 
 
 def schema_prompt_tags(n: int, seed: int) -> np.ndarray:
