@@ -114,13 +114,14 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
         # kernel), then the attention kernel over the layer's persisted history.
         tp = tags_t[t].data_ptr()
         for layer in range(L):
-            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, kp[layer], vp[layer], 0, sptr)
+            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, None, kp[layer], vp[layer], 0,
+                                    sptr)
             if st != 0:
                 raise pask.PaskError(st, "pask_kv_append")
             if events is not None:
                 events[layer][0].record(stream)
             st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, None, None, None,
-                                      C.c_float(scale), hint, ws, ws_bytes, sptr)
+                                      None, C.c_float(scale), hint, ws, ws_bytes, sptr)
             if st != 0:
                 raise pask.PaskError(st, "pask_decode_attn")
             if events is not None:

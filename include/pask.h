@@ -11,7 +11,9 @@
  * is persisted accordingly (the Persist step of Alg. 2): DROP releases it from
  * future attention, RETAIN-LOW keeps it at low precision, RETAIN-HIGH keeps it
  * at full precision (Section 3.1).  Decode attention then reads only the
- * persisted history.  The normalised KV cost C_KV is that of Eq. 1.
+ * persisted history.  The normalised KV cost C_KV is that of Eq. 1.  Given
+ * the parser state of each token, the online controller of Alg. 2 adjusts
+ * those actions to a running byte budget with a per-state reserve (Eq. 9-10).
  *
  * Formats chosen here where the paper is silent:
  *   RETAIN-HIGH  bf16 K and V.
@@ -69,7 +71,12 @@ enum {
   PASK_FLAG_HI_POOL_EXHAUSTED = 1u << 1,/* no HIGH page: token not stored      */
   PASK_FLAG_LO_POOL_EXHAUSTED = 1u << 2,/* no LOW page: token not stored       */
   PASK_FLAG_SEQ_CAPACITY = 1u << 3,     /* position >= max_tokens_per_seq      */
-  PASK_FLAG_BAD_COUNT = 1u << 4         /* n_new[b] outside [0, max_new]       */
+  PASK_FLAG_BAD_COUNT = 1u << 4,        /* n_new[b] outside [0, max_new]       */
+  PASK_FLAG_BAD_STATE = 1u << 5,        /* parser state >= n_states: decided
+                                           with Gamma = 0, not critical        */
+  PASK_FLAG_NO_BUDGET = 1u << 6         /* states given but no pask_budget_init
+                                           since the last init / reset: token
+                                           decided by Eq. 10 alone             */
 };
 
 /* ---- append flags -------------------------------------------------------- */
@@ -84,6 +91,7 @@ enum {
 #define PASK_MAX_LAYERS 128
 #define PASK_PAGE_TOKENS 16
 #define PASK_QGROUP 32
+#define PASK_MAX_STATES 64
 
 /* Cache geometry.  Supported: head_dim 64 or 128; n_kv_heads 1..8;
  * n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_tokens 16. */
@@ -107,6 +115,12 @@ typedef struct pask_policy {
   uint8_t floor_[PASK_MAX_TAGS][PASK_MAX_GROUPS];   /* protection floor a-    */
   float rho_up[PASK_MAX_TAGS][PASK_MAX_GROUPS][2];  /* Eq. 7: R->L, L->H      */
   uint64_t entry_bytes[3];  /* m(a) per (token, layer): DROP, LOW, HIGH       */
+  /* Online budget controller (Alg. 2; Eq. 9-10); absent when n_states == 0. */
+  uint32_t n_states;                    /* parser states the table knows         */
+  uint32_t beta_q;                      /* budget fraction beta, in 1/65536      */
+  uint32_t reserve_q[PASK_MAX_STATES];  /* Gamma(s), in 1/16 of the bytes of one
+                                           token kept HIGH in every layer        */
+  uint8_t crit[PASK_MAX_STATES];        /* 1: critical or lookahead-critical     */
 } pask_policy;
 
 /* A cache: geometry plus one caller-owned device buffer of
@@ -121,12 +135,14 @@ typedef struct pask_cache {
 typedef struct pask_cache_layout {
   uint64_t status_off;       /* u32 status word; u32 HI and LO page cursors at +8, +12 */
   uint64_t counters_off;     /* i32 [max_batch][n_layers][8]: n_hi, n_lo, n_pos,
-                                n_drop, n_forced, n_lost, 0, 0                      */
+                                n_drop, n_forced, n_lost, then the remaining
+                                budget R (int64, bytes; online controller)       */
   uint64_t block_table_off;  /* i32 [max_batch][n_layers][2][max_pages]: page ids,
                                 store 0 = HIGH, 1 = LOW                            */
   uint64_t index_list_off;   /* i32 [max_batch][n_layers][2][max_tokens_per_seq]:
                                 position of each slot of each store               */
   uint64_t staging_off;      /* i32 [max_batch][max_tokens_per_seq]: append plan   */
+  uint64_t budget_off;       /* the online controller's tables (pask_budget_init)  */
   uint64_t hi_pool_off;      /* hi_pages pages of hi_page_bytes                    */
   uint64_t lo_pool_off;      /* lo_pages pages of lo_page_bytes                    */
   uint64_t total_bytes;
@@ -162,19 +178,23 @@ typedef struct pask_stats {
 } pask_stats;
 
 /* Parse and validate a policy blob (the frozen table of the offline
- * calibration, Section 3.3; format version 1, see below) against a geometry.
+ * calibration, Section 3.3) against a geometry.
  *
- * Blob, little-endian: "PASK", u16 version = 1, u16 header bytes = 32,
+ * Blob, little-endian: "PASK", u16 version (1 or 2), u16 header bytes = 32,
  * u32 n_tags, n_groups, n_layers, n_sink, recent_window, payload bytes;
  * payload: u8 group_of_layer[n_layers], u8 action[n_tags][n_groups],
  * u8 floor[n_tags][n_groups], zero pad to 4, f32 rho_up[n_tags][n_groups][2];
- * then u32 FNV-1a hash of all preceding bytes.
+ * version 2 appends the online controller (Alg. 2): u32 n_states (1..64),
+ * u32 beta_q, u32 reserve_q[n_states] (the reserve Gamma(s) of Eq. 9, in
+ * sixteenths of one token's bytes at HIGH in every layer), u8
+ * crit[n_states] (0 or 1), zero pad to 4; then u32 FNV-1a hash of all
+ * preceding bytes.  A version-1 table loads with n_states = 0.
  *
  * Errors: PASK_E_ARG (null pointers), PASK_E_POLICY (bad magic, version,
  * sizes, hash, action or floor > 2, group id >= n_groups, rho not finite or
- * negative, n_tags/n_groups/n_layers out of range), PASK_E_SHAPE (n_layers !=
- * geometry's, or the geometry itself invalid), PASK_E_UNSUPPORTED
- * (recent_window != 0).  Host only: no HIP call. */
+ * negative, n_tags/n_groups/n_layers/n_states out of range, crit > 1),
+ * PASK_E_SHAPE (n_layers != geometry's, or the geometry itself invalid),
+ * PASK_E_UNSUPPORTED (recent_window != 0).  Host only: no HIP call. */
 int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pask_policy* out);
 
 /* Region offsets of a cache of this geometry.  PASK_E_SHAPE if unsupported. */
@@ -189,7 +209,8 @@ size_t pask_cache_bytes(const pask_geom* geom);
 int pask_cache_init(pask_cache* cache, const pask_geom* geom, void* base, size_t bytes,
                     hipStream_t stream);
 
-/* Empty every sequence: zero counters, page cursors and the status word (page
+/* Empty every sequence: zero counters (the remaining budgets included), page
+ * cursors and the status word, and forget the controller tables (page
  * contents are left as they are). */
 int pask_cache_reset(pask_cache* cache, hipStream_t stream);
 
@@ -203,12 +224,43 @@ int pask_cache_reset(pask_cache* cache, hipStream_t stream);
  * tags >= n_tags get RETAIN-HIGH.  Surviving tokens receive the next slots of
  * their store in position order; DROP tokens get none (release, Section 3.1).
  *
+ * states_dev (nullable; ignored by a KEEP_ALL call): parser states
+ * [batch][max_new] of the tokens.  Given, the online controller of Alg. 2
+ * decides instead, token after token in position order, from the sequence's
+ * remaining budget R in this layer (pask_budget_init): start from the Eq. 10
+ * actions of every group; while their bytes exceed B = max(0, R - Gamma(s))
+ * (Eq. 10), demote one step the group above its floor whose last upgrade
+ * scores lowest (rho, Eq. 7; lower group on ties); in a critical state, then
+ * promote one step the group whose next upgrade scores highest (positive
+ * score, fits in B; lower group on ties), repeatedly; R drops by the token's
+ * bytes over all groups.  Sinks and tags >= n_tags are RETAIN-HIGH in every
+ * group and charged.  This layer keeps its group's action; every layer holds
+ * its own copy of R.  Tokens past max_tokens_per_seq are neither persisted
+ * nor charged.
+ *
  * Errors: PASK_E_ARG (null or misaligned pointers, flags), PASK_E_SHAPE
  * (layer, batch or max_new out of range, policy / geometry mismatch),
+ * PASK_E_POLICY (states given to a policy without the controller),
  * PASK_E_HIP. */
 int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
                    const int32_t* n_new_dev, int32_t max_new, const uint8_t* tags_dev,
-                   const void* k_dev, const void* v_dev, uint32_t flags, hipStream_t stream);
+                   const uint8_t* states_dev, const void* k_dev, const void* v_dev, uint32_t flags,
+                   hipStream_t stream);
+
+/* Set up the online controller (Alg. 2) of sequences b < batch: copy the
+ * policy's controller tables into the cache, and set the remaining budget of
+ * every layer of those sequences to
+ *   R_0 = floor(beta_q * t_max * sum_c m(H, c) / 65536) bytes,
+ * m(a, c) being the bytes one token persists in the layers of group c under
+ * action a (Eq. 1's accounting); Gamma(s) = floor(reserve_q[s] *
+ * sum_c m(H, c) / 16).  Call after pask_cache_init / pask_cache_reset (both
+ * forget the tables) and before appends that pass parser states; the
+ * sequences' counters should be empty.  Synchronises `stream`.
+ *
+ * Errors: PASK_E_ARG (t_max < 0, R_0 >= 2^62), PASK_E_SHAPE, PASK_E_POLICY
+ * (policy without the controller), PASK_E_HIP. */
+int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch, int32_t t_max,
+                     hipStream_t stream);
 
 /* Workspace bytes pask_decode_attn needs for `batch` sequences when no
  * sequence holds more than max_ctx_hint persisted entries (a larger count is
@@ -216,8 +268,9 @@ int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, 
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint);
 
 /* One decode step of one layer: optionally persist one new token per sequence
- * (when tags_new_dev != NULL: tags [batch], k_new / v_new bf16
- * [batch][n_kv_heads][head_dim]; the same rules as pask_kv_append), then
+ * (when tags_new_dev != NULL: tags [batch], parser states [batch] (nullable),
+ * k_new / v_new bf16 [batch][n_kv_heads][head_dim]; the same rules as
+ * pask_kv_append), then
  * grouped-query attention of q_dev bf16 [batch][n_q_heads][head_dim] over the
  * persisted history of the layer (HIGH entries as stored, LOW entries
  * dequantised), query head h reading KV head h / (n_q_heads / n_kv_heads):
@@ -228,11 +281,11 @@ size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ct
  * max_ctx_hint) bytes, 256-byte aligned.
  *
  * Errors: PASK_E_ARG, PASK_E_SHAPE, PASK_E_CAPACITY (workspace too small),
- * PASK_E_HIP. */
+ * PASK_E_POLICY (states given to a policy without the controller), PASK_E_HIP. */
 int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
                      const void* q_dev, void* out_dev, float* lse_dev,
-                     const uint8_t* tags_new_dev, const void* k_new_dev, const void* v_new_dev,
-                     float softmax_scale, int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes,
+                     const uint8_t* tags_new_dev, const uint8_t* states_new_dev, const void* k_new_dev,
+                     const void* v_new_dev, float softmax_scale, int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes,
                      hipStream_t stream);
 
 /* Read the cache's counters (synchronises `stream`) and fill `out`: entry

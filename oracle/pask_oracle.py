@@ -17,7 +17,7 @@ What it computes, each piece following the passage named in its docstring:
   * decode attention over the persisted history, by the textbook definition
     softmax(q k^T * scale) v, in fp64;
   * the normalised KV cost C_KV of Eq. 1;
-  * the online budget controller of Alg. 2 (Eq. 8-10): the remaining budget
+  * the online budget controller of Alg. 2 (Eq. 9-10): the remaining budget
     R_t, B_t = max(0, R_t - Gamma(s_t)), demotions above the floors in
     ascending upgrade score, promotions in critical states in descending
     score, R_{t+1} = R_t - sum_c m(a_c, c), all in integer bytes.
@@ -411,7 +411,7 @@ def entry_bytes(n_kv_heads: int, head_dim: int):
 
 
 # --------------------------------------------------------------------------
-# Online budget controller (Eq. 8-10; Alg. 2)
+# Online budget controller (Eq. 9-10; Alg. 2)
 # --------------------------------------------------------------------------
 
 def group_costs(group_of_layer, n_groups: int, n_kv_heads: int, head_dim: int) -> np.ndarray:
@@ -431,7 +431,7 @@ def initial_budget(beta_q: int, t_max: int, m) -> int:
 
 
 def reserve_bytes(reserve_q, m) -> np.ndarray:
-    """Gamma(s) (Eq. 8) in bytes: reserve_q[s] sixteenths of sum_c m(H, c),
+    """Gamma(s) (Eq. 9) in bytes: reserve_q[s] sixteenths of sum_c m(H, c),
     rounded down."""
     full = int(np.asarray(m)[:, HIGH].sum())
     return np.array([(int(r) * full) // 16 for r in np.asarray(reserve_q)], dtype=np.int64)

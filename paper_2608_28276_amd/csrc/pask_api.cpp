@@ -57,7 +57,9 @@ bool layout_of(const pask_geom* g, pask_cache_layout* L) {
   L->index_list_off = off;
   off = align_up(off + B * NL * 2 * T * 4, kAlignSmall);
   L->staging_off = off;
-  off = align_up(off + B * T * 4, kAlignPool);
+  off = align_up(off + B * T * 4, kAlignSmall);
+  L->budget_off = off;
+  off = align_up(off + sizeof(pask::BudgetTable), kAlignPool);
   L->hi_pool_off = off;
   off = align_up(off + (uint64_t)g->hi_pages * L->hi_page_bytes, kAlignPool);
   L->lo_pool_off = off;
@@ -76,6 +78,7 @@ CacheView view_of(const pask_cache* c) {
   v.block_table = reinterpret_cast<int32_t*>(base + L.block_table_off);
   v.index_list = reinterpret_cast<int32_t*>(base + L.index_list_off);
   v.staging = reinterpret_cast<int32_t*>(base + L.staging_off);
+  v.budget = reinterpret_cast<pask::BudgetTable*>(base + L.budget_off);
   v.hi_pool = base + L.hi_pool_off;
   v.lo_pool = base + L.lo_pool_off;
   v.n_layers = c->geom.n_layers;
@@ -109,7 +112,19 @@ int check_policy(const pask_policy* p, const pask_cache* c) {
   if ((int32_t)p->n_layers != c->geom.n_layers) return PASK_E_SHAPE;
   for (uint32_t l = 0; l < p->n_layers; ++l)
     if (p->group_of_layer[l] >= p->n_groups) return PASK_E_POLICY;
+  if (p->n_states > PASK_MAX_STATES) return PASK_E_POLICY;
   return PASK_OK;
+}
+
+// Bytes one token persists in the layers of group c under action a (the
+// accounting of Eq. 1): the group's layer count times one entry's bytes.
+void group_costs(const pask_policy* p, const pask_geom& g, int64_t m[PASK_MAX_GROUPS][3]) {
+  const int64_t H = g.n_kv_heads, D = g.head_dim;
+  const int64_t entry[3] = {0, 2 * H * (D / 2 + 2 * (D / PASK_QGROUP)), 2 * H * D * 2};
+  int64_t layers[PASK_MAX_GROUPS] = {};
+  for (uint32_t l = 0; l < p->n_layers; ++l) ++layers[p->group_of_layer[l]];
+  for (int c = 0; c < PASK_MAX_GROUPS; ++c)
+    for (int a = 0; a < 3; ++a) m[c][a] = layers[c] * entry[a];
 }
 
 pask::TableColumn column_of(const pask_policy* p, int layer) {
@@ -122,6 +137,7 @@ pask::TableColumn column_of(const pask_policy* p, int layer) {
   }
   t.n_tags = p->n_tags;
   t.n_sink = p->n_sink;
+  t.group = (uint32_t)c;
   return t;
 }
 
@@ -191,14 +207,23 @@ int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pas
   const uint8_t* b = static_cast<const uint8_t*>(blob);
   if (nbytes < 36) return PASK_E_POLICY;
   if (memcmp(b, "PASK", 4) != 0) return PASK_E_POLICY;
-  if (rd<uint16_t>(b + 4) != 1 || rd<uint16_t>(b + 6) != 32) return PASK_E_POLICY;
+  const uint16_t version = rd<uint16_t>(b + 4);
+  if ((version != 1 && version != 2) || rd<uint16_t>(b + 6) != 32) return PASK_E_POLICY;
   const uint32_t T = rd<uint32_t>(b + 8), C = rd<uint32_t>(b + 12), NL = rd<uint32_t>(b + 16);
   const uint32_t n_sink = rd<uint32_t>(b + 20), window = rd<uint32_t>(b + 24);
   const uint32_t body = rd<uint32_t>(b + 28);
   if (T < 1 || T > PASK_MAX_TAGS || C < 1 || C > PASK_MAX_GROUPS || NL < 1 || NL > PASK_MAX_LAYERS)
     return PASK_E_POLICY;
   const uint64_t bytes_u8 = (uint64_t)NL + 2ull * T * C;
-  const uint64_t want_body = align_up(bytes_u8, 4) + 8ull * T * C;
+  const uint64_t table_body = align_up(bytes_u8, 4) + 8ull * T * C;
+  // Version 2: the controller section follows the table.
+  uint32_t S = 0;
+  if (version == 2) {
+    if (body < table_body + 8 || nbytes < 32 + table_body + 8) return PASK_E_POLICY;
+    S = rd<uint32_t>(b + 32 + table_body);
+    if (S < 1 || S > PASK_MAX_STATES) return PASK_E_POLICY;
+  }
+  const uint64_t want_body = version == 2 ? table_body + 8 + 4ull * S + align_up(S, 4) : table_body;
   if (body != want_body || nbytes != 32 + (uint64_t)body + 4) return PASK_E_POLICY;
   if (rd<uint32_t>(b + 32 + body) != fnv1a32(b, 32 + body)) return PASK_E_POLICY;
   const uint8_t* gol = b + 32;
@@ -207,6 +232,13 @@ int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pas
   const uint8_t* rho = b + 32 + align_up(bytes_u8, 4);
   for (uint64_t i = bytes_u8; i < align_up(bytes_u8, 4); ++i)
     if (b[32 + i] != 0) return PASK_E_POLICY;
+  const uint8_t* ctl = b + 32 + table_body;   // version 2: n_states, beta_q, reserve_q[S], crit[S]
+  if (version == 2) {
+    for (uint32_t i = 0; i < S; ++i)
+      if (ctl[8 + 4 * S + i] > 1) return PASK_E_POLICY;
+    for (uint64_t i = S; i < align_up(S, 4); ++i)
+      if (ctl[8 + 4 * S + i] != 0) return PASK_E_POLICY;
+  }
   for (uint32_t l = 0; l < NL; ++l)
     if (gol[l] >= C) return PASK_E_POLICY;
   for (uint32_t i = 0; i < T * C; ++i)
@@ -233,6 +265,14 @@ int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pas
       p.rho_up[z][c][0] = rd<float>(rho + 4 * (2 * (z * C + c)));
       p.rho_up[z][c][1] = rd<float>(rho + 4 * (2 * (z * C + c) + 1));
     }
+  if (version == 2) {
+    p.n_states = S;
+    p.beta_q = rd<uint32_t>(ctl + 4);
+    for (uint32_t i = 0; i < S; ++i) {
+      p.reserve_q[i] = rd<uint32_t>(ctl + 8 + 4 * i);
+      p.crit[i] = ctl[8 + 4 * S + i];
+    }
+  }
   if (geom) {
     const uint64_t H = (uint64_t)geom->n_kv_heads, D = (uint64_t)geom->head_dim;
     p.entry_bytes[PASK_DROP] = 0;
@@ -273,8 +313,9 @@ int pask_cache_init(pask_cache* cache, const pask_geom* geom, void* base, size_t
 }
 
 int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
-                   const int32_t* n_new_dev, int32_t max_new, const uint8_t* tags_dev, const void* k_dev,
-                   const void* v_dev, uint32_t flags, hipStream_t stream) {
+                   const int32_t* n_new_dev, int32_t max_new, const uint8_t* tags_dev,
+                   const uint8_t* states_dev, const void* k_dev, const void* v_dev, uint32_t flags,
+                   hipStream_t stream) {
   int st = check_cache(cache);
   if (st != PASK_OK) return st;
   st = check_policy(policy, cache);
@@ -287,12 +328,15 @@ int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, 
   if (!k_dev || !v_dev || !aligned(k_dev, 16) || !aligned(v_dev, 16)) return PASK_E_ARG;
   if (!tags_dev && !(flags & PASK_APPEND_KEEP_ALL)) return PASK_E_ARG;
   if (n_new_dev && !aligned(n_new_dev, 4)) return PASK_E_ARG;
+  const bool keep_all = (flags & PASK_APPEND_KEEP_ALL) != 0u;
+  if (states_dev && !keep_all && policy->n_states == 0) return PASK_E_POLICY;
   if (max_new == 0) return PASK_OK;
   pask::AppendArgs a;
   a.cv = view_of(cache);
   a.tab = column_of(policy, layer);
   a.n_new = n_new_dev;
   a.tags = tags_dev;
+  a.states = keep_all ? nullptr : states_dev;   // a keep-all append bypasses the controller
   a.k = static_cast<const uint16_t*>(k_dev);
   a.v = static_cast<const uint16_t*>(v_dev);
   a.layer = layer;
@@ -300,6 +344,46 @@ int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, 
   a.max_new = max_new;
   a.flags = flags;
   return pask::launch_append(a, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+}
+
+int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch, int32_t t_max,
+                     hipStream_t stream) {
+  int st = check_cache(cache);
+  if (st != PASK_OK) return st;
+  st = check_policy(policy, cache);
+  if (st != PASK_OK) return st;
+  const pask_geom& g = cache->geom;
+  if (batch < 1 || batch > g.max_batch) return PASK_E_SHAPE;
+  if (t_max < 0) return PASK_E_ARG;
+  if (policy->n_states == 0) return PASK_E_POLICY;
+  for (uint32_t z = 0; z < policy->n_tags; ++z)
+    for (uint32_t c = 0; c < policy->n_groups; ++c)
+      if (policy->action[z][c] > PASK_RETAIN_HIGH || policy->floor_[z][c] > PASK_RETAIN_HIGH) return PASK_E_POLICY;
+  pask::BudgetTable t;
+  memset(&t, 0, sizeof(t));
+  t.loaded = pask::kBudgetLoaded;
+  t.n_tags = policy->n_tags;
+  t.n_groups = policy->n_groups;
+  t.n_states = policy->n_states;
+  t.n_sink = policy->n_sink;
+  group_costs(policy, g, t.m);
+  int64_t full = 0;   // bytes of one token kept HIGH in every layer
+  for (uint32_t c = 0; c < policy->n_groups; ++c) full += t.m[c][PASK_RETAIN_HIGH];
+  const unsigned __int128 r0 = (unsigned __int128)policy->beta_q * (uint64_t)t_max * (uint64_t)full / 65536u;
+  if (r0 >= ((unsigned __int128)1 << 62)) return PASK_E_ARG;
+  for (uint32_t s = 0; s < policy->n_states; ++s) {
+    t.gamma[s] = (int64_t)(((unsigned __int128)policy->reserve_q[s] * (uint64_t)full) / 16u);
+    t.crit[s] = policy->crit[s] ? 1 : 0;
+  }
+  memcpy(t.action, policy->action, sizeof(t.action));
+  memcpy(t.floor_, policy->floor_, sizeof(t.floor_));
+  memcpy(t.rho_up, policy->rho_up, sizeof(t.rho_up));
+  const CacheView v = view_of(cache);
+  if (hipMemcpyAsync(v.budget, &t, sizeof(t), hipMemcpyHostToDevice, stream) != hipSuccess) return PASK_E_HIP;
+  const bool launched = pask::launch_budget_init(v, batch, (int64_t)r0, stream) == hipSuccess;
+  // `t` lives on this frame: the copy must be done before returning.
+  const bool synced = hipStreamSynchronize(stream) == hipSuccess;
+  return launched && synced ? PASK_OK : PASK_E_HIP;
 }
 
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint) {
@@ -310,7 +394,8 @@ size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ct
 
 int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
                      const void* q_dev, void* out_dev, float* lse_dev, const uint8_t* tags_new_dev,
-                     const void* k_new_dev, const void* v_new_dev, float softmax_scale,
+                     const uint8_t* states_new_dev, const void* k_new_dev, const void* v_new_dev,
+                     float softmax_scale,
                      int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes, hipStream_t stream) {
   int st = check_cache(cache);
   if (st != PASK_OK) return st;
@@ -323,6 +408,7 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
   if (lse_dev && !aligned(lse_dev, 4)) return PASK_E_ARG;
   if (tags_new_dev && (!k_new_dev || !v_new_dev || !aligned(k_new_dev, 16) || !aligned(v_new_dev, 16)))
     return PASK_E_ARG;
+  if (tags_new_dev && states_new_dev && policy->n_states == 0) return PASK_E_POLICY;
   if (!isfinite(softmax_scale)) return PASK_E_ARG;
   if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
   const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq));
@@ -336,6 +422,7 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
     a.tab = column_of(policy, layer);
     a.n_new = nullptr;
     a.tags = tags_new_dev;
+    a.states = states_new_dev;
     a.k = static_cast<const uint16_t*>(k_new_dev);
     a.v = static_cast<const uint16_t*>(v_new_dev);
     a.layer = layer;

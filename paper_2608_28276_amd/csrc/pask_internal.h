@@ -12,7 +12,8 @@
 namespace pask {
 
 enum Store { kHi = 0, kLo = 1 };
-enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4, kCntLost = 5 };
+enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4, kCntLost = 5,
+               kCntBudget = 6 };   // int64 remaining budget R in words 6, 7
 constexpr int kCounterStride = 8;
 constexpr int kPage = 16;          // tokens per page
 constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW vector
@@ -29,6 +30,22 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 constexpr int kUnitTokens = PASK_UNIT_TOKENS;   // slots per attention work unit (multiple of 16)
 constexpr uint32_t kKeepAll = 1u;
 
+// The online controller's inputs (Alg. 2; Eq. 9-10), one copy per cache.
+// `loaded` holds kBudgetLoaded once pask_budget_init has written the rest.
+constexpr uint32_t kBudgetLoaded = 0x42554447u;
+struct BudgetTable {
+  uint32_t loaded;
+  uint32_t n_tags, n_groups, n_states, n_sink;
+  uint32_t pad[3];
+  int64_t m[PASK_MAX_GROUPS][3];      // bytes a token persists in group c under action a
+  int64_t gamma[PASK_MAX_STATES];     // reserve Gamma(s), bytes (Eq. 9)
+  uint8_t crit[PASK_MAX_STATES];      // critical or lookahead-critical state
+  uint8_t action[PASK_MAX_TAGS][PASK_MAX_GROUPS];
+  uint8_t floor_[PASK_MAX_TAGS][PASK_MAX_GROUPS];
+  float rho_up[PASK_MAX_TAGS][PASK_MAX_GROUPS][2];   // Eq. 7: R->L, L->H
+};
+static_assert(sizeof(BudgetTable) % 16 == 0, "BudgetTable is copied in 16-byte words");
+
 // Device-side view of one cache buffer.
 struct CacheView {
   uint32_t* status;       // [0] status word, [2] HI cursor, [3] LO cursor
@@ -36,6 +53,7 @@ struct CacheView {
   int32_t* block_table;   // [max_batch][n_layers][2][max_pages]
   int32_t* index_list;    // [max_batch][n_layers][2][max_tokens]
   int32_t* staging;       // [max_batch][max_tokens]
+  BudgetTable* budget;
   uint8_t* hi_pool;
   uint8_t* lo_pool;
   int32_t n_layers, n_kv_heads, head_dim, max_tokens, max_pages, hi_pages, lo_pages;
@@ -48,6 +66,7 @@ struct TableColumn {
   uint8_t amin[64];
   uint32_t n_tags;
   uint32_t n_sink;
+  uint32_t group;           // the layer's group c
 };
 
 struct AppendArgs {
@@ -55,6 +74,7 @@ struct AppendArgs {
   TableColumn tab;
   const int32_t* n_new;     // [batch] or null (all max_new)
   const uint8_t* tags;      // [batch][max_new] or null (KEEP_ALL)
+  const uint8_t* states;    // [batch][max_new] parser states, or null (Eq. 10 alone)
   const uint16_t* k;        // bf16 bits [batch][max_new][Hkv][D]
   const uint16_t* v;
   int32_t layer, batch, max_new;
@@ -77,6 +97,7 @@ struct AttnArgs {
 hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, hipStream_t s);
 hipError_t launch_append_step(const AppendArgs& a, hipStream_t s);
+hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s);
 
 }  // namespace pask

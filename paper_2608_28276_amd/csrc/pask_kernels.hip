@@ -69,7 +69,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
 __global__ void reset_kernel(CacheView cv, size_t n_counters) {
   const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i0 < 4) cv.status[i0] = 0u;
+  if (i0 == 0) cv.budget->loaded = 0u;
   for (size_t i = i0; i < n_counters; i += (size_t)gridDim.x * blockDim.x) cv.counters[i] = 0;
+}
+
+// R_0 into every layer of sequences b < batch.
+__global__ void budget_init_kernel(CacheView cv, int32_t batch, int64_t r0) {
+  const size_t n = (size_t)batch * cv.n_layers;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    *reinterpret_cast<int64_t*>(cv.counters + i * kCounterStride + kCntBudget) = r0;
 }
 
 // ---------------------------------------------------------------------------
@@ -90,6 +98,89 @@ __device__ __forceinline__ int decide(const uint8_t* s_a0, const uint8_t* s_amin
   forced = false;
   const int a0 = s_a0[tag], am = s_amin[tag];
   return a0 > am ? a0 : am;
+}
+
+// The online controller for one token (Alg. 2 after the lookup; Eq. 9-10):
+// the token's actions in every group start at max(a0, a-) (Eq. 10); while
+// their bytes exceed B = max(0, R - Gamma(s)), the group above its floor whose
+// last upgrade scores lowest (rho, Eq. 7) steps down, lower group on ties; in
+// a critical state, the group whose next upgrade scores highest (positive,
+// fits in B) steps up, lower group on ties, until none fits.  A forced token
+// (sink, tag outside the table) is HIGH everywhere.  R drops by the token's
+// bytes over all groups; the action of group `group` is returned.  Actions
+// are kept two bits per group in one word.  `t` may point to LDS or global
+// memory.
+__device__ int budget_decide(const BudgetTable* t, int tag, int state, bool forced, int group, int64_t& R,
+                             uint32_t& flags) {
+  const int C = (int)t->n_groups;
+  int64_t cost = 0;
+  if (forced) {
+    for (int c = 0; c < C; ++c) cost += t->m[c][kHigh];
+    R -= cost;
+    return kHigh;
+  }
+  int64_t gamma = 0;
+  bool crit = false;
+  if ((uint32_t)state < t->n_states) {
+    gamma = t->gamma[state];
+    crit = t->crit[state] != 0;
+  } else {
+    flags |= PASK_FLAG_BAD_STATE;
+  }
+  const uint8_t* a0 = t->action[tag];
+  const uint8_t* fl = t->floor_[tag];
+  const float(*rho)[2] = t->rho_up[tag];
+  uint32_t A = 0u;
+  for (int c = 0; c < C; ++c) {
+    const int ac = a0[c] > fl[c] ? a0[c] : fl[c];
+    A |= (uint32_t)ac << (2 * c);
+    cost += t->m[c][ac];
+  }
+  const int64_t B = R - gamma > 0 ? R - gamma : 0;
+  while (cost > B) {                                   // demote
+    int best = -1;
+    float best_rho = 0.0f;
+    for (int c = 0; c < C; ++c) {
+      const int ac = (int)((A >> (2 * c)) & 3u);
+      if (ac > fl[c]) {
+        const float r = rho[c][ac - 1];
+        if (best < 0 || r < best_rho) {
+          best = c;
+          best_rho = r;
+        }
+      }
+    }
+    if (best < 0) break;
+    const int ac = (int)((A >> (2 * best)) & 3u);
+    cost -= t->m[best][ac] - t->m[best][ac - 1];
+    A -= 1u << (2 * best);
+  }
+  while (crit) {                                       // promote
+    int best = -1;
+    float best_rho = 0.0f;
+    int64_t best_extra = 0;
+    for (int c = 0; c < C; ++c) {
+      const int ac = (int)((A >> (2 * c)) & 3u);
+      if (ac < kHigh) {
+        const float r = rho[c][ac];
+        const int64_t extra = t->m[c][ac + 1] - t->m[c][ac];
+        if (r > 0.0f && cost + extra <= B && (best < 0 || r > best_rho)) {
+          best = c;
+          best_rho = r;
+          best_extra = extra;
+        }
+      }
+    }
+    if (best < 0) break;
+    cost += best_extra;
+    A += 1u << (2 * best);
+  }
+  R -= cost;
+  return (int)((A >> (2 * group)) & 3u);
+}
+
+__device__ __forceinline__ int64_t* budget_of(int32_t* cnt) {
+  return reinterpret_cast<int64_t*>(cnt + kCntBudget);
 }
 
 // Exclusive count of `pred` over a 256-thread block in thread order: wavefront
@@ -129,11 +220,17 @@ __device__ __forceinline__ int clamp_n_new(const AppendArgs& a, int b, uint32_t&
   return n;
 }
 
+// kBudget: the tokens carry parser states and the online controller decides
+// (one thread walks each chunk's tokens in position order, the table in LDS).
+template <bool kBudget>
 __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   __shared__ uint8_t s_a0[64], s_amin[64];
   __shared__ int s_wave[4];
   __shared__ unsigned s_page_base[2];
   __shared__ int s_granted[2];
+  struct Empty {};
+  __shared__ std::conditional_t<kBudget, BudgetTable, Empty> s_bud;
+  __shared__ uint8_t s_act[kBudget ? 256 : 1];
   const CacheView& cv = a.cv;
   const int b = blockIdx.x;
   load_table(a.tab, s_a0, s_amin);
@@ -141,6 +238,17 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   const int n = clamp_n_new(a, b, flags);
   int32_t* cnt = counters_of(cv, b, a.layer);
   const int pos0 = cnt[kCntPos];
+  bool budget = false;
+  int64_t R = 0;
+  if constexpr (kBudget) {
+    const uint4* src = reinterpret_cast<const uint4*>(cv.budget);
+    uint4* dst = reinterpret_cast<uint4*>(&s_bud);
+    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += 256) dst[i] = src[i];
+    __syncthreads();
+    budget = s_bud.loaded == kBudgetLoaded;
+    if (!budget && threadIdx.x == 0) flags |= PASK_FLAG_NO_BUDGET;
+    if (budget && threadIdx.x == 0) R = *budget_of(cnt);
+  }
   int nst[2] = {cnt[kCntHi], cnt[kCntLo]};
   int n_drop = 0, n_forced = 0, n_lost = 0, n_fit = 0;
   int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
@@ -155,11 +263,27 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
     const bool valid = j < n;
     const int pos = pos0 + j;
     const bool fits = valid && pos < cv.max_tokens;
+    if constexpr (kBudget) {
+      if (budget && threadIdx.x == 0) {
+        const int j1 = min(min(n, c0 + 256), cv.max_tokens - pos0);
+        const int group = (int)a.tab.group;
+        for (int jj = c0; jj < j1; ++jj) {
+          const size_t at = (size_t)b * a.max_new + jj;
+          const int tag = (int)a.tags[at];
+          const bool forced = (uint32_t)(pos0 + jj) < s_bud.n_sink || (uint32_t)tag >= s_bud.n_tags;
+          s_act[jj - c0] = (uint8_t)budget_decide(&s_bud, tag, (int)a.states[at], forced, group, R, flags);
+        }
+      }
+      __syncthreads();
+    }
     int act = kDrop;
     bool forced = false, bad = false;
     if (fits) {
       const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new + j] : 0;
       act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, keep_all, tag, pos, forced, bad);
+      if constexpr (kBudget) {
+        if (budget) act = s_act[threadIdx.x];
+      }
     }
     if (bad) flags |= PASK_FLAG_BAD_TAG;
     if (valid && !fits) flags |= PASK_FLAG_SEQ_CAPACITY;
@@ -223,6 +347,7 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
     cnt[kCntDrop] += n_drop;
     cnt[kCntForced] += n_forced;
     cnt[kCntLost] += n_lost;
+    if (budget) *budget_of(cnt) = R;
   }
   if (flags) atomicOr(cv.status, flags);
 }
@@ -380,9 +505,20 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
       } else {
         const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new] : 0;
         bool forced, bad;
-        const int act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, (a.flags & kKeepAll) != 0u,
-                               tag, pos, forced, bad);
+        int act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, (a.flags & kKeepAll) != 0u,
+                         tag, pos, forced, bad);
         if (bad) flags |= PASK_FLAG_BAD_TAG;
+        if (a.states) {
+          if (cv.budget->loaded == kBudgetLoaded) {
+            int64_t* r = budget_of(cnt);
+            int64_t R = *r;
+            act = budget_decide(cv.budget, tag, (int)a.states[(size_t)b * a.max_new], forced,
+                                (int)a.tab.group, R, flags);
+            *r = R;
+          } else {
+            flags |= PASK_FLAG_NO_BUDGET;
+          }
+        }
         if (act == kDrop) {
           cnt[kCntDrop] += 1;
         } else {
@@ -1049,9 +1185,17 @@ hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hipStream_t s) {
+  const size_t n = (size_t)batch * cv.n_layers;
+  const size_t blocks = std::min<size_t>((n + 255) / 256, 4096);
+  budget_init_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(cv, batch, r0);
+  return hipGetLastError();
+}
+
 hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
   if (a.max_new == 1 && a.n_new == nullptr) return launch_append_step(a, s);
-  append_plan_kernel<<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  else append_plan_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   const dim3 grid((a.max_new + kPackTokens - 1) / kPackTokens, a.batch);
   if (a.cv.head_dim == 64) append_pack_kernel<64><<<grid, dim3(256), 0, s>>>(a);
   else append_pack_kernel<128><<<grid, dim3(256), 0, s>>>(a);

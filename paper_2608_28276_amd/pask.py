@@ -31,12 +31,14 @@ PASK_FLAG_HI_POOL_EXHAUSTED = 1 << 1
 PASK_FLAG_LO_POOL_EXHAUSTED = 1 << 2
 PASK_FLAG_SEQ_CAPACITY = 1 << 3
 PASK_FLAG_BAD_COUNT = 1 << 4
+PASK_FLAG_BAD_STATE = 1 << 5
+PASK_FLAG_NO_BUDGET = 1 << 6
 PASK_APPEND_KEEP_ALL = 1 << 0
 
-PASK_MAX_TAGS, PASK_MAX_GROUPS, PASK_MAX_LAYERS = 64, 16, 128
+PASK_MAX_TAGS, PASK_MAX_GROUPS, PASK_MAX_LAYERS, PASK_MAX_STATES = 64, 16, 128, 64
 EXPORTS = ("pask_policy_load", "pask_cache_layout_query", "pask_cache_bytes", "pask_cache_init",
-           "pask_cache_reset", "pask_kv_append", "pask_workspace_bytes", "pask_decode_attn",
-           "pask_cache_stats", "pask_status_string")
+           "pask_cache_reset", "pask_kv_append", "pask_budget_init", "pask_workspace_bytes",
+           "pask_decode_attn", "pask_cache_stats", "pask_status_string")
 
 
 class PaskError(RuntimeError):
@@ -57,7 +59,9 @@ class pask_policy(C.Structure):
                 ("action", (C.c_uint8 * PASK_MAX_GROUPS) * PASK_MAX_TAGS),
                 ("floor_", (C.c_uint8 * PASK_MAX_GROUPS) * PASK_MAX_TAGS),
                 ("rho_up", ((C.c_float * 2) * PASK_MAX_GROUPS) * PASK_MAX_TAGS),
-                ("entry_bytes", C.c_uint64 * 3)]
+                ("entry_bytes", C.c_uint64 * 3),
+                ("n_states", C.c_uint32), ("beta_q", C.c_uint32),
+                ("reserve_q", C.c_uint32 * PASK_MAX_STATES), ("crit", C.c_uint8 * PASK_MAX_STATES)]
 
 
 class pask_cache(C.Structure):
@@ -66,7 +70,7 @@ class pask_cache(C.Structure):
 
 class pask_cache_layout(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in ("status_off", "counters_off", "block_table_off", "index_list_off",
-                                          "staging_off", "hi_pool_off", "lo_pool_off", "total_bytes",
+                                          "staging_off", "budget_off", "hi_pool_off", "lo_pool_off", "total_bytes",
                                           "hi_page_bytes", "lo_page_bytes")] + \
                [("max_pages", C.c_int32), ("counter_stride", C.c_int32)]
 
@@ -92,11 +96,12 @@ _lib.pask_cache_bytes.argtypes = [C.POINTER(pask_geom)]
 _lib.pask_cache_init.argtypes = [C.POINTER(pask_cache), C.POINTER(pask_geom), _P, C.c_size_t, _P]
 _lib.pask_cache_reset.argtypes = [C.POINTER(pask_cache), _P]
 _lib.pask_kv_append.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P,
-                                C.c_int32, _P, _P, _P, C.c_uint32, _P]
+                                C.c_int32, _P, _P, _P, _P, C.c_uint32, _P]
+_lib.pask_budget_init.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P]
 _lib.pask_workspace_bytes.restype = C.c_size_t
 _lib.pask_workspace_bytes.argtypes = [C.POINTER(pask_geom), C.c_int32, C.c_int32]
 _lib.pask_decode_attn.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P, _P,
-                                  _P, _P, _P, _P, C.c_float, C.c_int32, _P, C.c_size_t, _P]
+                                  _P, _P, _P, _P, _P, C.c_float, C.c_int32, _P, C.c_size_t, _P]
 _lib.pask_cache_stats.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32,
                                   C.POINTER(pask_stats), _P, _P]
 
@@ -160,10 +165,18 @@ def pask_cache_reset(cache: pask_cache, stream=0) -> None:
 
 
 def pask_kv_append(policy: pask_policy, cache: pask_cache, layer: int, batch: int, n_new, max_new: int,
-                   tags, k, v, flags: int = 0, stream=0) -> None:
+                   tags, k, v, flags: int = 0, stream=0, states=None) -> None:
+    """states (keyword here, after tags in the C signature): parser states
+    [batch][max_new] uint8 for the online controller, or None."""
     _check(_lib.pask_kv_append(C.byref(policy), C.byref(cache), int(layer), int(batch), _ptr(n_new),
-                               int(max_new), _ptr(tags), _ptr(k), _ptr(v), int(flags), _ptr(stream)),
+                               int(max_new), _ptr(tags), _ptr(states), _ptr(k), _ptr(v), int(flags),
+                               _ptr(stream)),
            "pask_kv_append")
+
+
+def pask_budget_init(policy: pask_policy, cache: pask_cache, batch: int, t_max: int, stream=0) -> None:
+    _check(_lib.pask_budget_init(C.byref(policy), C.byref(cache), int(batch), int(t_max), _ptr(stream)),
+           "pask_budget_init")
 
 
 def pask_workspace_bytes(geom: pask_geom, batch: int, max_ctx_hint: int) -> int:
@@ -172,9 +185,12 @@ def pask_workspace_bytes(geom: pask_geom, batch: int, max_ctx_hint: int) -> int:
 
 def pask_decode_attn(policy: pask_policy, cache: pask_cache, layer: int, batch: int, q, out, lse=None,
                      tags_new=None, k_new=None, v_new=None, softmax_scale: float = 1.0,
-                     max_ctx_hint: int = 0, ws=None, ws_bytes: int = 0, stream=0) -> None:
+                     max_ctx_hint: int = 0, ws=None, ws_bytes: int = 0, stream=0, states_new=None) -> None:
+    """states_new (keyword here, after tags_new in the C signature): parser
+    states [batch] uint8 of the fused append, or None."""
     _check(_lib.pask_decode_attn(C.byref(policy), C.byref(cache), int(layer), int(batch), _ptr(q), _ptr(out),
-                                 _ptr(lse), _ptr(tags_new), _ptr(k_new), _ptr(v_new), float(softmax_scale),
+                                 _ptr(lse), _ptr(tags_new), _ptr(states_new), _ptr(k_new), _ptr(v_new),
+                                 float(softmax_scale),
                                  int(max_ctx_hint), _ptr(ws), int(ws_bytes), _ptr(stream)),
            "pask_decode_attn")
 

@@ -41,20 +41,32 @@ class PaskSession:
         return torch.cuda.current_stream(self.device).cuda_stream
 
     # -- the hot path ------------------------------------------------------
-    def append(self, layer: int, tags, k, v, n_new=None, keep_all: bool = False, batch: int | None = None):
-        """k, v: bf16 [batch, max_new, Hkv, D]; tags: uint8 [batch, max_new]."""
+    def append(self, layer: int, tags, k, v, n_new=None, keep_all: bool = False, batch: int | None = None,
+               states=None):
+        """k, v: bf16 [batch, max_new, Hkv, D]; tags, states (parser states
+        for the online controller, optional): uint8 [batch, max_new]."""
         b = batch or k.shape[0]
         pask.pask_kv_append(self.policy, self.cache, layer, b, n_new, k.shape[1], tags, k, v,
-                            pask.PASK_APPEND_KEEP_ALL if keep_all else 0, self.stream)
+                            pask.PASK_APPEND_KEEP_ALL if keep_all else 0, self.stream, states=states)
+
+    def budget_init(self, t_max: int, batch: int | None = None):
+        """Online controller: tables into the cache, R_0 for every layer."""
+        pask.pask_budget_init(self.policy, self.cache, batch or self.geom.max_batch, t_max, self.stream)
 
     def decode(self, layer: int, q, out, lse=None, tags_new=None, k_new=None, v_new=None,
-               batch: int | None = None, max_ctx_hint: int | None = None):
+               batch: int | None = None, max_ctx_hint: int | None = None, states_new=None):
         """q, out: bf16 [batch, Hq, D]; optional fused append of one token per
-        sequence (tags_new uint8 [batch], k_new / v_new bf16 [batch, Hkv, D])."""
+        sequence (tags_new, states_new uint8 [batch], k_new / v_new bf16
+        [batch, Hkv, D])."""
         b = batch or q.shape[0]
         hint = max_ctx_hint or self.max_ctx_hint
         pask.pask_decode_attn(self.policy, self.cache, layer, b, q, out, lse, tags_new, k_new, v_new,
-                              self.softmax_scale, hint, self.ws, self.ws_bytes, self.stream)
+                              self.softmax_scale, hint, self.ws, self.ws_bytes, self.stream, states_new=states_new)
+
+    def budgets(self):
+        """Remaining budget R of every (sequence, layer), int64 [max_batch, n_layers]."""
+        c = self.counters()
+        return c[:, :, 6:8].contiguous().view(torch.int64)[:, :, 0]
 
     def stats(self, batch: int | None = None, per_seq: bool = False):
         import numpy as np

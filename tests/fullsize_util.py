@@ -12,7 +12,7 @@ import numpy as np
 import torch
 
 import oracle
-from tests.gpu_util import assert_attn_close, bf16_f64, bits16, policy_dict, say
+from tests.gpu_util import assert_attn_close, bf16_f64, bits16, budgets, policy_dict, say
 from workload.policy import pack_blob
 from workload.tensors import sub_seed
 
@@ -31,13 +31,16 @@ class DeviceRun:
     ones go through one-token appends with attention (`step`)."""
 
     def __init__(self, pol, *, n_layers, layers, Hq, Hkv, D, P, prompt_tags, gen_tags, sample, seed,
-                 n_bulk, n_steps, chunk=2048):
+                 n_bulk, n_steps, chunk=2048, gen_states=None, t_max=0):
         from paper_2608_28276_amd.session import PaskSession
         self.pol, self.layers, self.Hq, self.Hkv, self.D = pol, list(layers), Hq, Hkv, D
         self.P = np.asarray(P, dtype=np.int64)
         self.B = self.P.size
         self.prompt_tags = prompt_tags
         self.gen_tags = np.asarray(gen_tags, dtype=np.uint8)
+        # parser states of the generated tokens (online controller, R_0 from t_max)
+        self.gen_states = None if gen_states is None else np.asarray(gen_states, dtype=np.uint8)
+        self.t_max = t_max
         self.sample = list(sample)
         self.seed, self.chunk = seed, chunk
         self.n_bulk, self.n_steps = n_bulk, n_steps
@@ -55,32 +58,63 @@ class DeviceRun:
         self.oc = oracle.OracleCache(policy_dict(pol), Hkv, D)
         self.scale = self.sess.softmax_scale
         self.gen = torch.Generator(device=self.dev)
+        if self.gen_states is not None:
+            self.sess.budget_init(t_max, batch=self.B)
+            for (b, l) in self.sample:
+                self.oc.budget_init(b, [l], t_max)
 
     # -- expected decisions of every (sequence, layer group) ---------------
+    def _controller(self, b, p, n_gen):
+        """The oracle controller over sequence b's generated tokens: actions
+        [n_gen][n_groups] and the final R (the same in every layer)."""
+        pol = self.pol
+        m = oracle.group_costs(self.gol, pol.n_groups, self.Hkv, self.D)
+        gamma = oracle.reserve_bytes(pol.reserve_q, m)
+        R = oracle.initial_budget(pol.beta_q, self.t_max, m)
+        out = np.zeros((n_gen, pol.n_groups), np.uint8)
+        for i in range(n_gen):
+            z, s = int(self.gen_tags[b, i]), int(self.gen_states[b, i])
+            known = s < pol.n_states
+            forced = p + i < pol.n_sink or z >= pol.n_tags
+            out[i], cost = oracle.online_actions(z, s, R, pol.action, pol.floor, pol.rho_up, m,
+                                                 gamma[s] if known else 0, bool(pol.crit[s]) if known else False,
+                                                 forced)
+            R -= cost
+        return out, R
+
     def _expected(self, n_gen):
-        self.exp = {}
+        self.exp, self.exp_n_gen = {}, n_gen
         act, flo, ns = np.asarray(self.pol.action), np.asarray(self.pol.floor), int(self.pol.n_sink)
+        ctl = {} if self.gen_states is None else \
+            {b: self._controller(b, int(self.P[b]), n_gen) for b in range(self.B)}
         for c in sorted({int(self.gol[l]) for l in self.layers}):
             for b in range(self.B):
                 p = int(self.P[b])
                 ptags = np.zeros(p, np.uint8) if self.prompt_tags is None else self.prompt_tags[b, :p]
                 a0, f0, _ = oracle.decide(ptags, np.arange(p), c, act, flo, ns, self.prompt_tags is None)
                 a1, f1, _ = oracle.decide(self.gen_tags[b, :n_gen], p + np.arange(n_gen), c, act, flo, ns, False)
+                if b in ctl:
+                    a1 = ctl[b][0][:, c]
                 acts = np.concatenate([a0, a1])
                 hi, lo = oracle.compact(acts, np.arange(p + n_gen))
                 self.exp[(b, c)] = dict(hi=hi, lo=lo, drop=int((acts == oracle.DROP).sum()),
-                                        forced=int(f0.sum() + f1.sum()), pos=p + n_gen)
+                                        forced=int(f0.sum() + f1.sum()), pos=p + n_gen,
+                                        R=ctl[b][1] if b in ctl else 0)
 
     # -- inputs ------------------------------------------------------------
     def _randn(self, shape, *key):
         self.gen.manual_seed(sub_seed(self.seed, "device_inputs", *key))
         return torch.randn(shape, generator=self.gen, device=self.dev, dtype=torch.bfloat16)
 
-    def _feed_oracle(self, layer, k, v, n, tags, keep_all):
+    def _feed_oracle(self, layer, k, v, n, tags, keep_all, states=None):
         for (b, l) in self.sample:
             if l == layer and n[b] > 0:
                 t = np.zeros(n[b], np.uint8) if tags is None else tags[b, :n[b]]
-                self.oc.append(layer, b, t, bits16(k[b, :n[b]]), bits16(v[b, :n[b]]), keep_all=keep_all)
+                self.oc.append(layer, b, t, bits16(k[b, :n[b]]), bits16(v[b, :n[b]]), keep_all=keep_all,
+                               states=None if states is None else states[b, :n[b]])
+
+    def _gen_states(self, t0, t1):
+        return None if self.gen_states is None else np.ascontiguousarray(self.gen_states[:, t0:t1])
 
     def fill(self):
         """Prompts, then generated tokens 0..n_bulk-1, in token chunks."""
@@ -105,8 +139,10 @@ class DeviceRun:
                 k = self._randn((self.B, w, self.Hkv, self.D), 3, layer, t0)
                 v = self._randn((self.B, w, self.Hkv, self.D), 4, layer, t0)
                 tg = np.ascontiguousarray(self.gen_tags[:, t0:t0 + w])
-                self.sess.append(layer, torch.as_tensor(tg, device=self.dev), k, v)
-                self._feed_oracle(layer, k, v, np.full(self.B, w), tg, False)
+                st = self._gen_states(t0, t0 + w)
+                self.sess.append(layer, torch.as_tensor(tg, device=self.dev), k, v,
+                                 states=None if st is None else torch.as_tensor(st, device=self.dev))
+                self._feed_oracle(layer, k, v, np.full(self.B, w), tg, False, st)
                 del k, v
             if li == 0 or li == len(self.layers) - 1:
                 say(f"filled layer {layer}")
@@ -119,6 +155,8 @@ class DeviceRun:
         attention; the sampled pairs are compared when `check`."""
         t = self.t
         tg = torch.as_tensor(np.ascontiguousarray(self.gen_tags[:, t]), device=self.dev)
+        st = self._gen_states(t, t + 1)
+        sd = None if st is None else torch.as_tensor(np.ascontiguousarray(st[:, 0]), device=self.dev)
         worst = 0.0
         for layer in self.layers:
             q = self._randn((self.B, self.Hq, self.D), 5, layer, t)
@@ -127,11 +165,12 @@ class DeviceRun:
             out = torch.empty((self.B, self.Hq, self.D), dtype=torch.bfloat16, device=self.dev)
             lse = torch.empty((self.B, self.Hq), dtype=torch.float32, device=self.dev)
             if fused:
-                self.sess.decode(layer, q, out, lse, tg, k[:, 0].contiguous(), v[:, 0].contiguous())
+                self.sess.decode(layer, q, out, lse, tg, k[:, 0].contiguous(), v[:, 0].contiguous(), states_new=sd)
             else:
-                self.sess.append(layer, tg[:, None].contiguous(), k, v)
+                self.sess.append(layer, tg[:, None].contiguous(), k, v,
+                                 states=None if sd is None else sd[:, None].contiguous())
                 self.sess.decode(layer, q, out, lse)
-            self._feed_oracle(layer, k, v, np.ones(self.B, np.int64), self.gen_tags[:, t:t + 1], False)
+            self._feed_oracle(layer, k, v, np.ones(self.B, np.int64), self.gen_tags[:, t:t + 1], False, st)
             if not check:
                 continue
             o_gpu, l_gpu = bf16_f64(out), lse.cpu().double().numpy()
@@ -151,7 +190,7 @@ class DeviceRun:
     def check_lists(self):
         """Counters and index lists of every sequence in every driven layer."""
         n_gen = self.t
-        if n_gen != self.n_bulk + self.n_steps:
+        if n_gen != self.exp_n_gen:
             self._expected(n_gen)
         cnt = self.sess.counters().cpu().numpy()
         for layer in self.layers:
@@ -162,6 +201,7 @@ class DeviceRun:
                 got = cnt[b, layer]
                 assert (got[0], got[1], got[2], got[3], got[4], got[5]) == \
                     (e["hi"].size, e["lo"].size, e["pos"], e["drop"], e["forced"], 0), (layer, b, got)
+                assert int(budgets(got)) == e["R"], ("remaining budget", layer, b, int(budgets(got)), e["R"])
                 assert (il[b, 0, :e["hi"].size] == e["hi"]).all(), ("HIGH list", layer, b)
                 assert (il[b, 1, :e["lo"].size] == e["lo"]).all(), ("LOW list", layer, b)
         st, status, _ = self.sess.stats(batch=self.B)
@@ -178,4 +218,8 @@ class DeviceRun:
             okc, oks, ovc, ovs = self.oc.lo_entries(b, layer)
             assert (kc == okc).all() and (vc == ovc).all(), ("LOW codes", layer, b)
             assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
+        for (b, layer) in self.sample:
+            c = self.oc.counts(b, layer)
+            e = self.exp[(b, int(self.gol[layer]))]
+            assert (c["hi"], c["lo"], c["R"]) == (e["hi"].size, e["lo"].size, e["R"]), ("oracle replay", b, layer)
         say(f"stores of {len(self.sample)} sampled pairs bit-exact")

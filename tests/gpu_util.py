@@ -40,7 +40,16 @@ def assert_attn_close(gpu: np.ndarray, ref: np.ndarray, what: str):
 
 
 def policy_dict(pol):
-    return dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=pol.n_sink)
+    d = dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=pol.n_sink,
+             rho_up=pol.rho_up)
+    if pol.n_states:
+        d.update(n_states=pol.n_states, beta_q=pol.beta_q, reserve_q=pol.reserve_q, crit=pol.crit)
+    return d
+
+
+def budgets(cnt: np.ndarray) -> np.ndarray:
+    """Remaining budget R (int64) from host counters [..., 8] (words 6, 7)."""
+    return np.ascontiguousarray(cnt[..., 6:8]).view(np.int64)[..., 0]
 
 
 class Scenario:
@@ -49,11 +58,15 @@ class Scenario:
     attention at chosen steps.  Inputs are generated on the CPU."""
 
     def __init__(self, pol, *, B, L, Hq, Hkv, D, prompt_lens, gen_tags, seed, prompt_tags=None,
-                 max_ctx_hint=None, hi_pages=None, lo_pages=None, extra_bytes=0, outliers=0):
+                 max_ctx_hint=None, hi_pages=None, lo_pages=None, extra_bytes=0, outliers=0, gen_states=None,
+                 expect_flags=0):
         from paper_2608_28276_amd.session import PaskSession
         self.pol, self.B, self.L, self.Hq, self.Hkv, self.D = pol, B, L, Hq, Hkv, D
         self.P = np.asarray(prompt_lens, dtype=np.int64)
         self.gen_tags = np.asarray(gen_tags, dtype=np.uint8).reshape(B, -1)
+        # parser states of the generated tokens: the online controller decides
+        self.gen_states = None if gen_states is None else np.asarray(gen_states, dtype=np.uint8).reshape(B, -1)
+        self.expect_flags = expect_flags
         self.T = self.gen_tags.shape[1]
         self.prompt_tags = prompt_tags
         self.seed = seed
@@ -90,6 +103,14 @@ class Scenario:
         return bf16_normal((self.B, self.Hq, self.D), sub_seed(self.seed, "q", layer, t))
 
     # -- driving both sides ---------------------------------------------
+    def budget_init(self, t_max: int):
+        self.sess.budget_init(t_max, batch=self.B)
+        for b in range(self.B):
+            self.oc.budget_init(b, range(self.L), t_max)
+
+    def _states(self, t0, t1):
+        return None if self.gen_states is None else np.ascontiguousarray(self.gen_states[:, t0:t1])
+
     def fill_prompt(self, layers=None):
         for layer in (range(self.L) if layers is None else layers):
             k, v = self.prompt_kv(layer)
@@ -113,9 +134,12 @@ class Scenario:
         for layer in (range(self.L) if layers is None else layers):
             k, v = self.gen_kv(layer, t0, t1)
             tg = torch.as_tensor(np.ascontiguousarray(self.gen_tags[:, t0:t1]), device=self.dev)
-            self.sess.append(layer, tg, k.to(self.dev), v.to(self.dev))
+            st = self._states(t0, t1)
+            sd = None if st is None else torch.as_tensor(st, device=self.dev)
+            self.sess.append(layer, tg, k.to(self.dev), v.to(self.dev), states=sd)
             for b in range(self.B):
-                self.oc.append(layer, b, self.gen_tags[b, t0:t1], bits16(k[b]), bits16(v[b]))
+                self.oc.append(layer, b, self.gen_tags[b, t0:t1], bits16(k[b]), bits16(v[b]),
+                               states=None if st is None else st[b])
 
     def decode_step(self, t, layers=None, check=True, seqs=None):
         """Fused append of token t + attention, on every layer; compare."""
@@ -126,10 +150,13 @@ class Scenario:
             out = torch.empty((self.B, self.Hq, self.D), dtype=torch.bfloat16, device=self.dev)
             lse = torch.empty((self.B, self.Hq), dtype=torch.float32, device=self.dev)
             tg = torch.as_tensor(np.ascontiguousarray(self.gen_tags[:, t]), device=self.dev)
+            st = self._states(t, t + 1)
+            sd = None if st is None else torch.as_tensor(np.ascontiguousarray(st[:, 0]), device=self.dev)
             self.sess.decode(layer, q.to(self.dev), out, lse, tg, k[:, 0].contiguous().to(self.dev),
-                             v[:, 0].contiguous().to(self.dev))
+                             v[:, 0].contiguous().to(self.dev), states_new=sd)
             for b in range(self.B):
-                self.oc.append(layer, b, self.gen_tags[b, t:t + 1], bits16(k[b]), bits16(v[b]))
+                self.oc.append(layer, b, self.gen_tags[b, t:t + 1], bits16(k[b]), bits16(v[b]),
+                               states=None if st is None else st[b])
             if not check:
                 continue
             self.check_state(layers=[layer], seqs=seqs)
@@ -154,6 +181,8 @@ class Scenario:
                 got = cnt[b, layer]
                 assert (got[0], got[1], got[2], got[3], got[4], got[5]) == \
                     (c["hi"], c["lo"], c["pos"], c["drop"], c["forced"], 0), (layer, b, got, c)
+                if self.gen_states is not None:
+                    assert int(budgets(got)) == c["R"], ("remaining budget", layer, b, int(budgets(got)), c["R"])
                 hi, lo = self.oc.lists(b, layer)
                 assert (il[b, layer, 0, :hi.size] == hi).all(), ("HIGH list", layer, b)
                 assert (il[b, layer, 1, :lo.size] == lo).all(), ("LOW list", layer, b)
@@ -167,6 +196,6 @@ class Scenario:
                 assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
         st, status, _ = self.sess.stats(batch=self.B)
         sw = self.sess.status_words().cpu().numpy()
-        assert status == 0 and st.device_flags == 0, (
+        assert st.device_flags == self.expect_flags, (
             f"device flags {st.device_flags:#x}; cursors {sw[2]}, {sw[3]} of pools "
             f"{self.sess.geom.hi_pages}, {self.sess.geom.lo_pages}; lost {st.n_lost}")

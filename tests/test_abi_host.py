@@ -9,7 +9,7 @@ import struct
 import numpy as np
 import pytest
 
-from workload.policy import fnv1a32, make_policy, pack_blob
+from workload.policy import fnv1a32, make_policy, pack_blob, with_budget_controller
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 pask = pytest.importorskip("paper_2608_28276_amd.pask", reason="libpask.so not built")
@@ -22,7 +22,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     lib = pask.library()
     for n in names:
         assert hasattr(lib, n), n
@@ -55,6 +55,52 @@ def test_policy_load_roundtrip():
     assert list(p.entry_bytes) == [0, 144, 512]
 
 
+def blob_v2(T=6, C=2, L=2, S=7, beta=0.33, seed=1):
+    pol = make_policy(T, C, L, beta, seed)
+    rng = np.random.default_rng(seed)
+    traces = [(rng.integers(0, T, 200), rng.integers(0, S, 200)) for _ in range(3)]
+    pol = with_budget_controller(pol, traces, S, critical=(1, 2))
+    return pol, pack_blob(pol)
+
+
+def test_policy_load_v2_roundtrip():
+    pol, blob = blob_v2()
+    assert struct.unpack_from("<H", blob, 4)[0] == 2
+    p = pask.pask_policy_load(blob, geom())
+    assert (p.n_states, p.beta_q) == (7, pol.beta_q)
+    assert list(p.reserve_q[:7]) == pol.reserve_q.tolist() and list(p.crit[:7]) == pol.crit.tolist()
+    assert list(p.reserve_q[7:]) == [0] * 57 and list(p.crit[7:]) == [0] * 57
+    got_a = np.array([[p.action[z][c] for c in range(2)] for z in range(6)])
+    assert (got_a == pol.action).all()
+    p1 = pask.pask_policy_load(pack_blob(pol, version=1), geom())      # the table without the controller
+    assert p1.n_states == 0 and p1.beta_q == 0
+
+
+@pytest.mark.parametrize("case", ["states0", "states65", "crit2", "pad", "short", "long"])
+def test_policy_load_v2_rejects(case):
+    pol, blob = blob_v2()
+    L, T, C, S = 2, 6, 2, 7
+    ctl = 32 + ((L + 2 * T * C + 3) // 4) * 4 + 8 * T * C        # n_states, beta_q, reserve_q, crit
+    crit_at = ctl + 8 + 4 * S
+    if case == "states0":
+        bad = _patch(blob, ctl, "<I", 0)
+    elif case == "states65":
+        bad = _patch(blob, ctl, "<I", 65)
+    elif case == "crit2":
+        bad = _patch(blob, crit_at + 3, "<B", 2)
+    elif case == "pad":
+        bad = _patch(blob, crit_at + S, "<B", 1)
+    elif case == "short":                      # body one word short of what n_states needs
+        b = bytearray(blob[:-8] + blob[-4:])
+        struct.pack_into("<I", b, 28, struct.unpack_from("<I", b, 28)[0] - 4)
+        bad = _rehash(bytes(b))
+    else:                                      # n_states claims more than the body holds
+        bad = _patch(blob, ctl, "<I", 8)
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_policy_load(bad, geom())
+    assert e.value.status == pask.PASK_E_POLICY
+
+
 def _rehash(b: bytes) -> bytes:
     return b[:-4] + struct.pack("<I", fnv1a32(b[:-4]))
 
@@ -78,7 +124,7 @@ def test_policy_load_rejects(case, code):
     if case == "magic":
         bad = b"XASK" + blob[4:]
     elif case == "version":
-        bad = _patch(blob, 4, "<H", 2)
+        bad = _patch(blob, 4, "<H", 3)
     elif case == "hash":
         bad = blob[:-1] + bytes([blob[-1] ^ 1])
     elif case == "truncated":
@@ -115,12 +161,14 @@ def test_layout_and_sizes():
     assert L.hi_page_bytes == 2 * 2 * 16 * 64 * 2
     assert L.lo_page_bytes == 2 * 2 * (16 * 32 + 16 * 2 * 2)
     assert L.max_pages == 32 and L.counter_stride == 8
-    offs = [L.status_off, L.counters_off, L.block_table_off, L.index_list_off, L.staging_off, L.hi_pool_off,
-            L.lo_pool_off, L.total_bytes]
+    offs = [L.status_off, L.counters_off, L.block_table_off, L.index_list_off, L.staging_off, L.budget_off,
+            L.hi_pool_off, L.lo_pool_off, L.total_bytes]
     assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
     assert L.counters_off - L.status_off >= 16
     assert L.block_table_off - L.counters_off >= 4 * 2 * 8 * 4
     assert L.index_list_off - L.block_table_off >= 4 * 2 * 2 * 32 * 4
+    assert L.budget_off - L.staging_off >= 4 * 512 * 4
+    assert L.hi_pool_off - L.budget_off >= 11232 and L.hi_pool_off % 4096 == 0
     assert L.lo_pool_off - L.hi_pool_off >= 64 * L.hi_page_bytes
     assert L.total_bytes - L.lo_pool_off >= 64 * L.lo_page_bytes
     assert pask.pask_cache_bytes(g) == L.total_bytes
@@ -177,8 +225,12 @@ def test_append_and_attn_validation_before_any_hip_call():
         kw.update(over)
         with pytest.raises(pask.PaskError) as e:
             pask.pask_kv_append(p, c, kw["layer"], kw["batch"], kw["n_new"], kw["max_new"], kw["tags"], kw["k"],
-                                kw["v"], kw["flags"], 0)
+                                kw["v"], kw["flags"], 0, states=kw.get("states"))
         assert e.value.status == code, over
+    # parser states need a table that carries the controller (version 2)
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_kv_append(p, c, 0, 1, None, 4, A, A, A, 0, 0, states=A)
+    assert e.value.status == pask.PASK_E_POLICY
     small = _fake_cache(g)
     small.bytes = c.bytes - 1
     with pytest.raises(pask.PaskError) as e:
@@ -197,6 +249,28 @@ def test_append_and_attn_validation_before_any_hip_call():
             pask.pask_decode_attn(p, c, kw["layer"], 1, kw["q"], kw["out"], None, kw["tags"], kw["k"], kw["k"],
                                   kw["scale"], 512, kw["ws"], kw["ws_bytes"], 0)
         assert e.value.status == code, over
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_decode_attn(p, c, 0, 1, A, A, None, A, A, A, 0.125, 512, A, ws_need, 0, states_new=A)
+    assert e.value.status == pask.PASK_E_POLICY
+    # the controller's set-up
+    for args, code in [((p, c, 1, 100), pask.PASK_E_POLICY), ((p2 := pask.pask_policy_load(blob_v2()[1], g), c, 0, 100),
+                                                                 pask.PASK_E_SHAPE),
+                       ((p2, c, 5, 100), pask.PASK_E_SHAPE), ((p2, c, 1, -1), pask.PASK_E_ARG)]:
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_budget_init(*args, 0)
+        assert e.value.status == code, args[2:]
+    bad_act = pask.pask_policy_load(blob_v2()[1], g)
+    bad_act.action[1][0] = 3
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_budget_init(bad_act, c, 1, 100, 0)
+    assert e.value.status == pask.PASK_E_POLICY
+    # R_0 = beta_q * t_max * sum_c m(H, c) / 65536 must stay below 2^62
+    gb = geom(n_layers=128, n_q_heads=8, n_kv_heads=8, head_dim=128)
+    pb = pask.pask_policy_load(blob_v2(L=128)[1], gb)
+    pb.beta_q = 0xFFFFFFFF
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_budget_init(pb, _fake_cache(gb), 1, (1 << 31) - 1, 0)
+    assert e.value.status == pask.PASK_E_ARG
     other = pask.pask_policy_load(blob_for(L=4, C=2)[1], geom(n_layers=4))
     with pytest.raises(pask.PaskError) as e:
         pask.pask_kv_append(other, c, 0, 1, None, 4, A, A, A, 0, 0)

@@ -132,3 +132,36 @@ def test_qwen3_32b_attention_batch256_one_layer_group():
     run.step(check=True, fused=True)
     run.check_lists()
     run.check_stores()
+
+
+def test_qwen3_4b_batch64_online_controller():
+    """The timed workload's shapes under the online controller (Alg. 2): 64
+    sequences, 36 layers in 4 groups, prompts U{1024..8192} kept HIGH (they
+    bypass the controller), 512 generated tokens with walker tags and parser
+    states bulk-appended, then a one-token append step and two fused steps;
+    R_0 from the table's beta with T_max = 515.  Every counter, list and
+    remaining budget of all 64 sequences x 36 layers bit-exact; stores and
+    attention of 6 sequences x the first layer of each group."""
+    from bench import build_workload
+    from tests.fullsize_util import DeviceRun
+    from workload.policy import with_budget_controller
+    from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
+    cfg, P, tags, pol = build_workload(2)
+    say(f"case: {cfg.name} with the online controller")
+    n_gen = 515
+    ts = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
+    assert all((t == tags[b]).all() for b, (t, _) in enumerate(ts))
+    states = np.stack([s for _, s in ts])
+    cal = [walk_function_calls_with_states(n_gen, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
+    pol = with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES)
+    sample = [(b, l) for b in (0, 13, 31, 40, 52, 63) for l in (0, 9, 18, 27)]
+    run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
+                    Hkv=cfg.n_kv_heads, D=cfg.head_dim, P=P, prompt_tags=None, gen_tags=tags, sample=sample,
+                    seed=cfg.seed, n_bulk=512, n_steps=3, gen_states=states, t_max=n_gen)
+    run.fill()
+    run.check_lists()
+    run.step(check=False)
+    run.step(check=True, fused=True)
+    run.step(check=True, fused=True)
+    run.check_lists()
+    run.check_stores()

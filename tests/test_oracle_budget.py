@@ -1,4 +1,4 @@
-"""Pins of the oracle's online budget controller (Alg. 2; Eq. 8-10).
+"""Pins of the oracle's online budget controller (Alg. 2; Eq. 9-10).
 
 Hand-worked cases on a three-group table fix the demotion order (ascending
 upgrade score of the step being undone, lower group on ties), the floors'

@@ -29,7 +29,7 @@ Blob layout (little-endian), version 1:
      f32      rho_up[n_tags][n_groups][2]  (R->L, L->H)
   end u32     FNV-1a 32-bit hash of all preceding bytes
 Version 2 appends, after rho_up, the state of the online budget controller
-(Eq. 8-10, Alg. 2):
+(Eq. 9-10, Alg. 2):
      u32      n_states        (parser states s)
      u32      beta_q          target budget beta in units of 1/65536
      u32      reserve_q[n_states]  Gamma(s) in units of 1/16 of the bytes one token
@@ -164,7 +164,7 @@ def with_budget_controller(pol: PolicyTable, traces, n_states: int, critical, be
                            quantile: float = 0.5) -> PolicyTable:
     """Adds the online controller's state to a table.
 
-    traces: calibration (tags, states) pairs.  Gamma(s) follows Eq. 8: the
+    traces: calibration (tags, states) pairs.  Gamma(s) follows Eq. 9: the
     empirical quantile, over every position u of every trace whose state is s,
     of the floor cost of the positions after u (the protected history still to
     come); it is stored in sixteenths of a full-precision token.  A state that
