@@ -568,16 +568,29 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
 // decode attention
 // ---------------------------------------------------------------------------
 //
-// One wavefront per (split, KV head g, sequence b).  A split walks 256-slot
-// work units, HIGH units first, then LOW units; within a unit it streams
-// 16-slot pages and loads page p+1 while it computes page p.  Two lane maps
-// of a page:
-//   K map  lane = 4t + s: slot t, head_dim slice s (D/4 contiguous dims);
-//          q . k over the slice, then summed over the 4 lanes of a quad.
-//   V map  lane = (D/8) r + c: slots r + (64/(D/8)) i, dims 8c..8c+7; every
-//          lane accumulates 8 dims of the G heads' outputs.
-// Probabilities move from the K map to the V map through LDS.  Each split
-// leaves a partial (max, sum, unnormalised o); attn_merge combines them.
+// Stream-K: the work is the list of (sequence b, KV head g, page) triples,
+// HIGH pages of a (b, g) before its LOW pages, each page weighing 32 units
+// (PASK_WEIGHT_LO for a LOW page).  The grid holds one single-wave worker
+// per resident wave slot of the chip, and worker w takes the w-th of equal
+// contiguous unit ranges, so every worker starts at launch and all finish
+// together.  A range crossing a (b, g) boundary closes that segment with a
+// partial block; the range length is at least what keeps every (b, g) within
+// as many pieces as the workspace holds partials.
+//
+// Per page (16 slots x all G query heads of KV head g), one wave:
+//   scores  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: rows = slots, columns
+//           = query heads, so lane (q, n) holds the scores of head n for
+//           slots 4q..4q+3; a LOW code c becomes the bf16 value 136 + c
+//           (exact) and 136 * sum(q) is removed per 32-dim group before the
+//           K scale is applied;
+//   softmax online in base 2, per head, rescaling only when a max grows;
+//   values  O += P V on v_mfma_f32_16x16x16_bf16 with P (split into bf16
+//           high and low parts, so p keeps ~16 bits) as the A operand exactly
+//           as the score tile lies; LOW pages fold the V scale into p and
+//           remove the code offset once per segment.
+// The next page's operands are loaded while the current one is computed.
+// Each segment leaves (max, sum, unnormalised o) per head; attn_merge
+// combines the partials of a (b, g).
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
@@ -1118,6 +1131,23 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   const int H = a.cv.n_kv_heads;
   const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
   const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
+  const size_t blk0 = ((size_t)b * H + g) * a.splits;
+  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
+  float4 v[kBatch], mla[kBatch], mlb[kBatch];
+  auto load_batch = [&](int p0, int last) {       // pieces p0.., past `last` repeated (skipped later)
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const size_t pb = blk0 + min(p0 + u, last);
+      const float* ml = a.ws_ml + pb * G4 * 2 + 8 * q;
+      v[u] = *reinterpret_cast<const float4*>(a.ws_o + pb * (G4 * D) + t * 4);
+      mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
+      mlb[u] = *reinterpret_cast<const float4*>(ml + 4);   // (m, l) of heads 4q+2, 4q+3
+    }
+  };
+  // The first kBatch pieces are loaded before the piece count is known (slots
+  // below `splits` are in bounds; those past the count are skipped), so their
+  // latency overlaps that of the counters the count comes from.
+  load_batch(0, a.splits - 1);
   const FirstCounts f = first_counts(a);
   const SeqPages sp = seq_pages(a, f, b);
   if (sp.np == 0) {
@@ -1130,21 +1160,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
   const long long seg0 = (long long)excl * H + (long long)g * sp.len;
   const int nparts = (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
-  const size_t blk0 = ((size_t)b * H + g) * a.splits;
-  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f}, M[4], L[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int r = 0; r < 4; ++r) M[r] = -INFINITY;
   for (int p0 = 0; p0 < nparts; p0 += kBatch) {
-    float4 v[kBatch], mla[kBatch], mlb[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {            // past the last piece: repeat it, skipped below
-      const size_t pb = blk0 + min(p0 + u, nparts - 1);
-      const float* ml = a.ws_ml + pb * G4 * 2 + 8 * q;
-      v[u] = *reinterpret_cast<const float4*>(a.ws_o + pb * (G4 * D) + t * 4);
-      mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
-      mlb[u] = *reinterpret_cast<const float4*>(ml + 4);   // (m, l) of heads 4q+2, 4q+3
-    }
+    if (p0 > 0) load_batch(p0, nparts - 1);
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       if (p0 + u >= nparts) break;
