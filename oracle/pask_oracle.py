@@ -20,7 +20,11 @@ What it computes, each piece following the passage named in its docstring:
   * the online budget controller of Alg. 2 (Eq. 9-10): the remaining budget
     R_t, B_t = max(0, R_t - Gamma(s_t)), demotions above the floors in
     ascending upgrade score, promotions in critical states in descending
-    score, R_{t+1} = R_t - sum_c m(a_c, c), all in integer bytes.
+    score, R_{t+1} = R_t - sum_c m(a_c, c), all in integer bytes;
+  * the protected recent window of Section 3.1: the last W positions of a
+    sequence stay visible at full precision whatever their action, which
+    takes effect when a token leaves the window (release then removes it from
+    the attention that follows).
 
 Everything is plain numpy.  The attention is the definition written out
 (exact, up to fp64 rounding order); the decisions, compaction and codes are
@@ -276,18 +280,28 @@ class _SeqLayer:
     n_forced: int = 0
     n_drop: int = 0
     R: int = 0                                    # remaining budget (bytes) of the online controller
+    # tokens inside the protected recent window, in position order: decided,
+    # not yet persisted (positions, actions, forced flags, bf16 bits of K, V)
+    w_pos: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    w_act: np.ndarray = field(default_factory=lambda: np.zeros(0, np.uint8))
+    w_forced: np.ndarray = field(default_factory=lambda: np.zeros(0, bool))
+    w_k: np.ndarray = None
+    w_v: np.ndarray = None
 
 
 class OracleCache:
     """The persisted history of a set of sequences, replayed append by append.
 
-    policy: dict with action [T][C], floor [T][C], group_of_layer [L], n_sink."""
+    policy: dict with action [T][C], floor [T][C], group_of_layer [L], n_sink,
+    and optionally recent_window W (Section 3.1), rho_up and the controller's
+    n_states, beta_q, reserve_q, crit."""
 
     def __init__(self, policy: dict, n_kv_heads: int, head_dim: int):
         self.action = np.asarray(policy["action"])
         self.floor = np.asarray(policy["floor"])
         self.group_of_layer = np.asarray(policy["group_of_layer"])
         self.n_sink = int(policy.get("n_sink", 0))
+        self.window = int(policy.get("recent_window", 0))
         self.hkv = n_kv_heads
         self.d = head_dim
         self.state: dict = {}
@@ -336,7 +350,29 @@ class OracleCache:
                 acts[i] = a[c]
                 st.R -= cost
         self.bad_tag |= bool(bad.any())
-        st.n_forced += int(forced.sum())
+        if self.window == 0:
+            self._persist(st, pos, acts, forced, k_bits, v_bits)
+        else:
+            # Section 3.1: the decision is taken now; it takes effect when the
+            # token leaves the last W positions of the sequence.
+            if st.w_k is None:
+                st.w_k = np.zeros((0, self.hkv, self.d), np.uint16)
+                st.w_v = np.zeros((0, self.hkv, self.d), np.uint16)
+            wp = np.concatenate([st.w_pos, pos])
+            wa = np.concatenate([st.w_act, acts])
+            wf = np.concatenate([st.w_forced, forced])
+            wk = np.concatenate([st.w_k, k_bits])
+            wv = np.concatenate([st.w_v, v_bits])
+            out = wp < st.n_pos + n - self.window
+            self._persist(st, wp[out], wa[out], wf[out], wk[out], wv[out])
+            st.w_pos, st.w_act, st.w_forced, st.w_k, st.w_v = wp[~out], wa[~out], wf[~out], wk[~out], wv[~out]
+        st.n_pos += n
+        return acts
+
+    def _persist(self, st: _SeqLayer, pos, acts, forced, k_bits, v_bits):
+        """The Persist step of Alg. 2 for entries in position order: HIGH keeps
+        the bf16 bits, LOW the int4 codes and fp16 scales, DROP nothing."""
+        st.n_forced += int(np.asarray(forced).sum())
         hi = acts == HIGH
         lo = acts == LOW
         st.hi_pos.extend(pos[hi].tolist())
@@ -351,8 +387,6 @@ class OracleCache:
             st.lo_vc.append(vc)
             st.lo_vs.append(vs)
         st.n_drop += int((acts == DROP).sum())
-        st.n_pos += n
-        return acts
 
     def lists(self, seq: int, layer: int):
         st = self.sl(seq, layer)
@@ -375,13 +409,19 @@ class OracleCache:
         return f(st.hi_k), f(st.hi_v)
 
     def visible_kv(self, seq: int, layer: int):
-        """K and V of every persisted entry in position order, in fp64."""
+        """K and V of every visible entry in position order, in fp64: the
+        persisted stores and the tokens still inside the recent window."""
         hk, hv = self.hi_entries(seq, layer)
         kc, ks, vc, vs = self.lo_entries(seq, layer)
         hi_pos, lo_pos = self.lists(seq, layer)
         pos = np.concatenate([hi_pos, lo_pos])
         k = np.concatenate([bf16_to_f64(hk), dequant(kc, ks)])
         v = np.concatenate([bf16_to_f64(hv), dequant(vc, vs)])
+        st = self.sl(seq, layer)
+        if st.w_pos.size:
+            pos = np.concatenate([pos, st.w_pos])
+            k = np.concatenate([k, bf16_to_f64(st.w_k)])
+            v = np.concatenate([v, bf16_to_f64(st.w_v)])
         order = np.argsort(pos, kind="stable")
         return k[order], v[order]
 
@@ -395,7 +435,7 @@ class OracleCache:
     def counts(self, seq: int, layer: int):
         st = self.sl(seq, layer)
         return dict(hi=len(st.hi_pos), lo=len(st.lo_pos), pos=st.n_pos, drop=st.n_drop,
-                    forced=st.n_forced, R=st.R)
+                    forced=st.n_forced, R=st.R, window=int(st.w_pos.size))
 
 
 # --------------------------------------------------------------------------
