@@ -55,7 +55,21 @@ def build_workload(cfg_idx: int):
     return cfg, P, tags.astype(np.uint8), pol
 
 
-def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
+def controller_inputs(cfg, tags, pol):
+    """Parser states of the walker streams (the same seeds give the same tags)
+    and the table with the controller's reserve, calibrated on eight walker
+    traces of the generation length."""
+    from workload.policy import with_budget_controller
+    from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
+    from workload.tensors import sub_seed
+    ts = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
+    assert all((t == tags[b]).all() for b, (t, _) in enumerate(ts)), "controller runs need walker tags"
+    cal = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
+    pol = with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES)
+    return np.stack([s for _, s in ts]).astype(np.uint8), pol
+
+
+def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=None):
     import torch
 
     from paper_2608_28276_amd import pask
@@ -74,6 +88,9 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
                        head_dim=D, max_tokens_per_seq=max_tok, hi_pages=hi_pages, lo_pages=lo_pages,
                        max_ctx_hint=max_tok)
     log(f"cache {sess.nbytes / 2**30:.1f} GiB, workspace {sess.ws_bytes / 2**20:.1f} MiB")
+    if states is not None:
+        sess.budget_init(T, batch=B)                     # online controller: R_0 for T_max = T
+        states_dev = torch.as_tensor(states, dtype=torch.uint8, device=dev)
     g = torch.Generator(device=dev)
     g.manual_seed(cfg.seed)
     n_new = torch.as_tensor(P, dtype=torch.int32, device=dev)
@@ -87,7 +104,8 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
         if t_start:
             k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
             v = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-            sess.append(layer, tags_dev[:, :t_start].contiguous(), k, v)
+            sess.append(layer, tags_dev[:, :t_start].contiguous(), k, v,
+                        states=None if states is None else states_dev[:, :t_start].contiguous())
             del k, v
     torch.cuda.synchronize()
     log(f"prompt + {t_start} generated tokens persisted in {time.time() - t0:.1f} s")
@@ -97,6 +115,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
     vn = torch.randn((L, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
     out = torch.empty((L, B, Hq, D), dtype=torch.bfloat16, device=dev)
     tags_t = tags_dev.t().contiguous()                   # [T, B]
+    states_t = None if states is None else states_dev.t().contiguous()
     stream = torch.cuda.current_stream(dev)
     sptr = stream.cuda_stream
     pol_c, cache_c = sess.policy, sess.cache
@@ -113,8 +132,9 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
         # One decode step: per layer, persist the step's token (one-token append
         # kernel), then the attention kernel over the layer's persisted history.
         tp = tags_t[t].data_ptr()
+        sp = None if states_t is None else states_t[t].data_ptr()
         for layer in range(L):
-            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, None, kp[layer], vp[layer], 0,
+            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, sp, kp[layer], vp[layer], 0,
                                     sptr)
             if st != 0:
                 raise pask.PaskError(st, "pask_kv_append")
@@ -151,12 +171,15 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
     # every persisted entry read once (counts grow linearly over the region,
     # each launch sees its step's token), q read, o written.  The one-token
     # append adds the step's token in its stored form and one list entry.
-    kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL
+    W = int(pol.recent_window)
+    kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL + np.minimum(c[..., 2], W) * mH   # stores + window
     read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)          # per layer, summed over seqs
     qo = 2 * 2 * B * Hq * D
     attn_bytes = read + qo                                                 # [L]
     new_tok = (kv_bytes(cnt1) - kv_bytes(cnt0)).sum(axis=0) / steps      # per layer per step
     stored = ((cnt1[..., 0] + cnt1[..., 1]) - (cnt0[..., 0] + cnt0[..., 1])).sum(axis=0) / steps
+    if W:                                        # the token entering the window and the one leaving it
+        new_tok = new_tok + 2 * B * mH
     append_bytes = new_tok + 4 * stored + 2 * B * Hkv * D * 2             # stored form + lists + k/v read
     bytes_per_step = float((attn_bytes + append_bytes).sum())
     avg_attn_s = float(call_ms.mean()) / 1e3
@@ -172,7 +195,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int):
     return res
 
 
-def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
+def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None):
     """The oracle as it stands, on a bounded sample: n_seq sequences of the
     same workload (their prompt lengths and tag streams, seeded CPU inputs),
     history built untimed, then one timed decode step through all layers."""
@@ -182,17 +205,23 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
     import oracle
     from workload.tensors import bf16_normal, sub_seed
     L, Hq, Hkv, D = cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
-    oc = oracle.OracleCache(dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer,
-                                 n_sink=pol.n_sink), Hkv, D)
+    pd = dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=pol.n_sink,
+              rho_up=pol.rho_up, recent_window=pol.recent_window)
+    if states is not None:
+        pd.update(n_states=pol.n_states, beta_q=pol.beta_q, reserve_q=pol.reserve_q, crit=pol.crit)
+    oc = oracle.OracleCache(pd, Hkv, D)
+    st_of = (lambda b, t0, t1: None) if states is None else (lambda b, t0, t1: states[b, t0:t1])
     bits = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
     seqs = list(range(n_seq))
     for b in seqs:
+        if states is not None:
+            oc.budget_init(b, range(L), cfg.gen_tokens)
         for layer in range(L):
             p = int(P[b])
             k = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_k", layer, b))
             v = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_v", layer, b))
             oc.append(layer, b, np.zeros(p, np.uint8), bits(k[:p]), bits(v[:p]), keep_all=True)
-            oc.append(layer, b, tags[b, :t_start], bits(k[p:]), bits(v[p:]))
+            oc.append(layer, b, tags[b, :t_start], bits(k[p:]), bits(v[p:]), states=st_of(b, 0, t_start))
     q = bf16_normal((L, Hq, D), sub_seed(cfg.seed, "q", 0))
     kn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_k", 0))
     vn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_v", 0))
@@ -202,7 +231,8 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int):
     t0 = time.perf_counter()
     for b in seqs:
         for layer in range(L):
-            oc.append(layer, b, tags[b, t_start:t_start + 1], bits(kn[layer][None]), bits(vn[layer][None]))
+            oc.append(layer, b, tags[b, t_start:t_start + 1], bits(kn[layer][None]), bits(vn[layer][None]),
+                      states=st_of(b, t_start, t_start + 1))
             oc.attend(layer, b, bits(q[layer]), scale)
     el = time.perf_counter() - t0
     return dict(value=n_seq / el, unit="tokens/s", cores=int(threads), kind="oracle",
@@ -270,6 +300,10 @@ def main():
     ap.add_argument("--t-start", type=int, default=512, help="generated tokens persisted before timing")
     ap.add_argument("--cpu-seqs", type=int, default=3, help="sequences in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--window", type=int, default=0, metavar="W",
+                    help="protected recent window of W positions (Section 3.1); default 0")
+    ap.add_argument("--controller", action="store_true",
+                    help="parser states drive the online budget controller (Alg. 2)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -281,14 +315,18 @@ def main():
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
     cfg, P, tags, pol = build_workload(args.config)
+    pol.recent_window = args.window
+    states = None
+    if args.controller:
+        states, pol = controller_inputs(cfg, tags, pol)
     log(f"workload {cfg.name}: B={cfg.batch} L={cfg.n_layers} prompts {int(P.min())}..{int(P.max())}, "
         f"policy expected cost {pol.expected_cost:.3f}")
-    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start)
+    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, states)
     log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
         f"{g['achieved']:.0f} GB/s algorithmic")
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs)
+        cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs, states)
         log(f"cpu oracle: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
     line = {
         "metric": METRIC,
@@ -304,7 +342,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": cfg.name, "batch": cfg.batch, "layers": cfg.n_layers, "layer_groups": cfg.n_groups,
+            "workload": cfg.name + (f"+window{args.window}" if args.window else "") +
+                        ("+controller" if args.controller else ""), "batch": cfg.batch, "layers": cfg.n_layers, "layer_groups": cfg.n_groups,
             "q_heads": cfg.n_q_heads, "kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
             "prompt_tokens": f"U{{{cfg.prompt_min}..{cfg.prompt_max}}}", "generated_before_timing": args.t_start,
             "budget": 0.33, "realised_c_kv_generated": round(g["c_kv_governed"], 4),
@@ -312,6 +351,7 @@ def main():
             "mean_persisted_entries": round(g["mean_entries"], 1),
             "hbm_gb_per_step": round(g["bytes_per_step"] / 1e9, 3),
             "step_gbs": round(g["step_gbs"], 1),
+            "recent_window": args.window, "online_controller": bool(args.controller),
         },
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

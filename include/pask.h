@@ -22,7 +22,11 @@
  *                saturated at 65504; q_i = clamp(RNE(x_i / s), -7, 7), all 0
  *                when s == 0; two's-complement nibbles, element 2j in the low
  *                nibble of byte j.  Dequantised value q * s.
- *   Protected recent window: 0 (a window > 0 is rejected as unsupported).
+ *   Protected recent window (Section 3.1): the last W positions of every
+ *                (sequence, layer) stay visible at bf16 whatever their action;
+ *                a token's action (decided, and charged by the controller,
+ *                when it is appended) takes effect when it leaves the window.
+ *                W = 0: actions take effect at once.
  *
  * Conventions for every entry point:
  *   - Return an int status: PASK_OK (0) or a negative PASK_E_* code.  No
@@ -105,6 +109,7 @@ typedef struct pask_geom {
   int32_t max_tokens_per_seq;  /* positions per (sequence, layer)                */
   int32_t hi_pages;            /* pages in the RETAIN-HIGH pool (all layers)     */
   int32_t lo_pages;            /* pages in the RETAIN-LOW pool (all layers)      */
+  int32_t recent_window;       /* W, 0..max_tokens_per_seq (== the policy's W)   */
 } pask_geom;
 
 /* The frozen table Lambda after parsing (caller-owned plain data). */
@@ -143,7 +148,14 @@ typedef struct pask_cache_layout {
                                 position of each slot of each store               */
   uint64_t staging_off;      /* i32 [max_batch][max_tokens_per_seq]: append plan   */
   uint64_t budget_off;       /* the online controller's tables (pask_budget_init)  */
-  uint64_t hi_pool_off;      /* hi_pages pages of hi_page_bytes                    */
+  uint64_t ring_act_off;     /* u8 [max_batch][n_layers][W]: decided action | forced
+                                << 2 of the token in each recent-window slot       */
+  uint64_t hi_pool_off;      /* ring_pages + hi_pages pages of hi_page_bytes: the
+                                recent windows first (sequence b, layer l owns
+                                pages (b*n_layers + l)*ceil(W/16) + k; position p
+                                sits in window slot p mod W, i.e. page slot
+                                (p mod W) % 16 of its k = (p mod W) / 16), then
+                                the RETAIN-HIGH store pages                        */
   uint64_t lo_pool_off;      /* lo_pages pages of lo_page_bytes                    */
   uint64_t total_bytes;
   /* In both pools KV head g of page P sits in head slot h = (g + P) mod
@@ -162,6 +174,8 @@ typedef struct pask_cache_layout {
                                 slot t, e < 16), V scales [16][D/32] fp16       */
   int32_t max_pages;         /* ceil(max_tokens_per_seq / 16)                      */
   int32_t counter_stride;    /* 8                                                  */
+  int32_t ring_pages;        /* max_batch * n_layers * ceil(W / 16)                */
+  int32_t staging_stride;    /* i32 per sequence in the staging region             */
 } pask_cache_layout;
 
 /* Accounting of what a cache holds (Eq. 1).  Entry = one (token, layer). */
@@ -175,6 +189,7 @@ typedef struct pask_stats {
   double c_kv_all;         /* stored bytes / bf16 bytes over all entries       */
   uint32_t device_flags;
   uint32_t reserved;
+  int64_t n_window;        /* entries inside the recent windows (not persisted) */
 } pask_stats;
 
 /* Parse and validate a policy blob (the frozen table of the offline
@@ -193,8 +208,8 @@ typedef struct pask_stats {
  * Errors: PASK_E_ARG (null pointers), PASK_E_POLICY (bad magic, version,
  * sizes, hash, action or floor > 2, group id >= n_groups, rho not finite or
  * negative, n_tags/n_groups/n_layers/n_states out of range, crit > 1),
- * PASK_E_SHAPE (n_layers != geometry's, or the geometry itself invalid),
- * PASK_E_UNSUPPORTED (recent_window != 0).  Host only: no HIP call. */
+ * PASK_E_SHAPE (n_layers or recent_window != the geometry's, or the geometry
+ * itself invalid).  Host only: no HIP call. */
 int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pask_policy* out);
 
 /* Region offsets of a cache of this geometry.  PASK_E_SHAPE if unsupported. */
@@ -223,6 +238,9 @@ int pask_cache_reset(pask_cache* cache, hipStream_t stream);
  * positions below n_sink, tokens of a KEEP_ALL call (tags_dev may be NULL) and
  * tags >= n_tags get RETAIN-HIGH.  Surviving tokens receive the next slots of
  * their store in position order; DROP tokens get none (release, Section 3.1).
+ * With a recent window W > 0, a token enters the window at bf16 and is
+ * persisted by its action (taken now) when it leaves it; the tokens leaving
+ * during this call are persisted in position order.
  *
  * states_dev (nullable; ignored by a KEEP_ALL call): parser states
  * [batch][max_new] of the tokens.  Given, the online controller of Alg. 2
@@ -276,7 +294,8 @@ size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ct
  * dequantised), query head h reading KV head h / (n_q_heads / n_kv_heads):
  *   out[b][h] = sum_j softmax_j(softmax_scale * q . k_j) v_j   (bf16)
  *   lse_dev[b][h] = natural-log sum-exp of the scaled scores (fp32; nullable)
- * A sequence with no persisted entry gives out = 0 and lse = -inf.
+ * The history is the persisted entries plus the recent window (bf16).  A
+ * sequence with no visible entry gives out = 0 and lse = -inf.
  * ws_dev: device workspace of at least pask_workspace_bytes(geom, batch,
  * max_ctx_hint) bytes, 256-byte aligned.
  *

@@ -33,6 +33,9 @@ bool valid_geom(const pask_geom* g) {
   if (g->page_tokens != PASK_PAGE_TOKENS) return false;
   if (g->max_tokens_per_seq < 1 || g->max_tokens_per_seq > (1 << 28)) return false;
   if (g->hi_pages < 0 || g->lo_pages < 0) return false;
+  if (g->recent_window < 0 || g->recent_window > g->max_tokens_per_seq) return false;
+  const int64_t ring = (int64_t)g->max_batch * g->n_layers * ((g->recent_window + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS);
+  if (ring + g->hi_pages > INT32_MAX) return false;
   return true;
 }
 
@@ -43,8 +46,11 @@ bool layout_of(const pask_geom* g, pask_cache_layout* L) {
   const uint64_t B = (uint64_t)g->max_batch, NL = (uint64_t)g->n_layers;
   const uint64_t D = (uint64_t)g->head_dim, H = (uint64_t)g->n_kv_heads;
   const uint64_t T = (uint64_t)g->max_tokens_per_seq;
+  const uint64_t W = (uint64_t)g->recent_window;
   L->max_pages = (int32_t)((T + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS);
   L->counter_stride = pask::kCounterStride;
+  L->ring_pages = (int32_t)(B * NL * ((W + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS));
+  L->staging_stride = (int32_t)(T + W + 2);
   L->hi_page_bytes = H * 2 * PASK_PAGE_TOKENS * D * 2;
   L->lo_page_bytes = H * 2 * (PASK_PAGE_TOKENS * (D / 2) + PASK_PAGE_TOKENS * (D / PASK_QGROUP) * 2);
   uint64_t off = 0;
@@ -57,11 +63,13 @@ bool layout_of(const pask_geom* g, pask_cache_layout* L) {
   L->index_list_off = off;
   off = align_up(off + B * NL * 2 * T * 4, kAlignSmall);
   L->staging_off = off;
-  off = align_up(off + B * T * 4, kAlignSmall);
+  off = align_up(off + B * (uint64_t)L->staging_stride * 4, kAlignSmall);
   L->budget_off = off;
-  off = align_up(off + sizeof(pask::BudgetTable), kAlignPool);
+  off = align_up(off + sizeof(pask::BudgetTable), kAlignSmall);
+  L->ring_act_off = off;
+  off = align_up(off + B * NL * W, kAlignPool);
   L->hi_pool_off = off;
-  off = align_up(off + (uint64_t)g->hi_pages * L->hi_page_bytes, kAlignPool);
+  off = align_up(off + ((uint64_t)L->ring_pages + g->hi_pages) * L->hi_page_bytes, kAlignPool);
   L->lo_pool_off = off;
   off = align_up(off + (uint64_t)g->lo_pages * L->lo_page_bytes, kAlignPool);
   L->total_bytes = off;
@@ -79,6 +87,7 @@ CacheView view_of(const pask_cache* c) {
   v.index_list = reinterpret_cast<int32_t*>(base + L.index_list_off);
   v.staging = reinterpret_cast<int32_t*>(base + L.staging_off);
   v.budget = reinterpret_cast<pask::BudgetTable*>(base + L.budget_off);
+  v.ring_act = base + L.ring_act_off;
   v.hi_pool = base + L.hi_pool_off;
   v.lo_pool = base + L.lo_pool_off;
   v.n_layers = c->geom.n_layers;
@@ -86,7 +95,11 @@ CacheView view_of(const pask_cache* c) {
   v.head_dim = c->geom.head_dim;
   v.max_tokens = c->geom.max_tokens_per_seq;
   v.max_pages = L.max_pages;
-  v.hi_pages = c->geom.hi_pages;
+  v.hi_pages = L.ring_pages + c->geom.hi_pages;
+  v.hi_base = L.ring_pages;
+  v.window = c->geom.recent_window;
+  v.ring_pp = (c->geom.recent_window + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS;
+  v.staging_stride = L.staging_stride;
   v.lo_pages = c->geom.lo_pages;
   v.hi_page_bytes = (uint32_t)L.hi_page_bytes;
   v.lo_page_bytes = (uint32_t)L.lo_page_bytes;
@@ -110,6 +123,7 @@ int check_policy(const pask_policy* p, const pask_cache* c) {
   if (p->n_tags < 1 || p->n_tags > PASK_MAX_TAGS || p->n_groups < 1 || p->n_groups > PASK_MAX_GROUPS)
     return PASK_E_POLICY;
   if ((int32_t)p->n_layers != c->geom.n_layers) return PASK_E_SHAPE;
+  if ((int32_t)p->recent_window != c->geom.recent_window) return PASK_E_SHAPE;
   for (uint32_t l = 0; l < p->n_layers; ++l)
     if (p->group_of_layer[l] >= p->n_groups) return PASK_E_POLICY;
   if (p->n_states > PASK_MAX_STATES) return PASK_E_POLICY;
@@ -247,8 +261,8 @@ int pask_policy_load(const void* blob, size_t nbytes, const pask_geom* geom, pas
     const float r = rd<float>(rho + 4 * i);
     if (!(r >= 0.0f) || isinf(r)) return PASK_E_POLICY;
   }
-  if (geom && (int32_t)NL != geom->n_layers) return PASK_E_SHAPE;
-  if (window != 0) return PASK_E_UNSUPPORTED;
+  if (geom && ((int32_t)NL != geom->n_layers || (int64_t)window != (int64_t)geom->recent_window))
+    return PASK_E_SHAPE;
 
   pask_policy p;
   memset(&p, 0, sizeof(p));
@@ -478,6 +492,7 @@ int pask_cache_stats(const pask_policy* policy, const pask_cache* cache, int32_t
     for (int l = 0; l < g.n_layers; ++l) {
       const int32_t* c = &cnt[((size_t)b * g.n_layers + l) * pask::kCounterStride];
       s.n_entries += c[pask::kCntPos];
+      s.n_window += std::min<int64_t>(c[pask::kCntPos], g.recent_window);
       s.n_high += c[pask::kCntHi];
       s.n_low += c[pask::kCntLo];
       s.n_drop += c[pask::kCntDrop];
@@ -495,7 +510,11 @@ int pask_cache_stats(const pask_policy* policy, const pask_cache* cache, int32_t
     }
   s.bytes_high = s.n_high * mH;
   s.bytes_low = s.n_low * mL;
-  s.hi_pages_used = std::min<int64_t>(status[2], g.hi_pages);
+  {
+    pask_cache_layout L2;
+    layout_of(&g, &L2);
+    s.hi_pages_used = std::min<int64_t>(status[2], (int64_t)L2.ring_pages + g.hi_pages) - L2.ring_pages;
+  }
   s.lo_pages_used = std::min<int64_t>(status[3], g.lo_pages);
   const int64_t gov_high = s.n_high - s.n_forced_high;
   const int64_t gov = gov_high + s.n_low + s.n_drop;

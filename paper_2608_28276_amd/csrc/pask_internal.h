@@ -52,11 +52,17 @@ struct CacheView {
   int32_t* counters;      // [max_batch][n_layers][8]
   int32_t* block_table;   // [max_batch][n_layers][2][max_pages]
   int32_t* index_list;    // [max_batch][n_layers][2][max_tokens]
-  int32_t* staging;       // [max_batch][max_tokens]
+  int32_t* staging;       // [max_batch][staging_stride]
   BudgetTable* budget;
-  uint8_t* hi_pool;
+  uint8_t* ring_act;      // [max_batch][n_layers][window]: action | forced << 2
+  uint8_t* hi_pool;       // recent-window pages first, then the HIGH store
   uint8_t* lo_pool;
-  int32_t n_layers, n_kv_heads, head_dim, max_tokens, max_pages, hi_pages, lo_pages;
+  int32_t n_layers, n_kv_heads, head_dim, max_tokens, max_pages, lo_pages;
+  int32_t hi_pages;       // pool pages including the recent windows
+  int32_t hi_base;        // first page of the HIGH store (= recent-window pages)
+  int32_t window;         // W
+  int32_t ring_pp;        // pages of one (sequence, layer) window: ceil(W / 16)
+  int32_t staging_stride; // max_tokens + W + 2 (the last two: the append's p0, n_fit)
   uint32_t hi_page_bytes, lo_page_bytes;
 };
 
@@ -95,7 +101,7 @@ struct AttnArgs {
 
 // Launchers (pask_kernels.hip).  Return hipSuccess or the launch error.
 hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s);
-hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, hipStream_t s);        // chooses the windowed kernels when W > 0
 hipError_t launch_append_step(const AppendArgs& a, hipStream_t s);
 hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s);

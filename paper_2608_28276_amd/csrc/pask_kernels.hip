@@ -68,7 +68,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
 // ---------------------------------------------------------------------------
 __global__ void reset_kernel(CacheView cv, size_t n_counters) {
   const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i0 < 4) cv.status[i0] = 0u;
+  if (i0 < 4) cv.status[i0] = i0 == 2 ? (uint32_t)cv.hi_base : 0u;   // HIGH cursor after the windows
   if (i0 == 0) cv.budget->loaded = 0u;
   for (size_t i = i0; i < n_counters; i += (size_t)gridDim.x * blockDim.x) cv.counters[i] = 0;
 }
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   int n_drop = 0, n_forced = 0, n_lost = 0, n_fit = 0;
   int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
   int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
-  int32_t* stg = cv.staging + (size_t)b * cv.max_tokens;
+  int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
   const bool keep_all = (a.flags & kKeepAll) != 0u;
   const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
   __syncthreads();
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
   const int b = blockIdx.y;
   uint32_t unused = 0;
   const int n = clamp_n_new(a, b, unused);
-  const int32_t* stg = cv.staging + (size_t)b * cv.max_tokens;
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
   const size_t row = (size_t)cv.n_kv_heads * D;
   for (int jj = 0; jj < kPackTokens; ++jj) {
     const int j = (int)blockIdx.x * kPackTokens + jj;
@@ -480,6 +480,58 @@ __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
     if (st == kHi) write_hi<D>(cv, page, slot % kPage, kin, vin);
     else write_lo<D>(cv, page, slot % kPage, kin, vin);
   }
+}
+
+// One token of sequence b (thread 0 of the block): its action (Eq. 10, or
+// the online controller when parser states are given).
+__device__ __forceinline__ int decide_one(const AppendArgs& a, const uint8_t* s_a0, const uint8_t* s_amin, int b,
+                                          int32_t* cnt, int pos, bool& forced, uint32_t& flags) {
+  const CacheView& cv = a.cv;
+  const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new] : 0;
+  bool bad;
+  int act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, (a.flags & kKeepAll) != 0u, tag, pos, forced, bad);
+  if (bad) flags |= PASK_FLAG_BAD_TAG;
+  if (a.states) {
+    if (cv.budget->loaded == kBudgetLoaded) {
+      int64_t* r = budget_of(cnt);
+      int64_t R = *r;
+      act = budget_decide(cv.budget, tag, (int)a.states[(size_t)b * a.max_new], forced, (int)a.tab.group, R, flags);
+      *r = R;
+    } else {
+      flags |= PASK_FLAG_NO_BUDGET;
+    }
+  }
+  return act;
+}
+
+// Persist step of one entry at position pos (thread 0): DROP is counted; a
+// kept entry takes the next slot of its store (a new page when the slot
+// starts one) and its index-list entry.  Returns the store code (store << 30
+// | slot) and the page, or -1 when the entry is not stored.
+__device__ __forceinline__ int slot_one(const CacheView& cv, int b, int layer, int32_t* cnt, int act, bool forced,
+                                        int pos, int& page, uint32_t& flags) {
+  if (act == kDrop) {
+    cnt[kCntDrop] += 1;
+    return -1;
+  }
+  const int st = act == kHigh ? kHi : kLo;
+  const int slot = cnt[st];
+  int32_t* bt = block_table_of(cv, b, layer, st);
+  if (slot % kPage == 0) {
+    const unsigned pid = atomicAdd(&cv.status[2 + st], 1u);
+    const unsigned pool = st == kHi ? (unsigned)cv.hi_pages : (unsigned)cv.lo_pages;
+    if (pid >= pool) {
+      flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+      cnt[kCntLost] += 1;
+      return -1;
+    }
+    bt[slot / kPage] = (int)pid;
+  }
+  page = bt[slot / kPage];
+  index_list_of(cv, b, layer, st)[slot] = pos;
+  cnt[st] = slot + 1;
+  if (forced) cnt[kCntForced] += 1;
+  return (st << 30) | slot;
 }
 
 // One token per sequence: thread 0 decides and slots it, then the block
@@ -503,49 +555,9 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
         flags |= PASK_FLAG_SEQ_CAPACITY;
         cnt[kCntLost] += 1;
       } else {
-        const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new] : 0;
-        bool forced, bad;
-        int act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, (a.flags & kKeepAll) != 0u,
-                         tag, pos, forced, bad);
-        if (bad) flags |= PASK_FLAG_BAD_TAG;
-        if (a.states) {
-          if (cv.budget->loaded == kBudgetLoaded) {
-            int64_t* r = budget_of(cnt);
-            int64_t R = *r;
-            act = budget_decide(cv.budget, tag, (int)a.states[(size_t)b * a.max_new], forced,
-                                (int)a.tab.group, R, flags);
-            *r = R;
-          } else {
-            flags |= PASK_FLAG_NO_BUDGET;
-          }
-        }
-        if (act == kDrop) {
-          cnt[kCntDrop] += 1;
-        } else {
-          const int st = act == kHigh ? kHi : kLo;
-          const int slot = cnt[st];
-          int32_t* bt = block_table_of(cv, b, a.layer, st);
-          bool ok = true;
-          if (slot % kPage == 0) {
-            const unsigned pid = atomicAdd(&cv.status[2 + st], 1u);
-            const unsigned pool = st == kHi ? (unsigned)cv.hi_pages : (unsigned)cv.lo_pages;
-            if (pid >= pool) {
-              ok = false;
-              flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
-            } else {
-              bt[slot / kPage] = (int)pid;
-            }
-          }
-          if (ok) {
-            page = bt[slot / kPage];
-            index_list_of(cv, b, a.layer, st)[slot] = pos;
-            cnt[st] = slot + 1;
-            if (forced) cnt[kCntForced] += 1;
-            code = (st << 30) | slot;
-          } else {
-            cnt[kCntLost] += 1;
-          }
-        }
+        bool forced;
+        const int act = decide_one(a, s_a0, s_amin, b, cnt, pos, forced, flags);
+        code = slot_one(cv, b, a.layer, cnt, act, forced, pos, page, flags);
         cnt[kCntPos] = pos + 1;
       }
     }
@@ -562,6 +574,315 @@ __global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
   const int slot = code & 0x3FFFFFFF;
   if ((code >> 30) == kHi) write_hi<D>(cv, s_page, slot % kPage, kin, vin);
   else write_lo<D>(cv, s_page, slot % kPage, kin, vin);
+}
+
+// ---------------------------------------------------------------------------
+// the protected recent window (Section 3.1)
+// ---------------------------------------------------------------------------
+// With W > 0 a token is decided when it is appended (its action and forced
+// flag go to ring_act, the controller charges it then) and enters the window
+// of its (sequence, layer): window slot p mod W, held in HIGH page layout in
+// pages of the HIGH pool reserved for the windows.  It is persisted by its
+// action when position p + W is appended.
+
+__device__ __forceinline__ int ring_page(const CacheView& cv, int b, int layer, int k) {
+  return (b * cv.n_layers + layer) * cv.ring_pp + k;
+}
+__device__ __forceinline__ uint8_t* ring_act_of(const CacheView& cv, int b, int layer) {
+  return cv.ring_act + ((size_t)b * cv.n_layers + layer) * cv.window;
+}
+
+// The bf16 K and V rows [Hkv][D] of slot t of a HIGH-layout page (the
+// inverse of write_hi), into kout / vout, by the whole block.
+template <int D>
+__device__ __forceinline__ void read_hi_token(const CacheView& cv, int page, int t, uint16_t* kout, uint16_t* vout) {
+  using PL = PageLayout<D>;
+  const uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
+  const int nk = cv.n_kv_heads * (D / 8);
+  for (int x = threadIdx.x; x < nk; x += blockDim.x) {
+    const int g = x / (D / 8), c = x % (D / 8);
+    const int i = c / 4, q = c % 4;
+    const uint8_t* src = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + (i * 64 + q * 16 + t) * 16;
+    *reinterpret_cast<uint4*>(kout + g * D + c * 8) = *reinterpret_cast<const uint4*>(src);
+  }
+  const int nv = cv.n_kv_heads * D;
+  const int qq = t / 4, jj = t % 4;
+  for (int x = threadIdx.x; x < nv; x += blockDim.x) {
+    const int g = x / D, d = x % D;
+    const int m = d / 16, dd = d % 16;
+    const uint16_t* src =
+        reinterpret_cast<const uint16_t*>(pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + PL::kHiV);
+    vout[g * D + d] = src[(((m >> 1) * 64 + qq * 16 + dd) * 2 + (m & 1)) * 4 + jj];
+  }
+}
+
+// Bulk append with a window.  The call's combined index x covers positions
+// q = e0 + x, e0 = max(0, p0 - W): first the window's tokens from before the
+// call (x < nr = p0 - e0; their decisions in ring_act), then the new tokens
+// (j = x - nr).  Positions below e1 = max(e0, p0 + n_fit - W) leave the window
+// now and are slotted into the stores in position order as in
+// append_plan_kernel; the new tokens from e1 on enter the window and their
+// decisions go to ring_act (after every read of ring_act in the chunk: the
+// W positions of the window after the call have distinct slots, so no slot
+// still in the window is overwritten).  staging[x] gets the store code of x
+// or -1; the sequence's last two staging words keep p0 and n_fit for the
+// pack and window-fill kernels.
+template <bool kBudget>
+__global__ __launch_bounds__(256) void append_plan_window_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_wave[4];
+  __shared__ unsigned s_page_base[2];
+  __shared__ int s_granted[2];
+  struct Empty {};
+  __shared__ std::conditional_t<kBudget, BudgetTable, Empty> s_bud;
+  __shared__ uint8_t s_act[kBudget ? 256 : 1];
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  const int W = cv.window;
+  load_table(a.tab, s_a0, s_amin);
+  uint32_t flags = 0;
+  const int n = clamp_n_new(a, b, flags);
+  int32_t* cnt = counters_of(cv, b, a.layer);
+  const int p0 = cnt[kCntPos];
+  const int n_fit = max(0, min(n, cv.max_tokens - p0));
+  if (n_fit < n) flags |= PASK_FLAG_SEQ_CAPACITY;
+  const int e0 = max(0, p0 - W), nr = p0 - e0;
+  const int n_out = max(e0, p0 + n_fit - W) - e0;    // entries leaving the window now
+  const int n_x = nr + n_fit;
+  uint8_t* ract = ring_act_of(cv, b, a.layer);
+  bool budget = false;
+  int64_t R = 0;
+  if constexpr (kBudget) {
+    const uint4* src = reinterpret_cast<const uint4*>(cv.budget);
+    uint4* dst = reinterpret_cast<uint4*>(&s_bud);
+    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += 256) dst[i] = src[i];
+    __syncthreads();
+    budget = s_bud.loaded == kBudgetLoaded;
+    if (!budget && threadIdx.x == 0) flags |= PASK_FLAG_NO_BUDGET;
+    if (budget && threadIdx.x == 0) R = *budget_of(cnt);
+  }
+  int nst[2] = {cnt[kCntHi], cnt[kCntLo]};
+  int n_drop = 0, n_forced = 0, n_lost = 0;
+  int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
+  int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
+  int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const bool keep_all = (a.flags & kKeepAll) != 0u;
+  const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
+  __syncthreads();
+
+  for (int c0 = 0; c0 < n_x; c0 += 256) {
+    const int x = c0 + (int)threadIdx.x;
+    const bool valid = x < n_x;
+    const bool is_new = valid && x >= nr;
+    const int j = x - nr;
+    const int q = e0 + x;
+    if constexpr (kBudget) {
+      if (budget && threadIdx.x == 0) {              // the chunk's new tokens, in position order
+        const int j1 = min(n_fit, c0 + 256 - nr);
+        for (int jj = max(0, c0 - nr); jj < j1; ++jj) {
+          const size_t at = (size_t)b * a.max_new + jj;
+          const int tag = (int)a.tags[at];
+          const bool forced = (uint32_t)(p0 + jj) < s_bud.n_sink || (uint32_t)tag >= s_bud.n_tags;
+          s_act[jj + nr - c0] =
+              (uint8_t)budget_decide(&s_bud, tag, (int)a.states[at], forced, (int)a.tab.group, R, flags);
+        }
+      }
+      __syncthreads();
+    }
+    int act = kDrop;
+    bool forced = false, bad = false;
+    if (is_new) {
+      const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new + j] : 0;
+      act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, keep_all, tag, q, forced, bad);
+      if constexpr (kBudget) {
+        if (budget) act = s_act[threadIdx.x];
+      }
+    } else if (valid) {
+      const uint8_t byte = ract[q % W];
+      act = byte & 3;
+      forced = ((byte >> 2) & 1) != 0;
+    }
+    if (bad) flags |= PASK_FLAG_BAD_TAG;
+    const bool leaving = valid && x < n_out;
+    const int st = act == kHigh ? kHi : kLo;
+    const bool keep = leaving && act != kDrop;
+    int tot_hi, tot_lo, np_hi, np_lo;
+    const int r_hi = block_exclusive_count(keep && st == kHi, s_wave, tot_hi);
+    const int r_lo = block_exclusive_count(keep && st == kLo, s_wave, tot_lo);
+    const int slot = keep ? nst[st] + (st == kHi ? r_hi : r_lo) : 0;
+    const bool new_page = keep && (slot % kPage) == 0;
+    const int pr_hi = block_exclusive_count(new_page && st == kHi, s_wave, np_hi);
+    const int pr_lo = block_exclusive_count(new_page && st == kLo, s_wave, np_lo);
+    if (threadIdx.x == 0) {
+      const int np[2] = {np_hi, np_lo};
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        unsigned base = 0u;
+        int granted = 0;
+        if (np[y] > 0) {
+          base = atomicAdd(&cv.status[2 + y], (unsigned)np[y]);
+          granted = base >= pool[y] ? 0 : (int)min((unsigned)np[y], pool[y] - base);
+        }
+        s_page_base[y] = base;
+        s_granted[y] = granted;
+      }
+    }
+    __syncthreads();                                 // also: every read of ract in this chunk is done
+    int pages_before[2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y) pages_before[y] = (nst[y] + kPage - 1) / kPage;
+    bool stored = false;
+    if (keep) {
+      const int pidx = slot / kPage;
+      stored = pidx < pages_before[st] + s_granted[st];
+      if (stored) {
+        if (new_page) bt[st][pidx] = (int)(s_page_base[st] + (unsigned)(st == kHi ? pr_hi : pr_lo));
+        il[st][slot] = q;
+      } else {
+        flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+      }
+    }
+    if (valid) stg[x] = stored ? ((st << 30) | slot) : -1;
+    if (is_new && !leaving) ract[q % W] = (uint8_t)(act | (forced ? 4 : 0));
+    int c_drop, c_forced, c_lost;
+    block_exclusive_count(leaving && act == kDrop, s_wave, c_drop);
+    block_exclusive_count(stored && forced, s_wave, c_forced);
+    block_exclusive_count(keep && !stored, s_wave, c_lost);
+    const int tot[2] = {tot_hi, tot_lo};
+#pragma unroll
+    for (int y = 0; y < 2; ++y) nst[y] = min(nst[y] + tot[y], (pages_before[y] + s_granted[y]) * kPage);
+    n_drop += c_drop;
+    n_forced += c_forced;
+    n_lost += c_lost;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    cnt[kCntHi] = nst[0];
+    cnt[kCntLo] = nst[1];
+    cnt[kCntPos] = p0 + n_fit;
+    cnt[kCntDrop] += n_drop;
+    cnt[kCntForced] += n_forced;
+    cnt[kCntLost] += n_lost + (n - n_fit);
+    if (budget) *budget_of(cnt) = R;
+    stg[cv.staging_stride - 2] = p0;
+    stg[cv.staging_stride - 1] = n_fit;
+  }
+  if (flags) atomicOr(cv.status, flags);
+}
+
+// Persist the entries the plan marked (x < n_out): from the window (read
+// into LDS first) or from the call's input rows.
+template <int D>
+__global__ __launch_bounds__(256) void append_pack_window_kernel(AppendArgs a) {
+  __shared__ __align__(16) uint16_t s_kv[2][8 * D];   // one window token's K and V rows (Hkv <= 8)
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.y;
+  const int W = cv.window;
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const int p0 = stg[cv.staging_stride - 2], n_fit = stg[cv.staging_stride - 1];
+  const int e0 = max(0, p0 - W), nr = p0 - e0;
+  const int n_out = max(e0, p0 + n_fit - W) - e0;
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  for (int xx = 0; xx < kPackTokens; ++xx) {
+    const int x = (int)blockIdx.x * kPackTokens + xx;
+    if (x >= n_out) break;
+    const int code = stg[x];
+    if (code < 0) continue;
+    const int st = code >> 30, slot = code & 0x3FFFFFFF;
+    const int page = block_table_of(cv, b, a.layer, st)[slot / kPage];
+    const uint16_t *kin, *vin;
+    if (x < nr) {
+      const int ws = (e0 + x) % W;
+      read_hi_token<D>(cv, ring_page(cv, b, a.layer, ws / kPage), ws % kPage, s_kv[0], s_kv[1]);
+      __syncthreads();
+      kin = s_kv[0];
+      vin = s_kv[1];
+    } else {
+      kin = a.k + ((size_t)b * a.max_new + (x - nr)) * row;
+      vin = a.v + ((size_t)b * a.max_new + (x - nr)) * row;
+    }
+    if (st == kHi) write_hi<D>(cv, page, slot % kPage, kin, vin);
+    else write_lo<D>(cv, page, slot % kPage, kin, vin);
+    __syncthreads();                                 // s_kv is reused by the next entry
+  }
+}
+
+// The new tokens that stay in the window (the last min(n_fit, W) of the
+// call) into their window slots; after the pack kernel has read the slots
+// they replace.
+template <int D>
+__global__ __launch_bounds__(256) void append_window_fill_kernel(AppendArgs a) {
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.y;
+  const int W = cv.window;
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const int p0 = stg[cv.staging_stride - 2], n_fit = stg[cv.staging_stride - 1];
+  const int j0 = max(0, n_fit - W);
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  for (int kk = 0; kk < kPackTokens; ++kk) {
+    const int j = j0 + (int)blockIdx.x * kPackTokens + kk;
+    if (j >= n_fit) break;
+    const int ws = (p0 + j) % W;
+    write_hi<D>(cv, ring_page(cv, b, a.layer, ws / kPage), ws % kPage, a.k + ((size_t)b * a.max_new + j) * row,
+                a.v + ((size_t)b * a.max_new + j) * row);
+  }
+}
+
+// One token per sequence with a window: thread 0 decides the new token and,
+// when position pos - W leaves the window, slots that entry by its recorded
+// action; the block then reads the leaving entry from its window slot into
+// LDS, writes the new token into that slot, and persists the leaving entry.
+template <int D>
+__global__ __launch_bounds__(256) void append_step_window_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_code, s_page, s_ws;
+  __shared__ __align__(16) uint16_t s_kv[2][8 * D];
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  const int W = cv.window;
+  load_table(a.tab, s_a0, s_amin);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t flags = 0;
+    const int n = clamp_n_new(a, b, flags);
+    int code = -1, page = -1, ws = -1;
+    if (n > 0) {
+      int32_t* cnt = counters_of(cv, b, a.layer);
+      const int pos = cnt[kCntPos];
+      if (pos >= cv.max_tokens) {
+        flags |= PASK_FLAG_SEQ_CAPACITY;
+        cnt[kCntLost] += 1;
+      } else {
+        bool forced;
+        const int act = decide_one(a, s_a0, s_amin, b, cnt, pos, forced, flags);
+        uint8_t* ract = ring_act_of(cv, b, a.layer);
+        ws = pos % W;
+        if (pos >= W) {                              // position pos - W leaves the window
+          const uint8_t old = ract[ws];
+          code = slot_one(cv, b, a.layer, cnt, old & 3, ((old >> 2) & 1) != 0, pos - W, page, flags);
+        }
+        ract[ws] = (uint8_t)(act | (forced ? 4 : 0));
+        cnt[kCntPos] = pos + 1;
+      }
+    }
+    if (flags) atomicOr(cv.status, flags);
+    s_code = code;
+    s_page = page;
+    s_ws = ws;
+  }
+  __syncthreads();
+  const int code = s_code, ws = s_ws;
+  if (ws < 0) return;
+  const int rpage = ring_page(cv, b, a.layer, ws / kPage);
+  if (code >= 0) read_hi_token<D>(cv, rpage, ws % kPage, s_kv[0], s_kv[1]);
+  __syncthreads();                                   // the leaving entry is read before its slot is reused
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  write_hi<D>(cv, rpage, ws % kPage, a.k + (size_t)b * a.max_new * row, a.v + (size_t)b * a.max_new * row);
+  if (code >= 0) {
+    const int slot = code & 0x3FFFFFFF;
+    if ((code >> 30) == kHi) write_hi<D>(cv, s_page, slot % kPage, s_kv[0], s_kv[1]);
+    else write_lo<D>(cv, s_page, slot % kPage, s_kv[0], s_kv[1]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -847,65 +1168,74 @@ __device__ __forceinline__ int wave_inclusive_scan(int x) {
   return x;
 }
 
-// Pages of the HIGH and LOW stores of sequence b in the layer, and their
-// length in work units: the stream-K decomposition weighs a HIGH page
-// kWeightHi units and a LOW page kWeightLo (PASK_WEIGHT_LO).
+// Pages of sequence b in the layer: the HIGH store, the recent window (HIGH
+// layout, min(n_pos, W) slots) and the LOW store, in that order, and their
+// length in work units: the stream-K decomposition weighs a HIGH or window
+// page kWeightHi units and a LOW page kWeightLo (PASK_WEIGHT_LO).
 constexpr int kWeightHi = 32;
 constexpr int kWeightLo = PASK_WEIGHT_LO;
 static_assert(kWeightLo >= 1 && kWeightLo <= kWeightHi, "LOW page weight out of range");
 struct SeqPages {
-  int n_hi, n_lo, np_hi, np, len;
+  int n_hi, n_win, n_lo;   // slots of the HIGH store, the window, the LOW store
+  int np_hi, np_w, np;     // pages: HIGH store, + window (the HIGH-weight ones), all
+  int len;
 };
-__device__ __forceinline__ int len_of(int n_hi, int n_lo) {
-  return kWeightHi * cdiv(n_hi, kPage) + kWeightLo * cdiv(n_lo, kPage);
+__device__ __forceinline__ int len_of(int n_hi, int n_win, int n_lo) {
+  return kWeightHi * (cdiv(n_hi, kPage) + cdiv(n_win, kPage)) + kWeightLo * cdiv(n_lo, kPage);
 }
-__device__ __forceinline__ SeqPages make_pages(int n_hi, int n_lo) {
+__device__ __forceinline__ SeqPages make_pages(int n_hi, int n_win, int n_lo) {
   SeqPages s;
   s.n_hi = n_hi;
+  s.n_win = n_win;
   s.n_lo = n_lo;
   s.np_hi = cdiv(n_hi, kPage);
-  s.np = s.np_hi + cdiv(n_lo, kPage);
-  s.len = len_of(n_hi, n_lo);
+  s.np_w = s.np_hi + cdiv(n_win, kPage);
+  s.np = s.np_w + cdiv(n_lo, kPage);
+  s.len = len_of(n_hi, n_win, n_lo);
   return s;
 }
+__device__ __forceinline__ int window_slots(const AttnArgs& a, int n_pos) { return min(n_pos, a.cv.window); }
 
 // Store counts of sequence `lane` for the first 64 sequences, read once per
 // block: the plan, the search for a block's first sequence and the walk to
 // the next sequence take them from registers instead of memory.
 struct FirstCounts {
-  int n_hi, n_lo;   // 0 past the batch
+  int n_hi, n_lo, n_win;   // 0 past the batch
 };
 __device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
   const int lane = threadIdx.x & 63;
   const int32_t* c = counters_of(a.cv, lane < a.batch ? lane : 0, a.layer);
-  const int hi = c[kCntHi], lo = c[kCntLo];
+  const int hi = c[kCntHi], lo = c[kCntLo], pos = c[kCntPos];
   FirstCounts f;
   f.n_hi = lane < a.batch ? hi : 0;
   f.n_lo = lane < a.batch ? lo : 0;
+  f.n_win = lane < a.batch ? window_slots(a, pos) : 0;
   return f;
 }
 // Pages of sequence b (wave-uniform, < batch).
 __device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const FirstCounts& f, int b) {
-  if (b < 64) return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_lo, b));
+  if (b < 64)
+    return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_win, b),
+                      __builtin_amdgcn_readlane(f.n_lo, b));
   const int32_t* c = counters_of(a.cv, b, a.layer);
-  return make_pages(uni(c[kCntHi]), uni(c[kCntLo]));
+  return make_pages(uni(c[kCntHi]), uni(window_slots(a, c[kCntPos])), uni(c[kCntLo]));
 }
 // Length in units of sequence c0 + lane (c0 wave-uniform; 0 past `limit`).
 __device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f, int c0, int limit) {
   const int b = c0 + (int)(threadIdx.x & 63);
-  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_lo) : 0;
+  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_win, f.n_lo) : 0;
   const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
-  const int len = len_of(c[kCntHi], c[kCntLo]);
+  const int len = len_of(c[kCntHi], window_slots(a, c[kCntPos]), c[kCntLo]);
   return b < limit ? len : 0;
 }
-// Unit offset of page j (HIGH pages first, then LOW) inside its segment.
+// Unit offset of page j (HIGH-weight pages first, then LOW) inside its segment.
 __device__ __forceinline__ int page_start(const SeqPages& s, int j) {
-  return j < s.np_hi ? kWeightHi * j : kWeightHi * s.np_hi + kWeightLo * (j - s.np_hi);
+  return j < s.np_w ? kWeightHi * j : kWeightHi * s.np_w + kWeightLo * (j - s.np_w);
 }
 // First page whose unit offset is >= u (s.np when there is none).
 __device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
-  if (u <= kWeightHi * s.np_hi) return cdiv(u, kWeightHi);
-  return s.np_hi + min(s.np - s.np_hi, cdiv(u - kWeightHi * s.np_hi, kWeightLo));
+  if (u <= kWeightHi * s.np_w) return cdiv(u, kWeightHi);
+  return s.np_w + min(s.np - s.np_w, cdiv(u - kWeightHi * s.np_w, kWeightLo));
 }
 
 // Stream-K decomposition of one attention call, computed identically by every
@@ -972,9 +1302,11 @@ __device__ __forceinline__ void locate(const AttnArgs& a, const FirstCounts& f, 
 // over DRAM channels.
 constexpr int kIdChunk = 128;
 
-template <int D, int G, bool kIsHi>
+// kWindow: the pages are a recent window, consecutive pool pages from id0 on
+// (bt unused).
+template <int D, int G, bool kIsHi, bool kWindow = false>
 __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes, int head_bytes, int n_heads,
-                                          const int32_t* bt, int p0, int p1, int n_slots, int g,
+                                          const int32_t* bt, int id0, int p0, int p1, int n_slots, int g,
                                           AttnState<D, G>& st, float scale_log2, int q, int n) {
   using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
   const int lane = threadIdx.x & 63;
@@ -990,8 +1322,8 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
   };
   for (int c = p0; c < p1; c += kIdChunk) {
     const int cn = min(kIdChunk, p1 - c);
-    const int ids0 = bt[c + min(lane, cn - 1)];
-    const int ids1 = bt[c + min(64 + lane, cn - 1)];
+    const int ids0 = kWindow ? id0 + c + min(lane, cn - 1) : bt[c + min(lane, cn - 1)];
+    const int ids1 = kWindow ? id0 + c + min(64 + lane, cn - 1) : bt[c + min(64 + lane, cn - 1)];
     auto id = [&](int i) -> int {   // i: wave-uniform, < cn
       return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
     };
@@ -1008,8 +1340,8 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
   }
 }
 
-// Pages [j0, j1) of (b, g) (HIGH pages, then LOW pages).  Writes the output
-// when this block holds all pages of (b, g), else a partial.
+// Pages [j0, j1) of (b, g) (HIGH store, recent window, LOW store): this
+// piece's partial of (b, g), combined with the others by attn_merge.
 template <int D, int G>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
                                                long long seg0, int U, int q, int n) {
@@ -1038,18 +1370,22 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
     st.vw[i] = 0.0f;
   }
   if (j0 < sp.np_hi)
-    run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), j0,
+    run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), 0, j0,
                           min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, q, n);
-  if (j1 > sp.np_hi)
-    run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo),
-                           max(j0, sp.np_hi) - sp.np_hi, j1 - sp.np_hi, sp.n_lo, g, st, a.scale_log2, q, n);
+  if (j0 < sp.np_w && j1 > sp.np_hi)             // the recent window's pages
+    run_pages<D, G, true, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, nullptr,
+                                (b * cv.n_layers + a.layer) * cv.ring_pp, max(j0, sp.np_hi) - sp.np_hi,
+                                min(j1, sp.np_w) - sp.np_hi, sp.n_win, g, st, a.scale_log2, q, n);
+  if (j1 > sp.np_w)
+    run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo), 0,
+                           max(j0, sp.np_w) - sp.np_w, j1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n);
   // Partial of piece `slot` of (b, g): rows of G4 = max(G, 4) query heads,
   // stored as float4s of 4 heads at one dim (index ((q*NM + k)*16 + n)*4 + r
   // for head 4q + r, dim 16k + n): each store instruction writes 256
   // contiguous bytes, and the (max, sum) pairs of the G4 heads sit together.
   // Rows past G hold finite values that are never read into an output.
   constexpr int G4 = G > 4 ? G : 4;
-  if (j1 > sp.np_hi) {                           // remove the code offset of the LOW values
+  if (j1 > sp.np_w) {                            // remove the code offset of the LOW values
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
       const float off = kCodeOffset * head_sum(st.vw[i]);   // head n
@@ -1214,6 +1550,20 @@ hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hi
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
   if (a.max_new == 1 && a.n_new == nullptr) return launch_append_step(a, s);
+  if (a.cv.window > 0) {
+    if (a.states) append_plan_window_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    else append_plan_window_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    const dim3 gp((a.max_new + a.cv.window + kPackTokens - 1) / kPackTokens, a.batch);
+    const dim3 gf((std::min(a.max_new, a.cv.window) + kPackTokens - 1) / kPackTokens, a.batch);
+    if (a.cv.head_dim == 64) {
+      append_pack_window_kernel<64><<<gp, dim3(256), 0, s>>>(a);
+      append_window_fill_kernel<64><<<gf, dim3(256), 0, s>>>(a);
+    } else {
+      append_pack_window_kernel<128><<<gp, dim3(256), 0, s>>>(a);
+      append_window_fill_kernel<128><<<gf, dim3(256), 0, s>>>(a);
+    }
+    return hipGetLastError();
+  }
   if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   else append_plan_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   const dim3 grid((a.max_new + kPackTokens - 1) / kPackTokens, a.batch);
@@ -1223,6 +1573,11 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_append_step(const AppendArgs& a, hipStream_t s) {
+  if (a.cv.window > 0) {
+    if (a.cv.head_dim == 64) append_step_window_kernel<64><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    else append_step_window_kernel<128><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    return hipGetLastError();
+  }
   if (a.cv.head_dim == 64) append_step_kernel<64><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   else append_step_kernel<128><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   return hipGetLastError();

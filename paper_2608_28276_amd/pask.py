@@ -49,7 +49,8 @@ class PaskError(RuntimeError):
 
 class pask_geom(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("max_batch", "n_layers", "n_q_heads", "n_kv_heads", "head_dim",
-                                         "page_tokens", "max_tokens_per_seq", "hi_pages", "lo_pages")]
+                                         "page_tokens", "max_tokens_per_seq", "hi_pages", "lo_pages",
+                                         "recent_window")]
 
 
 class pask_policy(C.Structure):
@@ -70,16 +71,17 @@ class pask_cache(C.Structure):
 
 class pask_cache_layout(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in ("status_off", "counters_off", "block_table_off", "index_list_off",
-                                          "staging_off", "budget_off", "hi_pool_off", "lo_pool_off", "total_bytes",
-                                          "hi_page_bytes", "lo_page_bytes")] + \
-               [("max_pages", C.c_int32), ("counter_stride", C.c_int32)]
+                                          "staging_off", "budget_off", "ring_act_off", "hi_pool_off", "lo_pool_off",
+                                          "total_bytes", "hi_page_bytes", "lo_page_bytes")] + \
+               [("max_pages", C.c_int32), ("counter_stride", C.c_int32), ("ring_pages", C.c_int32),
+                ("staging_stride", C.c_int32)]
 
 
 class pask_stats(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("n_entries", "n_high", "n_low", "n_drop", "n_lost", "n_forced_high",
                                          "bytes_high", "bytes_low", "hi_pages_used", "lo_pages_used")] + \
                [("c_kv_governed", C.c_double), ("c_kv_all", C.c_double), ("device_flags", C.c_uint32),
-                ("reserved", C.c_uint32)]
+                ("reserved", C.c_uint32), ("n_window", C.c_int64)]
 
 
 if not os.path.exists(LIB_PATH):

@@ -6,6 +6,7 @@ libpask.so's kernels through the C ABI binding.
 from __future__ import annotations
 
 import math
+import struct
 
 import torch
 
@@ -19,9 +20,12 @@ class PaskSession:
                  head_dim: int, max_tokens_per_seq: int, hi_pages: int, lo_pages: int,
                  max_ctx_hint: int | None = None, device: str = "cuda:0", extra_bytes: int = 0):
         self.device = torch.device(device)
+        # the recent window W is the table's (blob header word at byte 24)
+        self.window = struct.unpack_from("<I", bytes(policy_blob[:28]), 24)[0] if len(policy_blob) >= 28 else 0
         self.geom = pask.make_geom(max_batch=max_batch, n_layers=n_layers, n_q_heads=n_q_heads,
                                    n_kv_heads=n_kv_heads, head_dim=head_dim,
-                                   max_tokens_per_seq=max_tokens_per_seq, hi_pages=hi_pages, lo_pages=lo_pages)
+                                   max_tokens_per_seq=max_tokens_per_seq, hi_pages=hi_pages, lo_pages=lo_pages,
+                                   recent_window=self.window)
         self.policy = pask.pask_policy_load(policy_blob, self.geom)
         self.nbytes = pask.pask_cache_bytes(self.geom)
         if self.nbytes == 0:
@@ -105,14 +109,47 @@ class PaskSession:
         return self._i32(self.layout.index_list_off, (g.max_batch, g.n_layers, 2, g.max_tokens_per_seq))
 
     def hi_pool(self):
+        """Every page of the HIGH pool: the recent windows, then the HIGH store."""
         L = self.layout
-        return self.buf[L.hi_pool_off:L.hi_pool_off + self.geom.hi_pages * L.hi_page_bytes].view(
-            self.geom.hi_pages, L.hi_page_bytes)
+        n = L.ring_pages + self.geom.hi_pages
+        return self.buf[L.hi_pool_off:L.hi_pool_off + n * L.hi_page_bytes].view(n, L.hi_page_bytes)
 
     def lo_pool(self):
         L = self.layout
         return self.buf[L.lo_pool_off:L.lo_pool_off + self.geom.lo_pages * L.lo_page_bytes].view(
             self.geom.lo_pages, L.lo_page_bytes)
+
+    def _decode_hi(self, raw, pages, n: int):
+        """(k bits, v bits) int64 [n, Hkv, D] of the first n slots of HIGH-layout pages."""
+        import numpy as np
+        D, H = self.geom.head_dim, self.geom.n_kv_heads
+        t = np.arange(16)[:, None]
+        d = np.arange(D)[None, :]
+        x = raw.view(np.uint16).reshape(-1, H, 2, 16 * D).astype(np.int64)
+        kidx = ((d // 32 * 64 + (d % 32) // 8 * 16 + t) * 8 + d % 8)
+        vidx = ((((d // 16) // 2) * 64 + t // 4 * 16 + d % 16) * 2 + (d // 16) % 2) * 4 + t % 4
+        x = x[np.arange(x.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]   # head slots
+        k = x[:, :, 0][:, :, kidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+        v = x[:, :, 1][:, :, vidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
+        return k, v
+
+    def gather_window(self, b: int, layer: int):
+        """The recent window of (b, layer): (positions int64 [m], k bits, v bits
+        int64 [m, Hkv, D]) in position order, m = min(n_pos, W); position p
+        sits in window slot p mod W."""
+        import numpy as np
+        W = self.window
+        n_pos = int(self.counters()[b, layer, 2].item())
+        m = min(n_pos, W)
+        if m == 0:
+            z = np.zeros((0, self.geom.n_kv_heads, self.geom.head_dim), np.int64)
+            return np.zeros(0, np.int64), z, z
+        pp = (W + 15) // 16
+        pages = (b * self.geom.n_layers + layer) * pp + np.arange(pp)
+        raw = self.hi_pool()[torch.as_tensor(pages, dtype=torch.long, device=self.device)].cpu().numpy()
+        k, v = self._decode_hi(raw, pages, W)
+        pos = np.arange(n_pos - m, n_pos)
+        return pos, k[pos % W], v[pos % W]
 
     def gather_store(self, b: int, layer: int, store: int):
         """Host copies of one store's entries, by slot, read through the block
@@ -136,13 +173,7 @@ class PaskSession:
         d = np.arange(D)[None, :]
         kidx = (((d % 32) // 8 * 16 + t) * NG + d // 32) * 8 + d % 8                      # [16, D], LOW K
         if store == 0:
-            x = raw.view(np.uint16).reshape(-1, H, 2, 16 * D).astype(np.int64)
-            kidx = ((d // 32 * 64 + (d % 32) // 8 * 16 + t) * 8 + d % 8)
-            vidx = ((((d // 16) // 2) * 64 + t // 4 * 16 + d % 16) * 2 + (d // 16) % 2) * 4 + t % 4
-            x = x[np.arange(x.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]   # head slots
-            k = x[:, :, 0][:, :, kidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
-            v = x[:, :, 1][:, :, vidx].transpose(0, 2, 1, 3).reshape(-1, H, D)[:n]
-            return k, v
+            return self._decode_hi(raw, pages, n)
         head = 16 * D + 64 * NG
         r = raw.reshape(-1, H, head)
         r = r[np.arange(r.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]       # head slots

@@ -95,10 +95,13 @@ class DeviceRun:
                 a1, f1, _ = oracle.decide(self.gen_tags[b, :n_gen], p + np.arange(n_gen), c, act, flo, ns, False)
                 if b in ctl:
                     a1 = ctl[b][0][:, c]
-                acts = np.concatenate([a0, a1])
-                hi, lo = oracle.compact(acts, np.arange(p + n_gen))
+                # with a recent window W, only the positions below pos - W are persisted (Section 3.1)
+                n_out = max(0, p + n_gen - int(self.pol.recent_window))
+                acts = np.concatenate([a0, a1])[:n_out]
+                forced = np.concatenate([f0, f1])[:n_out]
+                hi, lo = oracle.compact(acts, np.arange(n_out))
                 self.exp[(b, c)] = dict(hi=hi, lo=lo, drop=int((acts == oracle.DROP).sum()),
-                                        forced=int(f0.sum() + f1.sum()), pos=p + n_gen,
+                                        forced=int(forced.sum()), pos=p + n_gen,
                                         R=ctl[b][1] if b in ctl else 0)
 
     # -- inputs ------------------------------------------------------------
@@ -222,4 +225,9 @@ class DeviceRun:
             c = self.oc.counts(b, layer)
             e = self.exp[(b, int(self.gol[layer]))]
             assert (c["hi"], c["lo"], c["R"]) == (e["hi"].size, e["lo"].size, e["R"]), ("oracle replay", b, layer)
+            if self.sess.window:
+                wpos, wk, wv = self.sess.gather_window(b, layer)
+                sl = self.oc.sl(b, layer)
+                assert (wpos == sl.w_pos).all() and (wk == sl.w_k).all() and (wv == sl.w_v).all(), \
+                    ("window", b, layer)
         say(f"stores of {len(self.sample)} sampled pairs bit-exact")

@@ -41,7 +41,7 @@ def assert_attn_close(gpu: np.ndarray, ref: np.ndarray, what: str):
 
 def policy_dict(pol):
     d = dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=pol.n_sink,
-             rho_up=pol.rho_up)
+             rho_up=pol.rho_up, recent_window=pol.recent_window)
     if pol.n_states:
         d.update(n_states=pol.n_states, beta_q=pol.beta_q, reserve_q=pol.reserve_q, crit=pol.crit)
     return d
@@ -194,6 +194,12 @@ class Scenario:
                 assert (kc == okc).all(), ("LOW K codes", layer, b)
                 assert (vc == ovc).all(), ("LOW V codes", layer, b)
                 assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
+                if self.sess.window:
+                    wpos, wk, wv = self.sess.gather_window(b, layer)
+                    sl = self.oc.sl(b, layer)
+                    assert (wpos == sl.w_pos).all(), ("window positions", layer, b)
+                    if wpos.size:
+                        assert (wk == sl.w_k).all() and (wv == sl.w_v).all(), ("window bf16 bits", layer, b)
         st, status, _ = self.sess.stats(batch=self.B)
         sw = self.sess.status_words().cpu().numpy()
         assert st.device_flags == self.expect_flags, (

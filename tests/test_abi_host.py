@@ -115,7 +115,7 @@ def _patch(blob: bytes, off: int, fmt: str, val) -> bytes:
     ("magic", pask.PASK_E_POLICY), ("version", pask.PASK_E_POLICY), ("hash", pask.PASK_E_POLICY),
     ("truncated", pask.PASK_E_POLICY), ("action3", pask.PASK_E_POLICY), ("group_oob", pask.PASK_E_POLICY),
     ("rho_nan", pask.PASK_E_POLICY), ("rho_neg", pask.PASK_E_POLICY), ("n_tags0", pask.PASK_E_POLICY),
-    ("window", pask.PASK_E_UNSUPPORTED), ("layers_mismatch", pask.PASK_E_SHAPE), ("pad", pask.PASK_E_POLICY),
+    ("window", pask.PASK_E_SHAPE), ("layers_mismatch", pask.PASK_E_SHAPE), ("pad", pask.PASK_E_POLICY),
 ])
 def test_policy_load_rejects(case, code):
     pol, blob = blob_for()
@@ -153,6 +153,33 @@ def test_policy_load_rejects(case, code):
     with pytest.raises(pask.PaskError) as e:
         pask.pask_policy_load(bad, geom())
     assert e.value.status == code
+
+
+def test_recent_window_geometry_and_layout():
+    """The table's recent window W must equal the geometry's; the HIGH pool
+    starts with ceil(W/16) window pages per (sequence, layer) and the staging
+    rows grow by W + 2 words."""
+    pol, _ = blob_for()
+    pol.recent_window = 20
+    blob = pack_blob(pol)
+    p = pask.pask_policy_load(blob, geom(recent_window=20))
+    assert p.recent_window == 20
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_policy_load(blob, geom())
+    assert e.value.status == pask.PASK_E_SHAPE
+    L0 = pask.pask_cache_layout_query(geom())
+    L = pask.pask_cache_layout_query(geom(recent_window=20))
+    assert (L0.ring_pages, L0.staging_stride) == (0, 512 + 2)
+    assert (L.ring_pages, L.staging_stride) == (4 * 2 * 2, 512 + 20 + 2)
+    assert L.lo_pool_off - L.hi_pool_off >= (16 + 64) * L.hi_page_bytes
+    assert L.hi_pool_off - L.ring_act_off >= 4 * 2 * 20 and L.ring_act_off >= L.budget_off + 11232
+    assert pask.pask_cache_bytes(geom(recent_window=513)) == 0       # W <= max_tokens_per_seq
+    assert pask.pask_cache_bytes(geom(recent_window=-1)) == 0
+    c = _fake_cache(geom())
+    with pytest.raises(pask.PaskError) as e:                          # a W = 20 table on a W = 0 cache
+        pask.pask_kv_append(pask.pask_policy_load(blob, geom(recent_window=20)), c, 0, 1, None, 4, 1 << 41,
+                            1 << 41, 1 << 41, 0, 0)
+    assert e.value.status == pask.PASK_E_SHAPE
 
 
 def test_layout_and_sizes():

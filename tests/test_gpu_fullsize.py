@@ -165,3 +165,29 @@ def test_qwen3_4b_batch64_online_controller():
     run.step(check=True, fused=True)
     run.check_lists()
     run.check_stores()
+
+
+def test_qwen3_4b_batch64_recent_window():
+    """The timed workload's shapes with a protected recent window of 64
+    positions (Section 3.1): 64 sequences, 36 layers, prompts U{1024..8192}
+    kept HIGH (their last 64 positions pass through the window), 512
+    generated tokens bulk-appended, then a one-token append step and two
+    fused steps.  Every counter and list of all 64 sequences x 36 layers
+    bit-exact; window contents, stores and attention of 6 sequences x the
+    first layer of each group."""
+    from bench import build_workload
+    from tests.fullsize_util import DeviceRun
+    cfg, P, tags, pol = build_workload(2)
+    pol.recent_window = 64
+    say(f"case: {cfg.name} with a 64-position recent window")
+    sample = [(b, l) for b in (1, 17, 30, 44, 58, 62) for l in (0, 9, 18, 27)]
+    run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
+                    Hkv=cfg.n_kv_heads, D=cfg.head_dim, P=P, prompt_tags=None, gen_tags=tags, sample=sample,
+                    seed=cfg.seed, n_bulk=512, n_steps=3)
+    run.fill()
+    run.check_lists()
+    run.step(check=False)
+    run.step(check=True, fused=True)
+    run.step(check=True, fused=True)
+    run.check_lists()
+    run.check_stores()

@@ -20,7 +20,7 @@ Blob layout (little-endian), version 1:
   12 u32      n_groups
   16 u32      n_layers
   20 u32      n_sink          (leading positions of every sequence kept HIGH)
-  24 u32      recent_window   (protected recent window; only 0 is supported)
+  24 u32      recent_window   (protected recent window W, Section 3.1)
   28 u32      payload bytes
   32 u8       group_of_layer[n_layers]
      u8       action[n_tags][n_groups]   selected action a0
