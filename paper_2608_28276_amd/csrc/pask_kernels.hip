@@ -1314,9 +1314,11 @@ __device__ __forceinline__ void locate(const AttnArgs& a, const FirstCounts& f, 
 // Stream pages [p0, p1) of one store of (b, g), loading page p+1 while
 // computing page p.  The page ids come from the block table kIdChunk at a time, one per
 // lane, and are read with readlane, so a page's loads depend on no other
-// memory access.  The prefetches are unconditional (past the end the last
-// page is loaded again, an L2 hit): the loop body is straight-line code and
-// the compiler waits only for the current page's loads.  KV head g of a page
+// memory access.  The prefetches are unconditional (past the end they read
+// the pool's first head slot, which every worker reads there, so they hit in
+// the caches; the non-temporal page loads would not hit on a re-read of the
+// run's last page): the loop body is straight-line code and the compiler
+// waits only for the current page's loads.  KV head g of a page
 // sits in head slot (g + page) mod n_kv_heads, which spreads one head's data
 // over DRAM channels.
 constexpr int kIdChunk = 128;
@@ -1329,8 +1331,9 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
                                           AttnState<D, G>& st, float scale_log2, int q, int n) {
   using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
   const int lane = threadIdx.x & 63;
-  auto load = [&](int page) -> Raw {
+  auto load = [&](int page, bool real) -> Raw {
     const uint8_t* head = pool + (size_t)page * page_bytes + (size_t)((g + page) % n_heads) * head_bytes;
+    head = real ? head : pool;   // past the end: the pool's first head slot, read by every worker
     if constexpr (kIsHi) return load_hi<D>(head, q, n);
     else return load_lo<D>(head, q, n);
   };
@@ -1346,7 +1349,7 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
     auto id = [&](int i) -> int {   // i: wave-uniform, < cn
       return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
     };
-    auto ld = [&](int i) -> Raw { return load(id(min(i, cn - 1))); };
+    auto ld = [&](int i) -> Raw { return load(id(min(i, cn - 1)), i < cn); };
     // Two page buffers used in turn (unrolled by two), so no buffer is
     // copied while its loads are in flight.
     Raw x0 = ld(0);
