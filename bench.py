@@ -37,12 +37,16 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def build_workload(cfg_idx: int):
-    from workload import CONFIGS, make_policy, prompt_lengths, tag_mix, walk_function_calls
+def build_workload(cfg_idx: int, beta: float | None = None):
+    """Workload shapes, generated-token tags [B, T], the policy table and,
+    for the prompt-side workload, the prompt labels [B, max P] (else None)."""
+    from workload import CONFIGS, make_policy, prompt_lengths, schema_prompt_tags, tag_mix, walk_function_calls
     from workload.tags import iid_tags
     from workload.tensors import sub_seed
     cfg = CONFIGS[cfg_idx]
     P = prompt_lengths(cfg)
+    if beta is None:
+        beta = cfg.budgets[0] if len(cfg.budgets) == 1 else 0.33
     if cfg.tag_source == "walker":
         tags = np.stack([walk_function_calls(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b))
                          for b in range(cfg.batch)])
@@ -50,9 +54,17 @@ def build_workload(cfg_idx: int):
     else:
         tags = np.stack([iid_tags(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)])
         probs = None
-    beta = cfg.budgets[0] if len(cfg.budgets) == 1 else 0.33
-    pol = make_policy(6, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs)
-    return cfg, P, tags.astype(np.uint8), pol
+    ptags = None
+    if cfg.prompt_tagged:
+        # prompt-side companion: prompt labels under the same table (12 tags), sinks kept HIGH
+        ptags = np.zeros((cfg.batch, int(P.max())), np.uint8)
+        for b, p in enumerate(P):
+            ptags[b, :p] = schema_prompt_tags(int(p), sub_seed(cfg.seed, "prompt_tags", b))
+        probs = tag_mix(np.concatenate([ptags[b, :P[b]] for b in range(cfg.batch)] + [tags.ravel()]), 12)
+        pol = make_policy(12, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs, n_sink=cfg.n_sink)
+    else:
+        pol = make_policy(6, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs)
+    return cfg, P, tags.astype(np.uint8), pol, ptags
 
 
 def controller_inputs(cfg, tags, pol):
@@ -110,7 +122,32 @@ class HipEvent:
             HipEvent._hip.hipEventDestroy(self._e)
 
 
-def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=None):
+def plan_pool_pages(cfg, P, tags, pol, ptags, online: bool):
+    """Pages of the HIGH and LOW pools for the whole run (memory planning on
+    the host, as a server holding the table and the tag streams would do):
+    the frozen table's action of every (token, layer group) - the higher of
+    selected action and floor, sinks and keep-all prompts HIGH - counted per
+    (sequence, layer) store.  Under the online controller the actions move
+    with the budget, so every token gets room in both pools."""
+    B, L, T = cfg.batch, cfg.layers_resident, cfg.gen_tokens
+    pages = lambda n: int(np.sum((np.asarray(n) + 15) // 16))
+    if online:
+        return L * pages(P + T), L * pages((P if ptags is not None else 0) + np.full(B, T))
+    act = np.maximum(np.asarray(pol.action), np.asarray(pol.floor))          # [tags, groups]
+    gol = np.asarray(pol.group_of_layer)[:L]
+    hi = lo = 0
+    for b in range(B):
+        z = np.concatenate([ptags[b, :P[b]] if ptags is not None else np.zeros(P[b], np.uint8), tags[b, :T]])
+        forced = np.arange(z.size) < (pol.n_sink if ptags is not None else P[b])   # sinks / kept prompt
+        for c in np.unique(gol):
+            a = np.where(forced, 2, act[z, c])
+            n_layers_c = int(np.sum(gol == c))
+            hi += n_layers_c * pages(int(np.sum(a == 2)))
+            lo += n_layers_c * pages(int(np.sum(a == 1)))
+    return hi + L * B, lo + L * B                                            # + one spare page per store
+
+
+def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=None, ptags=None):
     import torch
 
     from paper_2608_28276_amd import pask
@@ -121,9 +158,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     B, L, Hq, Hkv, D = cfg.batch, cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     T = cfg.gen_tokens
     assert t_start + warmup + steps <= T, "not enough generated tokens for the requested steps"
-    pages = lambda n: int(np.sum((np.asarray(n) + 15) // 16))
-    hi_pages = L * pages(P + T)
-    lo_pages = L * pages(np.full(B, T))
+    hi_pages, lo_pages = plan_pool_pages(cfg, P, tags, pol, ptags, online=states is not None)
     max_tok = int(P.max()) + T
     sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=cfg.n_layers, n_q_heads=Hq, n_kv_heads=Hkv,
                        head_dim=D, max_tokens_per_seq=max_tok, hi_pages=hi_pages, lo_pages=lo_pages,
@@ -136,11 +171,15 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     g.manual_seed(cfg.seed)
     n_new = torch.as_tensor(P, dtype=torch.int32, device=dev)
     tags_dev = torch.as_tensor(tags, device=dev)
+    ptags_dev = None if ptags is None else torch.as_tensor(ptags, device=dev)
     t0 = time.time()
     for layer in range(L):
         k = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
         v = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-        sess.append(layer, None, k, v, n_new=n_new, keep_all=True)
+        if ptags_dev is None:                            # decode workloads: the prompt stays HIGH
+            sess.append(layer, None, k, v, n_new=n_new, keep_all=True)
+        else:                                            # prompt-side companion: labelled prompt, sinks HIGH
+            sess.append(layer, ptags_dev, k, v, n_new=n_new)
         del k, v
         if t_start:
             k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
@@ -235,7 +274,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     return res
 
 
-def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None):
+def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None, ptags=None):
     """The oracle as it stands, on a bounded sample: n_seq sequences of the
     same workload (their prompt lengths and tag streams, seeded CPU inputs),
     history built untimed, then one timed decode step through all layers."""
@@ -252,7 +291,7 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None):
     oc = oracle.OracleCache(pd, Hkv, D)
     st_of = (lambda b, t0, t1: None) if states is None else (lambda b, t0, t1: states[b, t0:t1])
     bits = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
-    seqs = list(range(n_seq))
+    seqs = list(range(min(n_seq, cfg.batch)))
     for b in seqs:
         if states is not None:
             oc.budget_init(b, range(L), cfg.gen_tokens)
@@ -260,7 +299,10 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None):
             p = int(P[b])
             k = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_k", layer, b))
             v = bf16_normal((p + t_start, Hkv, D), sub_seed(cfg.seed, "prompt_v", layer, b))
-            oc.append(layer, b, np.zeros(p, np.uint8), bits(k[:p]), bits(v[:p]), keep_all=True)
+            if ptags is None:
+                oc.append(layer, b, np.zeros(p, np.uint8), bits(k[:p]), bits(v[:p]), keep_all=True)
+            else:
+                oc.append(layer, b, ptags[b, :p], bits(k[:p]), bits(v[:p]))
             oc.append(layer, b, tags[b, :t_start], bits(k[p:]), bits(v[p:]), states=st_of(b, 0, t_start))
     q = bf16_normal((L, Hq, D), sub_seed(cfg.seed, "q", 0))
     kn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_k", 0))
@@ -275,8 +317,8 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None):
                       states=st_of(b, t_start, t_start + 1))
             oc.attend(layer, b, bits(q[layer]), scale)
     el = time.perf_counter() - t0
-    return dict(value=n_seq / el, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{n_seq} sequences (prompts {', '.join(str(int(P[b])) for b in seqs)} + {t_start} "
+    return dict(value=len(seqs) / el, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{len(seqs)} sequences (prompts {', '.join(str(int(P[b])) for b in seqs)} + {t_start} "
                        f"generated tokens) x 1 decode step x {L} layers, fp64 numpy, {el:.1f} s")
 
 
@@ -286,11 +328,18 @@ def kernel_source_digest() -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def traffic_record(cfg):
+def prompt_desc(cfg) -> str:
+    if cfg.prompt_dist == "fixed":
+        return str(cfg.prompt_min)
+    return f"{'logU' if cfg.prompt_dist == 'loguniform' else 'U'}{{{cfg.prompt_min}..{cfg.prompt_max}}}"
+
+
+def traffic_record(workload: str):
     """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary of this workload, or None when the kernel source has changed since
-    the counters were taken (or no summary exists)."""
-    path = os.path.join(ROOT, "profiles", f"attn_kernel_{cfg.name}.md")
+    summary of this workload (options included in its name), or None when the
+    kernel source has changed since the counters were taken (or no summary
+    exists)."""
+    path = os.path.join(ROOT, "profiles", f"attn_kernel_{workload}.md")
     if not os.path.exists(path):
         return None
     for line in open(path):
@@ -337,7 +386,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload index (default: the B=64 serving batch)")
-    ap.add_argument("--t-start", type=int, default=512, help="generated tokens persisted before timing")
+    ap.add_argument("--t-start", type=int, default=None,
+                    help="generated tokens persisted before timing (default: min(512, half the generation))")
+    ap.add_argument("--budget", type=float, default=None,
+                    help="KV budget of the policy table (default: the workload's; 0.33 for the budget sweep)")
     ap.add_argument("--cpu-seqs", type=int, default=3, help="sequences in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--window", type=int, default=0, metavar="W",
@@ -354,19 +406,26 @@ def main():
         print(f"bench.py runs on one GPU only: the PASK hot path here has no cross-GPU part "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
-    cfg, P, tags, pol = build_workload(args.config)
+    from workload import CONFIGS
+    cfg0 = CONFIGS[args.config]
+    beta = args.budget if args.budget is not None else (cfg0.budgets[0] if len(cfg0.budgets) == 1 else 0.33)
+    if args.t_start is None:
+        args.t_start = min(512, cfg0.gen_tokens // 2)
+    cfg, P, tags, pol, ptags = build_workload(args.config, beta)
     pol.recent_window = args.window
+    workload = (cfg.name + (f"_beta{beta:g}" if len(cfg.budgets) > 1 or beta not in cfg.budgets else "") +
+                (f"+window{args.window}" if args.window else "") + ("+controller" if args.controller else ""))
     states = None
     if args.controller:
         states, pol = controller_inputs(cfg, tags, pol)
     log(f"workload {cfg.name}: B={cfg.batch} L={cfg.n_layers} prompts {int(P.min())}..{int(P.max())}, "
         f"policy expected cost {pol.expected_cost:.3f}")
-    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, states)
+    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, states, ptags)
     log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
         f"{g['achieved']:.0f} GB/s algorithmic")
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs, states)
+        cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs, states, ptags)
         log(f"cpu oracle: {cpu['value']:.3f} tokens/s on {cpu['cores']} threads")
     line = {
         "metric": METRIC,
@@ -382,11 +441,12 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": cfg.name + (f"+window{args.window}" if args.window else "") +
-                        ("+controller" if args.controller else ""), "batch": cfg.batch, "layers": cfg.n_layers, "layer_groups": cfg.n_groups,
+            "workload": workload, "batch": cfg.batch, "layers": cfg.n_layers, "layer_groups": cfg.n_groups,
+            "resident_layers": cfg.layers_resident,
             "q_heads": cfg.n_q_heads, "kv_heads": cfg.n_kv_heads, "head_dim": cfg.head_dim,
-            "prompt_tokens": f"U{{{cfg.prompt_min}..{cfg.prompt_max}}}", "generated_before_timing": args.t_start,
-            "budget": 0.33, "realised_c_kv_generated": round(g["c_kv_governed"], 4),
+            "prompt_tokens": prompt_desc(cfg), "prompt_tagged": cfg.prompt_tagged, "n_sink": int(pol.n_sink),
+            "generated_before_timing": args.t_start,
+            "budget": beta, "realised_c_kv_governed": round(g["c_kv_governed"], 4),
             "realised_c_kv_all": round(g["c_kv_all"], 4), "page_tokens": 16,
             "mean_persisted_entries": round(g["mean_entries"], 1),
             "hbm_gb_per_step": round(g["bytes_per_step"] / 1e9, 3),
@@ -395,7 +455,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(cfg),
+            "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(workload),
             "kernel": f"attn_kernel<{cfg.head_dim}, {cfg.group_size}> + attn_merge_kernel<{cfg.head_dim}, "
                       f"{cfg.group_size}> (one pask_decode_attn call)",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),

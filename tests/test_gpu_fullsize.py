@@ -64,7 +64,7 @@ def test_qwen3_4b_batch64_bench_launch():
     sequences x the first layer of each group."""
     from bench import build_workload
     from tests.fullsize_util import DeviceRun
-    cfg, P, tags, pol = build_workload(2)
+    cfg, P, tags, pol, _ = build_workload(2)
     say(f"case: {cfg.name}")
     sample = [(b, l) for b in (0, 9, 21, 33, 42, 50, 63) for l in (0, 9, 18, 27)]
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
@@ -146,7 +146,7 @@ def test_qwen3_4b_batch64_online_controller():
     from tests.fullsize_util import DeviceRun
     from workload.policy import with_budget_controller
     from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
-    cfg, P, tags, pol = build_workload(2)
+    cfg, P, tags, pol, _ = build_workload(2)
     say(f"case: {cfg.name} with the online controller")
     n_gen = 515
     ts = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
@@ -177,7 +177,7 @@ def test_qwen3_4b_batch64_recent_window():
     first layer of each group."""
     from bench import build_workload
     from tests.fullsize_util import DeviceRun
-    cfg, P, tags, pol = build_workload(2)
+    cfg, P, tags, pol, _ = build_workload(2)
     pol.recent_window = 64
     say(f"case: {cfg.name} with a 64-position recent window")
     sample = [(b, l) for b in (1, 17, 30, 44, 58, 62) for l in (0, 9, 18, 27)]
