@@ -14,11 +14,13 @@
 //   attn         grouped-query flash-decode, stream-K: one single-wave block
 //                per resident wave slot, each streaming an equal contiguous
 //                range of the (sequence, KV head, page) list over the HIGH and
-//                LOW stores; q.k and p.v on bf16 MFMA (query heads as rows),
-//                int4 codes widened to bf16 in registers with an exact offset
-//                removed after the products, the K scale applied per 32-dim
-//                group and the V scale folded into p,
-//                online softmax in base 2, next page prefetched into registers.
+//                LOW stores; q.k on bf16 MFMA (query heads as columns), int4
+//                K codes widened exactly to bf16 in registers with the offset
+//                removed in the accumulator, the K scale applied per 32-dim
+//                group; p.v on bf16 MFMA for HIGH pages and on fp16 MFMA with
+//                exact fp16 V codes and the V scale folded into p for LOW
+//                pages; online softmax in base 2, next pages prefetched into
+//                registers.
 //   attn_merge   per (sequence, KV head): combine the partials of its pieces
 //                (max, sum, values) into bf16 outputs; zero for empty histories.
 #include <hip/hip_runtime.h>
@@ -902,14 +904,16 @@ __global__ __launch_bounds__(256) void append_step_window_kernel(AppendArgs a) {
 //   scores  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: rows = slots, columns
 //           = query heads, so lane (q, n) holds the scores of head n for
 //           slots 4q..4q+3; a LOW code c becomes the bf16 value 136 + c
-//           (exact) and 136 * sum(q) is removed per 32-dim group before the
-//           K scale is applied;
+//           (exact), the accumulation starts at -136 * sum(q) of the 32-dim
+//           group, and the K scale multiplies the group's result;
 //   softmax online in base 2, per head, rescaling only when a max grows;
-//   values  O += P V on v_mfma_f32_16x16x16_bf16 with P (split into bf16
-//           high and low parts, so p keeps ~16 bits) as the A operand exactly
-//           as the score tile lies; LOW pages fold the V scale into p and
-//           remove the code offset once per segment.
-// The next page's operands are loaded while the current one is computed.
+//   values  HIGH: O += P V on v_mfma_f32_16x16x16_bf16 with P (split into
+//           bf16 high and low parts, so p keeps ~16 bits) as the A operand
+//           exactly as the score tile lies; LOW: the weights p x (V scale)
+//           rounded to fp16 times the codes as exact fp16 values on
+//           v_mfma_f32_16x16x16_f16, into the same accumulators.
+// The next page's operands (three pages ahead for LOW pages, whose scales
+// take one register) are loaded while the current one is computed.
 // Each segment leaves (max, sum, unnormalised o) per head; attn_merge
 // combines the partials of a (b, g).
 
@@ -969,9 +973,8 @@ struct HiRaw {
 template <int D>
 struct LoRaw {
   uint32_t kc[PageLayout<D>::NG];      // NG x 8 int4 codes
-  uint32_t ks[2 * PageLayout<D>::NG];  // K scales of this lane's 4 slots (fp16)
   uint32_t vc[PageLayout<D>::NM / 2];  // 4 slots x NM/2 bytes of V code pairs
-  uint32_t vs[2 * PageLayout<D>::NG];  // V scales of this lane's 4 slots (fp16)
+  uint32_t sc;                         // word n of the row's scales (load_lo)
 };
 
 template <int D>
@@ -996,10 +999,17 @@ template <int D>
 __device__ __forceinline__ LoRaw<D> load_lo(const uint8_t* head, int q, int n) {
   using PL = PageLayout<D>;
   LoRaw<D> x;
+  constexpr int KW = 2 * PL::NG;                 // scale words of 4 slots
   load_words(head + (q * 16 + n) * PL::NG * 4, x.kc);
-  load_words(head + PL::kLoKS + 4 * q * PL::NG * 2, x.ks);
   load_words(head + PL::kLoVC + (q * 16 + n) * (PL::NM / 2) * 4, x.vc);
-  load_words(head + PL::kLoVS + 4 * q * PL::NG * 2, x.vs);
+  // Row q (slots 4q..4q+3) needs KW words of K scales and KW of V scales,
+  // the same for its 16 lanes: lane n loads one of them (n < KW: K word n,
+  // then V word n - KW; spare lanes repeat K word 0) and attend_page shares
+  // them across the row, so a page's scales cost one 4-byte load per lane
+  // and one register instead of 2 x KW per lane.
+  const int off = n < KW ? PL::kLoKS + 4 * (q * KW + n)
+                         : (n < 2 * KW ? PL::kLoVS + 4 * (q * KW + n - KW) : PL::kLoKS + 4 * q * KW);
+  x.sc = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(head + off));
   return x;
 }
 
@@ -1017,11 +1027,11 @@ __device__ __forceinline__ void split_bf16x4(const float (&x)[4], uint2& hi, uin
   r[3] = x[3] - bf16_hi(hi.y);
   lo = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
 }
-// int4 codes widened to bf16 with an offset: a nibble n (two's complement
+// K codes widened to bf16 with an offset: a nibble n (two's complement
 // code c) becomes the bf16 bit pattern 0x4300 | (n ^ 8), the exact value
 // 128 + (c + 8) = 136 + c (bf16 spacing is 1 on [128, 256)).  Two codes per
-// 32-bit word cost one byte permute and one xor; the offset 136 is removed
-// after the products (kOffset * sum of the other operand).
+// 32-bit word cost one byte permute and one xor; the offset is removed by
+// starting the q.k accumulation at -136 * (sum of q over the group).
 constexpr float kCodeOffset = 136.0f;
 constexpr uint32_t kCodeBias = 0x43084308u;
 // Codes 2e (low nibble) and 2e+1 (high nibble) of byte e of w, as a bf16 pair.
@@ -1031,10 +1041,18 @@ __device__ __forceinline__ uint32_t codes_pair_in_byte(uint32_t lo4, uint32_t hi
   // 4-7 bytes of the first (hi4), 0x0C gives zero.
   return __builtin_amdgcn_perm(hi4, lo4, 0x0C000C00u | ((4u + e) << 16) | e) ^ kCodeBias;
 }
-// Nibbles in bytes j0 and j1 of n4 (one nibble per byte) as a bf16 pair.
+// V codes as exact fp16 values.  After n ^ 8 (done once per word) a nibble
+// holds c + 8; the fp16 bit pattern 0x6400 | (c + 8) is 1024 + c + 8 (fp16
+// spacing is 1 on [1024, 2048)), and one packed fp16 subtraction of 1032
+// leaves c exactly.  Nibbles in bytes j0 and j1 of n4 (one per byte) as an
+// fp16 pair; the 0x64 bytes come from the constant first source.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 template <int j0, int j1>
-__device__ __forceinline__ uint32_t codes_pair_from_bytes(uint32_t n4) {
-  return __builtin_amdgcn_perm(n4, n4, 0x0C000C00u | (j1 << 16) | j0) ^ kCodeBias;
+__device__ __forceinline__ uint32_t vcodes_pair(uint32_t n4) {
+  const uint32_t w = __builtin_amdgcn_perm(0x64646464u, n4, 0x04000400u | (j1 << 16) | j0);
+  const f16x2_t c = __builtin_bit_cast(f16x2_t, w) - f16x2_t{(_Float16)1032.0f, (_Float16)1032.0f};
+  return __builtin_bit_cast(uint32_t, c);
 }
 
 // Per-wave attention state.  The score tile is S^T (MFMA row = slot 4q + r,
@@ -1044,10 +1062,9 @@ __device__ __forceinline__ uint32_t codes_pair_from_bytes(uint32_t n4) {
 template <int D, int G>
 struct AttnState {
   uint32_t qa[4 * PageLayout<D>::NG];   // QK B operands: q of head n, dims 32i + 8q + 0..7
-  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs (LOW values carry the code offset)
+  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs
   float m, l;                            // head n: running max (log2 units), lane-partial sum
-  float kq[PageLayout<D>::NG];           // head n: offset x sum of q over 32-dim group i
-  float vw[PageLayout<D>::NG];           // head n: lane-partial sum of p x (V scale of group i)
+  float kq[PageLayout<D>::NG];           // head n: -(K code offset) x sum of q over 32-dim group i
 };
 
 // Max / sum over the 64 lanes' copies of one head (lanes n, n+16, n+32,
@@ -1068,29 +1085,47 @@ __device__ __forceinline__ float head_sum(float x) {
   return __uint_as_float(t[0]) + __uint_as_float(t[1]);
 }
 
+// Word j of the row, for every lane of the row: DPP row_newbcast:j copies
+// lane j of each 16-lane row to the whole row.
+template <int J>
+__device__ __forceinline__ uint32_t row_word(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x150 + J, 0xF, 0xF, false);
+}
+// The row's KW K-scale words (lanes 0..KW-1) and KW V-scale words (lanes KW..2KW-1).
+template <int KW, int J = 0>
+__device__ __forceinline__ void row_words(uint32_t x, uint32_t (&k)[KW], uint32_t (&v)[KW]) {
+  if constexpr (J < KW) {
+    k[J] = row_word<J>(x);
+    v[J] = row_word<KW + J>(x);
+    row_words<KW, J + 1>(x, k, v);
+  }
+}
+
 // One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
 template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
 __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2,
                                             int q, int n) {
   using PL = PageLayout<D>;
   f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+  [[maybe_unused]] uint32_t ks[2 * PL::NG], vs[2 * PL::NG];   // LOW: the row's K / V scale words
   if constexpr (kIsHi) {
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i)
       sc = mfma_k32(make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]),
                     make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), sc);
   } else {
+    row_words<2 * PL::NG>(x.sc, ks, vs);
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
       const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;
-      const f32x4_t zero = {0.0f, 0.0f, 0.0f, 0.0f};
+      const f32x4_t off = {st.kq[i], st.kq[i], st.kq[i], st.kq[i]};   // removes the code offset
       const f32x4_t c = mfma_k32(make_uint4(codes_pair_in_byte<0>(lo4, hi4), codes_pair_in_byte<1>(lo4, hi4),
                                             codes_pair_in_byte<2>(lo4, hi4), codes_pair_in_byte<3>(lo4, hi4)),
-                                 make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), zero);
+                                 make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), off);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
         const int hidx = r * PL::NG + i;
-        sc[r] = fmaf(half_bits_to_float(x.ks[hidx / 2] >> (16 * (hidx % 2))), c[r] - st.kq[i], sc[r]);
+        sc[r] = fmaf(half_bits_to_float(ks[hidx / 2] >> (16 * (hidx % 2))), c[r], sc[r]);
       }
     }
   }
@@ -1103,13 +1138,9 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
   // Online softmax for head n: rescale only when some head's max grew.
   const float mn = fmaxf(st.m, head_max(mx));
   if (__ballot(mn > st.m)) {
-    const float alpha = exp2f(st.m - mn);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mn);
     st.l *= alpha;
     st.m = mn;
-    if constexpr (!kIsHi) {
-#pragma unroll
-      for (int i = 0; i < PL::NG; ++i) st.vw[i] *= alpha;
-    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {                   // output row 4q + r takes head 4q + r's factor
       const float ar = __shfl(alpha, 4 * q + r);
@@ -1117,10 +1148,12 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
       for (int k = 0; k < PL::NM; ++k) st.acc[k][r] *= ar;
     }
   }
+  // exp2 on v_exp_f32 directly: arguments are <= 0, and results that would
+  // be fp32 subnormals (weights below 2^-126 of the running max) become 0.
   float pr[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    pr[r] = exp2f(sc[r] - st.m);
+    pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
     st.l += pr[r];
   }
   if constexpr (kIsHi) {
@@ -1138,25 +1171,26 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
       st.acc[mm] = mfma_k16(pa_lo, make_uint2(v0, v1), st.acc[mm]);
     }
   } else {
+    // V: the weights p x (V scale of the slot's group), rounded once to
+    // fp16 (11 significant bits), times the exact fp16 codes on the fp16
+    // MFMA.  Slots past the end get weight 0 (their scales are not written).
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
       float w[4];
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
         const int hidx = jj * PL::NG + i;
-        const float vs = half_bits_to_float(x.vs[hidx / 2] >> (16 * (hidx % 2)));
-        w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vs : 0.0f;
+        const float vsc = half_bits_to_float(vs[hidx / 2] >> (16 * (hidx % 2)));
+        w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vsc : 0.0f;
       }
-      st.vw[i] += (w[0] + w[1]) + (w[2] + w[3]);
-      uint2 pa_hi, pa_lo;
-      split_bf16x4(w, pa_hi, pa_lo);
+      const f16x4_t wa = {(_Float16)w[0], (_Float16)w[1], (_Float16)w[2], (_Float16)w[3]};
+      const uint32_t vx = x.vc[i] ^ 0x88888888u;     // nibbles c + 8
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         // byte jj of vc[i]: slot 4q + jj, dim 32i + n (low nibble) and 32i + 16 + n (high)
-        const uint32_t n4 = (hh ? x.vc[i] >> 4 : x.vc[i]) & 0x0F0F0F0Fu;
-        const uint32_t b0 = codes_pair_from_bytes<0, 1>(n4), b1 = codes_pair_from_bytes<2, 3>(n4);
-        st.acc[2 * i + hh] = mfma_k16(pa_hi, make_uint2(b0, b1), st.acc[2 * i + hh]);
-        st.acc[2 * i + hh] = mfma_k16(pa_lo, make_uint2(b0, b1), st.acc[2 * i + hh]);
+        const uint32_t n4 = (hh ? vx >> 4 : vx) & 0x0F0F0F0Fu;
+        const f16x4_t vb = __builtin_bit_cast(f16x4_t, make_uint2(vcodes_pair<0, 1>(n4), vcodes_pair<2, 3>(n4)));
+        st.acc[2 * i + hh] = __builtin_amdgcn_mfma_f32_16x16x16f16(wa, vb, st.acc[2 * i + hh], 0, 0, 0);
       }
     }
   }
@@ -1350,14 +1384,30 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
       return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
     };
     auto ld = [&](int i) -> Raw { return load(id(min(i, cn - 1)), i < cn); };
-    // Two page buffers used in turn (unrolled by two), so no buffer is
-    // copied while its loads are in flight.
-    Raw x0 = ld(0);
-    for (int i = 0; i < cn; i += 2) {
-      const Raw x1 = ld(i + 1);
-      attend(x0, c + i);
-      x0 = ld(i + 2);
-      if (i + 1 < cn) attend(x1, c + i + 1);
+    if constexpr (kIsHi) {
+      // Two page buffers used in turn (unrolled by two), so no buffer is
+      // copied while its loads are in flight.
+      Raw x0 = ld(0);
+      for (int i = 0; i < cn; i += 2) {
+        const Raw x1 = ld(i + 1);
+        attend(x0, c + i);
+        x0 = ld(i + 2);
+        if (i + 1 < cn) attend(x1, c + i + 1);
+      }
+    } else {
+      // A LOW page is 2 + 2 KiB of codes and 2 x 128 B of scales per head
+      // (D 128): four buffers in turn keep three pages in flight.
+      Raw x0 = ld(0), x1 = ld(1), x2 = ld(2);
+      for (int i = 0; i < cn; i += 4) {
+        const Raw x3 = ld(i + 3);
+        attend(x0, c + i);
+        x0 = ld(i + 4);
+        if (i + 1 < cn) attend(x1, c + i + 1);
+        x1 = ld(i + 5);
+        if (i + 2 < cn) attend(x2, c + i + 2);
+        x2 = ld(i + 6);
+        if (i + 3 < cn) attend(x3, c + i + 3);
+      }
     }
   }
 }
@@ -1384,12 +1434,11 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   st.m = -INFINITY;
   st.l = 0.0f;
 #pragma unroll
-  for (int i = 0; i < PL::NG; ++i) {            // offset x sum of q over group i (head n)
+  for (int i = 0; i < PL::NG; ++i) {            // -offset x sum of q over group i (head n)
     float part = 0.0f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) part += bf16_lo(st.qa[4 * i + e]) + bf16_hi(st.qa[4 * i + e]);
-    st.kq[i] = kCodeOffset * head_sum(part);
-    st.vw[i] = 0.0f;
+    st.kq[i] = -kCodeOffset * head_sum(part);
   }
   if (j0 < sp.np_hi)
     run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), 0, j0,
@@ -1407,18 +1456,6 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   // contiguous bytes, and the (max, sum) pairs of the G4 heads sit together.
   // Rows past G hold finite values that are never read into an output.
   constexpr int G4 = G > 4 ? G : 4;
-  if (j1 > sp.np_w) {                            // remove the code offset of the LOW values
-#pragma unroll
-    for (int i = 0; i < PL::NG; ++i) {
-      const float off = kCodeOffset * head_sum(st.vw[i]);   // head n
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float o = __shfl(off, 4 * q + r);            // output row 4q + r
-        st.acc[2 * i][r] -= o;
-        st.acc[2 * i + 1][r] -= o;
-      }
-    }
-  }
   const float l_n = head_sum(st.l);              // head n, over all slots
   const int slot = (int)(w - seg0 / U);          // < a.splits by the choice of U
   const size_t blk = ((size_t)b * H + g) * a.splits + slot;
