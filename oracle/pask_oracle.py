@@ -24,7 +24,12 @@ What it computes, each piece following the passage named in its docstring:
   * the protected recent window of Section 3.1: the last W positions of a
     sequence stay visible at full precision whatever their action, which
     takes effect when a token leaves the window (release then removes it from
-    the attention that follows).
+    the attention that follows);
+  * the attention-output distortion D(q, a) of Eq. 4 (Section 3.3): one
+    bucket q = (z, c) intervened with action a while every other bucket stays
+    HIGH, the squared L2 distance of the attention outputs maximised over
+    query heads, averaged over the decode positions the bucket affects and
+    summed over the layers of group c.
 
 Everything is plain numpy.  The attention is the definition written out
 (exact, up to fp64 rounding order); the decisions, compaction and codes are
@@ -535,3 +540,73 @@ def c_kv(n_high: int, n_low: int, n_drop: int, n_kv_heads: int, head_dim: int) -
     if tot == 0:
         return float("nan")
     return (n_high * m[HIGH] + n_low * m[LOW]) / (tot * m[HIGH])
+
+
+# --------------------------------------------------------------------------
+# Attention-output distortion (Eq. 4, Section 3.3)
+# --------------------------------------------------------------------------
+
+def output_distortion(o_full, o_int) -> float:
+    """max over query heads h of ||o_full[h] - o_int[h]||_2^2: the quantity
+    inside the expectation of Eq. 4 for one layer and one decode position."""
+    d = np.asarray(o_full, dtype=np.float64) - np.asarray(o_int, dtype=np.float64)
+    return float(np.max(np.sum(d * d, axis=-1)))
+
+
+def intervention_table(n_tags: int, n_groups: int, tag: int, group: int, action: int):
+    """(action, floor) tables of a one-bucket intervention (Section 3.3):
+    bucket (tag, group) gets `action`, every other bucket HIGH, floors at
+    DROP so the lookup returns exactly those actions."""
+    a = np.full((n_tags, n_groups), HIGH, dtype=np.uint8)
+    a[tag, group] = action
+    return a, np.zeros_like(a)
+
+
+def distortion(tags, k_bits, v_bits, q_bits, prompt_len: int, group_of_layer, n_tags: int, tag: int, group: int,
+               action: int, scale: float):
+    """D(q, a) of Eq. 4 for bucket q = (tag, group) on reference trajectories.
+
+    tags [R, T]: tags of the T generated tokens of R trajectories; k_bits,
+    v_bits [R, L, P + T, Hkv, D]: bf16 K / V of every position and layer (the
+    P prompt positions first, kept HIGH in both runs); q_bits [R, L, T, Hq, D]:
+    the query of every decode step.  Step u appends position P + u, then
+    attends with its query (the token sees itself at its persisted precision).
+
+    The reference run keeps every bucket HIGH; the intervened run gives
+    bucket (tag, group) the action `action`.  S(q) holds the steps (r, u)
+    whose history contains a generated token with tag `tag`, i.e. the steps
+    from the bucket's first occurrence in r on.  Returns
+    sum over layers l of group `group` of the mean over S(q) of
+    max_h ||o_full - o_a||^2, and |S(q)|; D = 0 when S(q) is empty."""
+    tags = np.asarray(tags)
+    R, T = tags.shape
+    gol = np.asarray(group_of_layer)
+    L = gol.size
+    hkv, d = k_bits.shape[-2], k_bits.shape[-1]
+    layers = [l for l in range(L) if gol[l] == group]
+    full = dict(action=np.full((n_tags, int(gol.max()) + 1), HIGH, np.uint8), group_of_layer=gol, n_sink=0)
+    full["floor"] = np.zeros_like(full["action"])
+    a_int, f_int = intervention_table(n_tags, int(gol.max()) + 1, tag, group, action)
+    inter = dict(action=a_int, floor=f_int, group_of_layer=gol, n_sink=0)
+    total, n_s = 0.0, 0
+    for r in range(R):
+        ref, itv = OracleCache(full, hkv, d), OracleCache(inter, hkv, d)
+        for l in layers:
+            for c in (ref, itv):
+                c.append(l, 0, np.zeros(prompt_len, np.uint8), k_bits[r, l, :prompt_len], v_bits[r, l, :prompt_len],
+                         keep_all=True)
+        seen = False
+        for u in range(T):
+            seen |= int(tags[r, u]) == tag
+            for l in layers:
+                for c in (ref, itv):
+                    c.append(l, 0, tags[r, u:u + 1], k_bits[r, l, prompt_len + u][None],
+                             v_bits[r, l, prompt_len + u][None])
+            if not seen:
+                continue
+            n_s += 1
+            for l in layers:
+                o_full, _ = ref.attend(l, 0, q_bits[r, l, u], scale)
+                o_int, _ = itv.attend(l, 0, q_bits[r, l, u], scale)
+                total += output_distortion(o_full, o_int)
+    return (total / n_s if n_s else 0.0), n_s
