@@ -307,6 +307,31 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
                      const void* v_new_dev, float softmax_scale, int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes,
                      hipStream_t stream);
 
+/* Attention-output distortion of one layer for one decode step (Eq. 4,
+ * Section 3.3).  `ref` and `intervened` are two caches of the same geometry
+ * holding the same reference trajectories persisted under two tables: the
+ * reference run (every bucket RETAIN-HIGH) and a one-bucket intervention
+ * (bucket (z, c) given an action a, every other bucket RETAIN-HIGH).  With
+ * the same queries q_dev bf16 [batch][n_q_heads][head_dim], the attention of
+ * pask_decode_attn over the persisted history of `layer` in both caches, in
+ * fp32 before any rounding to bf16, and for every sequence b whose
+ * in_s_dev[b] != 0 (u8 [batch], device; NULL selects every sequence):
+ *   dist_dev[b] += max over query heads h of sum_d (o_ref[b][h][d] - o_int[b][h][d])^2
+ * (fp32 [batch], device, caller-owned: the caller zeroes it once).  Calling it
+ * for every layer of group c at every decode step of S(q) (in_s_dev marks the
+ * sequences whose bucket has occurred by that step), then dividing the sum
+ * over b by the number of flagged (sequence, step) pairs gives D(q, a).
+ * ws_dev: at least 2 * pask_workspace_bytes(&ref->geom, batch, max_ctx_hint)
+ * bytes, 256-byte aligned (one set of partials per cache).  No entry is
+ * appended and neither cache is modified.
+ *
+ * Errors: PASK_E_ARG (null or misaligned pointers), PASK_E_SHAPE (the
+ * geometries differ, layer or batch out of range), PASK_E_CAPACITY
+ * (workspace too small), PASK_E_HIP. */
+int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer, int32_t batch, const void* q_dev,
+                         const uint8_t* in_s_dev, float softmax_scale, int32_t max_ctx_hint, void* ws_dev,
+                         size_t ws_bytes, float* dist_dev, hipStream_t stream);
+
 /* Read the cache's counters (synchronises `stream`) and fill `out`: entry
  * counts per action, stored bytes, realised C_KV (Eq. 1) and the device
  * status word.  per_seq_group_head (nullable, host) receives int64

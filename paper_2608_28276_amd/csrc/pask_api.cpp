@@ -460,6 +460,49 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
   return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
 }
 
+int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer, int32_t batch, const void* q_dev,
+                         const uint8_t* in_s_dev, float softmax_scale, int32_t max_ctx_hint, void* ws_dev,
+                         size_t ws_bytes, float* dist_dev, hipStream_t stream) {
+  int st = check_cache(ref);
+  if (st != PASK_OK) return st;
+  st = check_cache(intervened);
+  if (st != PASK_OK) return st;
+  const pask_geom& g = ref->geom;
+  const pask_geom& h = intervened->geom;
+  if (g.n_layers != h.n_layers || g.n_q_heads != h.n_q_heads || g.n_kv_heads != h.n_kv_heads ||
+      g.head_dim != h.head_dim || g.recent_window != h.recent_window)
+    return PASK_E_SHAPE;
+  if (layer < 0 || layer >= g.n_layers) return PASK_E_SHAPE;
+  if (batch < 1 || batch > g.max_batch || batch > h.max_batch) return PASK_E_SHAPE;
+  if (!q_dev || !aligned(q_dev, 16) || !dist_dev || !aligned(dist_dev, 4)) return PASK_E_ARG;
+  if (!isfinite(softmax_scale)) return PASK_E_ARG;
+  if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
+  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq));   // any value is safe (U bounds the pieces)
+  const WsLayout w = ws_layout(&g, batch, splits);
+  if (!ws_dev || !aligned(ws_dev, 256)) return PASK_E_ARG;
+  if (ws_bytes < 2 * w.total) return PASK_E_CAPACITY;
+
+  pask::AttnArgs a[2];
+  pask_cache* caches[2] = {ref, intervened};
+  for (int i = 0; i < 2; ++i) {
+    uint8_t* base = static_cast<uint8_t*>(ws_dev) + i * w.total;
+    a[i].cv = view_of(caches[i]);
+    a[i].q = static_cast<const uint16_t*>(q_dev);
+    a[i].out = nullptr;
+    a[i].lse = nullptr;
+    a[i].ws_o = reinterpret_cast<float*>(base + w.o_off);
+    a[i].ws_ml = reinterpret_cast<float*>(base + w.ml_off);
+    a[i].scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
+    a[i].layer = layer;
+    a[i].batch = batch;
+    a[i].n_q_heads = g.n_q_heads;
+    a[i].splits = splits;
+  }
+  return pask::launch_distortion(a[0], a[1], g.n_q_heads / g.n_kv_heads, in_s_dev, dist_dev, stream) == hipSuccess
+             ? PASK_OK
+             : PASK_E_HIP;
+}
+
 int pask_cache_stats(const pask_policy* policy, const pask_cache* cache, int32_t batch, pask_stats* out,
                      int64_t* per_seq_group_head, hipStream_t stream) {
   int st = check_cache(cache);

@@ -25,7 +25,7 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #define PASK_WEIGHT_LO 32
 #endif
 #ifndef PASK_UNIT_TOKENS
-#define PASK_UNIT_TOKENS 256
+#define PASK_UNIT_TOKENS 128
 #endif
 constexpr int kUnitTokens = PASK_UNIT_TOKENS;   // slots per attention work unit (multiple of 16)
 constexpr uint32_t kKeepAll = 1u;
@@ -105,5 +105,9 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s);        // chooses 
 hipError_t launch_append_step(const AppendArgs& a, hipStream_t s);
 hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int group_size, hipStream_t s);
+// Attention over two caches with the same queries (partials in ref.ws_* and itv.ws_*), then
+// dist[b] += max over heads of the squared distance of the two outputs (Eq. 4).
+hipError_t launch_distortion(const AttnArgs& ref, const AttnArgs& itv, int group_size, const uint8_t* in_s,
+                             float* dist, hipStream_t s);
 
 }  // namespace pask

@@ -1305,7 +1305,7 @@ struct StreamPlan {
   long long total;   // units
   int U;             // units per block
 };
-constexpr int kMinPagesPerBlock = 16;
+constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
 
 __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
   int total = 0, mx = 0;
@@ -1506,30 +1506,30 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
   }
 }
 
-// One (sequence, KV head): combine the partials of its pieces (one or more)
-// into the bf16 outputs and log-sum-exps of its G query heads; zero output
-// and -inf for an empty history.  Thread t owns float4 position t of the
-// partial rows (4 heads at one dim) and merges it online over the pieces,
-// keeping the running (max, sum) of those 4 heads; the normalised rows are
-// staged in LDS and written as contiguous 16-byte pieces.
+// Online merge of the partials of one (sequence, KV head) by thread t of a
+// merge block: float4 position t of the partial rows, i.e. heads 4q..4q+3 at
+// one dim, with the running (max, sum) of those 4 heads.
 template <int D, int G>
 constexpr int merge_threads() { return (G > 4 ? G : 4) * D / 4; }
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merge_threads <= 256
-  constexpr int G4 = G > 4 ? G : 4;
-  constexpr int NM = D / 16;
-  constexpr int kBatch = 8;                      // pieces whose loads are issued together
-  static_assert(merge_threads<D, G>() % 64 == 0 && merge_threads<D, G>() <= 256, "merge block size");
-  __shared__ __align__(16) uint16_t s_out[G][D];
-  const int t = threadIdx.x;
-  const int H = a.cv.n_kv_heads;
-  const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
-  const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
-  const size_t blk0 = ((size_t)b * H + g) * a.splits;
-  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
+struct PieceMerge {
+  static constexpr int G4 = G > 4 ? G : 4;
+  static constexpr int kBatch = 8;               // pieces whose loads are issued together
   float4 v[kBatch], mla[kBatch], mlb[kBatch];
-  auto load_batch = [&](int p0, int last) {       // pieces p0.., past `last` repeated (skipped later)
+  float acc[4], M[4], L[4];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      acc[r] = 0.0f;
+      M[r] = -INFINITY;
+      L[r] = 0.0f;
+    }
+  }
+  // Loads pieces p0.. of the (b, g) whose first partial block is blk0; past
+  // `last` the last piece is repeated (fold skips it).
+  __device__ __forceinline__ void load(const AttnArgs& a, size_t blk0, int t, int q, int p0, int last) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const size_t pb = blk0 + min(p0 + u, last);
@@ -1538,31 +1538,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
       mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
       mlb[u] = *reinterpret_cast<const float4*>(ml + 4);   // (m, l) of heads 4q+2, 4q+3
     }
-  };
-  // The first kBatch pieces are loaded before the piece count is known (slots
-  // below `splits` are in bounds; those past the count are skipped), so their
-  // latency overlaps that of the counters the count comes from.
-  load_batch(0, a.splits - 1);
-  const FirstCounts f = first_counts(a);
-  const SeqPages sp = seq_pages(a, f, b);
-  if (sp.np == 0) {
-    for (int i = t; i < G * D; i += merge_threads<D, G>()) a.out[row0 * D + i] = 0;
-    if (a.lse && t < G) a.lse[row0 + t] = -INFINITY;
-    return;
   }
-  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
-  int excl = 0;                                   // units of the sequences before b
-  for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
-  const long long seg0 = (long long)excl * H + (long long)g * sp.len;
-  const int nparts = (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f}, M[4], L[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-  for (int r = 0; r < 4; ++r) M[r] = -INFINITY;
-  for (int p0 = 0; p0 < nparts; p0 += kBatch) {
-    if (p0 > 0) load_batch(p0, nparts - 1);
+  // Merges the first n (<= kBatch) loaded pieces.
+  __device__ __forceinline__ void fold(int n) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      if (p0 + u >= nparts) break;
+      if (u >= n) break;
       const float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
       const float mlv[8] = {mla[u].x, mla[u].y, mla[u].z, mla[u].w, mlb[u].x, mlb[u].y, mlb[u].z, mlb[u].w};
 #pragma unroll
@@ -1576,12 +1557,62 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
       }
     }
   }
+};
+
+// Pieces of segment (b, g) in the stream-K decomposition (sp: pages of b,
+// excl: units of the sequences before b; sp.np > 0).
+__device__ __forceinline__ int n_pieces(const StreamPlan& plan, const SeqPages& sp, int excl, int g, int H) {
+  const long long seg0 = (long long)excl * H + (long long)g * sp.len;
+  return (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
+}
+// Units of the sequences before b (wave-uniform).
+__device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts& f, int b) {
+  int excl = 0;
+  for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
+  return excl;
+}
+
+// One (sequence, KV head): combine the partials of its pieces (one or more)
+// into the bf16 outputs and log-sum-exps of its G query heads; zero output
+// and -inf for an empty history.  Thread t merges float4 position t of the
+// partial rows; the normalised rows are staged in LDS and written as
+// contiguous 16-byte pieces.
+template <int D, int G>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merge_threads <= 256
+  constexpr int NM = D / 16;
+  static_assert(merge_threads<D, G>() % 64 == 0 && merge_threads<D, G>() <= 256, "merge block size");
+  __shared__ __align__(16) uint16_t s_out[G][D];
+  const int t = threadIdx.x;
+  const int H = a.cv.n_kv_heads;
+  const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
+  const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
+  const size_t blk0 = ((size_t)b * H + g) * a.splits;
+  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
+  PieceMerge<D, G> pm;
+  // The first pieces are loaded before the piece count is known (slots
+  // below `splits` are in bounds; those past the count are skipped), so their
+  // latency overlaps that of the counters the count comes from.
+  pm.load(a, blk0, t, q, 0, a.splits - 1);
+  const FirstCounts f = first_counts(a);
+  const SeqPages sp = seq_pages(a, f, b);
+  if (sp.np == 0) {
+    for (int i = t; i < G * D; i += merge_threads<D, G>()) a.out[row0 * D + i] = 0;
+    if (a.lse && t < G) a.lse[row0 + t] = -INFINITY;
+    return;
+  }
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
+  pm.init();
+  for (int p0 = 0; p0 < nparts; p0 += PieceMerge<D, G>::kBatch) {
+    if (p0 > 0) pm.load(a, blk0, t, q, p0, nparts - 1);
+    pm.fold(nparts - p0);
+  }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int h = 4 * q + r;
     if (h < G) {
-      s_out[h][16 * k + n] = f32_to_bf16_rne_dev(acc[r] / L[r]);
-      if (a.lse && k == 0 && n == 0) a.lse[row0 + h] = (M[r] + log2f(L[r])) * 0.69314718055994530942f;
+      s_out[h][16 * k + n] = f32_to_bf16_rne_dev(pm.acc[r] / pm.L[r]);
+      if (a.lse && k == 0 && n == 0) a.lse[row0 + h] = (pm.M[r] + log2f(pm.L[r])) * 0.69314718055994530942f;
     }
   }
   __syncthreads();
@@ -1589,6 +1620,80 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   const uint4* src = reinterpret_cast<const uint4*>(&s_out[0][0]);
   uint4* dst = reinterpret_cast<uint4*>(a.out + row0 * D);
   for (int i = t; i < G * D / 8; i += merge_threads<D, G>()) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// attention-output distortion (Eq. 4)
+// ---------------------------------------------------------------------------
+
+// Normalised fp32 outputs of heads 4q..4q+3 at thread t's dim for (b, g):
+// the merge of its pieces, 0 for an empty history.
+template <int D, int G>
+__device__ __forceinline__ void merged_rows(const AttnArgs& a, const StreamPlan& plan, const SeqPages& sp, int excl,
+                                            int b, int g, int t, int q, float (&o)[4]) {
+  if (sp.np == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = 0.0f;
+    return;
+  }
+  const int H = a.cv.n_kv_heads;
+  const int nparts = n_pieces(plan, sp, excl, g, H);
+  const size_t blk0 = ((size_t)b * H + g) * a.splits;
+  PieceMerge<D, G> pm;
+  pm.init();
+  for (int p0 = 0; p0 < nparts; p0 += PieceMerge<D, G>::kBatch) {
+    pm.load(a, blk0, t, q, p0, nparts - 1);
+    pm.fold(nparts - p0);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) o[r] = pm.acc[r] / pm.L[r];
+}
+
+__device__ __forceinline__ float wave_sum_f(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// One block per sequence b: for every KV head g, the outputs of its G query
+// heads over the reference cache (partials of `ref`) and the intervened one
+// (`itv`) in fp32, the squared L2 distance of each head's rows summed over
+// the D dims, and the maximum over all query heads (Eq. 4, inside the
+// expectation), added to dist[b] when in_s is null or in_s[b] != 0.
+template <int D, int G>
+__global__ __launch_bounds__(256) void distortion_kernel(AttnArgs ref, AttnArgs itv, const uint8_t* in_s,
+                                                         float* dist) {
+  constexpr int NM = D / 16;
+  constexpr int G4 = G > 4 ? G : 4;
+  __shared__ float s_d2[G4];
+  const int t = threadIdx.x;
+  const int b = uni(blockIdx.x);
+  const int H = ref.cv.n_kv_heads;
+  const int q = t / (NM * 16);
+  if (in_s && in_s[b] == 0) return;
+  const FirstCounts fr = first_counts(ref), fi = first_counts(itv);
+  const StreamPlan pr = stream_plan(ref, fr, ref.attn_blocks), pi = stream_plan(itv, fi, itv.attn_blocks);
+  const SeqPages sr = seq_pages(ref, fr, b), si = seq_pages(itv, fi, b);
+  const int er = units_before(ref, fr, b), ei = units_before(itv, fi, b);
+  float worst = 0.0f;
+  for (int g = 0; g < H; ++g) {
+    if (t < G4) s_d2[t] = 0.0f;
+    __syncthreads();
+    float o_r[4], o_i[4];
+    merged_rows<D, G>(ref, pr, sr, er, b, g, t, q, o_r);
+    merged_rows<D, G>(itv, pi, si, ei, b, g, t, q, o_i);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {                // each wave holds 64 dims of heads 4q..4q+3
+      const float e = o_r[r] - o_i[r];
+      const float w = wave_sum_f(e * e);
+      if ((t & 63) == 0) atomicAdd(&s_d2[4 * q + r], w);
+    }
+    __syncthreads();
+    if (t == 0)
+      for (int h = 0; h < G; ++h) worst = fmaxf(worst, s_d2[h]);
+    __syncthreads();
+  }
+  if (t == 0) dist[b] += worst;
 }
 
 }  // namespace
@@ -1671,6 +1776,26 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
     attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
     attn_merge_kernel<DD, GG><<<dim3(a.batch * a.cv.n_kv_heads), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
+    return hipGetLastError();                                                    \
+  }
+  PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
+  PASK_CASE(128, 1) PASK_CASE(128, 2) PASK_CASE(128, 4) PASK_CASE(128, 8)
+#undef PASK_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args, int group_size,
+                             const uint8_t* in_s, float* dist, hipStream_t s) {
+  const int D = ref_args.cv.head_dim;
+  AttnArgs ref = ref_args, itv = itv_args;
+  const dim3 block(64);
+#define PASK_CASE(DD, GG)                                                        \
+  if (D == DD && group_size == GG) {                                             \
+    ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG>();                     \
+    if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
+    attn_kernel<DD, GG><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);            \
+    attn_kernel<DD, GG><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);            \
+    distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)

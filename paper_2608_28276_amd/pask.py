@@ -38,7 +38,7 @@ PASK_APPEND_KEEP_ALL = 1 << 0
 PASK_MAX_TAGS, PASK_MAX_GROUPS, PASK_MAX_LAYERS, PASK_MAX_STATES = 64, 16, 128, 64
 EXPORTS = ("pask_policy_load", "pask_cache_layout_query", "pask_cache_bytes", "pask_cache_init",
            "pask_cache_reset", "pask_kv_append", "pask_budget_init", "pask_workspace_bytes",
-           "pask_decode_attn", "pask_cache_stats", "pask_status_string")
+           "pask_decode_attn", "pask_attn_distortion", "pask_cache_stats", "pask_status_string")
 
 
 class PaskError(RuntimeError):
@@ -104,6 +104,8 @@ _lib.pask_workspace_bytes.restype = C.c_size_t
 _lib.pask_workspace_bytes.argtypes = [C.POINTER(pask_geom), C.c_int32, C.c_int32]
 _lib.pask_decode_attn.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P, _P,
                                   _P, _P, _P, _P, _P, C.c_float, C.c_int32, _P, C.c_size_t, _P]
+_lib.pask_attn_distortion.argtypes = [C.POINTER(pask_cache), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P, _P,
+                                      C.c_float, C.c_int32, _P, C.c_size_t, _P, _P]
 _lib.pask_cache_stats.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32,
                                   C.POINTER(pask_stats), _P, _P]
 
@@ -195,6 +197,15 @@ def pask_decode_attn(policy: pask_policy, cache: pask_cache, layer: int, batch: 
                                  float(softmax_scale),
                                  int(max_ctx_hint), _ptr(ws), int(ws_bytes), _ptr(stream)),
            "pask_decode_attn")
+
+
+def pask_attn_distortion(ref: pask_cache, intervened: pask_cache, layer: int, batch: int, q, in_s, softmax_scale: float,
+                         max_ctx_hint: int, ws, ws_bytes: int, dist, stream=0) -> None:
+    """dist[b] += max_h ||o_ref[b][h] - o_int[b][h]||^2 for the flagged sequences (Eq. 4)."""
+    _check(_lib.pask_attn_distortion(C.byref(ref), C.byref(intervened), int(layer), int(batch), _ptr(q), _ptr(in_s),
+                                     float(softmax_scale), int(max_ctx_hint), _ptr(ws), int(ws_bytes), _ptr(dist),
+                                     _ptr(stream)),
+           "pask_attn_distortion")
 
 
 def pask_cache_stats(policy: pask_policy, cache: pask_cache, batch: int, per_seq_group_head=None, stream=0):

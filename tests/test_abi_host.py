@@ -22,7 +22,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     lib = pask.library()
     for n in names:
         assert hasattr(lib, n), n
@@ -217,14 +217,40 @@ def test_unsupported_geometry(bad):
 
 def test_workspace_bytes():
     g = geom()
-    # splits = ceil(hint / 256) + 2; per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
+    # splits = ceil(hint / 128) + 2; per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
     # o: blocks*G4*D*4, ml: blocks*G4*2*4 (each 256-aligned)
     ws = pask.pask_workspace_bytes(g, 4, 512)
     G4 = max(4, g.n_q_heads // g.n_kv_heads)
-    blocks = 4 * g.n_kv_heads * 4
+    blocks = 4 * g.n_kv_heads * 6
     want = ((blocks * G4 * g.head_dim * 4 + 255) // 256) * 256
     want = ((want + blocks * G4 * 8 + 255) // 256) * 256
     assert ws == want
+
+
+def test_distortion_validation_before_any_hip_call():
+    g = geom()
+    ref, itv = _fake_cache(g), _fake_cache(g)
+    A = 1 << 41
+    ws_need = 2 * pask.pask_workspace_bytes(g, 2, 512)
+    other = _fake_cache(geom(n_kv_heads=4))
+    cases = [
+        (dict(layer=2), pask.PASK_E_SHAPE), (dict(batch=0), pask.PASK_E_SHAPE), (dict(batch=5), pask.PASK_E_SHAPE),
+        (dict(itv=other), pask.PASK_E_SHAPE), (dict(q=0), pask.PASK_E_ARG), (dict(q=A + 8), pask.PASK_E_ARG),
+        (dict(dist=0), pask.PASK_E_ARG), (dict(dist=A + 2), pask.PASK_E_ARG), (dict(ws=A + 128), pask.PASK_E_ARG),
+        (dict(ws_bytes=ws_need - 1), pask.PASK_E_CAPACITY), (dict(scale=float("nan")), pask.PASK_E_ARG),
+    ]
+    for over, code in cases:
+        kw = dict(itv=itv, layer=0, batch=2, q=A, dist=A, ws=A, ws_bytes=ws_need, scale=0.125)
+        kw.update(over)
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_attn_distortion(ref, kw["itv"], kw["layer"], kw["batch"], kw["q"], None, kw["scale"], 512,
+                                      kw["ws"], kw["ws_bytes"], kw["dist"], 0)
+        assert e.value.status == code, over
+    small = _fake_cache(g)
+    small.bytes = ref.bytes - 1
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_attn_distortion(ref, small, 0, 2, A, None, 0.125, 512, A, ws_need, A, 0)
+    assert e.value.status == pask.PASK_E_CAPACITY
 
 
 def _fake_cache(g):

@@ -1,0 +1,138 @@
+"""GPU parity of the attention-output distortion (Eq. 4) through the C ABI.
+
+Two caches hold the same trajectories: the reference run (every bucket
+HIGH) and a one-bucket intervention (bucket (z, c) DROP or LOW).  At every
+decode step from a sequence's first z on, pask_attn_distortion adds
+max_h ||o_ref - o_int||^2 for each layer of group c; each call's increment is
+compared with the oracle's value for that (sequence, step, layer), and the
+final D with the oracle's Eq. 4 outer loop.
+
+Tolerance: the GPU outputs are fp32 merges of split-K partials whose p.v
+weights carry >= 11 significant bits (fp16 on LOW pages), so each output
+element is within delta_o ~ 2^-11 |v| / sqrt(n_eff) of the fp64 one; over D
+dims the error vector has norm ||e|| <= delta = 4e-3 (generous for D <= 128),
+and ||d + e||^2 - ||d||^2 is within 2 delta ||d|| + delta^2."""
+
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import say
+from workload import make_policy
+from workload.policy import pack_blob
+from workload.tensors import bf16_normal, sub_seed
+
+pytestmark = pytest.mark.gpu
+
+DELTA = 4e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_28276_amd.pask  # noqa: F401  (fails loudly when libpask.so is missing)
+
+
+def _bits(t):
+    return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("action", [oracle.DROP, oracle.LOW])
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 64), (32, 8, 128), (16, 2, 128)])
+def test_distortion_matches_oracle(Hq, Hkv, D, action):
+    from paper_2608_28276_amd import pask
+    from paper_2608_28276_amd.session import PaskSession
+    say(f"case: distortion Hq {Hq} Hkv {Hkv} D {D} action {action}")
+    B, L, T, z, c = 4, 2, 24, 2, 1
+    P = np.array([5, 40, 70, 17])
+    seed = 4242 + D + Hq + action
+    rng = np.random.default_rng(seed)
+    tags = rng.integers(0, 6, size=(B, T)).astype(np.uint8)
+    tags[0, :3] = 0
+    tags[0, 3] = z                     # first occurrence at step 3
+    tags[1][tags[1] == z] = 1          # sequence 1: the bucket never occurs
+    base = make_policy(6, 2, L, 0.33, seed)
+    full_a = np.full((6, 2), oracle.HIGH, np.uint8)
+    int_a, zero = oracle.intervention_table(6, 2, z, c, action)
+    pol_ref = replace(base, action=full_a, floor=np.zeros_like(full_a))
+    pol_int = replace(base, action=int_a, floor=zero)
+    dev = torch.device("cuda:0")
+    mk = lambda pol: PaskSession(pack_blob(pol), max_batch=B, n_layers=L, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D,
+                                 max_tokens_per_seq=int(P.max()) + T, hi_pages=L * int(np.sum((P + T + 15) // 16)),
+                                 lo_pages=L * int(np.sum((P + T + 15) // 16)))
+    ref, itv = mk(pol_ref), mk(pol_int)
+    pd = lambda pol: dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=0)
+    o_ref, o_int = oracle.OracleCache(pd(pol_ref), Hkv, D), oracle.OracleCache(pd(pol_int), Hkv, D)
+    kv = {(b, l): (bf16_normal((int(P[b]) + T, Hkv, D), sub_seed(seed, "prompt_k", l, b)),
+                   bf16_normal((int(P[b]) + T, Hkv, D), sub_seed(seed, "prompt_v", l, b)))
+          for b in range(B) for l in range(L)}
+    q = bf16_normal((L, T, B, Hq, D), sub_seed(seed, "q", 0))
+    for l in range(L):
+        k = torch.zeros((B, int(P.max()), Hkv, D), dtype=torch.bfloat16)
+        v = torch.zeros_like(k)
+        for b in range(B):
+            k[b, :P[b]], v[b, :P[b]] = kv[(b, l)][0][:P[b]], kv[(b, l)][1][:P[b]]
+            for oc in (o_ref, o_int):
+                oc.append(l, b, np.zeros(P[b], np.uint8), _bits(kv[(b, l)][0][:P[b]]), _bits(kv[(b, l)][1][:P[b]]),
+                          keep_all=True)
+        n_new = torch.as_tensor(P, dtype=torch.int32, device=dev)
+        for s in (ref, itv):
+            s.append(l, None, k.to(dev), v.to(dev), n_new=n_new, keep_all=True)
+    ws_bytes = 2 * ref.ws_bytes
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    dist = torch.zeros(B, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    seen = np.zeros(B, bool)
+    n_s, worst = 0, 0.0
+    for u in range(T):
+        tdev = torch.as_tensor(tags[:, u:u + 1].copy(), device=dev)
+        for l in range(L):
+            kn = torch.stack([kv[(b, l)][0][P[b] + u] for b in range(B)])[:, None]
+            vn = torch.stack([kv[(b, l)][1][P[b] + u] for b in range(B)])[:, None]
+            for s in (ref, itv):
+                s.append(l, tdev, kn.to(dev), vn.to(dev))
+            for b in range(B):
+                for oc in (o_ref, o_int):
+                    oc.append(l, b, tags[b, u:u + 1], _bits(kn[b]), _bits(vn[b]))
+        seen |= tags[:, u] == z
+        if not seen.any():
+            continue
+        n_s += int(seen.sum())
+        in_s = torch.as_tensor(seen.astype(np.uint8), device=dev)
+        for l in range(L):
+            if int(pol_ref.group_of_layer[l]) != c:
+                continue
+            before = dist.clone()
+            qd = q[l, u].to(dev)
+            pask.pask_attn_distortion(ref.cache, itv.cache, l, B, qd, in_s, ref.softmax_scale, ref.max_ctx_hint, ws,
+                                      ws_bytes, dist, stream)
+            got = (dist - before).cpu().double().numpy()
+            for b in range(B):
+                if not seen[b]:
+                    assert got[b] == 0.0, (u, l, b)
+                    continue
+                qb = _bits(q[l, u, b])
+                want = oracle.output_distortion(o_ref.attend(l, b, qb, ref.softmax_scale)[0],
+                                                o_int.attend(l, b, qb, ref.softmax_scale)[0])
+                tol = 2 * DELTA * np.sqrt(want) + DELTA ** 2
+                assert abs(got[b] - want) <= tol, (u, l, b, got[b], want)
+                worst = max(worst, abs(got[b] - want) / tol)
+    assert n_s > 0 and dist[1].item() == 0.0
+    # D(q, a): the oracle's outer loop per sequence (ragged prompts), pooled over S(q)
+    d_gpu = float(dist.sum().item()) / n_s
+    tot, cnt = 0.0, 0
+    for b in range(B):
+        kb = np.stack([_bits(kv[(b, l)][0]) for l in range(L)])[None]
+        vb = np.stack([_bits(kv[(b, l)][1]) for l in range(L)])[None]
+        qb = np.stack([_bits(q[l, :, b]) for l in range(L)])[None]
+        d_b, n_b = oracle.distortion(tags[b:b + 1], kb, vb, qb, int(P[b]), pol_ref.group_of_layer, 6, z, c, action,
+                                     ref.softmax_scale)
+        tot += d_b * n_b
+        cnt += n_b
+    assert cnt == n_s
+    assert d_gpu == pytest.approx(tot / cnt, rel=2e-2)
+    say(f"D(q, a) gpu {d_gpu:.6e} oracle {tot / cnt:.6e}, |S(q)| = {n_s}, worst per-call error {worst:.2f} of tol")
