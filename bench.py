@@ -274,6 +274,114 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     return res
 
 
+def distortion_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, bucket):
+    """Attention-output distortion (Eq. 4) of bucket (z, c) with action a on
+    the workload's trajectories: a reference cache (every bucket HIGH) and an
+    intervened cache (bucket (z, c) -> a) hold the same tokens of the layers
+    of group c.  One step appends each sequence's next token to both caches
+    in every such layer, then pask_attn_distortion adds max_h ||o_ref - o_int||^2
+    of every layer for the sequences whose bucket has occurred (S(q))."""
+    import ctypes as C
+    from dataclasses import replace
+
+    import torch
+
+    from paper_2608_28276_amd import pask
+    from paper_2608_28276_amd.session import PaskSession
+    from workload.policy import pack_blob
+
+    z, c, act = bucket
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, D, T = cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.gen_tokens
+    layers = [l for l in range(cfg.layers_resident) if int(pol.group_of_layer[l]) == c]
+    full = np.full_like(np.asarray(pol.action), 2)
+    inter = full.copy()
+    inter[z, c] = act
+    pol_ref = replace(pol, action=full, floor=np.zeros_like(full))
+    pol_int = replace(pol, action=inter, floor=np.zeros_like(full))
+    pages = lambda n: int(np.sum((np.asarray(n) + 15) // 16))
+    hi = len(layers) * (pages(P + T) + B)
+    lo = len(layers) * (pages(np.full(B, T)) + B) if act == 1 else len(layers) * B
+    max_tok = int(P.max()) + T
+    mk = lambda pl, lo_pages: PaskSession(pack_blob(pl), max_batch=B, n_layers=cfg.n_layers, n_q_heads=Hq,
+                                          n_kv_heads=Hkv, head_dim=D, max_tokens_per_seq=max_tok, hi_pages=hi,
+                                          lo_pages=lo_pages, max_ctx_hint=max_tok)
+    ref, itv = mk(pol_ref, B), mk(pol_int, lo)
+    log(f"distortion of bucket (tag {z}, group {c}) -> action {act}: layers {layers[0]}..{layers[-1]}, "
+        f"caches {ref.nbytes / 2**30:.1f} + {itv.nbytes / 2**30:.1f} GiB")
+    g = torch.Generator(device=dev)
+    g.manual_seed(cfg.seed)
+    n_new = torch.as_tensor(P, dtype=torch.int32, device=dev)
+    tags_dev = torch.as_tensor(tags, device=dev)
+    for layer in layers:
+        k = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        v = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        for sess in (ref, itv):
+            sess.append(layer, None, k, v, n_new=n_new, keep_all=True)
+        k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        v = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        for sess in (ref, itv):
+            sess.append(layer, tags_dev[:, :t_start].contiguous(), k, v)
+        del k, v
+    seen = np.cumsum(tags == z, axis=1) > 0                                 # [B, T]: bucket occurred by step t
+    in_s = torch.as_tensor(seen.T.astype(np.uint8).copy(), device=dev)      # [T, B]
+    nL = len(layers)
+    q = torch.randn((nL, B, Hq, D), generator=g, device=dev, dtype=torch.bfloat16)
+    kn = torch.randn((nL, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+    vn = torch.randn((nL, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+    tags_t = tags_dev.t().contiguous()
+    ws_bytes = 2 * ref.ws_bytes
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    dist = torch.zeros(B, dtype=torch.float32, device=dev)
+    sptr = torch.cuda.current_stream(dev).cuda_stream
+    lib = pask.library()
+    r_pol, r_cache, i_pol, i_cache = (C.byref(ref.policy), C.byref(ref.cache), C.byref(itv.policy),
+                                      C.byref(itv.cache))
+    scale, hint = C.c_float(ref.softmax_scale), ref.max_ctx_hint
+
+    def step(t, events=None):
+        tp = tags_t[t].data_ptr()
+        for i, layer in enumerate(layers):
+            for pp, cc in ((r_pol, r_cache), (i_pol, i_cache)):
+                st = lib.pask_kv_append(pp, cc, layer, B, None, 1, tp, None, kn[i].data_ptr(), vn[i].data_ptr(), 0,
+                                        sptr)
+                if st != 0:
+                    raise pask.PaskError(st, "pask_kv_append")
+            if events is not None:
+                events[i][0].record(sptr)
+            st = lib.pask_attn_distortion(r_cache, i_cache, layer, B, q[i].data_ptr(), in_s[t].data_ptr(), scale,
+                                          hint, ws.data_ptr(), ws_bytes, dist.data_ptr(), sptr)
+            if st != 0:
+                raise pask.PaskError(st, "pask_attn_distortion")
+            if events is not None:
+                events[i][1].record(sptr)
+
+    for i in range(warmup):
+        step(t_start + i)
+    torch.cuda.synchronize()
+    cnt0 = [s.counters()[:B, layers].cpu().numpy().astype(np.int64) for s in (ref, itv)]
+    events = [[[HipEvent(), HipEvent()] for _ in layers] for _ in range(steps)]
+    dist.zero_()
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(steps):
+        step(t_start + warmup + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    cnt1 = [s.counters()[:B, layers].cpu().numpy().astype(np.int64) for s in (ref, itv)]
+    call_ms = np.array([[e[0].elapsed_ms(e[1]) for e in ev] for ev in events])
+    n_s = int(seen[:, t_start + warmup:t_start + warmup + steps].sum())
+    d = float(dist.sum().item()) / max(1, n_s)
+    mH = 2 * Hkv * D * 2
+    mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
+    kvb = lambda cn: cn[..., 0] * mH + cn[..., 1] * mL
+    read = sum(0.5 * (kvb(a) + kvb(b)).sum() for a, b in zip(cnt0, cnt1)) / nL     # both caches, per call
+    call_bytes = float(read + 2 * 2 * B * Hq * D)                                   # + q read by both passes
+    return dict(steps_per_s=B * steps / wall, ms_per_step=wall / steps * 1e3, avg_call_us=float(call_ms.mean()) * 1e3,
+                call_bytes=call_bytes, achieved=call_bytes / (float(call_ms.mean()) / 1e3) / 1e9, D=d, n_s=n_s,
+                layers=nL)
+
+
 def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None, ptags=None):
     """The oracle as it stands, on a bounded sample: n_seq sequences of the
     same workload (their prompt lengths and tag streams, seeded CPU inputs),
@@ -396,6 +504,9 @@ def main():
                     help="protected recent window of W positions (Section 3.1); default 0")
     ap.add_argument("--controller", action="store_true",
                     help="parser states drive the online budget controller (Alg. 2)")
+    ap.add_argument("--distortion", type=str, default=None, metavar="TAG,GROUP,ACTION",
+                    help="measure the attention-output distortion (Eq. 4) of one bucket instead "
+                         "(ACTION 0 = DROP, 1 = RETAIN-LOW)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -420,6 +531,29 @@ def main():
         states, pol = controller_inputs(cfg, tags, pol)
     log(f"workload {cfg.name}: B={cfg.batch} L={cfg.n_layers} prompts {int(P.min())}..{int(P.max())}, "
         f"policy expected cost {pol.expected_cost:.3f}")
+    if args.distortion:
+        z, c, a = (int(x) for x in args.distortion.split(","))
+        if a not in (0, 1) or not 0 <= z < pol.n_tags or not 0 <= c < pol.n_groups:
+            raise SystemExit("--distortion TAG,GROUP,ACTION: tag and group of the table, action 0 or 1")
+        d = distortion_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, (z, c, a))
+        log(f"distortion: {d['steps_per_s']:.0f} sequence-steps/s, call {d['avg_call_us']:.1f} us, "
+            f"{d['achieved']:.0f} GB/s, D = {d['D']:.4e} over |S| = {d['n_s']}")
+        print(json.dumps({
+            "metric": "attention-output distortion (Eq. 4) sequence-steps/s; achieved HBM GB/s vs MI355X peak",
+            "value": round(d["steps_per_s"], 1), "unit": "sequence-steps/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(d["ms_per_step"], 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{workload}+distortion(tag {z}, group {c}, action {a})", "batch": cfg.batch,
+                       "layers_of_group": d["layers"], "q_heads": cfg.n_q_heads, "kv_heads": cfg.n_kv_heads,
+                       "head_dim": cfg.head_dim, "prompt_tokens": prompt_desc(cfg),
+                       "generated_before_timing": args.t_start, "D": d["D"], "S_size": d["n_s"]},
+            "roofline": {"bound": "hbm", "achieved": round(d["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(d["achieved"] / HBM_PEAK_GBS, 4), "traffic": None,
+                         "kernel": f"2 x attn_kernel<{cfg.head_dim}, {cfg.group_size}> + distortion_kernel "
+                                   "(one pask_attn_distortion call)",
+                         "bytes_per_launch": round(d["call_bytes"]), "avg_launch_us": round(d["avg_call_us"], 2)},
+            "cpu_baseline": None}), flush=True)
+        return
     g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, states, ptags)
     log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
         f"{g['achieved']:.0f} GB/s algorithmic")
