@@ -1512,10 +1512,10 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
 template <int D, int G>
 constexpr int merge_threads() { return (G > 4 ? G : 4) * D / 4; }
 
-template <int D, int G>
+template <int D, int G, int kB = 8>
 struct PieceMerge {
   static constexpr int G4 = G > 4 ? G : 4;
-  static constexpr int kBatch = 8;               // pieces whose loads are issued together
+  static constexpr int kBatch = kB;              // pieces whose loads are issued together
   float4 v[kBatch], mla[kBatch], mlb[kBatch];
   float acc[4], M[4], L[4];
 
@@ -1626,27 +1626,32 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
 // attention-output distortion (Eq. 4)
 // ---------------------------------------------------------------------------
 
-// Normalised fp32 outputs of heads 4q..4q+3 at thread t's dim for (b, g):
-// the merge of its pieces, 0 for an empty history.
+// Normalised fp32 outputs of heads 4q..4q+3 at thread t's dim for (b, g) in
+// the reference (or_) and the intervened (oi) cache: both sets of partials
+// loaded before either is merged, so their latencies overlap; 0 for an
+// empty history.
 template <int D, int G>
-__device__ __forceinline__ void merged_rows(const AttnArgs& a, const StreamPlan& plan, const SeqPages& sp, int excl,
-                                            int b, int g, int t, int q, float (&o)[4]) {
-  if (sp.np == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = 0.0f;
-    return;
+__device__ __forceinline__ void merged_pair(const AttnArgs& ref, const StreamPlan& pr, const SeqPages& sr, int er,
+                                            const AttnArgs& itv, const StreamPlan& pi, const SeqPages& si, int ei,
+                                            int b, int g, int t, int q, float (&or_)[4], float (&oi)[4]) {
+  constexpr int kB = 4;                          // pieces per batch and cache: both in flight, no spills
+  const int H = ref.cv.n_kv_heads;
+  const int nr = sr.np ? n_pieces(pr, sr, er, g, H) : 0, ni = si.np ? n_pieces(pi, si, ei, g, H) : 0;
+  const size_t blk0 = ((size_t)b * H + g);
+  PieceMerge<D, G, kB> mr, mi;
+  mr.init();
+  mi.init();
+  for (int p0 = 0; p0 < max(nr, ni); p0 += kB) {
+    if (p0 < nr) mr.load(ref, blk0 * ref.splits, t, q, p0, nr - 1);
+    if (p0 < ni) mi.load(itv, blk0 * itv.splits, t, q, p0, ni - 1);
+    if (p0 < nr) mr.fold(nr - p0);
+    if (p0 < ni) mi.fold(ni - p0);
   }
-  const int H = a.cv.n_kv_heads;
-  const int nparts = n_pieces(plan, sp, excl, g, H);
-  const size_t blk0 = ((size_t)b * H + g) * a.splits;
-  PieceMerge<D, G> pm;
-  pm.init();
-  for (int p0 = 0; p0 < nparts; p0 += PieceMerge<D, G>::kBatch) {
-    pm.load(a, blk0, t, q, p0, nparts - 1);
-    pm.fold(nparts - p0);
-  }
 #pragma unroll
-  for (int r = 0; r < 4; ++r) o[r] = pm.acc[r] / pm.L[r];
+  for (int r = 0; r < 4; ++r) {
+    or_[r] = nr ? mr.acc[r] / mr.L[r] : 0.0f;
+    oi[r] = ni ? mi.acc[r] / mi.L[r] : 0.0f;
+  }
 }
 
 __device__ __forceinline__ float wave_sum_f(float x) {
@@ -1655,45 +1660,56 @@ __device__ __forceinline__ float wave_sum_f(float x) {
   return x;
 }
 
-// One block per sequence b: for every KV head g, the outputs of its G query
-// heads over the reference cache (partials of `ref`) and the intervened one
-// (`itv`) in fp32, the squared L2 distance of each head's rows summed over
-// the D dims, and the maximum over all query heads (Eq. 4, inside the
-// expectation), added to dist[b] when in_s is null or in_s[b] != 0.
+// KV heads a distortion block handles at once: that many merge groups of
+// merge_threads threads, at most 512 threads (256 VGPRs per thread).
 template <int D, int G>
-__global__ __launch_bounds__(256) void distortion_kernel(AttnArgs ref, AttnArgs itv, const uint8_t* in_s,
-                                                         float* dist) {
+constexpr int distortion_heads() { return 512 / merge_threads<D, G>() < 8 ? 512 / merge_threads<D, G>() : 8; }
+
+// One block per sequence b: for every KV head g (distortion_heads of them at
+// a time, one merge group each), the outputs of its G query heads over the
+// reference cache (partials of `ref`) and the intervened one (`itv`) in fp32,
+// the squared L2 distance of each head's rows summed over the D dims, and the
+// maximum over all query heads (Eq. 4, inside the expectation), added to
+// dist[b] when in_s is null or in_s[b] != 0.
+template <int D, int G>
+__global__ __launch_bounds__(512) void distortion_kernel(AttnArgs ref, AttnArgs itv, const uint8_t* in_s,
+                                                          float* dist) {
   constexpr int NM = D / 16;
   constexpr int G4 = G > 4 ? G : 4;
-  __shared__ float s_d2[G4];
-  const int t = threadIdx.x;
+  constexpr int MT = merge_threads<D, G>();
+  constexpr int GP = distortion_heads<D, G>();
+  __shared__ float s_d2[GP][G4];
   const int b = uni(blockIdx.x);
+  if (in_s && in_s[b] == 0) return;
+  const int gl = threadIdx.x / MT, t = threadIdx.x % MT;   // merge group, thread in it
   const int H = ref.cv.n_kv_heads;
   const int q = t / (NM * 16);
-  if (in_s && in_s[b] == 0) return;
   const FirstCounts fr = first_counts(ref), fi = first_counts(itv);
   const StreamPlan pr = stream_plan(ref, fr, ref.attn_blocks), pi = stream_plan(itv, fi, itv.attn_blocks);
   const SeqPages sr = seq_pages(ref, fr, b), si = seq_pages(itv, fi, b);
   const int er = units_before(ref, fr, b), ei = units_before(itv, fi, b);
   float worst = 0.0f;
-  for (int g = 0; g < H; ++g) {
-    if (t < G4) s_d2[t] = 0.0f;
+  for (int g0 = 0; g0 < H; g0 += GP) {
+    if (threadIdx.x < GP * G4) s_d2[threadIdx.x / G4][threadIdx.x % G4] = 0.0f;
     __syncthreads();
-    float o_r[4], o_i[4];
-    merged_rows<D, G>(ref, pr, sr, er, b, g, t, q, o_r);
-    merged_rows<D, G>(itv, pi, si, ei, b, g, t, q, o_i);
+    const int g = g0 + gl;
+    if (g < H) {                                 // whole merge groups (waves) take this branch alike
+      float o_r[4], o_i[4];
+      merged_pair<D, G>(ref, pr, sr, er, itv, pi, si, ei, b, g, t, q, o_r, o_i);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {                // each wave holds 64 dims of heads 4q..4q+3
-      const float e = o_r[r] - o_i[r];
-      const float w = wave_sum_f(e * e);
-      if ((t & 63) == 0) atomicAdd(&s_d2[4 * q + r], w);
+      for (int r = 0; r < 4; ++r) {              // each wave holds 64 dims of heads 4q..4q+3
+        const float e = o_r[r] - o_i[r];
+        const float w = wave_sum_f(e * e);
+        if ((t & 63) == 0) atomicAdd(&s_d2[gl][4 * q + r], w);
+      }
     }
     __syncthreads();
-    if (t == 0)
-      for (int h = 0; h < G; ++h) worst = fmaxf(worst, s_d2[h]);
+    if (threadIdx.x == 0)
+      for (int j = 0; j < GP && g0 + j < H; ++j)
+        for (int h = 0; h < G; ++h) worst = fmaxf(worst, s_d2[j][h]);
     __syncthreads();
   }
-  if (t == 0) dist[b] += worst;
+  if (threadIdx.x == 0) dist[b] += worst;
 }
 
 }  // namespace
@@ -1795,7 +1811,7 @@ hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args,
     if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
     attn_kernel<DD, GG><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);            \
     attn_kernel<DD, GG><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);            \
-    distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
+    distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>() * distortion_heads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
