@@ -90,7 +90,8 @@ def test_quantiser_exhaustive_absmax_on_gpu():
         assert (vc == vc_ref).all(), f"layer {layer}: V codes"
 
 
-@pytest.mark.parametrize("Hq,Hkv,D", [(8, 8, 64), (16, 8, 64), (8, 2, 64), (64, 8, 128), (32, 8, 128)])
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 8, 64), (16, 8, 64), (8, 2, 64), (16, 2, 64),
+                                      (8, 8, 128), (16, 8, 128), (32, 8, 128), (64, 8, 128)])
 def test_geometries_mixed_policy(Hq, Hkv, D):
     """Every supported (group size, head_dim) pair; ragged prompts (not page
     multiples), a batch of 5, mixed HIGH / LOW / DROP decode tokens."""
