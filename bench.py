@@ -173,13 +173,19 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     tags_dev = torch.as_tensor(tags, device=dev)
     ptags_dev = None if ptags is None else torch.as_tensor(ptags, device=dev)
     t0 = time.time()
+    sptr = torch.cuda.current_stream(dev).cuda_stream
+    fill_ev = [(HipEvent(), HipEvent()) for _ in range(L)]
+    after_prompt = []                                    # counters of each layer right after its prompt
     for layer in range(L):
         k = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
         v = torch.randn((B, int(P.max()), Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+        fill_ev[layer][0].record(sptr)
         if ptags_dev is None:                            # decode workloads: the prompt stays HIGH
             sess.append(layer, None, k, v, n_new=n_new, keep_all=True)
         else:                                            # prompt-side companion: labelled prompt, sinks HIGH
             sess.append(layer, ptags_dev, k, v, n_new=n_new)
+        fill_ev[layer][1].record(sptr)
+        after_prompt.append(sess.counters()[:B, layer, :2].clone())
         del k, v
         if t_start:
             k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
@@ -189,6 +195,19 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
             del k, v
     torch.cuda.synchronize()
     log(f"prompt + {t_start} generated tokens persisted in {time.time() - t0:.1f} s")
+    # The prompt's bulk append per layer (plan + pack kernels): algorithmic bytes = K / V read
+    # (bf16), tags read, the stored forms and index-list entries written.
+    mH = 2 * Hkv * D * 2
+    mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
+    n_prompt = int(P.sum())
+    ap = torch.stack(after_prompt).cpu().numpy().astype(np.int64)        # [L, B, 2]: n_hi, n_lo
+    pa_bytes = (n_prompt * (mH + (1 if ptags is not None else 0)) + ap[..., 0].sum(1) * (mH + 4)
+                + ap[..., 1].sum(1) * (mL + 4))                          # [L]
+    pa_ms = np.array([e0.elapsed_ms(e1) for e0, e1 in fill_ev])
+    prompt_append = dict(tokens_per_layer=n_prompt, us_per_layer=round(float(pa_ms.mean()) * 1e3, 1),
+                         algorithmic_gb_per_layer=round(float(pa_bytes.mean()) / 1e9, 4),
+                         achieved_gbs=round(float((pa_bytes / (pa_ms / 1e3)).mean()) / 1e9, 1))
+    log(f"prompt append: {prompt_append}")
 
     q = torch.randn((L, B, Hq, D), generator=g, device=dev, dtype=torch.bfloat16)
     kn = torch.randn((L, B, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
@@ -196,8 +215,6 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     out = torch.empty((L, B, Hq, D), dtype=torch.bfloat16, device=dev)
     tags_t = tags_dev.t().contiguous()                   # [T, B]
     states_t = None if states is None else states_dev.t().contiguous()
-    stream = torch.cuda.current_stream(dev)
-    sptr = stream.cuda_stream
     pol_c, cache_c = sess.policy, sess.cache
     ws, ws_bytes, hint, scale = sess.ws.data_ptr(), sess.ws_bytes, sess.max_ctx_hint, sess.softmax_scale
     qp = [q[i].data_ptr() for i in range(L)]
@@ -244,8 +261,6 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     if status != 0:
         raise RuntimeError(f"device flags set: {st.device_flags:#x}")
 
-    mH = 2 * Hkv * D * 2
-    mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
     # Algorithmic bytes of one attention launch, averaged over the timed ones:
     # every persisted entry read once (counts grow linearly over the region,
     # each launch sees its step's token), q read, o written.  The one-token
@@ -269,7 +284,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
         avg_call_us=avg_attn_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(attn_bytes.mean()),
         c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
         step_gbs=bytes_per_step / (wall / steps) / 1e9,
-        mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()),
+        mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()), prompt_append=prompt_append,
     )
     return res
 
@@ -586,6 +601,7 @@ def main():
             "hbm_gb_per_step": round(g["bytes_per_step"] / 1e9, 3),
             "step_gbs": round(g["step_gbs"], 1),
             "recent_window": args.window, "online_controller": bool(args.controller),
+            "prompt_append": g["prompt_append"],
         },
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
