@@ -499,18 +499,25 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
 }
 
 // Bulk persist of kPackTokens tokens of sequence blockIdx.y, after the plan
-// kernel has slotted them (staging code = store << 30 | slot, or -1).  The
-// block first reads the tokens' codes and page ids (one thread each), then
-// every thread loads its 16-byte chunk of every token's K / V row (chunk
-// k: K when k < Hkv*D/8, else V; head, then 8-dim piece) with all loads in
-// flight together, then persists them: RETAIN-HIGH chunks go to the page in
-// its MFMA operand order, RETAIN-LOW chunks are quantised by groups of 4
-// adjacent lanes (one 32-element group) and packed.
+// kernel has slotted them (staging code = store << 30 | slot, or -1).
+//   1. One thread per token reads its code and page id; thread 0 marks the
+//      runs of 4 tokens that fill a whole slot group (4 consecutive slots of
+//      one store, the first a multiple of 4).
+//   2. Every thread loads its 16-byte chunk of every token's K / V row (chunk
+//      k: K when k < Hkv*D/8, else V; head, then 8-dim piece), all in flight
+//      together (non-temporal: read once).
+//   3. K chunks (bf16, or int4 quantised by groups of 4 adjacent lanes with
+//      quant8) and scales go to the pages directly.  V tiles interleave the 4
+//      slots of a group at 2-byte (bf16) or 1-byte (int4 codes) granularity:
+//      for a whole group the lane holding a V chunk holds it for all 4 tokens
+//      and writes 8-byte (bf16) or 4-byte (codes) pieces; other tokens' V goes
+//      element by element.
 template <int D>
 __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
   using PL = PageLayout<D>;
   constexpr int kC = D / 8;                        // 16-byte chunks per head row
   __shared__ int s_code[kPackTokens], s_page[kPackTokens];
+  __shared__ uint32_t s_runs;                      // bit jj: tokens jj..jj+3 fill a slot group
   const CacheView& cv = a.cv;
   const int b = blockIdx.y;
   const int H = cv.n_kv_heads;
@@ -518,6 +525,7 @@ __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
   const int n = clamp_n_new(a, b, unused);
   const int j0 = (int)blockIdx.x * kPackTokens;
   if (j0 >= n) return;                             // the whole block
+  const int nt = min(kPackTokens, n - j0);
   if (threadIdx.x < kPackTokens) {
     const int j = j0 + (int)threadIdx.x;
     int code = -1, page = 0;
@@ -529,63 +537,124 @@ __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
     s_page[threadIdx.x] = page;
   }
   __syncthreads();
-  const int nt = min(kPackTokens, n - j0);
+  if (threadIdx.x == 0) {
+    uint32_t runs = 0u;
+    for (int jj = 0; jj + 4 <= nt;) {
+      const int c0 = s_code[jj];
+      bool full = c0 >= 0 && (c0 & 3) == 0;        // slot % 4 == 0 (the store bit is above)
+      for (int r = 1; full && r < 4; ++r) full = s_code[jj + r] == c0 + r;
+      if (full) {
+        runs |= 1u << jj;
+        jj += 4;
+      } else {
+        ++jj;
+      }
+    }
+    s_runs = runs;
+  }
+  __syncthreads();
+  const uint32_t runs = s_runs;
+  uint32_t covered = 0u;                           // tokens written by a whole-group piece
+#pragma unroll
+  for (int jj = 0; jj < kPackTokens; ++jj)
+    if (runs >> jj & 1u) covered |= 0xFu << jj;
   const size_t row = (size_t)H * D;
-  const int n_chunks = 2 * H * kC;                 // K and V chunks of one token
-  for (int base = 0; base < n_chunks; base += blockDim.x) {
-    const int k = base + (int)threadIdx.x;
-    const bool active = k < n_chunks;              // whole 4-lane groups alike (blockDim, H*kC multiples of 4)
-    const int kv = k / (H * kC), g = (k / kC) % H, c = k % kC;
-    const uint16_t* src = (kv ? a.v : a.k) + ((size_t)b * a.max_new + j0) * row + g * D + c * 8;
-    uint4 x[kPackTokens];
+  const int n_chunks = 2 * H * kC;                 // K and V chunks of one token (<= 256)
+  const int k = (int)threadIdx.x;
+  const bool active = k < n_chunks;                // whole 4-lane groups alike (H*kC is a multiple of 4)
+  const int kv = k / (H * kC), g = (k / kC) % H, c = k % kC;
+  const uint16_t* src = (kv ? a.v : a.k) + ((size_t)b * a.max_new + j0) * row + g * D + c * 8;
+  uint4 x[kPackTokens];
+  uint32_t packed[kPackTokens];                    // int4 codes of this lane's 8 elements, per LOW token
 #pragma unroll
-    for (int jj = 0; jj < kPackTokens; ++jj)      // every token's chunk in flight together
-      x[jj] = active && jj < nt ? stream_load16(reinterpret_cast<const uint8_t*>(src + jj * row))
-                                : make_uint4(0u, 0u, 0u, 0u);
+  for (int jj = 0; jj < kPackTokens; ++jj) {      // every token's chunk in flight together
+    x[jj] = active && jj < nt ? stream_load16(reinterpret_cast<const uint8_t*>(src + jj * row))
+                              : make_uint4(0u, 0u, 0u, 0u);
+    packed[jj] = 0u;
+  }
+  const int i = c / 4, q = c % 4;                  // int4: scale group i, dims 32i + 8q + 0..7
 #pragma unroll
-    for (int jj = 0; jj < kPackTokens; ++jj) {
-      const int code = s_code[jj];
-      if (jj >= nt || code < 0) continue;          // block-uniform
-      const int page = s_page[jj], t = (code & 0x3FFFFFFF) % kPage;
-      if ((code >> 30) == kHi) {
-        if (!active) continue;
-        uint8_t* hb = cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % H) * PL::kHiHead;
-        if (kv == 0) {                             // dims 8c..8c+7 = 32i + 8q + 0..7
-          *reinterpret_cast<uint4*>(hb + ((c / 4) * 64 + (c % 4) * 16 + t) * 16) = x[jj];
-        } else {                                   // dims 16m + dd, dd = 8(c%2) + e
-          uint16_t* vt = reinterpret_cast<uint16_t*>(hb + PL::kHiV);
-          const int m = c / 2;
-          const uint32_t w[4] = {x[jj].x, x[jj].y, x[jj].z, x[jj].w};
+  for (int jj = 0; jj < kPackTokens; ++jj) {
+    const int code = s_code[jj];
+    if (jj >= nt || code < 0) continue;            // block-uniform
+    const int page = s_page[jj], t = (code & 0x3FFFFFFF) % kPage;
+    const bool grouped = covered >> jj & 1u;
+    if ((code >> 30) == kHi) {
+      if (!active) continue;
+      uint8_t* hb = cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % H) * PL::kHiHead;
+      if (kv == 0) {                               // dims 8c..8c+7 = 32i + 8q + 0..7
+        *reinterpret_cast<uint4*>(hb + ((c / 4) * 64 + (c % 4) * 16 + t) * 16) = x[jj];
+      } else if (!grouped) {                       // dims 16m + dd, dd = 8(c%2) + e
+        uint16_t* vt = reinterpret_cast<uint16_t*>(hb + PL::kHiV);
+        const int m = c / 2;
+        const uint32_t w[4] = {x[jj].x, x[jj].y, x[jj].z, x[jj].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          vt[(((m >> 1) * 64 + (t / 4) * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4 + t % 4] =
+              (uint16_t)(w[e / 2] >> (16 * (e % 2)));
+      }
+    } else {
+      uint32_t sbits = 0u;
+      quant8(x[jj], packed[jj], sbits);            // every lane: the shuffles need whole groups
+      const uint32_t partner = __shfl_xor(packed[jj], 2, 4);   // V: dims 16 higher (lanes q < 2)
+      if (!active) continue;
+      uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
+      if (kv == 0) {
+        *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = packed[jj];
+        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      } else {
+        // byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i + dd (low nibble) and
+        // 32i + 16 + dd (high nibble), dd = 8q + e for lanes q < 2
+        if (q < 2 && !grouped) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const int dd = 8 * (c % 2) + e;
-            vt[(((m >> 1) * 64 + (t / 4) * 16 + dd) * 2 + (m & 1)) * 4 + t % 4] =
-                (uint16_t)(w[e / 2] >> (16 * (e % 2)));
+            const int dd = 8 * q + e;
+            hb[PL::kLoVC + (((t / 4) * 16 + dd) * (PL::NM / 2) + i) * 4 + t % 4] =
+                (uint8_t)(((packed[jj] >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4));
           }
         }
-      } else {
-        uint32_t packed = 0u, sbits = 0u;
-        quant8(x[jj], packed, sbits);              // every lane: the shuffles need whole groups
-        if (!active) continue;
-        uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
-        const int i = c / 4, q = c % 4;            // group i, dims 32i + 8q + 0..7
-        if (kv == 0) {
-          *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = packed;
-          if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
-        } else {
-          // byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i + dd (low nibble) and
-          // 32i + 16 + dd (high nibble): lanes q < 2 pair with lane q + 2
-          const uint32_t partner = __shfl_xor(packed, 2, 4);
-          if (q < 2) {
+        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      }
+    }
+  }
+  // Whole slot groups: tokens jj0..jj0+3 in slots 4u..4u+3 of one page.
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int dd = 8 * q + e;
-              const uint32_t byte = ((packed >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4);
-              hb[PL::kLoVC + (((t / 4) * 16 + dd) * (PL::NM / 2) + i) * 4 + t % 4] = (uint8_t)byte;
-            }
-          }
-          if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
-        }
+  for (int jj0 = 0; jj0 + 4 <= kPackTokens; ++jj0) {
+    if (!(runs >> jj0 & 1u)) continue;             // block-uniform
+    const int code = s_code[jj0], page = s_page[jj0], u = ((code & 0x3FFFFFFF) % kPage) / 4;
+    if ((code >> 30) == kHi) {
+      if (!active || kv == 0) continue;
+      // 8 bytes per (m, dd): the 4 slots' bf16 values, in slot order
+      uint16_t* vt = reinterpret_cast<uint16_t*>(cv.hi_pool + (size_t)page * cv.hi_page_bytes +
+                                                 (size_t)((g + page) % H) * PL::kHiHead + PL::kHiV);
+      const int m = c / 2;
+      const uint32_t w0[4] = {x[jj0].x, x[jj0].y, x[jj0].z, x[jj0].w};
+      const uint32_t w1[4] = {x[jj0 + 1].x, x[jj0 + 1].y, x[jj0 + 1].z, x[jj0 + 1].w};
+      const uint32_t w2[4] = {x[jj0 + 2].x, x[jj0 + 2].y, x[jj0 + 2].z, x[jj0 + 2].w};
+      const uint32_t w3[4] = {x[jj0 + 3].x, x[jj0 + 3].y, x[jj0 + 3].z, x[jj0 + 3].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = 16 * (e % 2);
+        const uint32_t lo = ((w0[e / 2] >> sh) & 0xFFFFu) | (((w1[e / 2] >> sh) & 0xFFFFu) << 16);
+        const uint32_t hi = ((w2[e / 2] >> sh) & 0xFFFFu) | (((w3[e / 2] >> sh) & 0xFFFFu) << 16);
+        *reinterpret_cast<uint2*>(vt + (((m >> 1) * 64 + u * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4) =
+            make_uint2(lo, hi);
+      }
+    } else {
+      // 4 bytes per (dd, i): the 4 slots' code bytes, in slot order
+      uint32_t pt[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) pt[r] = __shfl_xor(packed[jj0 + r], 2, 4);
+      if (!active || kv == 0 || q >= 2) continue;
+      uint8_t* vc = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead +
+                    PL::kLoVC;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint32_t word = 0u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          word |= (((packed[jj0 + r] >> (4 * e)) & 0xFu) | (((pt[r] >> (4 * e)) & 0xFu) << 4)) << (8 * r);
+        *reinterpret_cast<uint32_t*>(vc + ((u * 16 + 8 * q + e) * (PL::NM / 2) + i) * 4) = word;
       }
     }
   }
