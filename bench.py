@@ -446,9 +446,13 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None, ptags=None
 
 
 def kernel_source_digest() -> str:
+    """Digest of the attention kernels' sources (the kernels the traffic
+    counters measure): pask_device.h, then pask_attn.hip."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2608_28276_amd", "csrc", "pask_kernels.hip")
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in ("pask_device.h", "pask_attn.hip"):
+        h.update(open(os.path.join(ROOT, "paper_2608_28276_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def prompt_desc(cfg) -> str:

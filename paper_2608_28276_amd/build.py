@@ -22,6 +22,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpask.so")
+KERNEL_SOURCES = ("pask_append.hip", "pask_attn.hip")   # persisting entries; reading them
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -41,12 +42,14 @@ def _run(cmd):
 def build(verbose: bool = False) -> str:
     """Compile and link libpask.so; returns its path."""
     with tempfile.TemporaryDirectory(prefix="pask_build_") as tmp:
-        k_o = os.path.join(tmp, "pask_kernels.o")
-        a_o = os.path.join(tmp, "pask_api.o")
-        _run([HIPCC, *COMMON, *DEVICE, "-c", os.path.join(CSRC, "pask_kernels.hip"), "-o", k_o])
-        _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, "pask_api.cpp"), "-o", a_o])
+        objs = []
+        for src in KERNEL_SOURCES:
+            objs.append(os.path.join(tmp, src.replace(".hip", ".o")))
+            _run([HIPCC, *COMMON, *DEVICE, "-c", os.path.join(CSRC, src), "-o", objs[-1]])
+        objs.append(os.path.join(tmp, "pask_api.o"))
+        _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, "pask_api.cpp"), "-o", objs[-1]])
         tmp_lib = os.path.join(tmp, "libpask.so")
-        _run([HIPCC, *DEVICE, "-shared", "-fPIC", k_o, a_o, "-o", tmp_lib])
+        _run([HIPCC, *DEVICE, "-shared", "-fPIC", *objs, "-o", tmp_lib])
         shutil.move(tmp_lib, LIB)
     if verbose:
         print(f"built {LIB}")

@@ -1,0 +1,1048 @@
+// gfx950 kernels of the PASK hot path that persist entries.
+//
+//   reset        zero the status word, page cursors and per-(sequence, layer)
+//                counters of a cache.
+//   append_plan  per sequence: the action of every new token (table column in
+//                LDS, the higher of selected action and floor, Eq. 10),
+//                wavefront ballot + mbcnt prefix sums giving each surviving
+//                token its slot in the HIGH or LOW store in position order,
+//                page allocation, index lists and counters (the Persist step
+//                of Alg. 2).  DROP tokens get no slot (release, Section 3.1).
+//   append_pack  copy RETAIN-HIGH K/V (bf16) or quantise-and-pack RETAIN-LOW
+//                K/V (int4, one fp16 scale per 32 elements) into the pages.
+//   append_step  both of the above for one token per sequence (decode).
+//   window       the protected recent window (Section 3.1) variants of the
+//                three, and the online budget controller (Alg. 2) in the plan
+//                and step kernels.
+#include <hip/hip_runtime.h>
+
+#include <limits.h>
+#include <math.h>
+
+#include <type_traits>
+
+#include "pask_device.h"
+
+namespace pask {
+namespace {
+
+constexpr int kPackTokens = 16;   // tokens per append_pack block
+
+// ---------------------------------------------------------------------------
+// reset
+// ---------------------------------------------------------------------------
+__global__ void reset_kernel(CacheView cv, size_t n_counters) {
+  const size_t i0 = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i0 < 4) cv.status[i0] = i0 == 2 ? (uint32_t)cv.hi_base : 0u;   // HIGH cursor after the windows
+  if (i0 == 0) cv.budget->loaded = 0u;
+  for (size_t i = i0; i < n_counters; i += (size_t)gridDim.x * blockDim.x) cv.counters[i] = 0;
+}
+
+// R_0 into every layer of sequences b < batch.
+__global__ void budget_init_kernel(CacheView cv, int32_t batch, int64_t r0) {
+  const size_t n = (size_t)batch * cv.n_layers;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    *reinterpret_cast<int64_t*>(cv.counters + i * kCounterStride + kCntBudget) = r0;
+}
+
+// ---------------------------------------------------------------------------
+// decisions and slotting
+// ---------------------------------------------------------------------------
+
+// Action of one token (Eq. 10): the higher of the selected action and the
+// floor of its (tag, group) bucket.  Sinks, keep-all tokens and tags outside
+// the table are RETAIN-HIGH (the latter also flagged).
+__device__ __forceinline__ int decide(const uint8_t* s_a0, const uint8_t* s_amin, uint32_t n_tags,
+                                      uint32_t n_sink, bool keep_all, int tag, int pos,
+                                      bool& forced, bool& bad) {
+  bad = (uint32_t)tag >= n_tags;
+  if (keep_all || (uint32_t)pos < n_sink || bad) {
+    forced = true;
+    return kHigh;
+  }
+  forced = false;
+  const int a0 = s_a0[tag], am = s_amin[tag];
+  return a0 > am ? a0 : am;
+}
+
+// The online controller for one token (Alg. 2 after the lookup; Eq. 9-10):
+// the token's actions in every group start at max(a0, a-) (Eq. 10); while
+// their bytes exceed B = max(0, R - Gamma(s)), the group above its floor whose
+// last upgrade scores lowest (rho, Eq. 7) steps down, lower group on ties; in
+// a critical state, the group whose next upgrade scores highest (positive,
+// fits in B) steps up, lower group on ties, until none fits.  A forced token
+// (sink, tag outside the table) is HIGH everywhere.  R drops by the token's
+// bytes over all groups; the action of group `group` is returned.  Actions
+// are kept two bits per group in one word.  `t` may point to LDS or global
+// memory.
+__device__ int budget_decide(const BudgetTable* t, int tag, int state, bool forced, int group, int64_t& R,
+                             uint32_t& flags) {
+  const int C = (int)t->n_groups;
+  int64_t cost = 0;
+  if (forced) {
+    for (int c = 0; c < C; ++c) cost += t->m[c][kHigh];
+    R -= cost;
+    return kHigh;
+  }
+  int64_t gamma = 0;
+  bool crit = false;
+  if ((uint32_t)state < t->n_states) {
+    gamma = t->gamma[state];
+    crit = t->crit[state] != 0;
+  } else {
+    flags |= PASK_FLAG_BAD_STATE;
+  }
+  const uint8_t* a0 = t->action[tag];
+  const uint8_t* fl = t->floor_[tag];
+  const float(*rho)[2] = t->rho_up[tag];
+  uint32_t A = 0u;
+  for (int c = 0; c < C; ++c) {
+    const int ac = a0[c] > fl[c] ? a0[c] : fl[c];
+    A |= (uint32_t)ac << (2 * c);
+    cost += t->m[c][ac];
+  }
+  const int64_t B = R - gamma > 0 ? R - gamma : 0;
+  while (cost > B) {                                   // demote
+    int best = -1;
+    float best_rho = 0.0f;
+    for (int c = 0; c < C; ++c) {
+      const int ac = (int)((A >> (2 * c)) & 3u);
+      if (ac > fl[c]) {
+        const float r = rho[c][ac - 1];
+        if (best < 0 || r < best_rho) {
+          best = c;
+          best_rho = r;
+        }
+      }
+    }
+    if (best < 0) break;
+    const int ac = (int)((A >> (2 * best)) & 3u);
+    cost -= t->m[best][ac] - t->m[best][ac - 1];
+    A -= 1u << (2 * best);
+  }
+  while (crit) {                                       // promote
+    int best = -1;
+    float best_rho = 0.0f;
+    int64_t best_extra = 0;
+    for (int c = 0; c < C; ++c) {
+      const int ac = (int)((A >> (2 * c)) & 3u);
+      if (ac < kHigh) {
+        const float r = rho[c][ac];
+        const int64_t extra = t->m[c][ac + 1] - t->m[c][ac];
+        if (r > 0.0f && cost + extra <= B && (best < 0 || r > best_rho)) {
+          best = c;
+          best_rho = r;
+          best_extra = extra;
+        }
+      }
+    }
+    if (best < 0) break;
+    cost += best_extra;
+    A += 1u << (2 * best);
+  }
+  R -= cost;
+  return (int)((A >> (2 * group)) & 3u);
+}
+
+__device__ __forceinline__ int64_t* budget_of(int32_t* cnt) {
+  return reinterpret_cast<int64_t*>(cnt + kCntBudget);
+}
+
+// Exclusive count of `pred` over a 256-thread block in thread order: wavefront
+// ballot + popcount of the lanes below (mbcnt), plus the per-wave totals.
+// Also returns the block total.  Every thread of the block must call it.
+__device__ __forceinline__ int block_exclusive_count(bool pred, int* s_wave, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long mask = __ballot(pred);
+  const int below = __popcll(mask & ((1ull << lane) - 1ull));
+  if (lane == 0) s_wave[wave] = __popcll(mask);
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int cw = s_wave[w];
+    base += (w < wave) ? cw : 0;
+    total += cw;
+  }
+  __syncthreads();
+  return base + below;
+}
+
+__device__ __forceinline__ void load_table(const TableColumn& tab, uint8_t* s_a0, uint8_t* s_amin) {
+  if (threadIdx.x < 64) {
+    s_a0[threadIdx.x] = tab.a0[threadIdx.x];
+    s_amin[threadIdx.x] = tab.amin[threadIdx.x];
+  }
+}
+
+__device__ __forceinline__ int clamp_n_new(const AppendArgs& a, int b, uint32_t& flags) {
+  int n = a.n_new ? a.n_new[b] : a.max_new;
+  if (n < 0 || n > a.max_new) {
+    flags |= PASK_FLAG_BAD_COUNT;
+    n = n < 0 ? 0 : a.max_new;
+  }
+  return n;
+}
+
+// kBudget: the tokens carry parser states and the online controller decides
+// (one thread walks each chunk's tokens in position order, the table in LDS).
+template <bool kBudget>
+__global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_wave[4];
+  __shared__ unsigned s_page_base[2];
+  __shared__ int s_granted[2];
+  struct Empty {};
+  __shared__ std::conditional_t<kBudget, BudgetTable, Empty> s_bud;
+  __shared__ uint8_t s_act[kBudget ? 256 : 1];
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  load_table(a.tab, s_a0, s_amin);
+  uint32_t flags = 0;
+  const int n = clamp_n_new(a, b, flags);
+  int32_t* cnt = counters_of(cv, b, a.layer);
+  const int pos0 = cnt[kCntPos];
+  bool budget = false;
+  int64_t R = 0;
+  if constexpr (kBudget) {
+    const uint4* src = reinterpret_cast<const uint4*>(cv.budget);
+    uint4* dst = reinterpret_cast<uint4*>(&s_bud);
+    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += 256) dst[i] = src[i];
+    __syncthreads();
+    budget = s_bud.loaded == kBudgetLoaded;
+    if (!budget && threadIdx.x == 0) flags |= PASK_FLAG_NO_BUDGET;
+    if (budget && threadIdx.x == 0) R = *budget_of(cnt);
+  }
+  int nst[2] = {cnt[kCntHi], cnt[kCntLo]};
+  int n_drop = 0, n_forced = 0, n_lost = 0, n_fit = 0;
+  int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
+  int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
+  int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const bool keep_all = (a.flags & kKeepAll) != 0u;
+  const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
+  __syncthreads();
+
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    const int j = c0 + (int)threadIdx.x;
+    const bool valid = j < n;
+    const int pos = pos0 + j;
+    const bool fits = valid && pos < cv.max_tokens;
+    if constexpr (kBudget) {
+      if (budget && threadIdx.x == 0) {
+        const int j1 = min(min(n, c0 + 256), cv.max_tokens - pos0);
+        const int group = (int)a.tab.group;
+        for (int jj = c0; jj < j1; ++jj) {
+          const size_t at = (size_t)b * a.max_new + jj;
+          const int tag = (int)a.tags[at];
+          const bool forced = (uint32_t)(pos0 + jj) < s_bud.n_sink || (uint32_t)tag >= s_bud.n_tags;
+          s_act[jj - c0] = (uint8_t)budget_decide(&s_bud, tag, (int)a.states[at], forced, group, R, flags);
+        }
+      }
+      __syncthreads();
+    }
+    int act = kDrop;
+    bool forced = false, bad = false;
+    if (fits) {
+      const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new + j] : 0;
+      act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, keep_all, tag, pos, forced, bad);
+      if constexpr (kBudget) {
+        if (budget) act = s_act[threadIdx.x];
+      }
+    }
+    if (bad) flags |= PASK_FLAG_BAD_TAG;
+    if (valid && !fits) flags |= PASK_FLAG_SEQ_CAPACITY;
+    const int st = act == kHigh ? kHi : kLo;
+    const bool keep = fits && act != kDrop;
+    int tot_hi, tot_lo, np_hi, np_lo;
+    const int r_hi = block_exclusive_count(keep && st == kHi, s_wave, tot_hi);
+    const int r_lo = block_exclusive_count(keep && st == kLo, s_wave, tot_lo);
+    const int slot = keep ? nst[st] + (st == kHi ? r_hi : r_lo) : 0;
+    const bool new_page = keep && (slot % kPage) == 0;
+    const int pr_hi = block_exclusive_count(new_page && st == kHi, s_wave, np_hi);
+    const int pr_lo = block_exclusive_count(new_page && st == kLo, s_wave, np_lo);
+    if (threadIdx.x == 0) {
+      const int np[2] = {np_hi, np_lo};
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        unsigned base = 0u;
+        int granted = 0;
+        if (np[x] > 0) {
+          base = atomicAdd(&cv.status[2 + x], (unsigned)np[x]);
+          granted = base >= pool[x] ? 0 : (int)min((unsigned)np[x], pool[x] - base);
+        }
+        s_page_base[x] = base;
+        s_granted[x] = granted;
+      }
+    }
+    __syncthreads();
+    int pages_before[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) pages_before[x] = (nst[x] + kPage - 1) / kPage;
+    bool stored = false;
+    if (keep) {
+      const int pidx = slot / kPage;
+      stored = pidx < pages_before[st] + s_granted[st];
+      if (stored) {
+        if (new_page) bt[st][pidx] = (int)(s_page_base[st] + (unsigned)(st == kHi ? pr_hi : pr_lo));
+        il[st][slot] = pos;
+      } else {
+        flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+      }
+    }
+    if (valid) stg[j] = stored ? ((st << 30) | slot) : -1;
+    int c_drop, c_forced, c_lost, c_fit;
+    block_exclusive_count(fits && act == kDrop, s_wave, c_drop);
+    block_exclusive_count(stored && forced, s_wave, c_forced);
+    block_exclusive_count(valid && !stored && !(fits && act == kDrop), s_wave, c_lost);
+    block_exclusive_count(fits, s_wave, c_fit);
+    const int tot[2] = {tot_hi, tot_lo};
+#pragma unroll
+    for (int x = 0; x < 2; ++x) nst[x] = min(nst[x] + tot[x], (pages_before[x] + s_granted[x]) * kPage);
+    n_drop += c_drop;
+    n_forced += c_forced;
+    n_lost += c_lost;
+    n_fit += c_fit;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    cnt[kCntHi] = nst[0];
+    cnt[kCntLo] = nst[1];
+    cnt[kCntPos] = pos0 + n_fit;
+    cnt[kCntDrop] += n_drop;
+    cnt[kCntForced] += n_forced;
+    cnt[kCntLost] += n_lost;
+    if (budget) *budget_of(cnt) = R;
+  }
+  if (flags) atomicOr(cv.status, flags);
+}
+
+// ---------------------------------------------------------------------------
+// RETAIN-HIGH copy and RETAIN-LOW quantise-and-pack of one token
+// ---------------------------------------------------------------------------
+
+// Quantise 4 consecutive elements of a 32-element group held by 8 adjacent
+// lanes: s = fp16(absmax / 7) (correctly rounded division, saturated at 65504,
+// round-to-nearest-even conversion), q = clamp(rint(x / s), -7, 7).  Returns
+// the 4 codes as nibbles (element i in bits 4i..4i+3) and the scale bits.
+__device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& packed, uint32_t& sbits) {
+  float f[4] = {bf16_lo(x01), bf16_hi(x01), bf16_lo(x23), bf16_hi(x23)};
+  float am = fmaxf(fmaxf(fabsf(f[0]), fabsf(f[1])), fmaxf(fabsf(f[2]), fabsf(f[3])));
+  am = fmaxf(am, __shfl_xor(am, 1, 8));
+  am = fmaxf(am, __shfl_xor(am, 2, 8));
+  am = fmaxf(am, __shfl_xor(am, 4, 8));
+  const float s32 = fminf(am / 7.0f, 65504.0f);
+  const _Float16 h = (_Float16)s32;
+  const float s = (float)h;
+  sbits = (uint32_t)__builtin_bit_cast(uint16_t, h);
+  uint32_t p = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int q = 0;
+    if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
+    p |= ((uint32_t)q & 0xFu) << (4 * i);
+  }
+  packed = p;
+}
+
+// The same rule for 8 consecutive elements of a group held by 4 adjacent
+// lanes (element i of x in bits 4i..4i+3 of `packed`).
+__device__ __forceinline__ void quant8(const uint4& x, uint32_t& packed, uint32_t& sbits) {
+  const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
+                      bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
+  float am = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) am = fmaxf(am, fabsf(f[i]));
+  am = fmaxf(am, __shfl_xor(am, 1, 4));
+  am = fmaxf(am, __shfl_xor(am, 2, 4));
+  const float s32 = fminf(am / 7.0f, 65504.0f);
+  const _Float16 h = (_Float16)s32;
+  const float s = (float)h;
+  sbits = (uint32_t)__builtin_bit_cast(uint16_t, h);
+  uint32_t p = 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    int q = 0;
+    if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
+    p |= ((uint32_t)q & 0xFu) << (4 * i);
+  }
+  packed = p;
+}
+
+
+template <int D>
+__device__ __forceinline__ void write_hi(const CacheView& cv, int page, int t, const uint16_t* kin,
+                                         const uint16_t* vin) {
+  using PL = PageLayout<D>;
+  uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
+  const int nk = cv.n_kv_heads * (D / 8);          // 16-byte K chunks of the token
+  for (int x = threadIdx.x; x < nk; x += blockDim.x) {
+    const int g = x / (D / 8), c = x % (D / 8);      // dims 8c..8c+7 = 32i + 8q + 0..7
+    const int i = c / 4, q = c % 4;
+    uint8_t* dst = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + (i * 64 + q * 16 + t) * 16;
+    *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(kin + g * D + c * 8);
+  }
+  const int nv = cv.n_kv_heads * D;
+  const int qq = t / 4, jj = t % 4;
+  for (int x = threadIdx.x; x < nv; x += blockDim.x) {
+    const int g = x / D, d = x % D;
+    const int m = d / 16, dd = d % 16;
+    uint16_t* dst = reinterpret_cast<uint16_t*>(pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + PL::kHiV);
+    dst[(((m >> 1) * 64 + qq * 16 + dd) * 2 + (m & 1)) * 4 + jj] = vin[g * D + d];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, const uint16_t* kin,
+                                         const uint16_t* vin) {
+  using PL = PageLayout<D>;
+  const int n_tasks = cv.n_kv_heads * 2 * PL::NG * 8;               // 8 lanes per 32-element group
+  uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
+  const int qq = t / 4, jj = t % 4;
+  for (int base = 0; base < n_tasks; base += blockDim.x) {
+    const int task = base + (int)threadIdx.x;
+    if (task < n_tasks) {  // whole 8-lane groups are active together
+      const int gi = task >> 3, lig = task & 7;
+      const int i = gi % PL::NG, row = gi / PL::NG, g = row >> 1, kv = row & 1;
+      const uint16_t* src = (kv ? vin : kin) + g * D + i * kQGroup + lig * 4;   // dims 32i + 4lig + e
+      const uint2 raw = *reinterpret_cast<const uint2*>(src);
+      uint32_t packed, sbits;
+      quant4(raw.x, raw.y, packed, sbits);
+      uint8_t* hb = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kLoHead;
+      if (kv == 0) {
+        const int q = lig / 2, half = lig % 2;                        // j = 4*half + e
+        *reinterpret_cast<uint16_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4 + 2 * half) = (uint16_t)packed;
+        if (lig == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      } else {
+        const uint32_t partner = __shfl_xor(packed, 4, 8);           // dims 16 higher
+        if (lig < 4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int dd = 4 * lig + e;
+            const uint32_t b = ((packed >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4);
+            hb[PL::kLoVC + ((qq * 16 + dd) * (PL::NM / 2) + i) * 4 + jj] = (uint8_t)b;
+          }
+        }
+        if (lig == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      }
+    }
+  }
+}
+
+// Bulk persist of kPackTokens tokens of sequence blockIdx.y, after the plan
+// kernel has slotted them (staging code = store << 30 | slot, or -1).
+//   1. One thread per token reads its code and page id; thread 0 marks the
+//      runs of 4 tokens that fill a whole slot group (4 consecutive slots of
+//      one store, the first a multiple of 4).
+//   2. Every thread loads its 16-byte chunk of every token's K / V row (chunk
+//      k: K when k < Hkv*D/8, else V; head, then 8-dim piece), all in flight
+//      together (non-temporal: read once).
+//   3. K chunks (bf16, or int4 quantised by groups of 4 adjacent lanes with
+//      quant8) and scales go to the pages directly.  V tiles interleave the 4
+//      slots of a group at 2-byte (bf16) or 1-byte (int4 codes) granularity:
+//      for a whole group the lane holding a V chunk holds it for all 4 tokens
+//      and writes 8-byte (bf16) or 4-byte (codes) pieces; other tokens' V goes
+//      element by element.
+template <int D>
+__global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
+  using PL = PageLayout<D>;
+  constexpr int kC = D / 8;                        // 16-byte chunks per head row
+  __shared__ int s_code[kPackTokens], s_page[kPackTokens];
+  __shared__ uint32_t s_runs;                      // bit jj: tokens jj..jj+3 fill a slot group
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.y;
+  const int H = cv.n_kv_heads;
+  uint32_t unused = 0;
+  const int n = clamp_n_new(a, b, unused);
+  const int j0 = (int)blockIdx.x * kPackTokens;
+  if (j0 >= n) return;                             // the whole block
+  const int nt = min(kPackTokens, n - j0);
+  if (threadIdx.x < kPackTokens) {
+    const int j = j0 + (int)threadIdx.x;
+    int code = -1, page = 0;
+    if (j < n) {
+      code = cv.staging[(size_t)b * cv.staging_stride + j];
+      if (code >= 0) page = block_table_of(cv, b, a.layer, code >> 30)[(code & 0x3FFFFFFF) / kPage];
+    }
+    s_code[threadIdx.x] = code;
+    s_page[threadIdx.x] = page;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t runs = 0u;
+    for (int jj = 0; jj + 4 <= nt;) {
+      const int c0 = s_code[jj];
+      bool full = c0 >= 0 && (c0 & 3) == 0;        // slot % 4 == 0 (the store bit is above)
+      for (int r = 1; full && r < 4; ++r) full = s_code[jj + r] == c0 + r;
+      if (full) {
+        runs |= 1u << jj;
+        jj += 4;
+      } else {
+        ++jj;
+      }
+    }
+    s_runs = runs;
+  }
+  __syncthreads();
+  const uint32_t runs = s_runs;
+  uint32_t covered = 0u;                           // tokens written by a whole-group piece
+#pragma unroll
+  for (int jj = 0; jj < kPackTokens; ++jj)
+    if (runs >> jj & 1u) covered |= 0xFu << jj;
+  const size_t row = (size_t)H * D;
+  const int n_chunks = 2 * H * kC;                 // K and V chunks of one token (<= 256)
+  const int k = (int)threadIdx.x;
+  const bool active = k < n_chunks;                // whole 4-lane groups alike (H*kC is a multiple of 4)
+  const int kv = k / (H * kC), g = (k / kC) % H, c = k % kC;
+  const uint16_t* src = (kv ? a.v : a.k) + ((size_t)b * a.max_new + j0) * row + g * D + c * 8;
+  uint4 x[kPackTokens];
+  uint32_t packed[kPackTokens];                    // int4 codes of this lane's 8 elements, per LOW token
+#pragma unroll
+  for (int jj = 0; jj < kPackTokens; ++jj) {      // every token's chunk in flight together
+    x[jj] = active && jj < nt ? stream_load16(reinterpret_cast<const uint8_t*>(src + jj * row))
+                              : make_uint4(0u, 0u, 0u, 0u);
+    packed[jj] = 0u;
+  }
+  const int i = c / 4, q = c % 4;                  // int4: scale group i, dims 32i + 8q + 0..7
+#pragma unroll
+  for (int jj = 0; jj < kPackTokens; ++jj) {
+    const int code = s_code[jj];
+    if (jj >= nt || code < 0) continue;            // block-uniform
+    const int page = s_page[jj], t = (code & 0x3FFFFFFF) % kPage;
+    const bool grouped = covered >> jj & 1u;
+    if ((code >> 30) == kHi) {
+      if (!active) continue;
+      uint8_t* hb = cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % H) * PL::kHiHead;
+      if (kv == 0) {                               // dims 8c..8c+7 = 32i + 8q + 0..7
+        *reinterpret_cast<uint4*>(hb + ((c / 4) * 64 + (c % 4) * 16 + t) * 16) = x[jj];
+      } else if (!grouped) {                       // dims 16m + dd, dd = 8(c%2) + e
+        uint16_t* vt = reinterpret_cast<uint16_t*>(hb + PL::kHiV);
+        const int m = c / 2;
+        const uint32_t w[4] = {x[jj].x, x[jj].y, x[jj].z, x[jj].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          vt[(((m >> 1) * 64 + (t / 4) * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4 + t % 4] =
+              (uint16_t)(w[e / 2] >> (16 * (e % 2)));
+      }
+    } else {
+      uint32_t sbits = 0u;
+      quant8(x[jj], packed[jj], sbits);            // every lane: the shuffles need whole groups
+      const uint32_t partner = __shfl_xor(packed[jj], 2, 4);   // V: dims 16 higher (lanes q < 2)
+      if (!active) continue;
+      uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
+      if (kv == 0) {
+        *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = packed[jj];
+        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      } else {
+        // byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i + dd (low nibble) and
+        // 32i + 16 + dd (high nibble), dd = 8q + e for lanes q < 2
+        if (q < 2 && !grouped) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int dd = 8 * q + e;
+            hb[PL::kLoVC + (((t / 4) * 16 + dd) * (PL::NM / 2) + i) * 4 + t % 4] =
+                (uint8_t)(((packed[jj] >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4));
+          }
+        }
+        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      }
+    }
+  }
+  // Whole slot groups: tokens jj0..jj0+3 in slots 4u..4u+3 of one page.
+#pragma unroll
+  for (int jj0 = 0; jj0 + 4 <= kPackTokens; ++jj0) {
+    if (!(runs >> jj0 & 1u)) continue;             // block-uniform
+    const int code = s_code[jj0], page = s_page[jj0], u = ((code & 0x3FFFFFFF) % kPage) / 4;
+    if ((code >> 30) == kHi) {
+      if (!active || kv == 0) continue;
+      // 8 bytes per (m, dd): the 4 slots' bf16 values, in slot order
+      uint16_t* vt = reinterpret_cast<uint16_t*>(cv.hi_pool + (size_t)page * cv.hi_page_bytes +
+                                                 (size_t)((g + page) % H) * PL::kHiHead + PL::kHiV);
+      const int m = c / 2;
+      const uint32_t w0[4] = {x[jj0].x, x[jj0].y, x[jj0].z, x[jj0].w};
+      const uint32_t w1[4] = {x[jj0 + 1].x, x[jj0 + 1].y, x[jj0 + 1].z, x[jj0 + 1].w};
+      const uint32_t w2[4] = {x[jj0 + 2].x, x[jj0 + 2].y, x[jj0 + 2].z, x[jj0 + 2].w};
+      const uint32_t w3[4] = {x[jj0 + 3].x, x[jj0 + 3].y, x[jj0 + 3].z, x[jj0 + 3].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = 16 * (e % 2);
+        const uint32_t lo = ((w0[e / 2] >> sh) & 0xFFFFu) | (((w1[e / 2] >> sh) & 0xFFFFu) << 16);
+        const uint32_t hi = ((w2[e / 2] >> sh) & 0xFFFFu) | (((w3[e / 2] >> sh) & 0xFFFFu) << 16);
+        *reinterpret_cast<uint2*>(vt + (((m >> 1) * 64 + u * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4) =
+            make_uint2(lo, hi);
+      }
+    } else {
+      // 4 bytes per (dd, i): the 4 slots' code bytes, in slot order
+      uint32_t pt[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) pt[r] = __shfl_xor(packed[jj0 + r], 2, 4);
+      if (!active || kv == 0 || q >= 2) continue;
+      uint8_t* vc = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead +
+                    PL::kLoVC;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint32_t word = 0u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          word |= (((packed[jj0 + r] >> (4 * e)) & 0xFu) | (((pt[r] >> (4 * e)) & 0xFu) << 4)) << (8 * r);
+        *reinterpret_cast<uint32_t*>(vc + ((u * 16 + 8 * q + e) * (PL::NM / 2) + i) * 4) = word;
+      }
+    }
+  }
+}
+
+// One token of sequence b (thread 0 of the block): its action (Eq. 10, or
+// the online controller when parser states are given).
+__device__ __forceinline__ int decide_one(const AppendArgs& a, const uint8_t* s_a0, const uint8_t* s_amin, int b,
+                                          int32_t* cnt, int pos, bool& forced, uint32_t& flags) {
+  const CacheView& cv = a.cv;
+  const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new] : 0;
+  bool bad;
+  int act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, (a.flags & kKeepAll) != 0u, tag, pos, forced, bad);
+  if (bad) flags |= PASK_FLAG_BAD_TAG;
+  if (a.states) {
+    if (cv.budget->loaded == kBudgetLoaded) {
+      int64_t* r = budget_of(cnt);
+      int64_t R = *r;
+      act = budget_decide(cv.budget, tag, (int)a.states[(size_t)b * a.max_new], forced, (int)a.tab.group, R, flags);
+      *r = R;
+    } else {
+      flags |= PASK_FLAG_NO_BUDGET;
+    }
+  }
+  return act;
+}
+
+// Persist step of one entry at position pos (thread 0): DROP is counted; a
+// kept entry takes the next slot of its store (a new page when the slot
+// starts one) and its index-list entry.  Returns the store code (store << 30
+// | slot) and the page, or -1 when the entry is not stored.
+__device__ __forceinline__ int slot_one(const CacheView& cv, int b, int layer, int32_t* cnt, int act, bool forced,
+                                        int pos, int& page, uint32_t& flags) {
+  if (act == kDrop) {
+    cnt[kCntDrop] += 1;
+    return -1;
+  }
+  const int st = act == kHigh ? kHi : kLo;
+  const int slot = cnt[st];
+  int32_t* bt = block_table_of(cv, b, layer, st);
+  if (slot % kPage == 0) {
+    const unsigned pid = atomicAdd(&cv.status[2 + st], 1u);
+    const unsigned pool = st == kHi ? (unsigned)cv.hi_pages : (unsigned)cv.lo_pages;
+    if (pid >= pool) {
+      flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+      cnt[kCntLost] += 1;
+      return -1;
+    }
+    bt[slot / kPage] = (int)pid;
+  }
+  page = bt[slot / kPage];
+  index_list_of(cv, b, layer, st)[slot] = pos;
+  cnt[st] = slot + 1;
+  if (forced) cnt[kCntForced] += 1;
+  return (st << 30) | slot;
+}
+
+// One token per sequence: thread 0 decides and slots it, then the block
+// writes it.
+template <int D>
+__global__ __launch_bounds__(256) void append_step_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_code, s_page;
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  load_table(a.tab, s_a0, s_amin);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t flags = 0;
+    const int n = clamp_n_new(a, b, flags);
+    int code = -1, page = -1;
+    if (n > 0) {
+      int32_t* cnt = counters_of(cv, b, a.layer);
+      const int pos = cnt[kCntPos];
+      if (pos >= cv.max_tokens) {
+        flags |= PASK_FLAG_SEQ_CAPACITY;
+        cnt[kCntLost] += 1;
+      } else {
+        bool forced;
+        const int act = decide_one(a, s_a0, s_amin, b, cnt, pos, forced, flags);
+        code = slot_one(cv, b, a.layer, cnt, act, forced, pos, page, flags);
+        cnt[kCntPos] = pos + 1;
+      }
+    }
+    if (flags) atomicOr(cv.status, flags);
+    s_code = code;
+    s_page = page;
+  }
+  __syncthreads();
+  const int code = s_code;
+  if (code < 0) return;
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  const uint16_t* kin = a.k + (size_t)b * a.max_new * row;
+  const uint16_t* vin = a.v + (size_t)b * a.max_new * row;
+  const int slot = code & 0x3FFFFFFF;
+  if ((code >> 30) == kHi) write_hi<D>(cv, s_page, slot % kPage, kin, vin);
+  else write_lo<D>(cv, s_page, slot % kPage, kin, vin);
+}
+
+// ---------------------------------------------------------------------------
+// the protected recent window (Section 3.1)
+// ---------------------------------------------------------------------------
+// With W > 0 a token is decided when it is appended (its action and forced
+// flag go to ring_act, the controller charges it then) and enters the window
+// of its (sequence, layer): window slot p mod W, held in HIGH page layout in
+// pages of the HIGH pool reserved for the windows.  It is persisted by its
+// action when position p + W is appended.
+
+__device__ __forceinline__ int ring_page(const CacheView& cv, int b, int layer, int k) {
+  return (b * cv.n_layers + layer) * cv.ring_pp + k;
+}
+__device__ __forceinline__ uint8_t* ring_act_of(const CacheView& cv, int b, int layer) {
+  return cv.ring_act + ((size_t)b * cv.n_layers + layer) * cv.window;
+}
+
+// The bf16 K and V rows [Hkv][D] of slot t of a HIGH-layout page (the
+// inverse of write_hi), into kout / vout, by the whole block.
+template <int D>
+__device__ __forceinline__ void read_hi_token(const CacheView& cv, int page, int t, uint16_t* kout, uint16_t* vout) {
+  using PL = PageLayout<D>;
+  const uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
+  const int nk = cv.n_kv_heads * (D / 8);
+  for (int x = threadIdx.x; x < nk; x += blockDim.x) {
+    const int g = x / (D / 8), c = x % (D / 8);
+    const int i = c / 4, q = c % 4;
+    const uint8_t* src = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + (i * 64 + q * 16 + t) * 16;
+    *reinterpret_cast<uint4*>(kout + g * D + c * 8) = *reinterpret_cast<const uint4*>(src);
+  }
+  const int nv = cv.n_kv_heads * D;
+  const int qq = t / 4, jj = t % 4;
+  for (int x = threadIdx.x; x < nv; x += blockDim.x) {
+    const int g = x / D, d = x % D;
+    const int m = d / 16, dd = d % 16;
+    const uint16_t* src =
+        reinterpret_cast<const uint16_t*>(pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kHiHead + PL::kHiV);
+    vout[g * D + d] = src[(((m >> 1) * 64 + qq * 16 + dd) * 2 + (m & 1)) * 4 + jj];
+  }
+}
+
+// Bulk append with a window.  The call's combined index x covers positions
+// q = e0 + x, e0 = max(0, p0 - W): first the window's tokens from before the
+// call (x < nr = p0 - e0; their decisions in ring_act), then the new tokens
+// (j = x - nr).  Positions below e1 = max(e0, p0 + n_fit - W) leave the window
+// now and are slotted into the stores in position order as in
+// append_plan_kernel; the new tokens from e1 on enter the window and their
+// decisions go to ring_act (after every read of ring_act in the chunk: the
+// W positions of the window after the call have distinct slots, so no slot
+// still in the window is overwritten).  staging[x] gets the store code of x
+// or -1; the sequence's last two staging words keep p0 and n_fit for the
+// pack and window-fill kernels.
+template <bool kBudget>
+__global__ __launch_bounds__(256) void append_plan_window_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_wave[4];
+  __shared__ unsigned s_page_base[2];
+  __shared__ int s_granted[2];
+  struct Empty {};
+  __shared__ std::conditional_t<kBudget, BudgetTable, Empty> s_bud;
+  __shared__ uint8_t s_act[kBudget ? 256 : 1];
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  const int W = cv.window;
+  load_table(a.tab, s_a0, s_amin);
+  uint32_t flags = 0;
+  const int n = clamp_n_new(a, b, flags);
+  int32_t* cnt = counters_of(cv, b, a.layer);
+  const int p0 = cnt[kCntPos];
+  const int n_fit = max(0, min(n, cv.max_tokens - p0));
+  if (n_fit < n) flags |= PASK_FLAG_SEQ_CAPACITY;
+  const int e0 = max(0, p0 - W), nr = p0 - e0;
+  const int n_out = max(e0, p0 + n_fit - W) - e0;    // entries leaving the window now
+  const int n_x = nr + n_fit;
+  uint8_t* ract = ring_act_of(cv, b, a.layer);
+  bool budget = false;
+  int64_t R = 0;
+  if constexpr (kBudget) {
+    const uint4* src = reinterpret_cast<const uint4*>(cv.budget);
+    uint4* dst = reinterpret_cast<uint4*>(&s_bud);
+    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += 256) dst[i] = src[i];
+    __syncthreads();
+    budget = s_bud.loaded == kBudgetLoaded;
+    if (!budget && threadIdx.x == 0) flags |= PASK_FLAG_NO_BUDGET;
+    if (budget && threadIdx.x == 0) R = *budget_of(cnt);
+  }
+  int nst[2] = {cnt[kCntHi], cnt[kCntLo]};
+  int n_drop = 0, n_forced = 0, n_lost = 0;
+  int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
+  int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
+  int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const bool keep_all = (a.flags & kKeepAll) != 0u;
+  const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
+  __syncthreads();
+
+  for (int c0 = 0; c0 < n_x; c0 += 256) {
+    const int x = c0 + (int)threadIdx.x;
+    const bool valid = x < n_x;
+    const bool is_new = valid && x >= nr;
+    const int j = x - nr;
+    const int q = e0 + x;
+    if constexpr (kBudget) {
+      if (budget && threadIdx.x == 0) {              // the chunk's new tokens, in position order
+        const int j1 = min(n_fit, c0 + 256 - nr);
+        for (int jj = max(0, c0 - nr); jj < j1; ++jj) {
+          const size_t at = (size_t)b * a.max_new + jj;
+          const int tag = (int)a.tags[at];
+          const bool forced = (uint32_t)(p0 + jj) < s_bud.n_sink || (uint32_t)tag >= s_bud.n_tags;
+          s_act[jj + nr - c0] =
+              (uint8_t)budget_decide(&s_bud, tag, (int)a.states[at], forced, (int)a.tab.group, R, flags);
+        }
+      }
+      __syncthreads();
+    }
+    int act = kDrop;
+    bool forced = false, bad = false;
+    if (is_new) {
+      const int tag = a.tags ? (int)a.tags[(size_t)b * a.max_new + j] : 0;
+      act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, keep_all, tag, q, forced, bad);
+      if constexpr (kBudget) {
+        if (budget) act = s_act[threadIdx.x];
+      }
+    } else if (valid) {
+      const uint8_t byte = ract[q % W];
+      act = byte & 3;
+      forced = ((byte >> 2) & 1) != 0;
+    }
+    if (bad) flags |= PASK_FLAG_BAD_TAG;
+    const bool leaving = valid && x < n_out;
+    const int st = act == kHigh ? kHi : kLo;
+    const bool keep = leaving && act != kDrop;
+    int tot_hi, tot_lo, np_hi, np_lo;
+    const int r_hi = block_exclusive_count(keep && st == kHi, s_wave, tot_hi);
+    const int r_lo = block_exclusive_count(keep && st == kLo, s_wave, tot_lo);
+    const int slot = keep ? nst[st] + (st == kHi ? r_hi : r_lo) : 0;
+    const bool new_page = keep && (slot % kPage) == 0;
+    const int pr_hi = block_exclusive_count(new_page && st == kHi, s_wave, np_hi);
+    const int pr_lo = block_exclusive_count(new_page && st == kLo, s_wave, np_lo);
+    if (threadIdx.x == 0) {
+      const int np[2] = {np_hi, np_lo};
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        unsigned base = 0u;
+        int granted = 0;
+        if (np[y] > 0) {
+          base = atomicAdd(&cv.status[2 + y], (unsigned)np[y]);
+          granted = base >= pool[y] ? 0 : (int)min((unsigned)np[y], pool[y] - base);
+        }
+        s_page_base[y] = base;
+        s_granted[y] = granted;
+      }
+    }
+    __syncthreads();                                 // also: every read of ract in this chunk is done
+    int pages_before[2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y) pages_before[y] = (nst[y] + kPage - 1) / kPage;
+    bool stored = false;
+    if (keep) {
+      const int pidx = slot / kPage;
+      stored = pidx < pages_before[st] + s_granted[st];
+      if (stored) {
+        if (new_page) bt[st][pidx] = (int)(s_page_base[st] + (unsigned)(st == kHi ? pr_hi : pr_lo));
+        il[st][slot] = q;
+      } else {
+        flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+      }
+    }
+    if (valid) stg[x] = stored ? ((st << 30) | slot) : -1;
+    if (is_new && !leaving) ract[q % W] = (uint8_t)(act | (forced ? 4 : 0));
+    int c_drop, c_forced, c_lost;
+    block_exclusive_count(leaving && act == kDrop, s_wave, c_drop);
+    block_exclusive_count(stored && forced, s_wave, c_forced);
+    block_exclusive_count(keep && !stored, s_wave, c_lost);
+    const int tot[2] = {tot_hi, tot_lo};
+#pragma unroll
+    for (int y = 0; y < 2; ++y) nst[y] = min(nst[y] + tot[y], (pages_before[y] + s_granted[y]) * kPage);
+    n_drop += c_drop;
+    n_forced += c_forced;
+    n_lost += c_lost;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    cnt[kCntHi] = nst[0];
+    cnt[kCntLo] = nst[1];
+    cnt[kCntPos] = p0 + n_fit;
+    cnt[kCntDrop] += n_drop;
+    cnt[kCntForced] += n_forced;
+    cnt[kCntLost] += n_lost + (n - n_fit);
+    if (budget) *budget_of(cnt) = R;
+    stg[cv.staging_stride - 2] = p0;
+    stg[cv.staging_stride - 1] = n_fit;
+  }
+  if (flags) atomicOr(cv.status, flags);
+}
+
+// Persist the entries the plan marked (x < n_out): from the window (read
+// into LDS first) or from the call's input rows.
+template <int D>
+__global__ __launch_bounds__(256) void append_pack_window_kernel(AppendArgs a) {
+  __shared__ __align__(16) uint16_t s_kv[2][8 * D];   // one window token's K and V rows (Hkv <= 8)
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.y;
+  const int W = cv.window;
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const int p0 = stg[cv.staging_stride - 2], n_fit = stg[cv.staging_stride - 1];
+  const int e0 = max(0, p0 - W), nr = p0 - e0;
+  const int n_out = max(e0, p0 + n_fit - W) - e0;
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  for (int xx = 0; xx < kPackTokens; ++xx) {
+    const int x = (int)blockIdx.x * kPackTokens + xx;
+    if (x >= n_out) break;
+    const int code = stg[x];
+    if (code < 0) continue;
+    const int st = code >> 30, slot = code & 0x3FFFFFFF;
+    const int page = block_table_of(cv, b, a.layer, st)[slot / kPage];
+    const uint16_t *kin, *vin;
+    if (x < nr) {
+      const int ws = (e0 + x) % W;
+      read_hi_token<D>(cv, ring_page(cv, b, a.layer, ws / kPage), ws % kPage, s_kv[0], s_kv[1]);
+      __syncthreads();
+      kin = s_kv[0];
+      vin = s_kv[1];
+    } else {
+      kin = a.k + ((size_t)b * a.max_new + (x - nr)) * row;
+      vin = a.v + ((size_t)b * a.max_new + (x - nr)) * row;
+    }
+    if (st == kHi) write_hi<D>(cv, page, slot % kPage, kin, vin);
+    else write_lo<D>(cv, page, slot % kPage, kin, vin);
+    __syncthreads();                                 // s_kv is reused by the next entry
+  }
+}
+
+// The new tokens that stay in the window (the last min(n_fit, W) of the
+// call) into their window slots; after the pack kernel has read the slots
+// they replace.
+template <int D>
+__global__ __launch_bounds__(256) void append_window_fill_kernel(AppendArgs a) {
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.y;
+  const int W = cv.window;
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const int p0 = stg[cv.staging_stride - 2], n_fit = stg[cv.staging_stride - 1];
+  const int j0 = max(0, n_fit - W);
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  for (int kk = 0; kk < kPackTokens; ++kk) {
+    const int j = j0 + (int)blockIdx.x * kPackTokens + kk;
+    if (j >= n_fit) break;
+    const int ws = (p0 + j) % W;
+    write_hi<D>(cv, ring_page(cv, b, a.layer, ws / kPage), ws % kPage, a.k + ((size_t)b * a.max_new + j) * row,
+                a.v + ((size_t)b * a.max_new + j) * row);
+  }
+}
+
+// One token per sequence with a window: thread 0 decides the new token and,
+// when position pos - W leaves the window, slots that entry by its recorded
+// action; the block then reads the leaving entry from its window slot into
+// LDS, writes the new token into that slot, and persists the leaving entry.
+template <int D>
+__global__ __launch_bounds__(256) void append_step_window_kernel(AppendArgs a) {
+  __shared__ uint8_t s_a0[64], s_amin[64];
+  __shared__ int s_code, s_page, s_ws;
+  __shared__ __align__(16) uint16_t s_kv[2][8 * D];
+  const CacheView& cv = a.cv;
+  const int b = blockIdx.x;
+  const int W = cv.window;
+  load_table(a.tab, s_a0, s_amin);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t flags = 0;
+    const int n = clamp_n_new(a, b, flags);
+    int code = -1, page = -1, ws = -1;
+    if (n > 0) {
+      int32_t* cnt = counters_of(cv, b, a.layer);
+      const int pos = cnt[kCntPos];
+      if (pos >= cv.max_tokens) {
+        flags |= PASK_FLAG_SEQ_CAPACITY;
+        cnt[kCntLost] += 1;
+      } else {
+        bool forced;
+        const int act = decide_one(a, s_a0, s_amin, b, cnt, pos, forced, flags);
+        uint8_t* ract = ring_act_of(cv, b, a.layer);
+        ws = pos % W;
+        if (pos >= W) {                              // position pos - W leaves the window
+          const uint8_t old = ract[ws];
+          code = slot_one(cv, b, a.layer, cnt, old & 3, ((old >> 2) & 1) != 0, pos - W, page, flags);
+        }
+        ract[ws] = (uint8_t)(act | (forced ? 4 : 0));
+        cnt[kCntPos] = pos + 1;
+      }
+    }
+    if (flags) atomicOr(cv.status, flags);
+    s_code = code;
+    s_page = page;
+    s_ws = ws;
+  }
+  __syncthreads();
+  const int code = s_code, ws = s_ws;
+  if (ws < 0) return;
+  const int rpage = ring_page(cv, b, a.layer, ws / kPage);
+  if (code >= 0) read_hi_token<D>(cv, rpage, ws % kPage, s_kv[0], s_kv[1]);
+  __syncthreads();                                   // the leaving entry is read before its slot is reused
+  const size_t row = (size_t)cv.n_kv_heads * D;
+  write_hi<D>(cv, rpage, ws % kPage, a.k + (size_t)b * a.max_new * row, a.v + (size_t)b * a.max_new * row);
+  if (code >= 0) {
+    const int slot = code & 0x3FFFFFFF;
+    if ((code >> 30) == kHi) write_hi<D>(cv, s_page, slot % kPage, s_kv[0], s_kv[1]);
+    else write_lo<D>(cv, s_page, slot % kPage, s_kv[0], s_kv[1]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s) {
+  const size_t n = (size_t)max_batch * cv.n_layers * kCounterStride;
+  const size_t blocks = std::min<size_t>((n + 255) / 256 + 1, 4096);
+  reset_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(cv, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_budget_init(const CacheView& cv, int32_t batch, int64_t r0, hipStream_t s) {
+  const size_t n = (size_t)batch * cv.n_layers;
+  const size_t blocks = std::min<size_t>((n + 255) / 256, 4096);
+  budget_init_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(cv, batch, r0);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
+  if (a.max_new == 1 && a.n_new == nullptr) return launch_append_step(a, s);
+  if (a.cv.window > 0) {
+    if (a.states) append_plan_window_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    else append_plan_window_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    const dim3 gp((a.max_new + a.cv.window + kPackTokens - 1) / kPackTokens, a.batch);
+    const dim3 gf((std::min(a.max_new, a.cv.window) + kPackTokens - 1) / kPackTokens, a.batch);
+    if (a.cv.head_dim == 64) {
+      append_pack_window_kernel<64><<<gp, dim3(256), 0, s>>>(a);
+      append_window_fill_kernel<64><<<gf, dim3(256), 0, s>>>(a);
+    } else {
+      append_pack_window_kernel<128><<<gp, dim3(256), 0, s>>>(a);
+      append_window_fill_kernel<128><<<gf, dim3(256), 0, s>>>(a);
+    }
+    return hipGetLastError();
+  }
+  if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  else append_plan_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  const dim3 grid((a.max_new + kPackTokens - 1) / kPackTokens, a.batch);
+  if (a.cv.head_dim == 64) append_pack_kernel<64><<<grid, dim3(256), 0, s>>>(a);
+  else append_pack_kernel<128><<<grid, dim3(256), 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_step(const AppendArgs& a, hipStream_t s) {
+  if (a.cv.window > 0) {
+    if (a.cv.head_dim == 64) append_step_window_kernel<64><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    else append_step_window_kernel<128><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+    return hipGetLastError();
+  }
+  if (a.cv.head_dim == 64) append_step_kernel<64><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  else append_step_kernel<128><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace pask

@@ -1,0 +1,903 @@
+// gfx950 kernels of the PASK hot path that read the cache.
+//
+//   attn         grouped-query flash-decode, stream-K: one single-wave block
+//                per resident wave slot, each streaming an equal contiguous
+//                range of the (sequence, KV head, page) list over the HIGH and
+//                LOW stores; q.k on bf16 MFMA (query heads as columns), int4
+//                K codes widened exactly to bf16 in registers with the offset
+//                removed in the accumulator, the K scale applied per 32-dim
+//                group; p.v on bf16 MFMA for HIGH pages and on fp16 MFMA with
+//                exact fp16 V codes and the V scale folded into p for LOW
+//                pages; online softmax in base 2, next pages prefetched into
+//                registers.
+//   attn_merge   per (sequence, KV head): combine the partials of its pieces
+//                (max, sum, values) into bf16 outputs; zero for empty histories.
+//   distortion   the attention-output distortion of Eq. 4: the partials of a
+//                reference and an intervened cache merged in fp32, the squared
+//                distance of the outputs maximised over query heads.
+#include <hip/hip_runtime.h>
+
+#include <limits.h>
+#include <math.h>
+
+#include <type_traits>
+
+#include "pask_device.h"
+
+namespace pask {
+namespace {
+
+// ---------------------------------------------------------------------------
+// decode attention
+// ---------------------------------------------------------------------------
+//
+// Stream-K: the work is the list of (sequence b, KV head g, page) triples,
+// HIGH pages of a (b, g) before its LOW pages, each page weighing 32 units
+// (PASK_WEIGHT_LO for a LOW page).  The grid holds one single-wave worker
+// per resident wave slot of the chip, and worker w takes the w-th of equal
+// contiguous unit ranges, so every worker starts at launch and all finish
+// together.  A range crossing a (b, g) boundary closes that segment with a
+// partial block; the range length is at least what keeps every (b, g) within
+// as many pieces as the workspace holds partials.
+//
+// Per page (16 slots x all G query heads of KV head g), one wave:
+//   scores  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: rows = slots, columns
+//           = query heads, so lane (q, n) holds the scores of head n for
+//           slots 4q..4q+3; a LOW code c becomes the bf16 value 136 + c
+//           (exact), the accumulation starts at -136 * sum(q) of the 32-dim
+//           group, and the K scale multiplies the group's result;
+//   softmax online in base 2, per head, rescaling only when a max grows;
+//   values  HIGH: O += P V on v_mfma_f32_16x16x16_bf16 with P (split into
+//           bf16 high and low parts, so p keeps ~16 bits) as the A operand
+//           exactly as the score tile lies; LOW: the weights p x (V scale)
+//           rounded to fp16 times the codes as exact fp16 values on
+//           v_mfma_f32_16x16x16_f16, into the same accumulators.
+// The next page's operands (three pages ahead for LOW pages, whose scales
+// take one register) are loaded while the current one is computed.
+// Each segment leaves (max, sum, unnormalised o) per head; attn_merge
+// combines the partials of a (b, g).
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// D[16x16] += A[16x32] B[32x16], bf16 operands: lane l holds A[l%16][8(l/16)..+8],
+// B[8(l/16)..+8][l%16], D[4(l/16)..+4][l%16].
+__device__ __forceinline__ f32x4_t mfma_k32(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 c, 0, 0, 0);
+}
+// D[16x16] += A[16x16] B[16x16]: lane l holds A[l%16][4(l/16)..+4], B[4(l/16)..+4][l%16].
+__device__ __forceinline__ f32x4_t mfma_k16(uint2 a, uint2 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, a), __builtin_bit_cast(short4_t, b),
+                                                   c, 0, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t (&w)[N]) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int k = 0; k < N / 4; ++k) {
+      const uint4 x = stream_load16(p + 16 * k);
+      w[4 * k] = x.x; w[4 * k + 1] = x.y; w[4 * k + 2] = x.z; w[4 * k + 3] = x.w;
+    }
+  } else if constexpr (N % 2 == 0) {
+#pragma unroll
+    for (int k = 0; k < N / 2; ++k) {
+      const u32x2_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p) + k);
+      w[2 * k] = x[0]; w[2 * k + 1] = x[1];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + k);
+  }
+}
+
+// Raw operands of one page for one lane.
+template <int D>
+struct HiRaw {
+  uint32_t k[4 * PageLayout<D>::NG];   // QK A operands: NG x 8 bf16
+  uint32_t v[2 * PageLayout<D>::NM];   // PV B operands: NM x 4 bf16
+};
+template <int D>
+struct LoRaw {
+  uint32_t kc[PageLayout<D>::NG];      // NG x 8 int4 codes
+  uint32_t vc[PageLayout<D>::NM / 2];  // 4 slots x NM/2 bytes of V code pairs
+  uint32_t sc;                         // word n of the row's scales (load_lo)
+};
+
+template <int D>
+__device__ __forceinline__ HiRaw<D> load_hi(const uint8_t* head, int q, int n) {
+  using PL = PageLayout<D>;
+  HiRaw<D> x;
+  const int l = q * 16 + n;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {
+    const uint4 w = stream_load16(head + (i * 64 + l) * 16);
+    x.k[4 * i] = w.x; x.k[4 * i + 1] = w.y; x.k[4 * i + 2] = w.z; x.k[4 * i + 3] = w.w;
+  }
+#pragma unroll
+  for (int i = 0; i < PL::NM / 2; ++i) {
+    const uint4 w = stream_load16(head + PL::kHiV + (i * 64 + l) * 16);
+    x.v[4 * i] = w.x; x.v[4 * i + 1] = w.y; x.v[4 * i + 2] = w.z; x.v[4 * i + 3] = w.w;
+  }
+  return x;
+}
+
+template <int D>
+__device__ __forceinline__ LoRaw<D> load_lo(const uint8_t* head, int q, int n) {
+  using PL = PageLayout<D>;
+  LoRaw<D> x;
+  constexpr int KW = 2 * PL::NG;                 // scale words of 4 slots
+  load_words(head + (q * 16 + n) * PL::NG * 4, x.kc);
+  load_words(head + PL::kLoVC + (q * 16 + n) * (PL::NM / 2) * 4, x.vc);
+  // Row q (slots 4q..4q+3) needs KW words of K scales and KW of V scales,
+  // the same for its 16 lanes: lane n loads one of them (n < KW: K word n,
+  // then V word n - KW; spare lanes repeat K word 0) and attend_page shares
+  // them across the row, so a page's scales cost one 4-byte load per lane
+  // and one register instead of 2 x KW per lane.
+  const int off = n < KW ? PL::kLoKS + 4 * (q * KW + n)
+                         : (n < 2 * KW ? PL::kLoVS + 4 * (q * KW + n - KW) : PL::kLoKS + 4 * q * KW);
+  x.sc = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(head + off));
+  return x;
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+// x = hi + lo with hi = bf16(x) and lo = bf16(x - hi): 16 significant bits,
+// so the weights of the p.v MFMA carry fp32-like precision (two products).
+__device__ __forceinline__ void split_bf16x4(const float (&x)[4], uint2& hi, uint2& lo) {
+  float r[4];
+  hi = make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+  r[0] = x[0] - bf16_lo(hi.x);
+  r[1] = x[1] - bf16_hi(hi.x);
+  r[2] = x[2] - bf16_lo(hi.y);
+  r[3] = x[3] - bf16_hi(hi.y);
+  lo = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+}
+// K codes widened to bf16 with an offset: a nibble n (two's complement
+// code c) becomes the bf16 bit pattern 0x4300 | (n ^ 8), the exact value
+// 128 + (c + 8) = 136 + c (bf16 spacing is 1 on [128, 256)).  Two codes per
+// 32-bit word cost one byte permute and one xor; the offset is removed by
+// starting the q.k accumulation at -136 * (sum of q over the group).
+constexpr float kCodeOffset = 136.0f;
+constexpr uint32_t kCodeBias = 0x43084308u;
+// Codes 2e (low nibble) and 2e+1 (high nibble) of byte e of w, as a bf16 pair.
+template <int e>
+__device__ __forceinline__ uint32_t codes_pair_in_byte(uint32_t lo4, uint32_t hi4) {
+  // v_perm_b32: selector bytes 0-3 pick bytes of the second source (lo4),
+  // 4-7 bytes of the first (hi4), 0x0C gives zero.
+  return __builtin_amdgcn_perm(hi4, lo4, 0x0C000C00u | ((4u + e) << 16) | e) ^ kCodeBias;
+}
+// V codes as exact fp16 values.  After n ^ 8 (done once per word) a nibble
+// holds c + 8; the fp16 bit pattern 0x6400 | (c + 8) is 1024 + c + 8 (fp16
+// spacing is 1 on [1024, 2048)), and one packed fp16 subtraction of 1032
+// leaves c exactly.  Nibbles in bytes j0 and j1 of n4 (one per byte) as an
+// fp16 pair; the 0x64 bytes come from the constant first source.
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+template <int j0, int j1>
+__device__ __forceinline__ uint32_t vcodes_pair(uint32_t n4) {
+  const uint32_t w = __builtin_amdgcn_perm(0x64646464u, n4, 0x04000400u | (j1 << 16) | j0);
+  const f16x2_t c = __builtin_bit_cast(f16x2_t, w) - f16x2_t{(_Float16)1032.0f, (_Float16)1032.0f};
+  return __builtin_bit_cast(uint32_t, c);
+}
+
+// Per-wave attention state.  The score tile is S^T (MFMA row = slot 4q + r,
+// column = query head n), so lane (q, n) holds p of head n for slots
+// 4q..4q+3: the A operand of the p.v MFMA as it stands, with no transpose.
+// The output tile has row = query head 4q + r and column = dim 16m + n.
+template <int D, int G>
+struct AttnState {
+  uint32_t qa[4 * PageLayout<D>::NG];   // QK B operands: q of head n, dims 32i + 8q + 0..7
+  f32x4_t acc[PageLayout<D>::NM];        // unnormalised outputs
+  float m, l;                            // head n: running max (log2 units), lane-partial sum
+  float kq[PageLayout<D>::NG];           // head n: -(K code offset) x sum of q over 32-dim group i
+};
+
+// Max / sum over the 64 lanes' copies of one head (lanes n, n+16, n+32,
+// n+48) with gfx950's row swaps, on the VALU instead of through LDS.  With
+// both operands x, v_permlane16_swap yields rows (0, 0, 2, 2) and (1, 1, 3, 3)
+// of x, v_permlane32_swap rows (0, 1, 0, 1) and (2, 3, 2, 3); combining the
+// pair after each swap reduces lanes l and l ^ 16, then l and l ^ 32.
+__device__ __forceinline__ float head_max(float x) {
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(t[0]), __uint_as_float(t[1]));
+}
+__device__ __forceinline__ float head_sum(float x) {
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
+}
+
+// Word j of the row, for every lane of the row: DPP row_newbcast:j copies
+// lane j of each 16-lane row to the whole row.
+template <int J>
+__device__ __forceinline__ uint32_t row_word(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x150 + J, 0xF, 0xF, false);
+}
+// The row's KW K-scale words (lanes 0..KW-1) and KW V-scale words (lanes KW..2KW-1).
+template <int KW, int J = 0>
+__device__ __forceinline__ void row_words(uint32_t x, uint32_t (&k)[KW], uint32_t (&v)[KW]) {
+  if constexpr (J < KW) {
+    k[J] = row_word<J>(x);
+    v[J] = row_word<KW + J>(x);
+    row_words<KW, J + 1>(x, k, v);
+  }
+}
+
+// One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
+template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
+__device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2,
+                                            int q, int n) {
+  using PL = PageLayout<D>;
+  f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
+  [[maybe_unused]] uint32_t ks[2 * PL::NG], vs[2 * PL::NG];   // LOW: the row's K / V scale words
+  if constexpr (kIsHi) {
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i)
+      sc = mfma_k32(make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]),
+                    make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), sc);
+  } else {
+    row_words<2 * PL::NG>(x.sc, ks, vs);
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {
+      const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;
+      const f32x4_t off = {st.kq[i], st.kq[i], st.kq[i], st.kq[i]};   // removes the code offset
+      const f32x4_t c = mfma_k32(make_uint4(codes_pair_in_byte<0>(lo4, hi4), codes_pair_in_byte<1>(lo4, hi4),
+                                            codes_pair_in_byte<2>(lo4, hi4), codes_pair_in_byte<3>(lo4, hi4)),
+                                 make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), off);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
+        const int hidx = r * PL::NG + i;
+        sc[r] = fmaf(half_bits_to_float(ks[hidx / 2] >> (16 * (hidx % 2))), c[r], sc[r]);
+      }
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    sc[r] = (!kMasked || 4 * q + r < nvalid) ? sc[r] * scale_log2 : -INFINITY;
+    mx = fmaxf(mx, sc[r]);
+  }
+  // Online softmax for head n: rescale only when some head's max grew.
+  const float mn = fmaxf(st.m, head_max(mx));
+  if (__ballot(mn > st.m)) {
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mn);
+    st.l *= alpha;
+    st.m = mn;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {                   // output row 4q + r takes head 4q + r's factor
+      const float ar = __shfl(alpha, 4 * q + r);
+#pragma unroll
+      for (int k = 0; k < PL::NM; ++k) st.acc[k][r] *= ar;
+    }
+  }
+  // exp2 on v_exp_f32 directly: arguments are <= 0, and results that would
+  // be fp32 subnormals (weights below 2^-126 of the running max) become 0.
+  float pr[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    pr[r] = __builtin_amdgcn_exp2f(sc[r] - st.m);
+    st.l += pr[r];
+  }
+  if constexpr (kIsHi) {
+    uint2 pa_hi, pa_lo;
+    split_bf16x4(pr, pa_hi, pa_lo);
+#pragma unroll
+    for (int mm = 0; mm < PL::NM; ++mm) {
+      uint32_t v0 = x.v[2 * mm], v1 = x.v[2 * mm + 1];
+      if constexpr (kMasked) {   // zero V of slots past the end (their memory is not written)
+        const int t0 = 4 * q;
+        v0 = (t0 + 1 < nvalid) ? v0 : (t0 < nvalid ? (v0 & 0xFFFFu) : 0u);
+        v1 = (t0 + 3 < nvalid) ? v1 : (t0 + 2 < nvalid ? (v1 & 0xFFFFu) : 0u);
+      }
+      st.acc[mm] = mfma_k16(pa_hi, make_uint2(v0, v1), st.acc[mm]);
+      st.acc[mm] = mfma_k16(pa_lo, make_uint2(v0, v1), st.acc[mm]);
+    }
+  } else {
+    // V: the weights p x (V scale of the slot's group), rounded once to
+    // fp16 (11 significant bits), times the exact fp16 codes on the fp16
+    // MFMA.  Slots past the end get weight 0 (their scales are not written).
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {
+      float w[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int hidx = jj * PL::NG + i;
+        const float vsc = half_bits_to_float(vs[hidx / 2] >> (16 * (hidx % 2)));
+        w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vsc : 0.0f;
+      }
+      const f16x4_t wa = {(_Float16)w[0], (_Float16)w[1], (_Float16)w[2], (_Float16)w[3]};
+      const uint32_t vx = x.vc[i] ^ 0x88888888u;     // nibbles c + 8
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        // byte jj of vc[i]: slot 4q + jj, dim 32i + n (low nibble) and 32i + 16 + n (high)
+        const uint32_t n4 = (hh ? vx >> 4 : vx) & 0x0F0F0F0Fu;
+        const f16x4_t vb = __builtin_bit_cast(f16x4_t, make_uint2(vcodes_pair<0, 1>(n4), vcodes_pair<2, 3>(n4)));
+        st.acc[2 * i + hh] = __builtin_amdgcn_mfma_f32_16x16x16f16(wa, vb, st.acc[2 * i + hh], 0, 0, 0);
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ int cdiv(int x, int y) { return (x + y - 1) / y; }
+// A value the whole wave holds alike, moved to a scalar register so the
+// compiler treats what depends on it as uniform.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ int wave_sum(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+__device__ __forceinline__ int wave_max(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = max(x, __shfl_xor(x, off));
+  return x;
+}
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+// Pages of sequence b in the layer: the HIGH store, the recent window (HIGH
+// layout, min(n_pos, W) slots) and the LOW store, in that order, and their
+// length in work units: the stream-K decomposition weighs a HIGH or window
+// page kWeightHi units and a LOW page kWeightLo (PASK_WEIGHT_LO).
+constexpr int kWeightHi = 32;
+constexpr int kWeightLo = PASK_WEIGHT_LO;
+static_assert(kWeightLo >= 1 && kWeightLo <= kWeightHi, "LOW page weight out of range");
+struct SeqPages {
+  int n_hi, n_win, n_lo;   // slots of the HIGH store, the window, the LOW store
+  int np_hi, np_w, np;     // pages: HIGH store, + window (the HIGH-weight ones), all
+  int len;
+};
+__device__ __forceinline__ int len_of(int n_hi, int n_win, int n_lo) {
+  return kWeightHi * (cdiv(n_hi, kPage) + cdiv(n_win, kPage)) + kWeightLo * cdiv(n_lo, kPage);
+}
+__device__ __forceinline__ SeqPages make_pages(int n_hi, int n_win, int n_lo) {
+  SeqPages s;
+  s.n_hi = n_hi;
+  s.n_win = n_win;
+  s.n_lo = n_lo;
+  s.np_hi = cdiv(n_hi, kPage);
+  s.np_w = s.np_hi + cdiv(n_win, kPage);
+  s.np = s.np_w + cdiv(n_lo, kPage);
+  s.len = len_of(n_hi, n_win, n_lo);
+  return s;
+}
+__device__ __forceinline__ int window_slots(const AttnArgs& a, int n_pos) { return min(n_pos, a.cv.window); }
+
+// Store counts of sequence `lane` for the first 64 sequences, read once per
+// block: the plan, the search for a block's first sequence and the walk to
+// the next sequence take them from registers instead of memory.
+struct FirstCounts {
+  int n_hi, n_lo, n_win;   // 0 past the batch
+};
+__device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
+  const int lane = threadIdx.x & 63;
+  const int32_t* c = counters_of(a.cv, lane < a.batch ? lane : 0, a.layer);
+  const int hi = c[kCntHi], lo = c[kCntLo], pos = c[kCntPos];
+  FirstCounts f;
+  f.n_hi = lane < a.batch ? hi : 0;
+  f.n_lo = lane < a.batch ? lo : 0;
+  f.n_win = lane < a.batch ? window_slots(a, pos) : 0;
+  return f;
+}
+// Pages of sequence b (wave-uniform, < batch).
+__device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const FirstCounts& f, int b) {
+  if (b < 64)
+    return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_win, b),
+                      __builtin_amdgcn_readlane(f.n_lo, b));
+  const int32_t* c = counters_of(a.cv, b, a.layer);
+  return make_pages(uni(c[kCntHi]), uni(window_slots(a, c[kCntPos])), uni(c[kCntLo]));
+}
+// Length in units of sequence c0 + lane (c0 wave-uniform; 0 past `limit`).
+__device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f, int c0, int limit) {
+  const int b = c0 + (int)(threadIdx.x & 63);
+  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_win, f.n_lo) : 0;
+  const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
+  const int len = len_of(c[kCntHi], window_slots(a, c[kCntPos]), c[kCntLo]);
+  return b < limit ? len : 0;
+}
+// Unit offset of page j (HIGH-weight pages first, then LOW) inside its segment.
+__device__ __forceinline__ int page_start(const SeqPages& s, int j) {
+  return j < s.np_w ? kWeightHi * j : kWeightHi * s.np_w + kWeightLo * (j - s.np_w);
+}
+// First page whose unit offset is >= u (s.np when there is none).
+__device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
+  if (u <= kWeightHi * s.np_w) return cdiv(u, kWeightHi);
+  return s.np_w + min(s.np - s.np_w, cdiv(u - kWeightHi * s.np_w, kWeightLo));
+}
+
+// Stream-K decomposition of one attention call, computed identically by every
+// block of the attention and merge kernels.  The work list is the segments
+// (sequence b, KV head g) in that nesting order, each the pages of (b, g) laid
+// out in units; segment (b, g) starts at unit excl(b) * Hkv + g * len(b), where
+// excl(b) sums len over the sequences before b.  Block w takes the pages that
+// start in units [w*U, (w+1)*U): contiguous ranges of equal weight.  U is at
+// least one HIGH page and kWeightLo <= kWeightHi, so every block between the
+// first and the last one of a segment holds a page of it; U is also large
+// enough that no segment is cut into more than `splits` pieces (the workspace
+// bound).
+struct StreamPlan {
+  long long total;   // units
+  int U;             // units per block
+};
+constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
+
+__device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
+  int total = 0, mx = 0;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int len = lane_len(a, f, c0, a.batch);
+    total += uni(wave_sum(len));
+    mx = max(mx, uni(wave_max(len)));
+  }
+  StreamPlan pl;
+  pl.total = (long long)total * a.cv.n_kv_heads;
+  const long long even = (pl.total + n_blocks - 1) / n_blocks;
+  pl.U = max(kWeightHi * kMinPagesPerBlock, (int)min(even, (long long)INT_MAX));
+  pl.U = max(pl.U, cdiv(mx, a.splits - 1));
+  return pl;
+}
+
+// Sequence whose segments hold unit P, and the units of the sequences before it.
+__device__ __forceinline__ void locate(const AttnArgs& a, const FirstCounts& f, long long P, int& b_out,
+                                       int& excl_out) {
+  const long long H = a.cv.n_kv_heads;
+  int base = 0;
+  b_out = -1;
+  excl_out = 0;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int len = lane_len(a, f, c0, a.batch);
+    const int incl = wave_inclusive_scan(len) + base;
+    const int excl = incl - len;
+    const bool hit = len > 0 && (long long)excl * H <= P && P < (long long)incl * H;
+    const unsigned long long m = __ballot(hit);
+    if (m) {
+      const int src = __ffsll((long long)m) - 1;
+      b_out = uni(c0 + src);
+      excl_out = uni(__shfl(excl, src));
+      return;
+    }
+    base = uni(__shfl(incl, 63));
+  }
+}
+
+// Stream pages [p0, p1) of one store of (b, g), loading page p+1 while
+// computing page p.  The page ids come from the block table kIdChunk at a time, one per
+// lane, and are read with readlane, so a page's loads depend on no other
+// memory access.  The prefetches are unconditional (past the end they read
+// the pool's first head slot, which every worker reads there, so they hit in
+// the caches; the non-temporal page loads would not hit on a re-read of the
+// run's last page): the loop body is straight-line code and the compiler
+// waits only for the current page's loads.  KV head g of a page
+// sits in head slot (g + page) mod n_kv_heads, which spreads one head's data
+// over DRAM channels.
+constexpr int kIdChunk = 128;
+
+// kWindow: the pages are a recent window, consecutive pool pages from id0 on
+// (bt unused).
+template <int D, int G, bool kIsHi, bool kWindow = false>
+__device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes, int head_bytes, int n_heads,
+                                          const int32_t* bt, int id0, int p0, int p1, int n_slots, int g,
+                                          AttnState<D, G>& st, float scale_log2, int q, int n) {
+  using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
+  const int lane = threadIdx.x & 63;
+  auto load = [&](int page, bool real) -> Raw {
+    const uint8_t* head = pool + (size_t)page * page_bytes + (size_t)((g + page) % n_heads) * head_bytes;
+    head = real ? head : pool;   // past the end: the pool's first head slot, read by every worker
+    if constexpr (kIsHi) return load_hi<D>(head, q, n);
+    else return load_lo<D>(head, q, n);
+  };
+  auto attend = [&](const Raw& r, int p) {
+    const int nvalid = min(kPage, n_slots - p * kPage);
+    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, q, n);
+    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, q, n);
+  };
+  for (int c = p0; c < p1; c += kIdChunk) {
+    const int cn = min(kIdChunk, p1 - c);
+    const int ids0 = kWindow ? id0 + c + min(lane, cn - 1) : bt[c + min(lane, cn - 1)];
+    const int ids1 = kWindow ? id0 + c + min(64 + lane, cn - 1) : bt[c + min(64 + lane, cn - 1)];
+    auto id = [&](int i) -> int {   // i: wave-uniform, < cn
+      return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
+    };
+    auto ld = [&](int i) -> Raw { return load(id(min(i, cn - 1)), i < cn); };
+    if constexpr (kIsHi) {
+      // Two page buffers used in turn (unrolled by two), so no buffer is
+      // copied while its loads are in flight.
+      Raw x0 = ld(0);
+      for (int i = 0; i < cn; i += 2) {
+        const Raw x1 = ld(i + 1);
+        attend(x0, c + i);
+        x0 = ld(i + 2);
+        if (i + 1 < cn) attend(x1, c + i + 1);
+      }
+    } else {
+      // A LOW page is 2 + 2 KiB of codes and 2 x 128 B of scales per head
+      // (D 128): four buffers in turn keep three pages in flight.
+      Raw x0 = ld(0), x1 = ld(1), x2 = ld(2);
+      for (int i = 0; i < cn; i += 4) {
+        const Raw x3 = ld(i + 3);
+        attend(x0, c + i);
+        x0 = ld(i + 4);
+        if (i + 1 < cn) attend(x1, c + i + 1);
+        x1 = ld(i + 5);
+        if (i + 2 < cn) attend(x2, c + i + 2);
+        x2 = ld(i + 6);
+        if (i + 3 < cn) attend(x3, c + i + 3);
+      }
+    }
+  }
+}
+
+// Pages [j0, j1) of (b, g) (HIGH store, recent window, LOW store): this
+// piece's partial of (b, g), combined with the others by attn_merge.
+template <int D, int G>
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
+                                               long long seg0, int U, int q, int n) {
+  using PL = PageLayout<D>;
+  const CacheView& cv = a.cv;
+  const int H = cv.n_kv_heads;
+  const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;
+  AttnState<D, G> st;
+  // Columns n >= G repeat head G-1 (finite scores; their results are unused).
+  const uint16_t* qh = a.q + (bh0 + min(n, G - 1)) * D + 8 * q;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {
+    const uint4 w = *reinterpret_cast<const uint4*>(qh + 32 * i);
+    st.qa[4 * i] = w.x; st.qa[4 * i + 1] = w.y; st.qa[4 * i + 2] = w.z; st.qa[4 * i + 3] = w.w;
+  }
+#pragma unroll
+  for (int k = 0; k < PL::NM; ++k) st.acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  st.m = -INFINITY;
+  st.l = 0.0f;
+#pragma unroll
+  for (int i = 0; i < PL::NG; ++i) {            // -offset x sum of q over group i (head n)
+    float part = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part += bf16_lo(st.qa[4 * i + e]) + bf16_hi(st.qa[4 * i + e]);
+    st.kq[i] = -kCodeOffset * head_sum(part);
+  }
+  if (j0 < sp.np_hi)
+    run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), 0, j0,
+                          min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, q, n);
+  if (j0 < sp.np_w && j1 > sp.np_hi)             // the recent window's pages
+    run_pages<D, G, true, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, nullptr,
+                                (b * cv.n_layers + a.layer) * cv.ring_pp, max(j0, sp.np_hi) - sp.np_hi,
+                                min(j1, sp.np_w) - sp.np_hi, sp.n_win, g, st, a.scale_log2, q, n);
+  if (j1 > sp.np_w)
+    run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo), 0,
+                           max(j0, sp.np_w) - sp.np_w, j1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n);
+  // Partial of piece `slot` of (b, g): rows of G4 = max(G, 4) query heads,
+  // stored as float4s of 4 heads at one dim (index ((q*NM + k)*16 + n)*4 + r
+  // for head 4q + r, dim 16k + n): each store instruction writes 256
+  // contiguous bytes, and the (max, sum) pairs of the G4 heads sit together.
+  // Rows past G hold finite values that are never read into an output.
+  constexpr int G4 = G > 4 ? G : 4;
+  const float l_n = head_sum(st.l);              // head n, over all slots
+  const int slot = (int)(w - seg0 / U);          // < a.splits by the choice of U
+  const size_t blk = ((size_t)b * H + g) * a.splits + slot;
+  if (4 * q < G4) {
+    float* o = a.ws_o + blk * (G4 * D);
+#pragma unroll
+    for (int k = 0; k < PL::NM; ++k)
+      *reinterpret_cast<float4*>(o + ((q * PL::NM + k) * 16 + n) * 4) =
+          make_float4(st.acc[k][0], st.acc[k][1], st.acc[k][2], st.acc[k][3]);
+  }
+  if (q == 0 && n < G4) *reinterpret_cast<float2*>(a.ws_ml + (blk * G4 + n) * 2) = make_float2(st.m, l_n);
+}
+
+// One single-wave workgroup per stream-K worker w.
+template <int D, int G>
+__global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int w = uni(blockIdx.x);
+  const int q = lane >> 4, n = lane & 15;
+  const int H = a.cv.n_kv_heads;
+  const FirstCounts f = first_counts(a);
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const long long start = (long long)w * plan.U;
+  if (start >= plan.total) return;
+  const long long end = min(plan.total, start + plan.U);
+  int b, excl;
+  locate(a, f, start, b, excl);
+  if (b < 0) return;
+  SeqPages sp = seq_pages(a, f, b);
+  const long long rel = start - (long long)excl * H;
+  int g = (int)(rel / sp.len);
+  int j0 = first_page_at(sp, (int)(rel % sp.len));
+  while (true) {
+    const long long seg0 = (long long)excl * H + (long long)g * sp.len;
+    if (seg0 >= end) return;
+    const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
+    if (j0 < j1) attend_segment<D, G>(a, w, b, g, j0, j1, sp, seg0, plan.U, q, n);
+    if (j1 < sp.np) return;
+    j0 = 0;
+    if (++g == H) {                              // next sequence that holds any page
+      g = 0;
+      excl += sp.len;
+      do {
+        if (++b >= a.batch) return;
+        sp = seq_pages(a, f, b);
+      } while (sp.len == 0);
+    }
+  }
+}
+
+// Online merge of the partials of one (sequence, KV head) by thread t of a
+// merge block: float4 position t of the partial rows, i.e. heads 4q..4q+3 at
+// one dim, with the running (max, sum) of those 4 heads.
+template <int D, int G>
+constexpr int merge_threads() { return (G > 4 ? G : 4) * D / 4; }
+
+template <int D, int G, int kB = 8>
+struct PieceMerge {
+  static constexpr int G4 = G > 4 ? G : 4;
+  static constexpr int kBatch = kB;              // pieces whose loads are issued together
+  float4 v[kBatch], mla[kBatch], mlb[kBatch];
+  float acc[4], M[4], L[4];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      acc[r] = 0.0f;
+      M[r] = -INFINITY;
+      L[r] = 0.0f;
+    }
+  }
+  // Loads pieces p0.. of the (b, g) whose first partial block is blk0; past
+  // `last` the last piece is repeated (fold skips it).
+  __device__ __forceinline__ void load(const AttnArgs& a, size_t blk0, int t, int q, int p0, int last) {
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const size_t pb = blk0 + min(p0 + u, last);
+      const float* ml = a.ws_ml + pb * G4 * 2 + 8 * q;
+      v[u] = *reinterpret_cast<const float4*>(a.ws_o + pb * (G4 * D) + t * 4);
+      mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
+      mlb[u] = *reinterpret_cast<const float4*>(ml + 4);   // (m, l) of heads 4q+2, 4q+3
+    }
+  }
+  // Merges the first n (<= kBatch) loaded pieces.
+  __device__ __forceinline__ void fold(int n) {
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (u >= n) break;
+      const float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      const float mlv[8] = {mla[u].x, mla[u].y, mla[u].z, mla[u].w, mlb[u].x, mlb[u].y, mlb[u].z, mlb[u].w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float mp = mlv[2 * r], lp = mlv[2 * r + 1];
+        const float mn = fmaxf(M[r], mp);
+        const float alpha = exp2f(M[r] - mn), wgt = exp2f(mp - mn);
+        L[r] = L[r] * alpha + wgt * lp;
+        acc[r] = acc[r] * alpha + wgt * vv[r];
+        M[r] = mn;
+      }
+    }
+  }
+};
+
+// Pieces of segment (b, g) in the stream-K decomposition (sp: pages of b,
+// excl: units of the sequences before b; sp.np > 0).
+__device__ __forceinline__ int n_pieces(const StreamPlan& plan, const SeqPages& sp, int excl, int g, int H) {
+  const long long seg0 = (long long)excl * H + (long long)g * sp.len;
+  return (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
+}
+// Units of the sequences before b (wave-uniform).
+__device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts& f, int b) {
+  int excl = 0;
+  for (int c0 = 0; c0 < b; c0 += 64) excl += uni(wave_sum(lane_len(a, f, c0, b)));
+  return excl;
+}
+
+// One (sequence, KV head): combine the partials of its pieces (one or more)
+// into the bf16 outputs and log-sum-exps of its G query heads; zero output
+// and -inf for an empty history.  Thread t merges float4 position t of the
+// partial rows; the normalised rows are staged in LDS and written as
+// contiguous 16-byte pieces.
+template <int D, int G>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merge_threads <= 256
+  constexpr int NM = D / 16;
+  static_assert(merge_threads<D, G>() % 64 == 0 && merge_threads<D, G>() <= 256, "merge block size");
+  __shared__ __align__(16) uint16_t s_out[G][D];
+  const int t = threadIdx.x;
+  const int H = a.cv.n_kv_heads;
+  const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
+  const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
+  const size_t blk0 = ((size_t)b * H + g) * a.splits;
+  const int q = t / (NM * 16), k = (t / 16) % NM, n = t % 16;
+  PieceMerge<D, G> pm;
+  // The first pieces are loaded before the piece count is known (slots
+  // below `splits` are in bounds; those past the count are skipped), so their
+  // latency overlaps that of the counters the count comes from.
+  pm.load(a, blk0, t, q, 0, a.splits - 1);
+  const FirstCounts f = first_counts(a);
+  const SeqPages sp = seq_pages(a, f, b);
+  if (sp.np == 0) {
+    for (int i = t; i < G * D; i += merge_threads<D, G>()) a.out[row0 * D + i] = 0;
+    if (a.lse && t < G) a.lse[row0 + t] = -INFINITY;
+    return;
+  }
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
+  pm.init();
+  for (int p0 = 0; p0 < nparts; p0 += PieceMerge<D, G>::kBatch) {
+    if (p0 > 0) pm.load(a, blk0, t, q, p0, nparts - 1);
+    pm.fold(nparts - p0);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * q + r;
+    if (h < G) {
+      s_out[h][16 * k + n] = f32_to_bf16_rne_dev(pm.acc[r] / pm.L[r]);
+      if (a.lse && k == 0 && n == 0) a.lse[row0 + h] = (pm.M[r] + log2f(pm.L[r])) * 0.69314718055994530942f;
+    }
+  }
+  __syncthreads();
+  // G rows of D bf16 are contiguous in the output: 16-byte pieces.
+  const uint4* src = reinterpret_cast<const uint4*>(&s_out[0][0]);
+  uint4* dst = reinterpret_cast<uint4*>(a.out + row0 * D);
+  for (int i = t; i < G * D / 8; i += merge_threads<D, G>()) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// attention-output distortion (Eq. 4)
+// ---------------------------------------------------------------------------
+
+// Normalised fp32 outputs of heads 4q..4q+3 at thread t's dim for (b, g) in
+// the reference (or_) and the intervened (oi) cache: both sets of partials
+// loaded before either is merged, so their latencies overlap; 0 for an
+// empty history.
+template <int D, int G>
+__device__ __forceinline__ void merged_pair(const AttnArgs& ref, const StreamPlan& pr, const SeqPages& sr, int er,
+                                            const AttnArgs& itv, const StreamPlan& pi, const SeqPages& si, int ei,
+                                            int b, int g, int t, int q, float (&or_)[4], float (&oi)[4]) {
+  constexpr int kB = 4;                          // pieces per batch and cache: both in flight, no spills
+  const int H = ref.cv.n_kv_heads;
+  const int nr = sr.np ? n_pieces(pr, sr, er, g, H) : 0, ni = si.np ? n_pieces(pi, si, ei, g, H) : 0;
+  const size_t blk0 = ((size_t)b * H + g);
+  PieceMerge<D, G, kB> mr, mi;
+  mr.init();
+  mi.init();
+  for (int p0 = 0; p0 < max(nr, ni); p0 += kB) {
+    if (p0 < nr) mr.load(ref, blk0 * ref.splits, t, q, p0, nr - 1);
+    if (p0 < ni) mi.load(itv, blk0 * itv.splits, t, q, p0, ni - 1);
+    if (p0 < nr) mr.fold(nr - p0);
+    if (p0 < ni) mi.fold(ni - p0);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    or_[r] = nr ? mr.acc[r] / mr.L[r] : 0.0f;
+    oi[r] = ni ? mi.acc[r] / mi.L[r] : 0.0f;
+  }
+}
+
+__device__ __forceinline__ float wave_sum_f(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// KV heads a distortion block handles at once: that many merge groups of
+// merge_threads threads, at most 512 threads (256 VGPRs per thread).
+template <int D, int G>
+constexpr int distortion_heads() { return 512 / merge_threads<D, G>() < 8 ? 512 / merge_threads<D, G>() : 8; }
+
+// One block per sequence b: for every KV head g (distortion_heads of them at
+// a time, one merge group each), the outputs of its G query heads over the
+// reference cache (partials of `ref`) and the intervened one (`itv`) in fp32,
+// the squared L2 distance of each head's rows summed over the D dims, and the
+// maximum over all query heads (Eq. 4, inside the expectation), added to
+// dist[b] when in_s is null or in_s[b] != 0.
+template <int D, int G>
+__global__ __launch_bounds__(512) void distortion_kernel(AttnArgs ref, AttnArgs itv, const uint8_t* in_s,
+                                                          float* dist) {
+  constexpr int NM = D / 16;
+  constexpr int G4 = G > 4 ? G : 4;
+  constexpr int MT = merge_threads<D, G>();
+  constexpr int GP = distortion_heads<D, G>();
+  __shared__ float s_d2[GP][G4];
+  const int b = uni(blockIdx.x);
+  if (in_s && in_s[b] == 0) return;
+  const int gl = threadIdx.x / MT, t = threadIdx.x % MT;   // merge group, thread in it
+  const int H = ref.cv.n_kv_heads;
+  const int q = t / (NM * 16);
+  const FirstCounts fr = first_counts(ref), fi = first_counts(itv);
+  const StreamPlan pr = stream_plan(ref, fr, ref.attn_blocks), pi = stream_plan(itv, fi, itv.attn_blocks);
+  const SeqPages sr = seq_pages(ref, fr, b), si = seq_pages(itv, fi, b);
+  const int er = units_before(ref, fr, b), ei = units_before(itv, fi, b);
+  float worst = 0.0f;
+  for (int g0 = 0; g0 < H; g0 += GP) {
+    if (threadIdx.x < GP * G4) s_d2[threadIdx.x / G4][threadIdx.x % G4] = 0.0f;
+    __syncthreads();
+    const int g = g0 + gl;
+    if (g < H) {                                 // whole merge groups (waves) take this branch alike
+      float o_r[4], o_i[4];
+      merged_pair<D, G>(ref, pr, sr, er, itv, pi, si, ei, b, g, t, q, o_r, o_i);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {              // each wave holds 64 dims of heads 4q..4q+3
+        const float e = o_r[r] - o_i[r];
+        const float w = wave_sum_f(e * e);
+        if ((t & 63) == 0) atomicAdd(&s_d2[gl][4 * q + r], w);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0)
+      for (int j = 0; j < GP && g0 + j < H; ++j)
+        for (int h = 0; h < G; ++h) worst = fmaxf(worst, s_d2[j][h]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dist[b] += worst;
+}
+
+}  // namespace
+
+// Stream-K workers of attn_kernel<D, G> on the current device: as many waves
+// as can be resident at once (occupancy x compute units), so every worker
+// starts at launch.  Queried once per device and instance.
+template <int D, int G>
+int attn_grid() {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  if (cached[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64, 0) != hipSuccess || per_cu <= 0)
+      return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
+    cached[dev] = per_cu * cus;
+  }
+  return cached[dev];
+}
+
+hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s) {
+  const int D = args.cv.head_dim;
+  AttnArgs a = args;
+  const dim3 block(64);
+#define PASK_CASE(DD, GG)                                                        \
+  if (D == DD && group_size == GG) {                                             \
+    a.attn_blocks = attn_grid<DD, GG>();                                         \
+    if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
+    attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
+    attn_merge_kernel<DD, GG><<<dim3(a.batch * a.cv.n_kv_heads), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
+    return hipGetLastError();                                                    \
+  }
+  PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
+  PASK_CASE(128, 1) PASK_CASE(128, 2) PASK_CASE(128, 4) PASK_CASE(128, 8)
+#undef PASK_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args, int group_size,
+                             const uint8_t* in_s, float* dist, hipStream_t s) {
+  const int D = ref_args.cv.head_dim;
+  AttnArgs ref = ref_args, itv = itv_args;
+  const dim3 block(64);
+#define PASK_CASE(DD, GG)                                                        \
+  if (D == DD && group_size == GG) {                                             \
+    ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG>();                     \
+    if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
+    attn_kernel<DD, GG><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);            \
+    attn_kernel<DD, GG><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);            \
+    distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>() * distortion_heads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
+    return hipGetLastError();                                                    \
+  }
+  PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
+  PASK_CASE(128, 1) PASK_CASE(128, 2) PASK_CASE(128, 4) PASK_CASE(128, 8)
+#undef PASK_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace pask

@@ -1,0 +1,78 @@
+// Device-side helpers shared by the append kernels (pask_append.hip) and the
+// attention kernels (pask_attn.hip): addresses of a cache's counters, block
+// tables and index lists, bf16 helpers, non-temporal loads and the page
+// layout.  Included by those two files only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "pask_internal.h"
+
+namespace pask {
+namespace {
+
+constexpr int kDrop = 0, kHigh = 2;   // RETAIN-LOW is 1 (R < L < H)
+
+__device__ __forceinline__ size_t sl_index(const CacheView& cv, int b, int layer) {
+  return (size_t)b * cv.n_layers + layer;
+}
+__device__ __forceinline__ int32_t* counters_of(const CacheView& cv, int b, int layer) {
+  return cv.counters + sl_index(cv, b, layer) * kCounterStride;
+}
+__device__ __forceinline__ int32_t* block_table_of(const CacheView& cv, int b, int layer, int st) {
+  return cv.block_table + (sl_index(cv, b, layer) * 2 + st) * (size_t)cv.max_pages;
+}
+__device__ __forceinline__ int32_t* index_list_of(const CacheView& cv, int b, int layer, int st) {
+  return cv.index_list + (sl_index(cv, b, layer) * 2 + st) * (size_t)cv.max_tokens;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// fp32 -> bf16, round to nearest even: gfx950's v_cvt_pk_bf16_f32.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
+  return (uint16_t)pack_bf16x2(f, 0.0f);
+}
+
+
+// Data read once per call (pages in the attention, a bulk append's input
+// rows): non-temporal loads, so the streamed lines do not displace others in
+// the L2 and the last-level cache (the attention call on the 64-sequence
+// Qwen3-4B workload measured 10% faster than with plain loads).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
+  const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+
+// Page layout, per KV head, chosen so that the MFMA operands of the attention
+// kernel arrive by fully coalesced loads: load instruction i of lane l = 16q + n
+// reads bytes 1024 i + 16 l of a HIGH tile, so each instruction of the wave
+// covers 1 KiB contiguously.
+//   HIGH  K tile: element (t, d), d = 32i + 8q + j  at ((i*64 + q*16 + t)*8 + j)   (bf16)
+//         V tile: element (t, d), d = 16m + dd      at (((m/2)*64 + t/4*16 + dd)*2 + m%2)*4 + t%4
+//   LOW   K codes: nibble ((q*16 + t)*NG + i)*8 + j (element j of the 8 at byte j/2,
+//                  low nibble for even j); K scales [t][NG] fp16;
+//         V codes: byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i+dd (low
+//                  nibble) and 32i+16+dd (high nibble) of slot t; V scales [t][NG].
+// NG = D/32 scale groups, NM = D/16.  Every byte belongs to a single slot, so
+// appends of different slots never share a byte.  KV head g of page P is kept
+// in head slot (g + P) mod n_kv_heads of the page.
+template <int D>
+struct PageLayout {
+  static constexpr int NG = D / 32, NM = D / 16;
+  static constexpr int kHiHead = 64 * D, kHiV = 32 * D;
+  static constexpr int kLoKS = 8 * D, kLoVC = 8 * D + 32 * NG, kLoVS = 16 * D + 32 * NG;
+  static constexpr int kLoHead = 16 * D + 64 * NG;
+};
+
+}  // namespace
+}  // namespace pask

@@ -1,5 +1,5 @@
 // Internal declarations shared by the C ABI (pask_api.cpp) and the gfx950
-// kernels (pask_kernels.hip).  Not part of the public interface.
+// kernels (pask_append.hip, pask_attn.hip).  Not part of the public interface.
 #pragma once
 
 #include <stddef.h>
@@ -99,7 +99,8 @@ struct AttnArgs {
   int32_t attn_blocks;      // stream-K workers (waves) of the attention kernel, set at launch
 };
 
-// Launchers (pask_kernels.hip).  Return hipSuccess or the launch error.
+// Launchers (pask_append.hip: reset, budget init, append; pask_attn.hip:
+// attention, distortion).  Return hipSuccess or the launch error.
 hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s);
 hipError_t launch_append(const AppendArgs& a, hipStream_t s);        // chooses the windowed kernels when W > 0
 hipError_t launch_append_step(const AppendArgs& a, hipStream_t s);
