@@ -324,7 +324,8 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
 // Quantise 4 consecutive elements of a 32-element group held by 8 adjacent
 // lanes: s = fp16(absmax / 7) (correctly rounded division, saturated at 65504,
 // round-to-nearest-even conversion), q = clamp(rint(x / s), -7, 7).  Returns
-// the 4 codes as nibbles (element i in bits 4i..4i+3) and the scale bits.
+// the 4 codes as offset-binary nibbles q + 8 (element i in bits 4i..4i+3; the
+// pages hold codes in this form) and the scale bits.
 __device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& packed, uint32_t& sbits) {
   float f[4] = {bf16_lo(x01), bf16_hi(x01), bf16_lo(x23), bf16_hi(x23)};
   float am = fmaxf(fmaxf(fabsf(f[0]), fabsf(f[1])), fmaxf(fabsf(f[2]), fabsf(f[3])));
@@ -340,13 +341,13 @@ __device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& pac
   for (int i = 0; i < 4; ++i) {
     int q = 0;
     if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
-    p |= ((uint32_t)q & 0xFu) << (4 * i);
+    p |= (uint32_t)(q + 8) << (4 * i);
   }
   packed = p;
 }
 
 // The same rule for 8 consecutive elements of a group held by 4 adjacent
-// lanes (element i of x in bits 4i..4i+3 of `packed`).
+// lanes (element i of x in bits 4i..4i+3 of `packed`, offset binary).
 __device__ __forceinline__ void quant8(const uint4& x, uint32_t& packed, uint32_t& sbits) {
   const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
                       bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
@@ -364,9 +365,21 @@ __device__ __forceinline__ void quant8(const uint4& x, uint32_t& packed, uint32_
   for (int i = 0; i < 8; ++i) {
     int q = 0;
     if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
-    p |= ((uint32_t)q & 0xFu) << (4 * i);
+    p |= (uint32_t)(q + 8) << (4 * i);
   }
   packed = p;
+}
+
+// Nibbles 0..3 of p moved to the low nibbles of bytes 0..3.
+__device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t p) {
+  p &= 0xFFFFu;
+  p = (p | (p << 8)) & 0x00FF00FFu;
+  return (p | (p << 4)) & 0x0F0F0F0Fu;
+}
+// A K word in page order from 8 codes in element order: element e (< 4) in
+// the low nibble of byte e, element 4 + e in its high nibble.
+__device__ __forceinline__ uint32_t k_word(uint32_t packed) {
+  return nibbles_to_bytes(packed) | (nibbles_to_bytes(packed >> 16) << 4);
 }
 
 
@@ -410,8 +423,11 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
       quant4(raw.x, raw.y, packed, sbits);
       uint8_t* hb = pg + (size_t)((g + page) % cv.n_kv_heads) * PL::kLoHead;
       if (kv == 0) {
-        const int q = lig / 2, half = lig % 2;                        // j = 4*half + e
-        *reinterpret_cast<uint16_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4 + 2 * half) = (uint16_t)packed;
+        // Element j = 4*half + e of the lane pair's 8 goes to byte e, nibble `half`.
+        const int q = lig / 2, half = lig % 2;
+        const uint32_t mine = nibbles_to_bytes(packed) << (4 * half);
+        const uint32_t word = mine | __shfl_xor(mine, 1, 8);
+        if (half == 0) *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = word;
         if (lig == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
       } else {
         const uint32_t partner = __shfl_xor(packed, 4, 8);           // dims 16 higher
@@ -531,7 +547,7 @@ __global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
       if (!active) continue;
       uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
       if (kv == 0) {
-        *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = packed[jj];
+        *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = k_word(packed[jj]);
         if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
       } else {
         // byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i + dd (low nibble) and

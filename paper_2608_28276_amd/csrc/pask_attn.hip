@@ -46,13 +46,14 @@ namespace {
 //           slots 4q..4q+3; a LOW code c becomes the bf16 value 136 + c
 //           (exact), the accumulation starts at -136 * sum(q) of the 32-dim
 //           group, and the K scale multiplies the group's result;
-//   softmax online in base 2, per head, rescaling only when a max grows;
+//   softmax online in base 2, per head, rescaling only when a max grows
+//           (LOW pages two at a time under one max and rescale);
 //   values  HIGH: O += P V on v_mfma_f32_16x16x16_bf16 with P (split into
 //           bf16 high and low parts, so p keeps ~16 bits) as the A operand
 //           exactly as the score tile lies; LOW: the weights p x (V scale)
 //           rounded to fp16 times the codes as exact fp16 values on
 //           v_mfma_f32_16x16x16_f16, into the same accumulators.
-// The next page's operands (three pages ahead for LOW pages, whose scales
+// The next page's operands (four pages ahead for LOW pages, whose scales
 // take one register) are loaded while the current one is computed.
 // Each segment leaves (max, sum, unnormalised o) per head; attn_merge
 // combines the partials of a (b, g).
@@ -156,25 +157,26 @@ __device__ __forceinline__ void split_bf16x4(const float (&x)[4], uint2& hi, uin
   r[3] = x[3] - bf16_hi(hi.y);
   lo = make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
 }
-// K codes widened to bf16 with an offset: a nibble n (two's complement
-// code c) becomes the bf16 bit pattern 0x4300 | (n ^ 8), the exact value
-// 128 + (c + 8) = 136 + c (bf16 spacing is 1 on [128, 256)).  Two codes per
-// 32-bit word cost one byte permute and one xor; the offset is removed by
-// starting the q.k accumulation at -136 * (sum of q over the group).
+// K codes widened to bf16 with an offset: the pages hold a code c as the
+// offset-binary nibble c + 8, and the bf16 bit pattern 0x4300 | (c + 8) is
+// the exact value 128 + c + 8 = 136 + c (bf16 spacing is 1 on [128, 256)).
+// A K word holds elements 0..3 in the low nibbles of its bytes and 4..7 in
+// the high nibbles, so after one mask per nibble plane each pair of elements
+// is one byte permute that also inserts the 0x43 bytes; the offset is removed
+// by starting the q.k accumulation at -136 * (sum of q over the group).
 constexpr float kCodeOffset = 136.0f;
-constexpr uint32_t kCodeBias = 0x43084308u;
-// Codes 2e (low nibble) and 2e+1 (high nibble) of byte e of w, as a bf16 pair.
+// bf16 pair of the nibbles in bytes e and e + 1 of a nibble plane (one
+// nibble per byte); v_perm_b32 selector bytes 0-3 pick bytes of the second
+// source, 4-7 bytes of the first (the constant).
 template <int e>
-__device__ __forceinline__ uint32_t codes_pair_in_byte(uint32_t lo4, uint32_t hi4) {
-  // v_perm_b32: selector bytes 0-3 pick bytes of the second source (lo4),
-  // 4-7 bytes of the first (hi4), 0x0C gives zero.
-  return __builtin_amdgcn_perm(hi4, lo4, 0x0C000C00u | ((4u + e) << 16) | e) ^ kCodeBias;
+__device__ __forceinline__ uint32_t kcodes_pair(uint32_t plane) {
+  return __builtin_amdgcn_perm(0x43434343u, plane, 0x04000400u | ((e + 1) << 16) | e);
 }
-// V codes as exact fp16 values.  After n ^ 8 (done once per word) a nibble
-// holds c + 8; the fp16 bit pattern 0x6400 | (c + 8) is 1024 + c + 8 (fp16
-// spacing is 1 on [1024, 2048)), and one packed fp16 subtraction of 1032
-// leaves c exactly.  Nibbles in bytes j0 and j1 of n4 (one per byte) as an
-// fp16 pair; the 0x64 bytes come from the constant first source.
+// V codes as exact fp16 values: the fp16 bit pattern 0x6400 | (c + 8) is
+// 1024 + c + 8 (fp16 spacing is 1 on [1024, 2048)), and one packed fp16
+// subtraction of 1032 leaves c exactly.  Nibbles in bytes j0 and j1 of n4
+// (one per byte) as an fp16 pair; the 0x64 bytes come from the constant
+// first source.
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 template <int j0, int j1>
@@ -220,36 +222,36 @@ template <int J>
 __device__ __forceinline__ uint32_t row_word(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x150 + J, 0xF, 0xF, false);
 }
-// The row's KW K-scale words (lanes 0..KW-1) and KW V-scale words (lanes KW..2KW-1).
-template <int KW, int J = 0>
-__device__ __forceinline__ void row_words(uint32_t x, uint32_t (&k)[KW], uint32_t (&v)[KW]) {
+// Words OFF..OFF+KW-1 of the row (DPP row_newbcast from lanes OFF..).
+template <int KW, int OFF, int J = 0>
+__device__ __forceinline__ void row_words(uint32_t x, uint32_t (&w)[KW]) {
   if constexpr (J < KW) {
-    k[J] = row_word<J>(x);
-    v[J] = row_word<KW + J>(x);
-    row_words<KW, J + 1>(x, k, v);
+    w[J] = row_word<OFF + J>(x);
+    row_words<KW, OFF, J + 1>(x, w);
   }
 }
 
-// One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
+// Scores of one page in log2 units (-inf for slots past nvalid when kMasked):
+// lane (q, n) gets head n at slots 4q..4q+3.
 template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
-__device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2,
-                                            int q, int n) {
+__device__ __forceinline__ f32x4_t page_scores(const Raw& x, const AttnState<D, G>& st, int nvalid,
+                                               float scale_log2, int q) {
   using PL = PageLayout<D>;
   f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
-  [[maybe_unused]] uint32_t ks[2 * PL::NG], vs[2 * PL::NG];   // LOW: the row's K / V scale words
   if constexpr (kIsHi) {
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i)
       sc = mfma_k32(make_uint4(x.k[4 * i], x.k[4 * i + 1], x.k[4 * i + 2], x.k[4 * i + 3]),
                     make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), sc);
   } else {
-    row_words<2 * PL::NG>(x.sc, ks, vs);
+    uint32_t ks[2 * PL::NG];                        // the row's K scale words
+    row_words<2 * PL::NG, 0>(x.sc, ks);
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
-      const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;
+      const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;   // elements 0-3, 4-7
       const f32x4_t off = {st.kq[i], st.kq[i], st.kq[i], st.kq[i]};   // removes the code offset
-      const f32x4_t c = mfma_k32(make_uint4(codes_pair_in_byte<0>(lo4, hi4), codes_pair_in_byte<1>(lo4, hi4),
-                                            codes_pair_in_byte<2>(lo4, hi4), codes_pair_in_byte<3>(lo4, hi4)),
+      const f32x4_t c = mfma_k32(make_uint4(kcodes_pair<0>(lo4), kcodes_pair<2>(lo4), kcodes_pair<0>(hi4),
+                                            kcodes_pair<2>(hi4)),
                                  make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), off);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
@@ -258,13 +260,16 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
       }
     }
   }
-  float mx = -INFINITY;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    sc[r] = (!kMasked || 4 * q + r < nvalid) ? sc[r] * scale_log2 : -INFINITY;
-    mx = fmaxf(mx, sc[r]);
-  }
-  // Online softmax for head n: rescale only when some head's max grew.
+  for (int r = 0; r < 4; ++r) sc[r] = (!kMasked || 4 * q + r < nvalid) ? sc[r] * scale_log2 : -INFINITY;
+  return sc;
+}
+
+// Online softmax for head n given the lane's max of new scores: rescale the
+// outputs and the sum only when some head's max grew.
+template <int D, int G>
+__device__ __forceinline__ void softmax_step(AttnState<D, G>& st, float mx, int q) {
+  using PL = PageLayout<D>;
   const float mn = fmaxf(st.m, head_max(mx));
   if (__ballot(mn > st.m)) {
     const float alpha = __builtin_amdgcn_exp2f(st.m - mn);
@@ -277,6 +282,23 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
       for (int k = 0; k < PL::NM; ++k) st.acc[k][r] *= ar;
     }
   }
+}
+
+// fp16 pair (p0 x half H of s0, p1 x half H of s1), each product rounded
+// once to fp16 (the compiler makes a v_fma_mixlo_f16 / v_fma_mixhi_f16 pair
+// of the fma with a zero addend).
+template <int H>
+__device__ __forceinline__ uint32_t mix_pair(float p0, float p1, uint32_t s0, uint32_t s1) {
+  const float a = half_bits_to_float(s0 >> (16 * H)), b = half_bits_to_float(s1 >> (16 * H));
+  const f16x2_t r = {(_Float16)__builtin_fmaf(p0, a, 0.0f), (_Float16)__builtin_fmaf(p1, b, 0.0f)};
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// Weights p = exp2(score - max) of one page (summed into l) and O += P V.
+template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
+__device__ __forceinline__ void page_values(const Raw& x, AttnState<D, G>& st, const f32x4_t& sc, int nvalid,
+                                            int q) {
+  using PL = PageLayout<D>;
   // exp2 on v_exp_f32 directly: arguments are <= 0, and results that would
   // be fp32 subnormals (weights below 2^-126 of the running max) become 0.
   float pr[4];
@@ -302,27 +324,57 @@ __device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, i
   } else {
     // V: the weights p x (V scale of the slot's group), rounded once to
     // fp16 (11 significant bits), times the exact fp16 codes on the fp16
-    // MFMA.  Slots past the end get weight 0 (their scales are not written).
+    // MFMA.  Slots past the end get scale 0, so weight 0 (their scales are
+    // not written); their codes are finite by construction.
+    uint32_t vs[2 * PL::NG];                        // the row's V scale words: slot 4q + jj at jj*NG/2..
+    row_words<2 * PL::NG, 2 * PL::NG>(x.sc, vs);
+    if constexpr (kMasked) {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int e = 0; e < PL::NG / 2; ++e)
+          vs[jj * (PL::NG / 2) + e] = 4 * q + jj < nvalid ? vs[jj * (PL::NG / 2) + e] : 0u;
+    }
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
-      float w[4];
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int hidx = jj * PL::NG + i;
-        const float vsc = half_bits_to_float(vs[hidx / 2] >> (16 * (hidx % 2)));
-        w[jj] = (!kMasked || 4 * q + jj < nvalid) ? pr[jj] * vsc : 0.0f;
-      }
-      const f16x4_t wa = {(_Float16)w[0], (_Float16)w[1], (_Float16)w[2], (_Float16)w[3]};
-      const uint32_t vx = x.vc[i] ^ 0x88888888u;     // nibbles c + 8
+      // slot 4q + jj, group i: half i % 2 of word jj * NG/2 + i/2
+      const int w0 = i / 2;
+      const uint32_t wlo = (i & 1) ? mix_pair<1>(pr[0], pr[1], vs[w0], vs[PL::NG / 2 + w0])
+                                   : mix_pair<0>(pr[0], pr[1], vs[w0], vs[PL::NG / 2 + w0]);
+      const uint32_t whi = (i & 1) ? mix_pair<1>(pr[2], pr[3], vs[PL::NG + w0], vs[3 * PL::NG / 2 + w0])
+                                   : mix_pair<0>(pr[2], pr[3], vs[PL::NG + w0], vs[3 * PL::NG / 2 + w0]);
+      const f16x4_t wa = __builtin_bit_cast(f16x4_t, make_uint2(wlo, whi));
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         // byte jj of vc[i]: slot 4q + jj, dim 32i + n (low nibble) and 32i + 16 + n (high)
-        const uint32_t n4 = (hh ? vx >> 4 : vx) & 0x0F0F0F0Fu;
+        const uint32_t n4 = (hh ? x.vc[i] >> 4 : x.vc[i]) & 0x0F0F0F0Fu;
         const f16x4_t vb = __builtin_bit_cast(f16x4_t, make_uint2(vcodes_pair<0, 1>(n4), vcodes_pair<2, 3>(n4)));
         st.acc[2 * i + hh] = __builtin_amdgcn_mfma_f32_16x16x16f16(wa, vb, st.acc[2 * i + hh], 0, 0, 0);
       }
     }
   }
+}
+
+__device__ __forceinline__ float max4(const f32x4_t& v) { return fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])); }
+
+// One page of HIGH (kIsHi) or LOW slots; kMasked when fewer than 16 are valid.
+template <int D, int G, bool kIsHi, bool kMasked, typename Raw>
+__device__ __forceinline__ void attend_page(const Raw& x, AttnState<D, G>& st, int nvalid, float scale_log2, int q) {
+  const f32x4_t sc = page_scores<D, G, kIsHi, kMasked>(x, st, nvalid, scale_log2, q);
+  softmax_step(st, max4(sc), q);
+  page_values<D, G, kIsHi, kMasked>(x, st, sc, nvalid, q);
+}
+
+// Two pages under one softmax step (one max reduction and at most one
+// rescale for both): page a is full, page b holds nvb valid slots.
+template <int D, int G, bool kIsHi, bool kMaskedB, typename Raw>
+__device__ __forceinline__ void attend_pair(const Raw& xa, const Raw& xb, AttnState<D, G>& st, int nvb,
+                                            float scale_log2, int q) {
+  const f32x4_t sa = page_scores<D, G, kIsHi, false>(xa, st, kPage, scale_log2, q);
+  const f32x4_t sb = page_scores<D, G, kIsHi, kMaskedB>(xb, st, nvb, scale_log2, q);
+  softmax_step(st, fmaxf(max4(sa), max4(sb)), q);
+  page_values<D, G, kIsHi, false>(xa, st, sa, kPage, q);
+  page_values<D, G, kIsHi, kMaskedB>(xb, st, sb, nvb, q);
 }
 
 __device__ __forceinline__ int cdiv(int x, int y) { return (x + y - 1) / y; }
@@ -502,8 +554,8 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
   };
   auto attend = [&](const Raw& r, int p) {
     const int nvalid = min(kPage, n_slots - p * kPage);
-    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, q, n);
-    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, q, n);
+    if (nvalid == kPage) attend_page<D, G, kIsHi, false>(r, st, nvalid, scale_log2, q);
+    else attend_page<D, G, kIsHi, true>(r, st, nvalid, scale_log2, q);
   };
   for (int c = p0; c < p1; c += kIdChunk) {
     const int cn = min(kIdChunk, p1 - c);
@@ -524,18 +576,28 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
         if (i + 1 < cn) attend(x1, c + i + 1);
       }
     } else {
-      // A LOW page is 2 + 2 KiB of codes and 2 x 128 B of scales per head
-      // (D 128): four buffers in turn keep three pages in flight.
-      Raw x0 = ld(0), x1 = ld(1), x2 = ld(2);
-      for (int i = 0; i < cn; i += 4) {
-        const Raw x3 = ld(i + 3);
-        attend(x0, c + i);
-        x0 = ld(i + 4);
-        if (i + 1 < cn) attend(x1, c + i + 1);
-        x1 = ld(i + 5);
-        if (i + 2 < cn) attend(x2, c + i + 2);
-        x2 = ld(i + 6);
-        if (i + 3 < cn) attend(x3, c + i + 3);
+      // LOW pages (2 + 2 KiB of codes and 2 x 128 B of scales per head at
+      // D 128) in pairs under one softmax step; six buffers in turn keep
+      // four pages in flight while a pair is computed.
+      auto pair = [&](const Raw& xa, const Raw& xb, int i) {   // pages c+i and c+i+1 (when < cn)
+        if (i + 1 < cn) {                          // page c+i is then not the store's last: full
+          const int nvb = min(kPage, n_slots - (c + i + 1) * kPage);
+          if (nvb == kPage) attend_pair<D, G, false, false>(xa, xb, st, nvb, scale_log2, q);
+          else attend_pair<D, G, false, true>(xa, xb, st, nvb, scale_log2, q);
+        } else {
+          attend(xa, c + i);
+        }
+      };
+      Raw x0 = ld(0), x1 = ld(1), x2 = ld(2), x3 = ld(3);
+      for (int i = 0; i < cn; i += 6) {
+        const Raw x4 = ld(i + 4), x5 = ld(i + 5);
+        pair(x0, x1, i);
+        x0 = ld(i + 6);
+        x1 = ld(i + 7);
+        if (i + 2 < cn) pair(x2, x3, i + 2);
+        x2 = ld(i + 8);
+        x3 = ld(i + 9);
+        if (i + 4 < cn) pair(x4, x5, i + 4);
       }
     }
   }

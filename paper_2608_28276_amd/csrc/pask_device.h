@@ -59,8 +59,10 @@ __device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
 // covers 1 KiB contiguously.
 //   HIGH  K tile: element (t, d), d = 32i + 8q + j  at ((i*64 + q*16 + t)*8 + j)   (bf16)
 //         V tile: element (t, d), d = 16m + dd      at (((m/2)*64 + t/4*16 + dd)*2 + m%2)*4 + t%4
-//   LOW   K codes: nibble ((q*16 + t)*NG + i)*8 + j (element j of the 8 at byte j/2,
-//                  low nibble for even j); K scales [t][NG] fp16;
+//   LOW   codes are offset-binary nibbles c + 8 (c in [-7, 7]).
+//         K codes: word (q*16 + t)*NG + i holds d = 32i + 8q + j, j = 0..7: element
+//                  j < 4 in the low nibble of byte j, element 4 + j' in the high
+//                  nibble of byte j'; K scales [t][NG] fp16;
 //         V codes: byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i+dd (low
 //                  nibble) and 32i+16+dd (high nibble) of slot t; V scales [t][NG].
 // NG = D/32 scale groups, NM = D/16.  Every byte belongs to a single slot, so

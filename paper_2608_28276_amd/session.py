@@ -156,7 +156,7 @@ class PaskSession:
         table and decoded from the page layout (KV head g of page P sits in
         head slot (g + P) mod Hkv).  HIGH: (k bits, v bits) int64
         [n, Hkv, D].  LOW: (k codes int8 [n, Hkv, D], k scale bits [n, Hkv, D/32],
-        v codes, v scale bits)."""
+        v codes, v scale bits); the pages hold each code c as the nibble c + 8."""
         import numpy as np
         g = self.geom
         D, H = g.head_dim, g.n_kv_heads
@@ -171,20 +171,21 @@ class PaskSession:
             np.zeros((0, nbytes), np.uint8)
         t = np.arange(16)[:, None]
         d = np.arange(D)[None, :]
-        kidx = (((d % 32) // 8 * 16 + t) * NG + d // 32) * 8 + d % 8                      # [16, D], LOW K
+        # LOW K: word ((d%32)//8*16 + t)*NG + d//32, element j = d%8 in byte j%4, nibble j//4
+        kbyte = (((d % 32) // 8 * 16 + t) * NG + d // 32) * 4 + (d % 8) % 4                  # [16, D]
+        khalf = (d % 8) // 4
         if store == 0:
             return self._decode_hi(raw, pages, n)
         head = 16 * D + 64 * NG
         r = raw.reshape(-1, H, head)
         r = r[np.arange(r.shape[0])[:, None], (np.arange(H)[None, :] + pages[:, None]) % H]       # head slots
-        nib = lambda by, idx: ((by[..., idx // 2] >> (4 * (idx % 2))) & 0xF).astype(np.int8)
-        sext = lambda c: np.where(c >= 8, c - 16, c).astype(np.int8)
-        kc = sext(nib(r[:, :, :8 * D], kidx))                                            # [P, H, 16, D]
+        unbias = lambda c: (c.astype(np.int16) - 8).astype(np.int8)                          # offset binary
+        kc = unbias((r[:, :, :8 * D][..., kbyte] >> (4 * khalf)) & 0xF)                   # [P, H, 16, D]
         ks = r[:, :, 8 * D:8 * D + 32 * NG].copy().view(np.uint16).reshape(-1, H, 16, NG)
         vbyte = ((t // 4 * 16 + d % 16) * (NM // 2) + d // 32) * 4 + t % 4
         vhalf = (d % 32) // 16
         vb = r[:, :, 8 * D + 32 * NG:16 * D + 32 * NG]
-        vc = sext(((vb[..., vbyte] >> (4 * vhalf)) & 0xF).astype(np.int8))
+        vc = unbias((vb[..., vbyte] >> (4 * vhalf)) & 0xF)
         vs = r[:, :, 16 * D + 32 * NG:].copy().view(np.uint16).reshape(-1, H, 16, NG)
         fix = lambda a: a.transpose(0, 2, 1, 3).reshape(-1, H, a.shape[-1])[:n]
         return fix(kc), fix(ks).astype(np.int64), fix(vc), fix(vs).astype(np.int64)
