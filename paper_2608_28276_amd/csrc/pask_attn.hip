@@ -246,17 +246,21 @@ __device__ __forceinline__ f32x4_t page_scores(const Raw& x, const AttnState<D, 
   } else {
     uint32_t ks[2 * PL::NG];                        // the row's K scale words
     row_words<2 * PL::NG, 0>(x.sc, ks);
+    f32x4_t c[PL::NG];
 #pragma unroll
     for (int i = 0; i < PL::NG; ++i) {
       const uint32_t lo4 = x.kc[i] & 0x0F0F0F0Fu, hi4 = (x.kc[i] >> 4) & 0x0F0F0F0Fu;   // elements 0-3, 4-7
       const f32x4_t off = {st.kq[i], st.kq[i], st.kq[i], st.kq[i]};   // removes the code offset
-      const f32x4_t c = mfma_k32(make_uint4(kcodes_pair<0>(lo4), kcodes_pair<2>(lo4), kcodes_pair<0>(hi4),
-                                            kcodes_pair<2>(hi4)),
-                                 make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), off);
+      c[i] = mfma_k32(make_uint4(kcodes_pair<0>(lo4), kcodes_pair<2>(lo4), kcodes_pair<0>(hi4),
+                                 kcodes_pair<2>(hi4)),
+                      make_uint4(st.qa[4 * i], st.qa[4 * i + 1], st.qa[4 * i + 2], st.qa[4 * i + 3]), off);
+    }
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {                 // K scale of slot 4q + r, group i
         const int hidx = r * PL::NG + i;
-        sc[r] = fmaf(half_bits_to_float(ks[hidx / 2] >> (16 * (hidx % 2))), c[r], sc[r]);
+        sc[r] = fmaf(half_bits_to_float(ks[hidx / 2] >> (16 * (hidx % 2))), c[i][r], sc[r]);
       }
     }
   }
