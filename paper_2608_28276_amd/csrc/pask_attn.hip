@@ -544,10 +544,17 @@ constexpr int kIdChunk = 128;
 
 // kWindow: the pages are a recent window, consecutive pool pages from id0 on
 // (bt unused).
-template <int D, int G, bool kIsHi, bool kWindow = false>
+// `prologue` runs once, after the first block-table loads are issued and
+// before the first page is loaded, so work that waits for earlier loads (the
+// LOW code offsets wait for q) overlaps the block-table latency.
+struct NoPrologue {
+  __device__ __forceinline__ void operator()() const {}
+};
+template <int D, int G, bool kIsHi, bool kWindow = false, typename Prologue = NoPrologue>
 __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes, int head_bytes, int n_heads,
                                           const int32_t* bt, int id0, int p0, int p1, int n_slots, int g,
-                                          AttnState<D, G>& st, float scale_log2, int q, int n) {
+                                          AttnState<D, G>& st, float scale_log2, int q, int n,
+                                          Prologue prologue = Prologue()) {
   using Raw = typename std::conditional<kIsHi, HiRaw<D>, LoRaw<D>>::type;
   const int lane = threadIdx.x & 63;
   auto load = [&](int page, bool real) -> Raw {
@@ -565,6 +572,7 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
     const int cn = min(kIdChunk, p1 - c);
     const int ids0 = kWindow ? id0 + c + min(lane, cn - 1) : bt[c + min(lane, cn - 1)];
     const int ids1 = kWindow ? id0 + c + min(64 + lane, cn - 1) : bt[c + min(64 + lane, cn - 1)];
+    if (c == p0) prologue();
     auto id = [&](int i) -> int {   // i: wave-uniform, < cn
       return i < 64 ? __builtin_amdgcn_readlane(ids0, i) : __builtin_amdgcn_readlane(ids1, i - 64);
     };
@@ -628,13 +636,17 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   for (int k = 0; k < PL::NM; ++k) st.acc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   st.m = -INFINITY;
   st.l = 0.0f;
+  // -offset x sum of q over group i (head n), for LOW pages only: computed in
+  // the LOW run's prologue, after its block-table loads are issued.
+  auto code_offsets = [&]() {
 #pragma unroll
-  for (int i = 0; i < PL::NG; ++i) {            // -offset x sum of q over group i (head n)
-    float part = 0.0f;
+    for (int i = 0; i < PL::NG; ++i) {
+      float part = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) part += bf16_lo(st.qa[4 * i + e]) + bf16_hi(st.qa[4 * i + e]);
-    st.kq[i] = -kCodeOffset * head_sum(part);
-  }
+      for (int e = 0; e < 4; ++e) part += bf16_lo(st.qa[4 * i + e]) + bf16_hi(st.qa[4 * i + e]);
+      st.kq[i] = -kCodeOffset * head_sum(part);
+    }
+  };
   if (j0 < sp.np_hi)
     run_pages<D, G, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, block_table_of(cv, b, a.layer, kHi), 0, j0,
                           min(j1, sp.np_hi), sp.n_hi, g, st, a.scale_log2, q, n);
@@ -644,7 +656,8 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
                                 min(j1, sp.np_w) - sp.np_hi, sp.n_win, g, st, a.scale_log2, q, n);
   if (j1 > sp.np_w)
     run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo), 0,
-                           max(j0, sp.np_w) - sp.np_w, j1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n);
+                           max(j0, sp.np_w) - sp.np_w, j1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n,
+                           code_offsets);
   // Partial of piece `slot` of (b, g): rows of G4 = max(G, 4) query heads,
   // stored as float4s of 4 heads at one dim (index ((q*NM + k)*16 + n)*4 + r
   // for head 4q + r, dim 16k + n): each store instruction writes 256
