@@ -165,13 +165,15 @@ typedef struct pask_cache_layout {
                                 (i*64 + q*16 + t)*8 + j; V element (t, d),
                                 d = 16m + e, at (((m/2)*64 + t/4*16 + e)*2 + m%2)*4
                                 + t%4 (the bf16 MFMA operand order)              */
-  uint64_t lo_page_bytes;    /* head slot h at h * (16*D + 64*D/32): K codes (8*D
-                                bytes: element (t, d), d = 32i + 8q + j, is nibble
-                                ((q*16 + t)*D/32 + i)*8 + j, low nibble first),
-                                K scales [16][D/32] fp16, V codes (8*D bytes:
-                                byte ((t/4*16 + e)*D/32 + i)*4 + t%4 holds dims
-                                32i + e (low nibble) and 32i + 16 + e (high) of
-                                slot t, e < 16), V scales [16][D/32] fp16       */
+  uint64_t lo_page_bytes;    /* head slot h at h * (16*D + 64*D/32); every code c
+                                is stored as the nibble c + 8.  K codes (8*D
+                                bytes: element (t, d), d = 32i + 8q + j, is in
+                                byte ((q*16 + t)*D/32 + i)*4 + j%4, low nibble for
+                                j < 4, high nibble for j >= 4), K scales
+                                [16][D/32] fp16, V codes (8*D bytes: byte
+                                ((t/4*16 + e)*D/32 + i)*4 + t%4 holds dims 32i + e
+                                (low nibble) and 32i + 16 + e (high) of slot t,
+                                e < 16), V scales [16][D/32] fp16               */
   int32_t max_pages;         /* ceil(max_tokens_per_seq / 16)                      */
   int32_t counter_stride;    /* 8                                                  */
   int32_t ring_pages;        /* max_batch * n_layers * ceil(W / 16)                */
@@ -282,7 +284,10 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
 
 /* Workspace bytes pask_decode_attn needs for `batch` sequences when no
  * sequence holds more than max_ctx_hint persisted entries (a larger count is
- * still correct, only less parallel). */
+ * still correct, only less parallel): batch * n_kv_heads * S partial blocks
+ * of max(G, 4) * (head_dim + 2) fp32, S = ceil(hint / 128) + 2, or for
+ * batch * n_kv_heads <= 64 the larger of that and min(ceil(hint / 16) + 2,
+ * 4096 / (batch * n_kv_heads)). */
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint);
 
 /* One decode step of one layer: optionally persist one new token per sequence

@@ -173,10 +173,14 @@ T rd(const uint8_t* p) {
 
 // Partials one (sequence, KV head) may be cut into: the attention kernel picks
 // its pages-per-block so that this bound holds for any counts; the hint only
-// sizes the workspace.
-int splits_for(int32_t max_ctx_hint) {
-  const int units = (max_ctx_hint + pask::kUnitTokens - 1) / pask::kUnitTokens;
-  return units + 2;
+// sizes the workspace.  Pieces of kUnitTokens tokens; for calls with few
+// segments, pieces down to one page while the call holds at most
+// kSmallPartials partials.
+int splits_for(int32_t max_ctx_hint, int64_t segments) {
+  const int coarse = (max_ctx_hint + pask::kUnitTokens - 1) / pask::kUnitTokens + 2;
+  if (segments > pask::kSmallSegments) return coarse;
+  const int fine = (max_ctx_hint + pask::kPage - 1) / pask::kPage + 2;
+  return std::max(coarse, std::min(fine, (int)(pask::kSmallPartials / std::max<int64_t>(segments, 1))));
 }
 
 
@@ -403,7 +407,7 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint) {
   if (!valid_geom(geom) || batch < 1) return 0;
   if (max_ctx_hint < 1) max_ctx_hint = geom->max_tokens_per_seq;
-  return (size_t)ws_layout(geom, batch, splits_for(max_ctx_hint)).total;
+  return (size_t)ws_layout(geom, batch, splits_for(max_ctx_hint, (int64_t)batch * geom->n_kv_heads)).total;
 }
 
 int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
@@ -425,7 +429,7 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
   if (tags_new_dev && states_new_dev && policy->n_states == 0) return PASK_E_POLICY;
   if (!isfinite(softmax_scale)) return PASK_E_ARG;
   if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
-  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq));
+  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq), (int64_t)batch * g.n_kv_heads);
   const WsLayout w = ws_layout(&g, batch, splits);
   if (!ws_dev || !aligned(ws_dev, 256)) return PASK_E_ARG;
   if (ws_bytes < w.total) return PASK_E_CAPACITY;
@@ -477,7 +481,7 @@ int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer,
   if (!q_dev || !aligned(q_dev, 16) || !dist_dev || !aligned(dist_dev, 4)) return PASK_E_ARG;
   if (!isfinite(softmax_scale)) return PASK_E_ARG;
   if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
-  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq));   // any value is safe (U bounds the pieces)
+  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq), (int64_t)batch * g.n_kv_heads);
   const WsLayout w = ws_layout(&g, batch, splits);
   if (!ws_dev || !aligned(ws_dev, 256)) return PASK_E_ARG;
   if (ws_bytes < 2 * w.total) return PASK_E_CAPACITY;

@@ -12,6 +12,9 @@
 //                registers.
 //   attn_merge   per (sequence, KV head): combine the partials of its pieces
 //                (max, sum, values) into bf16 outputs; zero for empty histories.
+//                Calls with few (sequence, KV head) segments cut them into
+//                pieces of 4 pages and spread each segment's merge over
+//                several single-wave blocks (attn_merge_sliced).
 //   distortion   the attention-output distortion of Eq. 4: the partials of a
 //                reference and an intervened cache merged in fp32, the squared
 //                distance of the outputs maximised over query heads.
@@ -491,6 +494,10 @@ struct StreamPlan {
   int U;             // units per block
 };
 constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
+// Calls with few segments: workers of 4 pages (8 and 2 measured slower at
+// one Qwen3-4B-shaped sequence of 2.5k entries: fewer workers, or more
+// pieces to merge).
+constexpr int kSmallMinPages = 4;
 
 __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
   int total = 0, mx = 0;
@@ -502,7 +509,7 @@ __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const First
   StreamPlan pl;
   pl.total = (long long)total * a.cv.n_kv_heads;
   const long long even = (pl.total + n_blocks - 1) / n_blocks;
-  pl.U = max(kWeightHi * kMinPagesPerBlock, (int)min(even, (long long)INT_MAX));
+  pl.U = max(kWeightHi * a.min_pages, (int)min(even, (long long)INT_MAX));
   pl.U = max(pl.U, cdiv(mx, a.splits - 1));
   return pl;
 }
@@ -735,12 +742,13 @@ struct PieceMerge {
       L[r] = 0.0f;
     }
   }
-  // Loads pieces p0.. of the (b, g) whose first partial block is blk0; past
-  // `last` the last piece is repeated (fold skips it).
-  __device__ __forceinline__ void load(const AttnArgs& a, size_t blk0, int t, int q, int p0, int last) {
+  // Loads pieces p0, p0 + stride, ... of the (b, g) whose first partial
+  // block is blk0; past `last` the last piece is repeated (fold skips it).
+  __device__ __forceinline__ void load(const AttnArgs& a, size_t blk0, int t, int q, int p0, int last,
+                                       int stride = 1) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const size_t pb = blk0 + min(p0 + u, last);
+      const size_t pb = blk0 + min(p0 + stride * u, last);
       const float* ml = a.ws_ml + pb * G4 * 2 + 8 * q;
       v[u] = *reinterpret_cast<const float4*>(a.ws_o + pb * (G4 * D) + t * 4);
       mla[u] = *reinterpret_cast<const float4*>(ml);       // (m, l) of heads 4q, 4q+1
@@ -751,17 +759,18 @@ struct PieceMerge {
   __device__ __forceinline__ void fold(int n) {
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      if (u >= n) break;
-      const float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-      const float mlv[8] = {mla[u].x, mla[u].y, mla[u].z, mla[u].w, mlb[u].x, mlb[u].y, mlb[u].z, mlb[u].w};
+      if (u < n) {
+        const float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+        const float mlv[8] = {mla[u].x, mla[u].y, mla[u].z, mla[u].w, mlb[u].x, mlb[u].y, mlb[u].z, mlb[u].w};
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float mp = mlv[2 * r], lp = mlv[2 * r + 1];
-        const float mn = fmaxf(M[r], mp);
-        const float alpha = exp2f(M[r] - mn), wgt = exp2f(mp - mn);
-        L[r] = L[r] * alpha + wgt * lp;
-        acc[r] = acc[r] * alpha + wgt * vv[r];
-        M[r] = mn;
+        for (int r = 0; r < 4; ++r) {
+          const float mp = mlv[2 * r], lp = mlv[2 * r + 1];
+          const float mn = fmaxf(M[r], mp);
+          const float alpha = exp2f(M[r] - mn), wgt = exp2f(mp - mn);
+          L[r] = L[r] * alpha + wgt * lp;
+          acc[r] = acc[r] * alpha + wgt * vv[r];
+          M[r] = mn;
+        }
       }
     }
   }
@@ -828,6 +837,69 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   const uint4* src = reinterpret_cast<const uint4*>(&s_out[0][0]);
   uint4* dst = reinterpret_cast<uint4*>(a.out + row0 * D);
   for (int i = t; i < G * D / 8; i += merge_threads<D, G>()) dst[i] = src[i];
+}
+
+// The same merge for calls with few segments, whose segments hold many
+// pieces: the merge of one segment is spread over NM * G4 / 4 single-wave
+// blocks (one per 16 float4 positions of the partial rows: query heads
+// 4q..4q+3 at dims 16k..16k+15), so the pieces' bytes are read by many CUs.
+// Lane 16j + n merges position n of the block over the pieces p = j (mod 4);
+// the four lane groups are then combined across lanes.
+constexpr int kSlicedBatch = 12;                 // pieces per lane group and round
+template <int D, int G>
+__global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
+  constexpr int NM = D / 16, X = merge_threads<D, G>() / 16;
+  const int lane = threadIdx.x, j = lane >> 4, n = lane & 15;
+  const int H = a.cv.n_kv_heads;
+  const int seg = uni(blockIdx.x / X), x = uni(blockIdx.x % X);
+  const int b = seg / H, g = seg % H;
+  const int q = x / NM, k = x % NM, t = 16 * x + n;
+  const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;
+  const size_t blk0 = (size_t)seg * a.splits;
+  PieceMerge<D, G, kSlicedBatch> pm;
+  constexpr int kB = kSlicedBatch;
+  pm.load(a, blk0, t, q, j, a.splits - 1, 4);    // before the piece count is known
+  const FirstCounts f = first_counts(a);
+  const SeqPages sp = seq_pages(a, f, b);
+  if (sp.np == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (j == 0 && 4 * q + r < G) a.out[(row0 + 4 * q + r) * D + 16 * k + n] = 0;
+    if (a.lse && j == 0 && k == 0 && n < 4 && 4 * q + n < G) a.lse[row0 + 4 * q + n] = -INFINITY;
+    return;
+  }
+  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
+  pm.init();
+  for (int p0 = 0; p0 < nparts; p0 += 4 * kB) {
+    const int first = p0 + j;
+    if (p0 > 0) pm.load(a, blk0, t, q, first, nparts - 1, 4);
+    pm.fold(first < nparts ? (nparts - 1 - first) / 4 + 1 : 0);
+  }
+#pragma unroll
+  for (int off = 16; off <= 32; off *= 2) {      // lanes n, n+16, n+32, n+48
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float m2 = __shfl_xor(pm.M[r], off), l2 = __shfl_xor(pm.L[r], off), v2 = __shfl_xor(pm.acc[r], off);
+      if (m2 != -INFINITY) {
+        const float mn = fmaxf(pm.M[r], m2);
+        const float alpha = exp2f(pm.M[r] - mn), wgt = exp2f(m2 - mn);
+        pm.L[r] = pm.L[r] * alpha + wgt * l2;
+        pm.acc[r] = pm.acc[r] * alpha + wgt * v2;
+        pm.M[r] = mn;
+      }
+    }
+  }
+  if (j == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * q + r;
+      if (h < G) {
+        a.out[(row0 + h) * D + 16 * k + n] = f32_to_bf16_rne_dev(pm.acc[r] / pm.L[r]);
+        if (a.lse && k == 0 && n == 0) a.lse[row0 + h] = (pm.M[r] + log2f(pm.L[r])) * 0.69314718055994530942f;
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -945,12 +1017,18 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
   const int D = args.cv.head_dim;
   AttnArgs a = args;
   const dim3 block(64);
+  const int segs = a.batch * a.cv.n_kv_heads;
+  const bool small = segs <= kSmallSegments;
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
     a.attn_blocks = attn_grid<DD, GG>();                                         \
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
+    a.min_pages = small ? kSmallMinPages : kMinPagesPerBlock;                    \
     attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
-    attn_merge_kernel<DD, GG><<<dim3(a.batch * a.cv.n_kv_heads), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
+    if (small)                                                                   \
+      attn_merge_sliced_kernel<DD, GG><<<dim3(segs * (merge_threads<DD, GG>() / 16)), dim3(64), 0, s>>>(a); \
+    else                                                                         \
+      attn_merge_kernel<DD, GG><<<dim3(segs), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
@@ -967,6 +1045,7 @@ hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args,
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
     ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG>();                     \
+    ref.min_pages = itv.min_pages = kMinPagesPerBlock;                           \
     if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
     attn_kernel<DD, GG><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);            \
     attn_kernel<DD, GG><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);            \

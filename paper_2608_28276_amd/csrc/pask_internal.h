@@ -97,7 +97,15 @@ struct AttnArgs {
   float scale_log2;         // softmax_scale * log2(e)
   int32_t layer, batch, n_q_heads, splits;   // splits: partials per (b, g) the workspace holds
   int32_t attn_blocks;      // stream-K workers (waves) of the attention kernel, set at launch
+  int32_t min_pages;        // fewest pages a worker takes (HIGH-page weight), set at launch
 };
+
+// Calls with at most kSmallSegments (sequence, KV head) segments cut them
+// finer (pieces down to kSmallMinPages pages, the workspace holding up to
+// kSmallPartials partials in all) and merge each segment's pieces with
+// several thread groups at once.
+constexpr int kSmallSegments = 64;
+constexpr int kSmallPartials = 4096;
 
 // Launchers (pask_append.hip: reset, budget init, append; pask_attn.hip:
 // attention, distortion).  Return hipSuccess or the launch error.

@@ -215,16 +215,25 @@ def test_unsupported_geometry(bad):
     assert e.value.status == pask.PASK_E_SHAPE
 
 
-def test_workspace_bytes():
-    g = geom()
-    # splits = ceil(hint / 128) + 2; per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
+def _ws_want(g, batch, hint):
+    # splits = ceil(hint / 128) + 2; with at most 64 (sequence, KV head) segments, pieces down to
+    # one page while the call holds at most 4096 partials: max(that, min(ceil(hint / 16) + 2,
+    # 4096 // segments)).  Per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
     # o: blocks*G4*D*4, ml: blocks*G4*2*4 (each 256-aligned)
-    ws = pask.pask_workspace_bytes(g, 4, 512)
+    segs = batch * g.n_kv_heads
+    splits = -(-hint // 128) + 2
+    if segs <= 64:
+        splits = max(splits, min(-(-hint // 16) + 2, 4096 // segs))
     G4 = max(4, g.n_q_heads // g.n_kv_heads)
-    blocks = 4 * g.n_kv_heads * 6
+    blocks = segs * splits
     want = ((blocks * G4 * g.head_dim * 4 + 255) // 256) * 256
-    want = ((want + blocks * G4 * 8 + 255) // 256) * 256
-    assert ws == want
+    return ((want + blocks * G4 * 8 + 255) // 256) * 256
+
+
+@pytest.mark.parametrize("batch,hint", [(4, 512), (8, 512), (9, 512), (1, 100000), (32, 100000), (64, 9000)])
+def test_workspace_bytes(batch, hint):
+    g = geom(max_batch=64)
+    assert pask.pask_workspace_bytes(g, batch, hint) == _ws_want(g, batch, hint)
 
 
 def test_distortion_validation_before_any_hip_call():

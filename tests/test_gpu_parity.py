@@ -109,6 +109,24 @@ def test_geometries_mixed_policy(Hq, Hkv, D):
     sc.check_state()
 
 
+@pytest.mark.parametrize("B", [8, 9])
+def test_segment_count_boundary(B):
+    """8 sequences x 8 KV heads = 64 segments take the few-segment path
+    (pieces of 4 pages, sliced merge), 9 x 8 = 72 the general one; prompts of
+    18-40 pages so every segment is cut into several pieces."""
+    say(f"case: segment boundary B={B}")
+    pol = make_policy(6, 2, 2, 0.33, seed=500 + B)
+    P = [280 + 37 * b for b in range(B)]
+    T = 6
+    tags = np.stack([walk_function_calls(T, 70 + b) for b in range(B)])
+    sc = Scenario(pol, B=B, L=2, Hq=32, Hkv=8, D=128, prompt_lens=P, gen_tags=tags, seed=300 + B)
+    sc.fill_prompt()
+    sc.append_steps(0, 4)
+    sc.decode_step(4)
+    sc.decode_step(5)
+    sc.check_state()
+
+
 def test_all_drop_and_empty_history():
     """All-DROP table: a sequence with no prompt has an empty history
     (out = 0, lse = -inf); one with a prompt sees only the prompt."""
