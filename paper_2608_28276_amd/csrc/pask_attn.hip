@@ -37,11 +37,14 @@ namespace {
 // Stream-K: the work is the list of (sequence b, KV head g, page) triples,
 // HIGH pages of a (b, g) before its LOW pages, each page weighing 32 units
 // (PASK_WEIGHT_LO for a LOW page).  The grid holds one single-wave worker
-// per resident wave slot of the chip, and worker w takes the w-th of equal
-// contiguous unit ranges, so every worker starts at launch and all finish
-// together.  A range crossing a (b, g) boundary closes that segment with a
-// partial block; the range length is at least what keeps every (b, g) within
-// as many pieces as the workspace holds partials.
+// per resident wave slot of the chip, and worker w takes the w-th of
+// contiguous unit ranges, so every worker starts at launch.  Workers on the
+// odd-numbered XCDs (blockIdx odd) take 14/16 of an even one's range: their
+// waves stream pages about 10% slower, so with equal ranges the even XCDs
+// idle through the last ~15 us of the call.  A range crossing a (b, g)
+// boundary closes that segment with a partial block; every range is at least
+// what keeps every (b, g) within as many pieces as the workspace holds
+// partials.
 //
 // Per page (16 slots x all G query heads of KV head g), one wave:
 //   scores  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: rows = slots, columns
@@ -484,20 +487,41 @@ __device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
 // (sequence b, KV head g) in that nesting order, each the pages of (b, g) laid
 // out in units; segment (b, g) starts at unit excl(b) * Hkv + g * len(b), where
 // excl(b) sums len over the sequences before b.  Block w takes the pages that
-// start in units [w*U, (w+1)*U): contiguous ranges of equal weight.  U is at
-// least one HIGH page and kWeightLo <= kWeightHi, so every block between the
-// first and the last one of a segment holds a page of it; U is also large
-// enough that no segment is cut into more than `splits` pieces (the workspace
-// bound).
+// start in its contiguous unit range [start_of(w), start_of(w) + size_of(w)),
+// size_of(w) = weight(w) x step.  Every range is at least one HIGH page and
+// kWeightLo <= kWeightHi, so every block between the first and the last one
+// of a segment holds a page of it; every range is also large enough that no
+// segment is cut into more than `splits` pieces (the workspace bound).
 struct StreamPlan {
   long long total;   // units
-  int U;             // units per block
+  int step;          // units per sixteenth of weight
+  // Block w runs on XCD w % 8.  A block on an odd XCD weighs PASK_ODD_WEIGHT
+  // sixteenths, one on an even XCD 16: eight consecutive blocks weigh kOctet.
+  static constexpr int kOctet = 4 * 16 + 4 * PASK_ODD_WEIGHT;
+  __device__ __forceinline__ static int weight(int w) { return (w & 1) ? PASK_ODD_WEIGHT : 16; }
+  __device__ __forceinline__ static int weight_before(int w) {   // of blocks 0..w-1
+    return (w >> 3) * kOctet + ((w & 7) + 1) / 2 * 16 + ((w & 7) / 2) * PASK_ODD_WEIGHT;
+  }
+  __device__ __forceinline__ long long start_of(int w) const { return (long long)weight_before(w) * step; }
+  __device__ __forceinline__ int size_of(int w) const { return weight(w) * step; }
+  // Block whose range holds unit u.
+  __device__ __forceinline__ long long block_of(long long u) const {
+    const long long wu = u / step;                 // sixteenths of weight before u
+    const long long o = wu / kOctet;
+    int r = (int)(wu - o * kOctet), w = 0;
+    while (r >= weight(w)) {
+      r -= weight(w);
+      ++w;
+    }
+    return o * 8 + w;
+  }
 };
 constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
 // Calls with few segments: workers of 4 pages (8 and 2 measured slower at
 // one Qwen3-4B-shaped sequence of 2.5k entries: fewer workers, or more
 // pieces to merge).
 constexpr int kSmallMinPages = 4;
+static_assert(PASK_ODD_WEIGHT >= 1 && PASK_ODD_WEIGHT <= 16, "odd-XCD block weight out of range");
 
 __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
   int total = 0, mx = 0;
@@ -508,9 +532,11 @@ __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const First
   }
   StreamPlan pl;
   pl.total = (long long)total * a.cv.n_kv_heads;
-  const long long even = (pl.total + n_blocks - 1) / n_blocks;
-  pl.U = max(kWeightHi * a.min_pages, (int)min(even, (long long)INT_MAX));
-  pl.U = max(pl.U, cdiv(mx, a.splits - 1));
+  const long long weights = StreamPlan::weight_before(n_blocks);
+  long long step = (pl.total + weights - 1) / weights;
+  const long long lo = max(kWeightHi * a.min_pages, cdiv(mx, a.splits - 1));
+  step = max(step, (lo + PASK_ODD_WEIGHT - 1) / PASK_ODD_WEIGHT);   // every range size >= lo
+  pl.step = (int)min(step, (long long)(INT_MAX / 16));
   return pl;
 }
 
@@ -626,7 +652,7 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
 // piece's partial of (b, g), combined with the others by attn_merge.
 template <int D, int G>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
-                                               long long seg0, int U, int q, int n) {
+                                               long long seg0, const StreamPlan& plan, int q, int n) {
   using PL = PageLayout<D>;
   const CacheView& cv = a.cv;
   const int H = cv.n_kv_heads;
@@ -672,7 +698,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   // Rows past G hold finite values that are never read into an output.
   constexpr int G4 = G > 4 ? G : 4;
   const float l_n = head_sum(st.l);              // head n, over all slots
-  const int slot = (int)(w - seg0 / U);          // < a.splits by the choice of U
+  const int slot = (int)(w - plan.block_of(seg0));   // < a.splits by the choice of U
   const size_t blk = ((size_t)b * H + g) * a.splits + slot;
   if (4 * q < G4) {
     float* o = a.ws_o + blk * (G4 * D);
@@ -693,9 +719,9 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
   const int H = a.cv.n_kv_heads;
   const FirstCounts f = first_counts(a);
   const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
-  const long long start = (long long)w * plan.U;
+  const long long start = plan.start_of(w);
   if (start >= plan.total) return;
-  const long long end = min(plan.total, start + plan.U);
+  const long long end = min(plan.total, start + plan.size_of(w));
   int b, excl;
   locate(a, f, start, b, excl);
   if (b < 0) return;
@@ -707,7 +733,7 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
     const long long seg0 = (long long)excl * H + (long long)g * sp.len;
     if (seg0 >= end) return;
     const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
-    if (j0 < j1) attend_segment<D, G>(a, w, b, g, j0, j1, sp, seg0, plan.U, q, n);
+    if (j0 < j1) attend_segment<D, G>(a, w, b, g, j0, j1, sp, seg0, plan, q, n);
     if (j1 < sp.np) return;
     j0 = 0;
     if (++g == H) {                              // next sequence that holds any page
@@ -780,7 +806,7 @@ struct PieceMerge {
 // excl: units of the sequences before b; sp.np > 0).
 __device__ __forceinline__ int n_pieces(const StreamPlan& plan, const SeqPages& sp, int excl, int g, int H) {
   const long long seg0 = (long long)excl * H + (long long)g * sp.len;
-  return (int)((seg0 + page_start(sp, sp.np - 1)) / plan.U - seg0 / plan.U) + 1;
+  return (int)(plan.block_of(seg0 + page_start(sp, sp.np - 1)) - plan.block_of(seg0)) + 1;
 }
 // Units of the sequences before b (wave-uniform).
 __device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts& f, int b) {

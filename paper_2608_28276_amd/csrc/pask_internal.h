@@ -24,6 +24,13 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #ifndef PASK_WEIGHT_LO
 #define PASK_WEIGHT_LO 32
 #endif
+// Range an attention worker on an odd-numbered XCD takes, in sixteenths of
+// an even-XCD worker's: measured per-XCD finish times show the odd XCDs
+// streaming pages about 10% slower (two boxes, every call); 14 measured
+// fastest of 13..16 on the Qwen3-4B and Qwen3-32B-shaped workloads.
+#ifndef PASK_ODD_WEIGHT
+#define PASK_ODD_WEIGHT 14
+#endif
 #ifndef PASK_UNIT_TOKENS
 #define PASK_UNIT_TOKENS 128
 #endif
