@@ -539,12 +539,14 @@ def main():
     from workload import CONFIGS
     cfg0 = CONFIGS[args.config]
     beta = args.budget if args.budget is not None else (cfg0.budgets[0] if len(cfg0.budgets) == 1 else 0.33)
+    t_default = min(512, cfg0.gen_tokens // 2)
     if args.t_start is None:
-        args.t_start = min(512, cfg0.gen_tokens // 2)
+        args.t_start = t_default
     cfg, P, tags, pol, ptags = build_workload(args.config, beta)
     pol.recent_window = args.window
     workload = (cfg.name + (f"_beta{beta:g}" if len(cfg.budgets) > 1 or beta not in cfg.budgets else "") +
-                (f"+window{args.window}" if args.window else "") + ("+controller" if args.controller else ""))
+                (f"+window{args.window}" if args.window else "") + ("+controller" if args.controller else "") +
+                (f"+t{args.t_start}" if args.t_start != t_default else ""))
     states = None
     if args.controller:
         states, pol = controller_inputs(cfg, tags, pol)

@@ -70,3 +70,13 @@ def test_pool_plan_covers_the_stores(idx, beta):
     assert need_hi <= hi and need_lo <= lo
     assert hi - need_hi <= cfg.layers_resident * cfg.batch       # the plan's only slack: a spare page per store
     assert lo - need_lo <= cfg.layers_resident * cfg.batch
+
+
+def test_traffic_record_only_for_its_workload_and_sources(monkeypatch):
+    """The committed counter summary is used only for the workload it was
+    taken on (a run from another start position names itself apart) and
+    only while the attention sources are the ones it was taken with."""
+    name = "qwen3_4b_b64_p1k-8k_g1024"
+    assert bench.traffic_record(name + "+t0") is None
+    monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 16)
+    assert bench.traffic_record(name) is None
