@@ -482,6 +482,13 @@ __device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
   return s.np_w + min(s.np - s.np_w, cdiv(u - kWeightHi * s.np_w, kWeightLo));
 }
 
+// a / b for 0 <= a, 0 < b (wave-uniform): 32-bit division when both fit, as
+// they do for any call below 2^31 units; the 64-bit expansion otherwise.
+__device__ __forceinline__ long long udiv(long long a, long long b) {
+  if ((((unsigned long long)a | (unsigned long long)b) >> 32) == 0) return (long long)((uint32_t)a / (uint32_t)b);
+  return a / b;
+}
+
 // Stream-K decomposition of one attention call, computed identically by every
 // block of the attention and merge kernels.  The work list is the segments
 // (sequence b, KV head g) in that nesting order, each the pages of (b, g) laid
@@ -495,20 +502,25 @@ __device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
 struct StreamPlan {
   long long total;   // units
   int step;          // units per sixteenth of weight
-  // Block w runs on XCD w % 8.  A block on an odd XCD weighs PASK_ODD_WEIGHT
-  // sixteenths, one on an even XCD 16: eight consecutive blocks weigh kOctet.
-  static constexpr int kOctet = 4 * 16 + 4 * PASK_ODD_WEIGHT;
-  __device__ __forceinline__ static int weight(int w) { return (w & 1) ? PASK_ODD_WEIGHT : 16; }
-  __device__ __forceinline__ static int weight_before(int w) {   // of blocks 0..w-1
-    return (w >> 3) * kOctet + ((w & 7) + 1) / 2 * 16 + ((w & 7) / 2) * PASK_ODD_WEIGHT;
+  // Block w runs on XCD w % 8.  A block on an odd XCD weighs `odd`
+  // sixteenths (PASK_ODD_WEIGHT, or 16 when the ranges are at their minimum
+  // size), one on an even XCD 16: eight consecutive blocks weigh octet().
+  int odd;
+  __device__ __forceinline__ int octet() const { return 4 * 16 + 4 * odd; }
+  __device__ __forceinline__ int weight(int w) const { return (w & 1) ? odd : 16; }
+  __device__ __forceinline__ long long weight_before(int w) const {   // of blocks 0..w-1
+    return (long long)(w >> 3) * octet() + ((w & 7) + 1) / 2 * 16 + ((w & 7) / 2) * odd;
   }
-  __device__ __forceinline__ long long start_of(int w) const { return (long long)weight_before(w) * step; }
+  __device__ __forceinline__ long long start_of(int w) const {
+    return odd == 16 ? (long long)w * (16 * step) : weight_before(w) * step;
+  }
   __device__ __forceinline__ int size_of(int w) const { return weight(w) * step; }
   // Block whose range holds unit u.
   __device__ __forceinline__ long long block_of(long long u) const {
-    const long long wu = u / step;                 // sixteenths of weight before u
-    const long long o = wu / kOctet;
-    int r = (int)(wu - o * kOctet), w = 0;
+    if (odd == 16) return udiv(u, 16 * step);
+    const long long wu = udiv(u, step);            // sixteenths of weight before u
+    const long long o = udiv(wu, octet());
+    int r = (int)(wu - o * octet()), w = 0;
     while (r >= weight(w)) {
       r -= weight(w);
       ++w;
@@ -532,12 +544,49 @@ __device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const First
   }
   StreamPlan pl;
   pl.total = (long long)total * a.cv.n_kv_heads;
-  const long long weights = StreamPlan::weight_before(n_blocks);
-  long long step = (pl.total + weights - 1) / weights;
   const long long lo = max(kWeightHi * a.min_pages, cdiv(mx, a.splits - 1));
-  step = max(step, (lo + PASK_ODD_WEIGHT - 1) / PASK_ODD_WEIGHT);   // every range size >= lo
+  // Weighted ranges while every range stays above the minimum size; a call
+  // whose ranges are at the minimum (a few sequences: latency-bound) splits
+  // evenly, so no worker takes more than the minimum.
+  pl.odd = PASK_ODD_WEIGHT;
+  long long step = udiv(pl.total + pl.weight_before(n_blocks) - 1, pl.weight_before(n_blocks));
+  if (step * PASK_ODD_WEIGHT < lo) {
+    pl.odd = 16;
+    step = max(udiv(pl.total + pl.weight_before(n_blocks) - 1, pl.weight_before(n_blocks)), (lo + 15) / 16);
+  }
   pl.step = (int)min(step, (long long)(INT_MAX / 16));
   return pl;
+}
+
+// The same decomposition with equal ranges of U units, for calls with at
+// most kSmallSegments segments: their workers hold a few pages each and the
+// call is bound by latency, where the weighted plan's extra arithmetic before
+// the first page load measured 0.5-0.9 us slower per call at batch 1.
+struct EvenPlan {
+  long long total;   // units
+  int U;             // units per block
+  __device__ __forceinline__ long long start_of(int w) const { return (long long)w * U; }
+  __device__ __forceinline__ int size_of(int) const { return U; }
+  __device__ __forceinline__ long long block_of(long long u) const { return u / U; }
+};
+__device__ __forceinline__ EvenPlan even_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
+  int total = 0, mx = 0;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int len = lane_len(a, f, c0, a.batch);
+    total += uni(wave_sum(len));
+    mx = max(mx, uni(wave_max(len)));
+  }
+  EvenPlan pl;
+  pl.total = (long long)total * a.cv.n_kv_heads;
+  const long long even = (pl.total + n_blocks - 1) / n_blocks;
+  pl.U = max(kWeightHi * a.min_pages, (int)min(even, (long long)INT_MAX));
+  pl.U = max(pl.U, cdiv(mx, a.splits - 1));
+  return pl;
+}
+template <typename Plan>
+__device__ __forceinline__ Plan make_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
+  if constexpr (std::is_same<Plan, EvenPlan>::value) return even_plan(a, f, n_blocks);
+  else return stream_plan(a, f, n_blocks);
 }
 
 // Sequence whose segments hold unit P, and the units of the sequences before it.
@@ -650,9 +699,9 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
 
 // Pages [j0, j1) of (b, g) (HIGH store, recent window, LOW store): this
 // piece's partial of (b, g), combined with the others by attn_merge.
-template <int D, int G>
+template <int D, int G, typename Plan>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
-                                               long long seg0, const StreamPlan& plan, int q, int n) {
+                                               long long seg0, const Plan& plan, int q, int n) {
   using PL = PageLayout<D>;
   const CacheView& cv = a.cv;
   const int H = cv.n_kv_heads;
@@ -710,15 +759,17 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   if (q == 0 && n < G4) *reinterpret_cast<float2*>(a.ws_ml + (blk * G4 + n) * 2) = make_float2(st.m, l_n);
 }
 
-// One single-wave workgroup per stream-K worker w.
-template <int D, int G>
+// One single-wave workgroup per stream-K worker w; kWeighted: the per-XCD
+// weighted ranges (StreamPlan), else equal ranges (EvenPlan).
+template <int D, int G, bool kWeighted>
 __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
+  using Plan = typename std::conditional<kWeighted, StreamPlan, EvenPlan>::type;
   const int lane = threadIdx.x & 63;
   const int w = uni(blockIdx.x);
   const int q = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
   const FirstCounts f = first_counts(a);
-  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const Plan plan = make_plan<Plan>(a, f, a.attn_blocks);
   const long long start = plan.start_of(w);
   if (start >= plan.total) return;
   const long long end = min(plan.total, start + plan.size_of(w));
@@ -727,13 +778,13 @@ __global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
   if (b < 0) return;
   SeqPages sp = seq_pages(a, f, b);
   const long long rel = start - (long long)excl * H;
-  int g = (int)(rel / sp.len);
-  int j0 = first_page_at(sp, (int)(rel % sp.len));
+  int g = (int)udiv(rel, sp.len);
+  int j0 = first_page_at(sp, (int)(rel - (long long)g * sp.len));
   while (true) {
     const long long seg0 = (long long)excl * H + (long long)g * sp.len;
     if (seg0 >= end) return;
     const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
-    if (j0 < j1) attend_segment<D, G>(a, w, b, g, j0, j1, sp, seg0, plan, q, n);
+    if (j0 < j1) attend_segment<D, G, Plan>(a, w, b, g, j0, j1, sp, seg0, plan, q, n);
     if (j1 < sp.np) return;
     j0 = 0;
     if (++g == H) {                              // next sequence that holds any page
@@ -804,7 +855,8 @@ struct PieceMerge {
 
 // Pieces of segment (b, g) in the stream-K decomposition (sp: pages of b,
 // excl: units of the sequences before b; sp.np > 0).
-__device__ __forceinline__ int n_pieces(const StreamPlan& plan, const SeqPages& sp, int excl, int g, int H) {
+template <typename Plan>
+__device__ __forceinline__ int n_pieces(const Plan& plan, const SeqPages& sp, int excl, int g, int H) {
   const long long seg0 = (long long)excl * H + (long long)g * sp.len;
   return (int)(plan.block_of(seg0 + page_start(sp, sp.np - 1)) - plan.block_of(seg0)) + 1;
 }
@@ -894,7 +946,7 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
     if (a.lse && j == 0 && k == 0 && n < 4 && 4 * q + n < G) a.lse[row0 + 4 * q + n] = -INFINITY;
     return;
   }
-  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
+  const EvenPlan plan = even_plan(a, f, a.attn_blocks);
   const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
   pm.init();
   for (int p0 = 0; p0 < nparts; p0 += 4 * kB) {
@@ -1031,7 +1083,8 @@ int attn_grid() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
   if (cached[dev] == 0) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G>, 64, 0) != hipSuccess || per_cu <= 0)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G, true>, 64, 0) != hipSuccess ||
+        per_cu <= 0)
       return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
     cached[dev] = per_cu * cus;
@@ -1050,11 +1103,13 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
     a.attn_blocks = attn_grid<DD, GG>();                                         \
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
     a.min_pages = small ? kSmallMinPages : kMinPagesPerBlock;                    \
-    attn_kernel<DD, GG><<<dim3(a.attn_blocks), block, 0, s>>>(a);                \
-    if (small)                                                                   \
+    if (small) {                                                                 \
+      attn_kernel<DD, GG, false><<<dim3(a.attn_blocks), block, 0, s>>>(a);       \
       attn_merge_sliced_kernel<DD, GG><<<dim3(segs * (merge_threads<DD, GG>() / 16)), dim3(64), 0, s>>>(a); \
-    else                                                                         \
+    } else {                                                                     \
+      attn_kernel<DD, GG, true><<<dim3(a.attn_blocks), block, 0, s>>>(a);        \
       attn_merge_kernel<DD, GG><<<dim3(segs), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
+    }                                                                            \
     return hipGetLastError();                                                    \
   }
   PASK_CASE(64, 1) PASK_CASE(64, 2) PASK_CASE(64, 4) PASK_CASE(64, 8)
@@ -1073,8 +1128,8 @@ hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args,
     ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG>();                     \
     ref.min_pages = itv.min_pages = kMinPagesPerBlock;                           \
     if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
-    attn_kernel<DD, GG><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);            \
-    attn_kernel<DD, GG><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);            \
+    attn_kernel<DD, GG, true><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);      \
+    attn_kernel<DD, GG, true><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);      \
     distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>() * distortion_heads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
     return hipGetLastError();                                                    \
   }
