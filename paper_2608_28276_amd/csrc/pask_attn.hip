@@ -38,10 +38,11 @@ namespace {
 // HIGH pages of a (b, g) before its LOW pages, each page weighing 32 units
 // (PASK_WEIGHT_LO for a LOW page).  The grid holds one single-wave worker
 // per resident wave slot of the chip, and worker w takes the w-th of
-// contiguous unit ranges, so every worker starts at launch.  Workers on the
-// odd-numbered XCDs (blockIdx odd) take 14/16 of an even one's range: their
-// waves stream pages about 10% slower, so with equal ranges the even XCDs
-// idle through the last ~15 us of the call.  A range crossing a (b, g)
+// contiguous unit ranges, so every worker starts at launch.  In calls with
+// more than 64 (b, g) segments, workers on the odd-numbered XCDs (blockIdx
+// odd) take 14/16 of an even one's range: their waves stream pages about 10%
+// slower, so with equal ranges the even XCDs idle through the last ~15 us of
+// the call.  A range crossing a (b, g)
 // boundary closes that segment with a partial block; every range is at least
 // what keeps every (b, g) within as many pieces as the workspace holds
 // partials.
@@ -483,7 +484,7 @@ __device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
 }
 
 // a / b for 0 <= a, 0 < b (wave-uniform): 32-bit division when both fit, as
-// they do for any call below 2^31 units; the 64-bit expansion otherwise.
+// they do for any call below 2^32 units; the 64-bit expansion otherwise.
 __device__ __forceinline__ long long udiv(long long a, long long b) {
   if ((((unsigned long long)a | (unsigned long long)b) >> 32) == 0) return (long long)((uint32_t)a / (uint32_t)b);
   return a / b;
@@ -747,7 +748,7 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   // Rows past G hold finite values that are never read into an output.
   constexpr int G4 = G > 4 ? G : 4;
   const float l_n = head_sum(st.l);              // head n, over all slots
-  const int slot = (int)(w - plan.block_of(seg0));   // < a.splits by the choice of U
+  const int slot = (int)(w - plan.block_of(seg0));   // < a.splits by the choice of range sizes
   const size_t blk = ((size_t)b * H + g) * a.splits + slot;
   if (4 * q < G4) {
     float* o = a.ws_o + blk * (G4 * D);
