@@ -500,6 +500,7 @@ __device__ __forceinline__ long long udiv(long long a, long long b) {
 // kWeightLo <= kWeightHi, so every block between the first and the last one
 // of a segment holds a page of it; every range is also large enough that no
 // segment is cut into more than `splits` pieces (the workspace bound).
+constexpr int kWpb = PASK_ATTN_WPB;   // workers (waves) per workgroup of the weighted attention kernel
 struct StreamPlan {
   long long total;   // units
   int step;          // units per sixteenth of weight
@@ -507,10 +508,12 @@ struct StreamPlan {
   // sixteenths (PASK_ODD_WEIGHT, or 16 when the ranges are at their minimum
   // size), one on an even XCD 16: eight consecutive blocks weigh octet().
   int odd;
-  __device__ __forceinline__ int octet() const { return 4 * 16 + 4 * odd; }
-  __device__ __forceinline__ int weight(int w) const { return (w & 1) ? odd : 16; }
-  __device__ __forceinline__ long long weight_before(int w) const {   // of blocks 0..w-1
-    return (long long)(w >> 3) * octet() + ((w & 7) + 1) / 2 * 16 + ((w & 7) / 2) * odd;
+  // Workers w run in workgroup w / kWpb on XCD (w / kWpb) % 8.
+  __device__ __forceinline__ int octet() const { return kWpb * (4 * 16 + 4 * odd); }   // 8 workgroups
+  __device__ __forceinline__ int weight(int w) const { return ((w / kWpb) & 1) ? odd : 16; }
+  __device__ __forceinline__ long long weight_before(int w) const {   // of workers 0..w-1
+    const int wg = w / kWpb, j = wg & 7;
+    return (long long)(wg >> 3) * octet() + kWpb * ((j + 1) / 2 * 16 + (j / 2) * odd) + (w % kWpb) * weight(w);
   }
   __device__ __forceinline__ long long start_of(int w) const {
     return odd == 16 ? (long long)w * (16 * step) : weight_before(w) * step;
@@ -521,12 +524,12 @@ struct StreamPlan {
     if (odd == 16) return udiv(u, 16 * step);
     const long long wu = udiv(u, step);            // sixteenths of weight before u
     const long long o = udiv(wu, octet());
-    int r = (int)(wu - o * octet()), w = 0;
-    while (r >= weight(w)) {
-      r -= weight(w);
-      ++w;
+    int r = (int)(wu - o * octet()), j = 0;
+    while (r >= kWpb * weight(j * kWpb)) {
+      r -= kWpb * weight(j * kWpb);
+      ++j;
     }
-    return o * 8 + w;
+    return o * 8 * kWpb + j * kWpb + r / weight(j * kWpb);
   }
 };
 constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
@@ -763,10 +766,11 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
 // One single-wave workgroup per stream-K worker w; kWeighted: the per-XCD
 // weighted ranges (StreamPlan), else equal ranges (EvenPlan).
 template <int D, int G, bool kWeighted>
-__global__ __launch_bounds__(64, 2) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(AttnArgs a) {
   using Plan = typename std::conditional<kWeighted, StreamPlan, EvenPlan>::type;
+  constexpr int kWaves = kWeighted ? kWpb : 1;   // workers per workgroup
   const int lane = threadIdx.x & 63;
-  const int w = uni(blockIdx.x);
+  const int w = uni(blockIdx.x * kWaves + (int)(threadIdx.x >> 6));
   const int q = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
   const FirstCounts f = first_counts(a);
@@ -1076,19 +1080,21 @@ __global__ __launch_bounds__(512) void distortion_kernel(AttnArgs ref, AttnArgs 
 // Stream-K workers of attn_kernel<D, G> on the current device: as many waves
 // as can be resident at once (occupancy x compute units), so every worker
 // starts at launch.  Queried once per device and instance.
-template <int D, int G>
+template <int D, int G, bool kWeighted>
 int attn_grid() {
+  constexpr int kWaves = kWeighted ? kWpb : 1;
   constexpr int kMaxDevices = 64;
   static int cached[kMaxDevices] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
   if (cached[dev] == 0) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G, true>, 64, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_kernel<D, G, kWeighted>, 64 * kWaves, 0) !=
+            hipSuccess ||
         per_cu <= 0)
       return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
-    cached[dev] = per_cu * cus;
+    cached[dev] = per_cu * cus * kWaves;
   }
   return cached[dev];
 }
@@ -1096,19 +1102,18 @@ int attn_grid() {
 hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s) {
   const int D = args.cv.head_dim;
   AttnArgs a = args;
-  const dim3 block(64);
   const int segs = a.batch * a.cv.n_kv_heads;
   const bool small = segs <= kSmallSegments;
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
-    a.attn_blocks = attn_grid<DD, GG>();                                         \
+    a.attn_blocks = small ? attn_grid<DD, GG, false>() : attn_grid<DD, GG, true>(); \
     if (a.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;                \
     a.min_pages = small ? kSmallMinPages : kMinPagesPerBlock;                    \
     if (small) {                                                                 \
-      attn_kernel<DD, GG, false><<<dim3(a.attn_blocks), block, 0, s>>>(a);       \
+      attn_kernel<DD, GG, false><<<dim3(a.attn_blocks), dim3(64), 0, s>>>(a);    \
       attn_merge_sliced_kernel<DD, GG><<<dim3(segs * (merge_threads<DD, GG>() / 16)), dim3(64), 0, s>>>(a); \
     } else {                                                                     \
-      attn_kernel<DD, GG, true><<<dim3(a.attn_blocks), block, 0, s>>>(a);        \
+      attn_kernel<DD, GG, true><<<dim3(a.attn_blocks / kWpb), dim3(64 * kWpb), 0, s>>>(a); \
       attn_merge_kernel<DD, GG><<<dim3(segs), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
     }                                                                            \
     return hipGetLastError();                                                    \
@@ -1123,14 +1128,14 @@ hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args,
                              const uint8_t* in_s, float* dist, hipStream_t s) {
   const int D = ref_args.cv.head_dim;
   AttnArgs ref = ref_args, itv = itv_args;
-  const dim3 block(64);
+  const dim3 block(64 * kWpb);
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
-    ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG>();                     \
+    ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG, true>();               \
     ref.min_pages = itv.min_pages = kMinPagesPerBlock;                           \
     if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
-    attn_kernel<DD, GG, true><<<dim3(ref.attn_blocks), block, 0, s>>>(ref);      \
-    attn_kernel<DD, GG, true><<<dim3(itv.attn_blocks), block, 0, s>>>(itv);      \
+    attn_kernel<DD, GG, true><<<dim3(ref.attn_blocks / kWpb), block, 0, s>>>(ref); \
+    attn_kernel<DD, GG, true><<<dim3(itv.attn_blocks / kWpb), block, 0, s>>>(itv); \
     distortion_kernel<DD, GG><<<dim3(ref.batch), dim3(merge_threads<DD, GG>() * distortion_heads<DD, GG>()), 0, s>>>(ref, itv, in_s, dist); \
     return hipGetLastError();                                                    \
   }
