@@ -460,6 +460,16 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+def attn_kernels(cfg) -> str:
+    """The kernels of one pask_decode_attn call: calls with at most 64
+    (sequence, KV head) segments use the equal-range attention and the
+    sliced merge, larger ones the per-XCD weighted attention and the merge."""
+    D, G = cfg.head_dim, cfg.group_size
+    if cfg.batch * cfg.n_kv_heads <= 64:
+        return f"attn_kernel<{D}, {G}, false> + attn_merge_sliced_kernel<{D}, {G}>"
+    return f"attn_kernel<{D}, {G}, true> + attn_merge_kernel<{D}, {G}>"
+
+
 def prompt_desc(cfg) -> str:
     if cfg.prompt_dist == "fixed":
         return str(cfg.prompt_min)
@@ -575,7 +585,7 @@ def main():
                        "generated_before_timing": args.t_start, "D": d["D"], "S_size": d["n_s"]},
             "roofline": {"bound": "hbm", "achieved": round(d["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(d["achieved"] / HBM_PEAK_GBS, 4), "traffic": None,
-                         "kernel": f"2 x attn_kernel<{cfg.head_dim}, {cfg.group_size}> + distortion_kernel "
+                         "kernel": f"2 x attn_kernel<{cfg.head_dim}, {cfg.group_size}, true> + distortion_kernel "
                                    "(one pask_attn_distortion call)",
                          "bytes_per_launch": round(d["call_bytes"]), "avg_launch_us": round(d["avg_call_us"], 2)},
             "cpu_baseline": None}), flush=True)
@@ -617,8 +627,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(workload),
-            "kernel": f"attn_kernel<{cfg.head_dim}, {cfg.group_size}> + attn_merge_kernel<{cfg.head_dim}, "
-                      f"{cfg.group_size}> (one pask_decode_attn call)",
+            "kernel": attn_kernels(cfg) + " (one pask_decode_attn call)",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
         },
         "cpu_baseline": cpu,
