@@ -40,7 +40,7 @@ namespace {
 // per resident wave slot of the chip, and worker w takes the w-th of
 // contiguous unit ranges, so every worker starts at launch.  In calls with
 // more than 64 (b, g) segments, workers on the odd-numbered XCDs (blockIdx
-// odd) take 14/16 of an even one's range: their waves stream pages about 10%
+// odd) take 15/16 of an even one's range: their waves stream pages about 10%
 // slower, so with equal ranges the even XCDs idle through the last ~15 us of
 // the call.  A range crossing a (b, g)
 // boundary closes that segment with a partial block; every range is at least

@@ -26,10 +26,12 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #endif
 // Range an attention worker on an odd-numbered XCD takes, in sixteenths of
 // an even-XCD worker's: measured per-XCD finish times show the odd XCDs
-// streaming pages about 10% slower (two boxes, every call); 14 measured
-// fastest of 13..16 on the Qwen3-4B and Qwen3-32B-shaped workloads.
+// streaming pages about 10% slower (two boxes, every call).  With four
+// workers per workgroup 15 and 14 tie on the batch-64 Qwen3-4B call, 15 is
+// 2% faster on the int4-heavy prompt-side call and 0.4% slower on the
+// Qwen3-32B-shaped one; 13 is slower on all.
 #ifndef PASK_ODD_WEIGHT
-#define PASK_ODD_WEIGHT 14
+#define PASK_ODD_WEIGHT 15
 #endif
 // Stream-K workers (single waves) per workgroup of the attention kernel for
 // calls with more than 64 segments: 2,048 single-wave workgroups took 4.5 us
