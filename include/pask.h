@@ -19,9 +19,12 @@
  *   RETAIN-HIGH  bf16 K and V.
  *   RETAIN-LOW   int4, symmetric: per 32 consecutive head_dim elements of one
  *                (token, layer, KV head, K or V) vector, s = RNE_fp16(absmax/7)
- *                saturated at 65504; q_i = clamp(RNE(x_i / s), -7, 7), all 0
- *                when s == 0; two's-complement nibbles, element 2j in the low
- *                nibble of byte j.  Dequantised value q * s.
+ *                saturated at 65504; code q_i = clamp(RNE(x_i / s), -7, 7),
+ *                all 0 when s == 0; dequantised value q_i * s.  Stored form:
+ *                each code as the offset-binary nibble q_i + 8 (1..15), in the
+ *                attention kernel's operand order (pask_cache_layout,
+ *                lo_page_bytes), with the fp16 scales beside the codes; the
+ *                stored nibble n dequantises as (n - 8) * s.
  *   Protected recent window (Section 3.1): the last W positions of every
  *                (sequence, layer) stay visible at bf16 whatever their action;
  *                a token's action (decided, and charged by the controller,
@@ -290,7 +293,10 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
  * 4096 / (batch * n_kv_heads)). */
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint);
 
-/* One decode step of one layer: optionally persist one new token per sequence
+/* One decode step of one layer: the Persist step of Alg. 2 for the token just
+ * accepted, then the future long-term attention over the persisted history
+ * (Section 3.1: a released entry leaves it, a RETAIN-LOW entry stays in it at
+ * low precision).  Optionally persist one new token per sequence
  * (when tags_new_dev != NULL: tags [batch], parser states [batch] (nullable),
  * k_new / v_new bf16 [batch][n_kv_heads][head_dim]; the same rules as
  * pask_kv_append), then
