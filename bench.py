@@ -8,7 +8,7 @@ attention over the layer's mixed bf16 / int4 cache.  Prints one JSON line.
 
 Workload (default): Qwen3-4B attention geometry (36 layers in 4 groups,
 32 query / 8 KV heads, head_dim 128), batch 64, prompts U{1024..8192} kept
-RETAIN-HIGH, function-call tag streams from the seeded grammar walker, a
+RETAIN-HIGH, function-call tag streams read by the tagger from seeded tool-call output, a
 6 x 4 policy table at budget 0.33.  512 generated tokens are persisted
 before timing; the timed steps continue the same streams.  Synthetic data,
 random values; inputs are resident in HBM before the timed region.
@@ -40,17 +40,17 @@ def log(*a):
 def build_workload(cfg_idx: int, beta: float | None = None):
     """Workload shapes, generated-token tags [B, T], the policy table and,
     for the prompt-side workload, the prompt labels [B, max P] (else None)."""
-    from workload import CONFIGS, make_policy, prompt_lengths, schema_prompt_tags, tag_mix, walk_function_calls
+    from workload import CONFIGS, make_policy, prompt_lengths, schema_prompt_tags, tag_mix, function_call_tags
     from workload.tags import iid_tags
     from workload.tensors import sub_seed
     cfg = CONFIGS[cfg_idx]
     P = prompt_lengths(cfg)
     if beta is None:
         beta = cfg.budgets[0] if len(cfg.budgets) == 1 else 0.33
-    if cfg.tag_source == "walker":
-        tags = np.stack([walk_function_calls(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b))
+    if cfg.tag_source == "calls":
+        tags = np.stack([function_call_tags(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b))
                          for b in range(cfg.batch)])
-        probs = tag_mix(walk_function_calls(200000, sub_seed(cfg.seed, "tags", 1 << 20)), 6)
+        probs = tag_mix(function_call_tags(200000, sub_seed(cfg.seed, "tags", 1 << 20)), 6)
     else:
         tags = np.stack([iid_tags(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)])
         probs = None
@@ -68,15 +68,15 @@ def build_workload(cfg_idx: int, beta: float | None = None):
 
 
 def controller_inputs(cfg, tags, pol):
-    """Parser states of the walker streams (the same seeds give the same tags)
-    and the table with the controller's reserve, calibrated on eight walker
+    """Parser states of the tagged tool-call streams (the same seeds give the same tags)
+    and the table with the controller's reserve, calibrated on eight tagged
     traces of the generation length."""
     from workload.policy import with_budget_controller
-    from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
+    from workload.tags import CRITICAL_STATES, PARSER_STATES, function_call_tags_with_states
     from workload.tensors import sub_seed
-    ts = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
-    assert all((t == tags[b]).all() for b, (t, _) in enumerate(ts)), "controller runs need walker tags"
-    cal = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
+    ts = [function_call_tags_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
+    assert all((t == tags[b]).all() for b, (t, _) in enumerate(ts)), "controller runs need tagger tags"
+    cal = [function_call_tags_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
     pol = with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES)
     return np.stack([s for _, s in ts]).astype(np.uint8), pol
 

@@ -11,7 +11,7 @@ import oracle
 from tests.gpu_util import Scenario, bits16, budgets, policy_dict, say
 from workload import make_policy
 from workload.policy import pack_blob, with_budget_controller
-from workload.tags import CRITICAL_STATES, PARSER_STATES, tag_mix, walk_function_calls_with_states
+from workload.tags import CRITICAL_STATES, PARSER_STATES, tag_mix, function_call_tags_with_states
 from workload.tensors import bf16_normal, sub_seed
 
 pytestmark = pytest.mark.gpu
@@ -25,9 +25,9 @@ def _gpu():
 
 
 def controller_policy(n_groups, n_layers, beta, seed, n_sink, cal_len):
-    """A 6-tag table plus the controller's reserve, calibrated on four walker
+    """A 6-tag table plus the controller's reserve, calibrated on four tagged
     traces of cal_len tokens."""
-    cal = [walk_function_calls_with_states(cal_len, sub_seed(seed, "tags", 100 + i)) for i in range(4)]
+    cal = [function_call_tags_with_states(cal_len, sub_seed(seed, "tags", 100 + i)) for i in range(4)]
     probs = tag_mix(np.concatenate([c[0] for c in cal]), 6)
     pol = make_policy(6, n_groups, n_layers, beta, seed, tag_probs=probs, n_sink=n_sink)
     return with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES)
@@ -56,7 +56,7 @@ def replay_changes(pol, tags, states, t_max, Hkv, D):
 def test_controller_bulk_step_and_fused(Hq, Hkv, D):
     """3 sequences, 4 layers in 2 groups, 3 sinks; prompts of 0 / 37 / 300
     tokens kept HIGH (they bypass the controller), then 600 generated tokens
-    with walker tags and parser states: 0..519 bulk-appended in two calls
+    with tagger tags and parser states: 0..519 bulk-appended in two calls
     (the controller walks several 256-token chunks), 520..539 one-token
     appends, 540..599 fused append + attention.  R_0 from beta = 0.33 and
     T_max = 600 runs out part-way, so tokens are both demoted and promoted and
@@ -65,7 +65,7 @@ def test_controller_bulk_step_and_fused(Hq, Hkv, D):
     say(f"case: controller Hq={Hq} Hkv={Hkv} D={D}")
     T, seed = 600, 11
     pol = controller_policy(2, 4, 0.33, seed, n_sink=3, cal_len=600)
-    ts = [walk_function_calls_with_states(T, sub_seed(seed, "tags", b)) for b in range(3)]
+    ts = [function_call_tags_with_states(T, sub_seed(seed, "tags", b)) for b in range(3)]
     tags = np.stack([t for t, _ in ts])
     states = np.stack([s for _, s in ts]).astype(np.uint8)
     states[2, 100] = 200
@@ -107,7 +107,7 @@ def test_controller_without_budget_init_and_keep_all_bypass():
     sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=2, n_q_heads=8, n_kv_heads=Hkv, head_dim=D,
                        max_tokens_per_seq=2 * n, hi_pages=2 * B * 2 * n // 16, lo_pages=2 * B * 2 * n // 16)
     dev = sess.device
-    ts = [walk_function_calls_with_states(n, sub_seed(5, "tags", b)) for b in range(B)]
+    ts = [function_call_tags_with_states(n, sub_seed(5, "tags", b)) for b in range(B)]
     tags = np.stack([t for t, _ in ts])
     states = np.stack([s for _, s in ts]).astype(np.uint8)
     k = bf16_normal((B, n, Hkv, D), 1)
@@ -152,7 +152,7 @@ def test_controller_one_token_path_matches_oracle_every_step():
     say("case: controller, fused steps only")
     T = 160
     pol = controller_policy(2, 2, 0.25, 23, n_sink=16, cal_len=T)
-    tags, states = walk_function_calls_with_states(T, sub_seed(23, "tags", 0))
+    tags, states = function_call_tags_with_states(T, sub_seed(23, "tags", 0))
     sc = Scenario(pol, B=1, L=2, Hq=8, Hkv=2, D=64, prompt_lens=[0], gen_tags=tags[None],
                   gen_states=states[None], seed=23)
     sc.budget_init(T // 2)

@@ -6,7 +6,7 @@ import torch
 
 import oracle
 from tests.gpu_util import Scenario, assert_attn_close, bits16, say
-from workload import CONFIGS, make_policy, walk_function_calls
+from workload import CONFIGS, make_policy, function_call_tags
 from workload.policy import uniform_policy
 from workload.tags import iid_tags, tag_mix
 from workload.tensors import sub_seed
@@ -99,7 +99,7 @@ def test_geometries_mixed_policy(Hq, Hkv, D):
     pol = make_policy(6, 2, 4, 0.33, seed=Hq * 100 + D)
     P = [1, 15, 17, 33, 300]
     T = 40
-    tags = np.stack([walk_function_calls(T, 50 + b) for b in range(5)])
+    tags = np.stack([function_call_tags(T, 50 + b) for b in range(5)])
     sc = Scenario(pol, B=5, L=4, Hq=Hq, Hkv=Hkv, D=D, prompt_lens=P, gen_tags=tags, seed=77 + D + Hq)
     sc.fill_prompt()
     sc.append_steps(0, 20)
@@ -118,7 +118,7 @@ def test_segment_count_boundary(B):
     pol = make_policy(6, 2, 2, 0.33, seed=500 + B)
     P = [280 + 37 * b for b in range(B)]
     T = 6
-    tags = np.stack([walk_function_calls(T, 70 + b) for b in range(B)])
+    tags = np.stack([function_call_tags(T, 70 + b) for b in range(B)])
     sc = Scenario(pol, B=B, L=2, Hq=32, Hkv=8, D=128, prompt_lens=P, gen_tags=tags, seed=300 + B)
     sc.fill_prompt()
     sc.append_steps(0, 4)
@@ -163,7 +163,7 @@ def test_prompt_side_persistence_tagged_prompt():
     ptags = np.zeros((3, max(P)), np.uint8)
     for b, p in enumerate(P):
         ptags[b, :p] = schema_prompt_tags(p, 20 + b)
-    tags = np.stack([walk_function_calls(24, 30 + b) for b in range(3)])
+    tags = np.stack([function_call_tags(24, 30 + b) for b in range(3)])
     sc = Scenario(pol, B=3, L=2, Hq=8, Hkv=2, D=64, prompt_lens=P, gen_tags=tags, seed=13, prompt_tags=ptags)
     sc.fill_prompt()
     sc.decode_step(0)
@@ -199,7 +199,7 @@ def test_batch_beyond_64_sequences():
     P[rng.random(B) < 0.2] = 0
     P[[5, 70, 140]] = [700, 1000, 913]
     pol = make_policy(6, 2, 2, 0.33, seed=21)
-    tags = np.stack([walk_function_calls(12, 60 + b) for b in range(B)])
+    tags = np.stack([function_call_tags(12, 60 + b) for b in range(B)])
     sc = Scenario(pol, B=B, L=2, Hq=8, Hkv=2, D=64, prompt_lens=P, gen_tags=tags, seed=21)
     sc.fill_prompt()
     sc.decode_step(0)
@@ -246,7 +246,7 @@ def test_flags_bad_tag_capacity_and_pool_exhaustion():
 def test_stats_ckv_matches_oracle_counts():
     say("case: stats")
     pol = make_policy(6, 2, 4, 0.33, seed=16)
-    tags = np.stack([walk_function_calls(64, 60 + b) for b in range(3)])
+    tags = np.stack([function_call_tags(64, 60 + b) for b in range(3)])
     sc = Scenario(pol, B=3, L=4, Hq=8, Hkv=2, D=64, prompt_lens=[10, 20, 30], gen_tags=tags, seed=17)
     sc.fill_prompt()
     sc.append_steps(0, 64)

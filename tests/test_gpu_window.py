@@ -11,9 +11,9 @@ import torch
 
 import oracle
 from tests.gpu_util import Scenario, budgets, say
-from workload import make_policy, walk_function_calls
+from workload import make_policy, function_call_tags
 from workload.policy import uniform_policy, with_budget_controller
-from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
+from workload.tags import CRITICAL_STATES, PARSER_STATES, function_call_tags_with_states
 from workload.tensors import sub_seed
 
 pytestmark = pytest.mark.gpu
@@ -35,13 +35,13 @@ def _windowed(pol, W):
 def test_window_bulk_step_and_fused(Hq, Hkv, D, W):
     """3 sequences, 4 layers in 2 groups, 3 sinks, prompts of 0 / 37 / 300
     tokens kept HIGH (they pass through the window too), then 900 generated
-    walker-tagged tokens: bulk appends of 5, 195 and 600 tokens (several
+    tagger-tagged tokens: bulk appends of 5, 195 and 600 tokens (several
     256-entry chunks, entries leaving from the window and from the call
     itself), one-token appends, then fused append + attention steps."""
     say(f"case: window W={W} Hq={Hq} Hkv={Hkv} D={D}")
     T = 900
     pol = _windowed(make_policy(6, 2, 4, 0.33, seed=W + D, n_sink=3), W)
-    tags = np.stack([walk_function_calls(T, sub_seed(W, "tags", b)) for b in range(3)])
+    tags = np.stack([function_call_tags(T, sub_seed(W, "tags", b)) for b in range(3)])
     sc = Scenario(pol, B=3, L=4, Hq=Hq, Hkv=Hkv, D=D, prompt_lens=[0, 37, 300], gen_tags=tags, seed=W * 7 + D)
     sc.fill_prompt()
     sc.check_state()
@@ -66,7 +66,7 @@ def test_window_all_drop_sees_prompt_and_last_w():
     say("case: window, all-DROP")
     pol = _windowed(uniform_policy(6, 2, 2, oracle.DROP), 24)
     T = 70
-    tags = np.stack([walk_function_calls(T, 3 + b) for b in range(2)])
+    tags = np.stack([function_call_tags(T, 3 + b) for b in range(2)])
     sc = Scenario(pol, B=2, L=2, Hq=8, Hkv=2, D=64, prompt_lens=[0, 40], gen_tags=tags, seed=5)
     sc.fill_prompt()
     for t in range(T):
@@ -82,7 +82,7 @@ def test_window_larger_than_the_sequence():
     attended at bf16 and the stores stay empty."""
     say("case: window covering the sequence")
     T = 48
-    tags = walk_function_calls(T, 9)[None]
+    tags = function_call_tags(T, 9)[None]
     pol = _windowed(make_policy(6, 2, 2, 0.33, seed=4), 16 + T)
     sc = Scenario(pol, B=1, L=2, Hq=8, Hkv=2, D=64, prompt_lens=[16], gen_tags=tags, seed=6)
     sc.fill_prompt()
@@ -101,10 +101,10 @@ def test_window_with_the_online_controller():
     from paper_2608_28276_amd.pask import PASK_FLAG_BAD_STATE
     say("case: window + controller")
     T, W = 400, 20
-    cal = [walk_function_calls_with_states(T, sub_seed(31, "tags", 100 + i)) for i in range(4)]
+    cal = [function_call_tags_with_states(T, sub_seed(31, "tags", 100 + i)) for i in range(4)]
     pol = make_policy(6, 2, 4, 0.33, seed=31, n_sink=2)
     pol = _windowed(with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES), W)
-    ts = [walk_function_calls_with_states(T, sub_seed(31, "tags", b)) for b in range(2)]
+    ts = [function_call_tags_with_states(T, sub_seed(31, "tags", b)) for b in range(2)]
     tags = np.stack([t for t, _ in ts])
     states = np.stack([s for _, s in ts]).astype(np.uint8)
     states[1, 50] = 99

@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 from workload.policy import contiguous_groups, make_policy, uniform_policy
-from workload.tags import iid_tags, walk_function_calls
+from workload.tags import iid_tags, function_call_tags
 
 # The paper's order R < L < H written as a truth table of "the higher of two".
 PAPER_MAX = {("R", "R"): "R", ("R", "L"): "L", ("R", "H"): "H",
@@ -76,7 +76,7 @@ def test_exhaustive_tiny_tables():
 def test_counts_closed_form_from_table():
     """n_H, n_L, n_R per group equal tag counts weighted by the table."""
     pol = make_policy(6, 4, 36, 0.33, seed=11)
-    tags = walk_function_calls(5000, 3)
+    tags = function_call_tags(5000, 3)
     counts = np.bincount(tags, minlength=6)
     eff = np.maximum(pol.action, pol.floor)
     cache = oracle.OracleCache(dict(action=pol.action, floor=pol.floor,
@@ -123,7 +123,7 @@ def test_lists_identical_across_layers_of_a_group():
     pol = make_policy(6, 4, 36, 0.33, seed=2)
     p = dict(action=pol.action, floor=pol.floor, group_of_layer=pol.group_of_layer, n_sink=0)
     cache = oracle.OracleCache(p, 1, 32)
-    tags = walk_function_calls(400, 9)
+    tags = function_call_tags(400, 9)
     kv = np.zeros((400, 1, 32), dtype=np.int64)
     for layer in range(36):
         cache.append(layer, 0, tags, kv, kv)

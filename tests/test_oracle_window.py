@@ -13,7 +13,7 @@ import oracle
 from tests import pins
 from workload import make_policy
 from workload.policy import uniform_policy, with_budget_controller
-from workload.tags import iid_tags, walk_function_calls_with_states, CRITICAL_STATES, PARSER_STATES
+from workload.tags import iid_tags, function_call_tags_with_states, CRITICAL_STATES, PARSER_STATES
 
 
 def _bits(t: torch.Tensor) -> np.ndarray:
@@ -94,7 +94,7 @@ def test_low_tokens_are_full_precision_until_they_leave():
 
 @pytest.mark.parametrize("W", [1, 4, 33])
 def test_stores_equal_the_w0_stores_of_the_prefix_that_left(W):
-    """Mixed walker table with sinks: after each append, the stores (lists,
+    """Mixed table with sinks: after each append, the stores (lists,
     bf16 bits, codes, scales, counters) equal those of a W = 0 cache fed the
     same stream without its last W tokens; bulk and one-by-one appends agree."""
     pol = make_policy(6, 2, 4, 0.33, seed=3, n_sink=5)
@@ -128,9 +128,9 @@ def test_controller_charges_at_decision_time():
     the window only delays the Persist step: R after every append is the
     same for W = 0 and W = 9, and so are the eventual stores."""
     T = 120
-    tags, states = walk_function_calls_with_states(T, 5)
+    tags, states = function_call_tags_with_states(T, 5)
     pol = make_policy(6, 2, 4, 0.33, seed=8, n_sink=2)
-    pol = with_budget_controller(pol, [walk_function_calls_with_states(T, 50 + i) for i in range(3)],
+    pol = with_budget_controller(pol, [function_call_tags_with_states(T, 50 + i) for i in range(3)],
                                  len(PARSER_STATES), CRITICAL_STATES)
     k, v = _rand_bf16((T, HKV, D), 11), _rand_bf16((T, HKV, D), 12)
     caches = {W: oracle.OracleCache(_pd(pol, W), HKV, D) for W in (0, 9)}

@@ -4,15 +4,15 @@ import struct
 
 import numpy as np
 
-from workload import CONFIGS, make_policy, pack_blob, prompt_lengths, tag_mix, walk_function_calls
+from workload import CONFIGS, make_policy, pack_blob, prompt_lengths, tag_mix, function_call_tags
 from workload.policy import fnv1a32
 from workload.tags import schema_prompt_tags
 from workload.tensors import bf16_normal
 
 
-def test_walker_deterministic_and_mix():
-    a = walk_function_calls(50000, 17)
-    assert (a == walk_function_calls(50000, 17)).all()
+def test_call_tags_deterministic_and_mix():
+    a = function_call_tags(50000, 17)
+    assert (a == function_call_tags(50000, 17)).all() and a.size == 50000
     m = tag_mix(a, 6)
     # ~35% scaffold+boundary, 25% keys, 30% argument values, 10% free text.
     assert abs(m[3] + m[4] - 0.35) < 0.07
@@ -50,20 +50,25 @@ def test_bf16_normal_seeded():
     assert (a == b).all() and a.shape == (4, 8)
 
 
-def test_walker_states_align_with_tags_and_reserve_follows_eq8():
-    """Parser states come with the same tag stream; keys are produced in key
-    states and enum values in enum states; Gamma(s) is the median future floor
-    cost, so it shrinks toward the end of a trace and a state that never
-    occurs reserves nothing."""
-    from workload.tags import (walk_function_calls_with_states, ST_KEY, ST_ENUM, ST_TEXT, CRITICAL_STATES,
-                               PARSER_STATES, REQUIRED_KEY, ENUM_VALUE, FREE_TEXT)
+def test_tagger_states_align_with_tags_and_reserve_follows_eq8():
+    """Parser states come with the same tag stream: free text is read outside
+    calls, enum values and keys inside their strings or right at their end;
+    Gamma(s) is the median future floor cost, so it shrinks toward the end
+    of a trace and a state that never occurs reserves nothing."""
+    from paper_2608_28276_amd import tagger as tg
+    from workload.tags import (function_call_tags_with_states, CRITICAL_STATES, PARSER_STATES, REQUIRED_KEY,
+                               ENUM_VALUE, FREE_TEXT)
     from workload.policy import with_budget_controller, pack_blob, floor_cost
-    tags, states = walk_function_calls_with_states(5000, 17)
-    assert (tags == walk_function_calls(5000, 17)).all()
-    assert states.max() < len(PARSER_STATES)
-    assert (states[tags == REQUIRED_KEY] == ST_KEY).all()
-    assert (states[tags == ENUM_VALUE] == ST_ENUM).all()
-    assert (states[tags == FREE_TEXT] == ST_TEXT).all()
+    tags, states = function_call_tags_with_states(5000, 17)
+    assert (tags == function_call_tags(5000, 17)).all()
+    assert states.max() < len(PARSER_STATES) == tg.N_STATES
+    lex = states // 3
+    assert set(lex[tags == FREE_TEXT]) <= {tg.S_TEXT}
+    assert set(lex[tags == REQUIRED_KEY]) <= {tg.S_IN_KEY, tg.S_EXPECT_COLON, tg.S_EXPECT_VALUE, tg.S_IN_STRING,
+                                             tg.S_IN_ENUM}
+    assert set(lex[tags == ENUM_VALUE]) <= {tg.S_IN_ENUM, tg.S_AFTER_VALUE, tg.S_EXPECT_KEY, tg.S_EXPECT_VALUE,
+                                           tg.S_END}
+    assert (lex[tags == REQUIRED_KEY] == tg.S_IN_KEY).mean() > 0.9
     pol = make_policy(6, 2, 4, 0.33, seed=3)
     trace = (tags[:200], states[:200])
     bp = with_budget_controller(pol, [trace], len(PARSER_STATES) + 1, CRITICAL_STATES)

@@ -12,7 +12,7 @@ from .tags import (  # noqa: F401
     DECODE_TAGS,
     PROMPT_TAGS,
     iid_tags,
-    walk_function_calls,
+    function_call_tags,
     schema_prompt_tags,
     tag_mix,
 )

@@ -25,7 +25,7 @@ class Config:
     prompt_max: int
     prompt_dist: str          # "fixed" | "uniform" | "loguniform"
     gen_tokens: int
-    tag_source: str           # "iid" | "walker"
+    tag_source: str           # "iid" | "calls" (tool-call output read by the tagger)
     prompt_tagged: bool       # prompt KV governed by the table (prompt-side companion)
     budgets: Tuple[float, ...]
     n_sink: int
@@ -63,28 +63,28 @@ CONFIGS = [
         name="qwen3_4b_b1_p2048_g512",
         batch=1, n_layers=36, n_groups=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
         prompt_min=2048, prompt_max=2048, prompt_dist="fixed",
-        gen_tokens=512, tag_source="walker", prompt_tagged=False,
+        gen_tokens=512, tag_source="calls", prompt_tagged=False,
         budgets=(0.33,), n_sink=0, seed=1001,
     ),
     Config(
         name="qwen3_4b_b64_p1k-8k_g1024",
         batch=64, n_layers=36, n_groups=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
         prompt_min=1024, prompt_max=8192, prompt_dist="uniform",
-        gen_tokens=1024, tag_source="walker", prompt_tagged=False,
+        gen_tokens=1024, tag_source="calls", prompt_tagged=False,
         budgets=(0.33,), n_sink=0, seed=1002,
     ),
     Config(
         name="qwen3_4b_b128_p4k-16k_tagged_g512",
         batch=128, n_layers=36, n_groups=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
         prompt_min=4096, prompt_max=16384, prompt_dist="uniform",
-        gen_tokens=512, tag_source="walker", prompt_tagged=True,
+        gen_tokens=512, tag_source="calls", prompt_tagged=True,
         budgets=(0.25, 0.33, 0.5, 1.0), n_sink=16, seed=1003,
     ),
     Config(
         name="qwen3_32b_attn_b256_p16k-32k_g2048",
         batch=256, n_layers=64, n_groups=8, n_q_heads=64, n_kv_heads=8, head_dim=128,
         prompt_min=16384, prompt_max=32768, prompt_dist="loguniform",
-        gen_tokens=2048, tag_source="walker", prompt_tagged=False,
+        gen_tokens=2048, tag_source="calls", prompt_tagged=False,
         budgets=(0.33,), n_sink=0, seed=1004, resident_layers=8,
         notes="one layer group (8 layers) resident: one GPU's share of a 64-layer cache",
     ),

@@ -3,31 +3,35 @@
 The paper derives a tag for every generated token from the accepted parser
 transition of a grammar-constrained decoder (Section 3.2, Eq. 3), and labels
 prompt tokens by input-derived semantic classes for its prefill companion
-(Section 3.5).  No decoder, grammar engine or benchmark data is used here:
-these seeded generators emit tag ids with the shape of function-call output
-(a JSON object per call, keys, enum / string / number arguments, nested
-objects) and of tool-schema prompts.  Nothing is taken from any benchmark.
+(Section 3.5).  Generated tokens: seeded tool-call output (workload.calls)
+read by the tagger's pushdown automaton (paper_2608_28276_amd.tagger), which
+gives each token its tag and parser state.  Prompt tokens: a seeded labeller
+with the shape of tool-schema prompts.  No model, grammar package or
+benchmark data is used; nothing is taken from any benchmark.
 """
 
 from __future__ import annotations
 
 import numpy as np
 
-# Six decode tags (generated tokens) and six prompt labels (prompt tokens).
-DECODE_TAGS = ("required_key", "enum_value", "arg_value", "boundary", "scaffold", "free_text")
+from paper_2608_28276_amd import tagger as _tagger
+
+from .calls import function_call_output
+
+# Six decode tags (generated tokens; the tagger's map from z_t) and six prompt
+# labels (prompt tokens).
+DECODE_TAGS = _tagger.TAG_NAMES
 PROMPT_TAGS = ("protected_content", "function_name", "param_key", "constraint",
                "schema_scaffold", "instruction_text")
 REQUIRED_KEY, ENUM_VALUE, ARG_VALUE, BOUNDARY, SCAFFOLD, FREE_TEXT = range(6)
 PROTECTED, FUNC_NAME, PARAM_KEY, CONSTRAINT, SCHEMA_SCAFFOLD, INSTRUCTION = range(6, 12)
 
 
-# Parser states of the synthetic function-call grammar (the s_t of the online
-# lookup, Section 3.4): where the parser frontier is when a token is accepted.
-PARSER_STATES = ("text", "expect_key", "key", "expect_value", "enum", "argument", "close")
-ST_TEXT, ST_EXPECT_KEY, ST_KEY, ST_EXPECT_VALUE, ST_ENUM, ST_ARG, ST_CLOSE = range(7)
-# Critical or lookahead-critical states: a key or an enumerated value is being
-# produced, or the next token must be one.
-CRITICAL_STATES = (ST_EXPECT_KEY, ST_KEY, ST_EXPECT_VALUE, ST_ENUM)
+# Parser states and Crit(s) of the tagger's automaton (the s_t of the online
+# lookup, Section 3.4): the parser position after a token combined with what
+# the frontier must produce next.
+PARSER_STATES = tuple(f"{lex}/{nxt}" for lex in _tagger.LEX for nxt in _tagger.NEXTS)
+CRITICAL_STATES = _tagger.CRITICAL_STATES
 
 
 def iid_tags(n: int, seed: int, n_tags: int = 6) -> np.ndarray:
@@ -35,72 +39,19 @@ def iid_tags(n: int, seed: int, n_tags: int = 6) -> np.ndarray:
     return rng.integers(0, n_tags, size=n).astype(np.uint8)
 
 
-class _Walker:
-    """Emits the tags of back-to-back function calls.
-
-    Each call is an optional free-text preamble followed by
-    {"name": <function>, "arguments": {k1: v1, ...}} with 1-6 keys; values are
-    enum, string or number tokens or a nested object (depth <= 3).  Quotes and
-    fixed template words are scaffold, delimiters are boundary."""
-
-    def __init__(self, rng: np.random.Generator):
-        self.rng = rng
-        self.out: list[int] = []
-        self.states: list[int] = []
-
-    def emit(self, tag: int, state: int, n: int = 1):
-        self.out.extend([tag] * n)
-        self.states.extend([state] * n)
-
-    def value(self, depth: int):
-        r = self.rng.random()
-        if depth < 3 and r < 0.10:
-            self.obj(depth + 1, int(self.rng.integers(1, 4)))
-        elif r < 0.40:                       # enum value, quoted
-            self.emit(SCAFFOLD, ST_ENUM)
-            self.emit(ENUM_VALUE, ST_ENUM, int(self.rng.integers(1, 3)))
-        elif r < 0.80:                       # string argument, quoted
-            self.emit(SCAFFOLD, ST_ARG)
-            self.emit(ARG_VALUE, ST_ARG, int(self.rng.integers(1, 11)))
-        else:                                # number argument
-            self.emit(ARG_VALUE, ST_ARG, int(self.rng.integers(1, 4)))
-
-    def obj(self, depth: int, n_keys: int):
-        self.emit(BOUNDARY, ST_EXPECT_KEY)   # {
-        for i in range(n_keys):
-            if i:
-                self.emit(BOUNDARY, ST_EXPECT_KEY)   # ,
-            if self.rng.random() < 0.5:
-                self.emit(SCAFFOLD, ST_KEY)  # opening quote as its own token
-            self.emit(REQUIRED_KEY, ST_KEY, int(self.rng.integers(1, 6)))
-            self.emit(BOUNDARY, ST_EXPECT_VALUE)     # ":
-            self.value(depth)
-        self.emit(BOUNDARY, ST_CLOSE)        # }
-
-    def call(self):
-        if self.rng.random() < 0.7:
-            self.emit(FREE_TEXT, ST_TEXT, int(self.rng.integers(3, 16)))
-        self.emit(BOUNDARY, ST_EXPECT_KEY)   # {
-        self.emit(SCAFFOLD, ST_KEY, 2)       # "name":
-        self.emit(ENUM_VALUE, ST_ENUM, int(self.rng.integers(1, 4)))
-        self.emit(BOUNDARY, ST_EXPECT_KEY)   # ,
-        self.emit(SCAFFOLD, ST_KEY, 2)       # "arguments":
-        self.obj(1, int(self.rng.integers(1, 7)))
-        self.emit(BOUNDARY, ST_CLOSE)        # }
+def function_call_tags_with_states(n: int, seed: int):
+    """(tags, parser states) of n generated tokens of back-to-back calls to a
+    seeded set of invented tools: the token stream of workload.calls, read by
+    the tagger's pushdown automaton (structural tag z_t -> decode tag id;
+    parser state id for the controller)."""
+    tools, toks = function_call_output(n, seed)
+    tags, states = _tagger.tag_stream(tools, toks[:n])
+    return np.asarray(tags, dtype=np.uint8), np.asarray(states, dtype=np.uint8)
 
 
-def walk_function_calls(n: int, seed: int) -> np.ndarray:
-    """Tags of n generated tokens from back-to-back synthetic function calls."""
-    return walk_function_calls_with_states(n, seed)[0]
-
-
-def walk_function_calls_with_states(n: int, seed: int):
-    """(tags, parser states) of n generated tokens; the tags are those of
-    walk_function_calls with the same seed."""
-    w = _Walker(np.random.default_rng(seed))
-    while len(w.out) < n:
-        w.call()
-    return np.asarray(w.out[:n], dtype=np.uint8), np.asarray(w.states[:n], dtype=np.uint8)
+def function_call_tags(n: int, seed: int) -> np.ndarray:
+    """Decode tags of n generated tokens (function_call_tags_with_states)."""
+    return function_call_tags_with_states(n, seed)[0]
 
 
 def schema_prompt_tags(n: int, seed: int) -> np.ndarray:
