@@ -177,9 +177,13 @@ class DeviceRun:
             if not check:
                 continue
             o_gpu, l_gpu = bf16_f64(out), lse.cpu().double().numpy()
+            done = 0
             for (b, l) in self.sample:
                 if l != layer:
                     continue
+                if done and done % 16 == 0:
+                    say(f"step {t} layer {layer}: {done} sequences compared")
+                done += 1
                 o_ref, lse_ref = self.oc.attend(layer, b, bits16(q[b]), self.scale)
                 assert_attn_close(o_gpu[b], o_ref, f"attention step {t} layer {layer} seq {b}")
                 assert np.abs(l_gpu[b] - lse_ref).max() <= 1e-4 + 1e-5 * np.abs(lse_ref).max()

@@ -59,7 +59,7 @@ class Scenario:
 
     def __init__(self, pol, *, B, L, Hq, Hkv, D, prompt_lens, gen_tags, seed, prompt_tags=None,
                  max_ctx_hint=None, hi_pages=None, lo_pages=None, extra_bytes=0, outliers=0, gen_states=None,
-                 expect_flags=0):
+                 expect_flags=0, q_scale=1.0, v_scale=1.0):
         from paper_2608_28276_amd.session import PaskSession
         self.pol, self.B, self.L, self.Hq, self.Hkv, self.D = pol, B, L, Hq, Hkv, D
         self.P = np.asarray(prompt_lens, dtype=np.int64)
@@ -82,13 +82,18 @@ class Scenario:
         self.oc = oracle.OracleCache(policy_dict(pol), Hkv, D)
         self.scale = self.sess.softmax_scale
         self.outliers = outliers
+        # powers of two scale q and V exactly in bf16 (stress inputs: large
+        # scores, small V scales)
+        for x in (q_scale, v_scale):
+            assert x > 0 and math.frexp(x)[0] == 0.5, "q_scale and v_scale must be powers of two"
+        self.q_scale, self.v_scale = q_scale, v_scale
         self.dev = self.sess.device
 
     # -- inputs ----------------------------------------------------------
     def prompt_kv(self, layer):
         shape = (self.B, int(self.P.max()), self.Hkv, self.D)
         k = bf16_normal(shape, sub_seed(self.seed, "prompt_k", layer), outlier_channels=self.outliers)
-        v = bf16_normal(shape, sub_seed(self.seed, "prompt_v", layer))
+        v = bf16_normal(shape, sub_seed(self.seed, "prompt_v", layer)) * self.v_scale
         return k, v
 
     def gen_kv(self, layer, t0, t1):
@@ -96,11 +101,11 @@ class Scenario:
         k = torch.stack([bf16_normal((self.B, self.Hkv, self.D), sub_seed(self.seed, "gen_k", layer, t),
                                      outlier_channels=self.outliers) for t in range(t0, t1)], dim=1)
         v = torch.stack([bf16_normal((self.B, self.Hkv, self.D), sub_seed(self.seed, "gen_v", layer, t))
-                         for t in range(t0, t1)], dim=1)
+                         for t in range(t0, t1)], dim=1) * self.v_scale
         return k, v
 
     def q(self, layer, t):
-        return bf16_normal((self.B, self.Hq, self.D), sub_seed(self.seed, "q", layer, t))
+        return bf16_normal((self.B, self.Hq, self.D), sub_seed(self.seed, "q", layer, t)) * self.q_scale
 
     # -- driving both sides ---------------------------------------------
     def budget_init(self, t_max: int):
@@ -165,6 +170,9 @@ class Scenario:
             for b in (range(self.B) if seqs is None else seqs):
                 o_ref, lse_ref = self.oc.attend(layer, b, bits16(q[b]), self.scale)
                 assert_attn_close(o_gpu[b], o_ref, f"attention step {t} layer {layer} seq {b}")
+                if self.v_scale != 1.0:   # the same bound in units of the V scale
+                    assert_attn_close(o_gpu[b] / self.v_scale, o_ref / self.v_scale,
+                                      f"attention / v_scale, step {t} layer {layer} seq {b}")
                 fin = np.isfinite(lse_ref)
                 assert (np.isneginf(l_gpu[b]) == ~fin).all()
                 assert np.abs(l_gpu[b][fin] - lse_ref[fin]).max(initial=0) <= 1e-4 + 1e-5 * np.abs(lse_ref[fin]).max(initial=0)

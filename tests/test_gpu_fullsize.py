@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from tests.gpu_util import Scenario, say
-from workload import CONFIGS, make_policy, prompt_lengths, tag_mix, walk_function_calls
+from workload import CONFIGS, make_policy, prompt_lengths, tag_mix, function_call_tags
 from workload.tags import schema_prompt_tags
 from workload.tensors import sub_seed
 
@@ -23,25 +23,25 @@ def _gpu():
     import paper_2608_28276_amd.pask  # noqa: F401  (fails loudly when libpask.so is missing)
 
 
-def _walker_tags(cfg, n):
-    return np.stack([walk_function_calls(n, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)])
+def _call_tags(cfg, n):
+    return np.stack([function_call_tags(n, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)])
 
 
-def _walker_policy(cfg, beta=0.33):
-    probs = tag_mix(walk_function_calls(200000, sub_seed(cfg.seed, "tags", 1 << 20)), 6)
+def _calls_policy(cfg, beta=0.33):
+    probs = tag_mix(function_call_tags(200000, sub_seed(cfg.seed, "tags", 1 << 20)), 6)
     return make_policy(6, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs)
 
 
 def test_qwen3_4b_one_sequence_every_step():
     """1 sequence, 36 layers in 4 groups, 32 query / 8 KV heads, head_dim 128,
-    a 2048-token prompt kept HIGH and 512 generated tokens with walker tags,
+    a 2048-token prompt kept HIGH and 512 generated tokens with tagger tags,
     each through the fused append + attention call on every layer: every
     decision, list, code and scale bit-exact; attention at steps 0, 1, 127,
     255 and 511 on all 36 layers."""
     cfg = CONFIGS[1]
     say(f"case: {cfg.name}")
-    pol = _walker_policy(cfg)
-    tags = _walker_tags(cfg, cfg.gen_tokens)
+    pol = _calls_policy(cfg)
+    tags = _call_tags(cfg, cfg.gen_tokens)
     sc = Scenario(pol, B=1, L=cfg.n_layers, Hq=cfg.n_q_heads, Hkv=cfg.n_kv_heads, D=cfg.head_dim,
                   prompt_lens=prompt_lengths(cfg), gen_tags=tags, seed=cfg.seed)
     sc.fill_prompt()
@@ -60,13 +60,15 @@ def test_qwen3_4b_batch64_bench_launch():
     sequences, prompts U{1024..8192} kept HIGH, 512 generated tokens
     bulk-appended, then decode steps of one-token appends and attention over
     all 36 layers with the bench's workspace hint.  Every counter and list of
-    all 64 sequences x 36 layers bit-exact; stores and attention of 7
-    sequences x the first layer of each group."""
+    all 64 sequences x 36 layers bit-exact; stores and attention of all 64
+    sequences in layer 27 and of 7 sequences x the first layer of each
+    group."""
     from bench import build_workload
     from tests.fullsize_util import DeviceRun
     cfg, P, tags, pol, _ = build_workload(2)
     say(f"case: {cfg.name}")
-    sample = [(b, l) for b in (0, 9, 21, 33, 42, 50, 63) for l in (0, 9, 18, 27)]
+    sample = sorted({(b, l) for b in (0, 9, 21, 33, 42, 50, 63) for l in (0, 9, 18, 27)} |
+                    {(b, 27) for b in range(cfg.batch)})
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
                     Hkv=cfg.n_kv_heads, D=cfg.head_dim, P=P, prompt_tags=None, gen_tags=tags, sample=sample,
                     seed=cfg.seed, n_bulk=512, n_steps=3)
@@ -85,7 +87,8 @@ def test_qwen3_4b_batch128_tagged_prompts_budget_sweep(beta):
     companion, 16 sinks), bulk-appended after prefill, then 64 generated
     tokens and two fused decode steps, at budgets 0.25 / 0.33 / 0.5 / 1.0.
     Driven layers: the first of each of the 4 groups.  Every counter and list
-    bit-exact; stores and attention of 3 sequences x 4 layers."""
+    bit-exact; stores and attention of 3 sequences x 4 layers, and at budget
+    0.33 of 5 more sequences in layer 27."""
     from tests.fullsize_util import DeviceRun
     cfg = CONFIGS[3]
     say(f"case: {cfg.name} at budget {beta}")
@@ -93,12 +96,14 @@ def test_qwen3_4b_batch128_tagged_prompts_budget_sweep(beta):
     ptags = np.zeros((cfg.batch, int(P.max())), np.uint8)
     for b, p in enumerate(P):
         ptags[b, :p] = schema_prompt_tags(int(p), sub_seed(cfg.seed, "prompt_tags", b))
-    gtags = _walker_tags(cfg, 66)
+    gtags = _call_tags(cfg, 66)
     probs = tag_mix(np.concatenate([ptags[b, :P[b]] for b in range(cfg.batch)] + [gtags.ravel()]), 12)
     pol = make_policy(12, cfg.n_groups, cfg.n_layers, beta, cfg.seed, tag_probs=probs, n_sink=cfg.n_sink)
     say(f"policy expected cost {pol.expected_cost:.3f}")
     layers = (0, 9, 18, 27)
     sample = [(b, l) for b in (3, 64, 127) for l in layers]
+    if beta == 0.33:
+        sample += [(b, 27) for b in (17, 40, 77, 100, 115)]
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=layers, Hq=cfg.n_q_heads, Hkv=cfg.n_kv_heads,
                     D=cfg.head_dim, P=P, prompt_tags=ptags, gen_tags=gtags, sample=sample, seed=cfg.seed,
                     n_bulk=64, n_steps=2)
@@ -120,8 +125,8 @@ def test_qwen3_32b_attention_batch256_one_layer_group():
     cfg = CONFIGS[4]
     say(f"case: {cfg.name}")
     P = prompt_lengths(cfg)
-    tags = _walker_tags(cfg, 258)
-    pol = _walker_policy(cfg)
+    tags = _call_tags(cfg, 258)
+    pol = _calls_policy(cfg)
     layers = (0, 5)
     sample = [(b, l) for b in (0, 63, 64, 130, 200, 255) for l in layers]
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=layers, Hq=cfg.n_q_heads, Hkv=cfg.n_kv_heads,
@@ -137,7 +142,7 @@ def test_qwen3_32b_attention_batch256_one_layer_group():
 def test_qwen3_4b_batch64_online_controller():
     """The timed workload's shapes under the online controller (Alg. 2): 64
     sequences, 36 layers in 4 groups, prompts U{1024..8192} kept HIGH (they
-    bypass the controller), 512 generated tokens with walker tags and parser
+    bypass the controller), 512 generated tokens with tagger tags and parser
     states bulk-appended, then a one-token append step and two fused steps;
     R_0 from the table's beta with T_max = 515.  Every counter, list and
     remaining budget of all 64 sequences x 36 layers bit-exact; stores and
@@ -145,14 +150,14 @@ def test_qwen3_4b_batch64_online_controller():
     from bench import build_workload
     from tests.fullsize_util import DeviceRun
     from workload.policy import with_budget_controller
-    from workload.tags import CRITICAL_STATES, PARSER_STATES, walk_function_calls_with_states
+    from workload.tags import CRITICAL_STATES, PARSER_STATES, function_call_tags_with_states
     cfg, P, tags, pol, _ = build_workload(2)
     say(f"case: {cfg.name} with the online controller")
     n_gen = 515
-    ts = [walk_function_calls_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
+    ts = [function_call_tags_with_states(cfg.gen_tokens, sub_seed(cfg.seed, "tags", b)) for b in range(cfg.batch)]
     assert all((t == tags[b]).all() for b, (t, _) in enumerate(ts))
     states = np.stack([s for _, s in ts])
-    cal = [walk_function_calls_with_states(n_gen, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
+    cal = [function_call_tags_with_states(n_gen, sub_seed(cfg.seed, "tags", 1000 + i)) for i in range(8)]
     pol = with_budget_controller(pol, cal, len(PARSER_STATES), CRITICAL_STATES)
     sample = [(b, l) for b in (0, 13, 31, 40, 52, 63) for l in (0, 9, 18, 27)]
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
