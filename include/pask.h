@@ -38,7 +38,8 @@
  *     returns an error and touches neither the cache nor the stream.
  *   - Device pointers are HIP device memory owned by the caller; the library
  *     never allocates or frees device memory and keeps no pointer after a call
- *     returns.  Work is enqueued on the caller's stream and is asynchronous
+ *     returns.  Its only device memory of its own is the static scratch array
+ *     of pask_decode_attn_noalloc (PASK_NOALLOC_SCRATCH_BYTES per GPU).  Work is enqueued on the caller's stream and is asynchronous
  *     except where stated (pask_cache_stats synchronises its stream).
  *   - Calls on one cache must be ordered on one stream (append before the
  *     attention that must see it).  Distinct caches may run concurrently.
@@ -99,6 +100,8 @@ enum {
 #define PASK_PAGE_TOKENS 16
 #define PASK_QGROUP 32
 #define PASK_MAX_STATES 64
+/* Bytes of the library-owned device scratch of pask_decode_attn_noalloc. */
+#define PASK_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
 
 /* Cache geometry.  Supported: head_dim 64 or 128; n_kv_heads 1..8;
  * n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_tokens 16. */
@@ -317,6 +320,30 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
                      const uint8_t* tags_new_dev, const uint8_t* states_new_dev, const void* k_new_dev,
                      const void* v_new_dev, float softmax_scale, int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes,
                      hipStream_t stream);
+
+/* pask_decode_attn for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same append and attention, with no caller workspace.  The
+ * attention partials go to a device array the library owns,
+ * PASK_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU, held from the first call on
+ * that GPU until the process ends; the call makes no allocation of any kind.
+ * Arguments and results are those of pask_decode_attn without ws_dev /
+ * ws_bytes.  A (sequence, KV head) is cut into as many pieces as fit in the
+ * scratch (at least two): results agree with pask_decode_attn's within the
+ * attention tolerance, and are bit-identical when both use the same number of
+ * pieces.  Every call on one GPU shares that GPU's scratch and overwrites it:
+ * calls that overlap on one GPU (concurrent streams, or several host threads)
+ * race and give undefined results; calls ordered on one stream are safe.
+ *
+ * Errors: those of pask_decode_attn, and PASK_E_CAPACITY when even two pieces
+ * per (sequence, KV head) exceed the scratch: batch * n_kv_heads * 2 *
+ * (max(G, 4) * (head_dim + 2) * 4) bytes (plus alignment) above
+ * PASK_NOALLOC_SCRATCH_BYTES, e.g. batch above 504 at 8 KV heads, G 8,
+ * head_dim 128. */
+int pask_decode_attn_noalloc(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
+                             const void* q_dev, void* out_dev, float* lse_dev, const uint8_t* tags_new_dev,
+                             const uint8_t* states_new_dev, const void* k_new_dev, const void* v_new_dev,
+                             float softmax_scale, int32_t max_ctx_hint, hipStream_t stream);
 
 /* Attention-output distortion of one layer for one decode step (Eq. 4,
  * Section 3.3).  `ref` and `intervened` are two caches of the same geometry

@@ -201,6 +201,73 @@ WsLayout ws_layout(const pask_geom* g, int32_t batch, int splits) {
   return w;
 }
 
+// One decode step of one layer (pask_decode_attn): validation, then the
+// optional one-token append and the attention launches.  use_scratch: the
+// partials go to this device's library-owned scratch (kScratchBytes) instead
+// of the caller's workspace, with as many pieces per (sequence, KV head) as
+// fit there (at least two; fewer pieces only make the per-worker page ranges
+// longer, the results are the same).
+int decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch, const void* q_dev,
+                void* out_dev, float* lse_dev, const uint8_t* tags_new_dev, const uint8_t* states_new_dev,
+                const void* k_new_dev, const void* v_new_dev, float softmax_scale, int32_t max_ctx_hint,
+                void* ws_dev, size_t ws_bytes, bool use_scratch, hipStream_t stream) {
+  int st = check_cache(cache);
+  if (st != PASK_OK) return st;
+  st = check_policy(policy, cache);
+  if (st != PASK_OK) return st;
+  const pask_geom& g = cache->geom;
+  if (layer < 0 || layer >= g.n_layers) return PASK_E_SHAPE;
+  if (batch < 1 || batch > g.max_batch) return PASK_E_SHAPE;
+  if (!q_dev || !out_dev || !aligned(q_dev, 16) || !aligned(out_dev, 16)) return PASK_E_ARG;
+  if (lse_dev && !aligned(lse_dev, 4)) return PASK_E_ARG;
+  if (tags_new_dev && (!k_new_dev || !v_new_dev || !aligned(k_new_dev, 16) || !aligned(v_new_dev, 16)))
+    return PASK_E_ARG;
+  if (tags_new_dev && states_new_dev && policy->n_states == 0) return PASK_E_POLICY;
+  if (!isfinite(softmax_scale)) return PASK_E_ARG;
+  if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
+  int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq), (int64_t)batch * g.n_kv_heads);
+  if (use_scratch) {
+    while (splits > 2 && ws_layout(&g, batch, splits).total > pask::kScratchBytes) --splits;
+    if (ws_layout(&g, batch, splits).total > pask::kScratchBytes) return PASK_E_CAPACITY;
+  }
+  const WsLayout w = ws_layout(&g, batch, splits);
+  if (!use_scratch) {
+    if (!ws_dev || !aligned(ws_dev, 256)) return PASK_E_ARG;
+    if (ws_bytes < w.total) return PASK_E_CAPACITY;
+  } else if (pask::scratch_workspace(&ws_dev) != hipSuccess) {   // first HIP call of the scratch path
+    return PASK_E_HIP;
+  }
+
+  if (tags_new_dev) {
+    pask::AppendArgs a;
+    a.cv = view_of(cache);
+    a.tab = column_of(policy, layer);
+    a.n_new = nullptr;
+    a.tags = tags_new_dev;
+    a.states = states_new_dev;
+    a.k = static_cast<const uint16_t*>(k_new_dev);
+    a.v = static_cast<const uint16_t*>(v_new_dev);
+    a.layer = layer;
+    a.batch = batch;
+    a.max_new = 1;
+    a.flags = 0;
+    if (pask::launch_append_step(a, stream) != hipSuccess) return PASK_E_HIP;
+  }
+  pask::AttnArgs a;
+  a.cv = view_of(cache);
+  a.q = static_cast<const uint16_t*>(q_dev);
+  a.out = static_cast<uint16_t*>(out_dev);
+  a.lse = lse_dev;
+  a.ws_o = reinterpret_cast<float*>(static_cast<uint8_t*>(ws_dev) + w.o_off);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(ws_dev) + w.ml_off);
+  a.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
+  a.layer = layer;
+  a.batch = batch;
+  a.n_q_heads = g.n_q_heads;
+  a.splits = splits;
+  return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -415,53 +482,16 @@ int pask_decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer
                      const uint8_t* states_new_dev, const void* k_new_dev, const void* v_new_dev,
                      float softmax_scale,
                      int32_t max_ctx_hint, void* ws_dev, size_t ws_bytes, hipStream_t stream) {
-  int st = check_cache(cache);
-  if (st != PASK_OK) return st;
-  st = check_policy(policy, cache);
-  if (st != PASK_OK) return st;
-  const pask_geom& g = cache->geom;
-  if (layer < 0 || layer >= g.n_layers) return PASK_E_SHAPE;
-  if (batch < 1 || batch > g.max_batch) return PASK_E_SHAPE;
-  if (!q_dev || !out_dev || !aligned(q_dev, 16) || !aligned(out_dev, 16)) return PASK_E_ARG;
-  if (lse_dev && !aligned(lse_dev, 4)) return PASK_E_ARG;
-  if (tags_new_dev && (!k_new_dev || !v_new_dev || !aligned(k_new_dev, 16) || !aligned(v_new_dev, 16)))
-    return PASK_E_ARG;
-  if (tags_new_dev && states_new_dev && policy->n_states == 0) return PASK_E_POLICY;
-  if (!isfinite(softmax_scale)) return PASK_E_ARG;
-  if (max_ctx_hint < 1) max_ctx_hint = g.max_tokens_per_seq;
-  const int splits = splits_for(std::min(max_ctx_hint, g.max_tokens_per_seq), (int64_t)batch * g.n_kv_heads);
-  const WsLayout w = ws_layout(&g, batch, splits);
-  if (!ws_dev || !aligned(ws_dev, 256)) return PASK_E_ARG;
-  if (ws_bytes < w.total) return PASK_E_CAPACITY;
+  return decode_attn(policy, cache, layer, batch, q_dev, out_dev, lse_dev, tags_new_dev, states_new_dev, k_new_dev,
+                     v_new_dev, softmax_scale, max_ctx_hint, ws_dev, ws_bytes, false, stream);
+}
 
-  if (tags_new_dev) {
-    pask::AppendArgs a;
-    a.cv = view_of(cache);
-    a.tab = column_of(policy, layer);
-    a.n_new = nullptr;
-    a.tags = tags_new_dev;
-    a.states = states_new_dev;
-    a.k = static_cast<const uint16_t*>(k_new_dev);
-    a.v = static_cast<const uint16_t*>(v_new_dev);
-    a.layer = layer;
-    a.batch = batch;
-    a.max_new = 1;
-    a.flags = 0;
-    if (pask::launch_append_step(a, stream) != hipSuccess) return PASK_E_HIP;
-  }
-  pask::AttnArgs a;
-  a.cv = view_of(cache);
-  a.q = static_cast<const uint16_t*>(q_dev);
-  a.out = static_cast<uint16_t*>(out_dev);
-  a.lse = lse_dev;
-  a.ws_o = reinterpret_cast<float*>(static_cast<uint8_t*>(ws_dev) + w.o_off);
-  a.ws_ml = reinterpret_cast<float*>(static_cast<uint8_t*>(ws_dev) + w.ml_off);
-  a.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
-  a.layer = layer;
-  a.batch = batch;
-  a.n_q_heads = g.n_q_heads;
-  a.splits = splits;
-  return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+int pask_decode_attn_noalloc(const pask_policy* policy, pask_cache* cache, int32_t layer, int32_t batch,
+                             const void* q_dev, void* out_dev, float* lse_dev, const uint8_t* tags_new_dev,
+                             const uint8_t* states_new_dev, const void* k_new_dev, const void* v_new_dev,
+                             float softmax_scale, int32_t max_ctx_hint, hipStream_t stream) {
+  return decode_attn(policy, cache, layer, batch, q_dev, out_dev, lse_dev, tags_new_dev, states_new_dev, k_new_dev,
+                     v_new_dev, softmax_scale, max_ctx_hint, nullptr, 0, true, stream);
 }
 
 int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer, int32_t batch, const void* q_dev,

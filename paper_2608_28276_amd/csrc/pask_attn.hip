@@ -23,6 +23,7 @@
 #include <limits.h>
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "pask_device.h"
@@ -1076,6 +1077,33 @@ __global__ __launch_bounds__(512) void distortion_kernel(AttnArgs ref, AttnArgs 
 }
 
 }  // namespace
+
+// Partials of pask_decode_attn_noalloc (which has no caller workspace): a
+// device array the library owns, one copy per GPU, kept until the process
+// ends.  Host code never passes its name to a kernel (in host code the name
+// is a host-side stand-in, not a device address); it passes the address
+// scratch_workspace resolved for the current device.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+hipError_t scratch_workspace(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r != hipSuccess) return r;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 // Stream-K workers of attn_kernel<D, G> on the current device: as many waves
 // as can be resident at once (occupancy x compute units), so every worker

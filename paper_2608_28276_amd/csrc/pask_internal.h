@@ -122,6 +122,13 @@ struct AttnArgs {
 constexpr int kSmallSegments = 64;
 constexpr int kSmallPartials = 4096;
 
+// The library-owned scratch of pask_decode_attn_noalloc: a device array of
+// kScratchBytes in pask_attn.hip, one copy per GPU.  scratch_workspace gives
+// the current device's address of it (hipGetSymbolAddress, taken once per
+// device with that device current, then cached).
+constexpr size_t kScratchBytes = PASK_NOALLOC_SCRATCH_BYTES;
+hipError_t scratch_workspace(void** ptr);
+
 // Launchers (pask_append.hip: reset, budget init, append; pask_attn.hip:
 // attention, distortion).  Return hipSuccess or the launch error.
 hipError_t launch_reset(const CacheView& cv, int32_t max_batch, hipStream_t s);

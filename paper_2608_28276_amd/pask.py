@@ -38,7 +38,9 @@ PASK_APPEND_KEEP_ALL = 1 << 0
 PASK_MAX_TAGS, PASK_MAX_GROUPS, PASK_MAX_LAYERS, PASK_MAX_STATES = 64, 16, 128, 64
 EXPORTS = ("pask_policy_load", "pask_cache_layout_query", "pask_cache_bytes", "pask_cache_init",
            "pask_cache_reset", "pask_kv_append", "pask_budget_init", "pask_workspace_bytes",
-           "pask_decode_attn", "pask_attn_distortion", "pask_cache_stats", "pask_status_string")
+           "pask_decode_attn", "pask_decode_attn_noalloc", "pask_attn_distortion", "pask_cache_stats",
+           "pask_status_string")
+PASK_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class PaskError(RuntimeError):
@@ -104,6 +106,8 @@ _lib.pask_workspace_bytes.restype = C.c_size_t
 _lib.pask_workspace_bytes.argtypes = [C.POINTER(pask_geom), C.c_int32, C.c_int32]
 _lib.pask_decode_attn.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P, _P,
                                   _P, _P, _P, _P, _P, C.c_float, C.c_int32, _P, C.c_size_t, _P]
+_lib.pask_decode_attn_noalloc.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P,
+                                          _P, _P, _P, _P, _P, _P, C.c_float, C.c_int32, _P]
 _lib.pask_attn_distortion.argtypes = [C.POINTER(pask_cache), C.POINTER(pask_cache), C.c_int32, C.c_int32, _P, _P,
                                       C.c_float, C.c_int32, _P, C.c_size_t, _P, _P]
 _lib.pask_cache_stats.argtypes = [C.POINTER(pask_policy), C.POINTER(pask_cache), C.c_int32,
@@ -197,6 +201,17 @@ def pask_decode_attn(policy: pask_policy, cache: pask_cache, layer: int, batch: 
                                  float(softmax_scale),
                                  int(max_ctx_hint), _ptr(ws), int(ws_bytes), _ptr(stream)),
            "pask_decode_attn")
+
+
+def pask_decode_attn_noalloc(policy: pask_policy, cache: pask_cache, layer: int, batch: int, q, out, lse=None,
+                             tags_new=None, k_new=None, v_new=None, softmax_scale: float = 1.0,
+                             max_ctx_hint: int = 0, stream=0, states_new=None) -> None:
+    """pask_decode_attn with the library's own device scratch in place of a
+    caller workspace (no allocation in the call)."""
+    _check(_lib.pask_decode_attn_noalloc(C.byref(policy), C.byref(cache), int(layer), int(batch), _ptr(q), _ptr(out),
+                                         _ptr(lse), _ptr(tags_new), _ptr(states_new), _ptr(k_new), _ptr(v_new),
+                                         float(softmax_scale), int(max_ctx_hint), _ptr(stream)),
+           "pask_decode_attn_noalloc")
 
 
 def pask_attn_distortion(ref: pask_cache, intervened: pask_cache, layer: int, batch: int, q, in_s, softmax_scale: float,

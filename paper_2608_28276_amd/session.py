@@ -67,6 +67,15 @@ class PaskSession:
         pask.pask_decode_attn(self.policy, self.cache, layer, b, q, out, lse, tags_new, k_new, v_new,
                               self.softmax_scale, hint, self.ws, self.ws_bytes, self.stream, states_new=states_new)
 
+    def decode_noalloc(self, layer: int, q, out, lse=None, tags_new=None, k_new=None, v_new=None,
+                       batch: int | None = None, max_ctx_hint: int | None = None, states_new=None):
+        """decode() through pask_decode_attn_noalloc: no workspace argument,
+        the partials go to the library's own device scratch."""
+        b = batch or q.shape[0]
+        hint = max_ctx_hint or self.max_ctx_hint
+        pask.pask_decode_attn_noalloc(self.policy, self.cache, layer, b, q, out, lse, tags_new, k_new, v_new,
+                                      self.softmax_scale, hint, self.stream, states_new=states_new)
+
     def budgets(self):
         """Remaining budget R of every (sequence, layer), int64 [max_batch, n_layers]."""
         c = self.counters()

@@ -22,7 +22,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     lib = pask.library()
     for n in names:
         assert hasattr(lib, n), n
@@ -337,6 +337,31 @@ def test_append_and_attn_validation_before_any_hip_call():
     with pytest.raises(pask.PaskError) as e:
         pask.pask_kv_append(other, c, 0, 1, None, 4, A, A, A, 0, 0)
     assert e.value.status == pask.PASK_E_SHAPE
+
+
+def test_noalloc_attn_validation_before_any_hip_call():
+    """pask_decode_attn_noalloc: the checks of pask_decode_attn, and a batch
+    whose partials cannot fit the library's scratch even at two pieces per
+    (sequence, KV head) (505 sequences x 8 KV heads at group 8, head_dim 128)."""
+    A = 1 << 41
+    g = geom()
+    p = pask.pask_policy_load(blob_for()[1], g)
+    c = _fake_cache(g)
+    for over, code in [(dict(q=A + 8), pask.PASK_E_ARG), (dict(out=0), pask.PASK_E_ARG),
+                       (dict(scale=float("nan")), pask.PASK_E_ARG), (dict(layer=2), pask.PASK_E_SHAPE),
+                       (dict(batch=5), pask.PASK_E_SHAPE), (dict(tags=A, k=0), pask.PASK_E_ARG)]:
+        kw = dict(layer=0, batch=1, q=A, out=A, tags=None, k=None, scale=0.125)
+        kw.update(over)
+        with pytest.raises(pask.PaskError) as e:
+            pask.pask_decode_attn_noalloc(p, c, kw["layer"], kw["batch"], kw["q"], kw["out"], None, kw["tags"],
+                                          kw["k"], kw["k"], kw["scale"], 512, 0)
+        assert e.value.status == code, over
+    gb = geom(max_batch=600, n_q_heads=64, n_kv_heads=8, head_dim=128, max_tokens_per_seq=64)
+    pb = pask.pask_policy_load(blob_for()[1], gb)
+    cb = _fake_cache(gb)
+    with pytest.raises(pask.PaskError) as e:
+        pask.pask_decode_attn_noalloc(pb, cb, 0, 505, A, A, None, None, None, None, 0.125, 64, 0)
+    assert e.value.status == pask.PASK_E_CAPACITY
 
 
 def test_status_strings():
