@@ -147,7 +147,11 @@ def plan_pool_pages(cfg, P, tags, pol, ptags, online: bool):
     return hi + L * B, lo + L * B                                            # + one spare page per store
 
 
-def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=None, ptags=None):
+def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, ptags=None):
+    """Times the decode step at each position t of `positions` (generated
+    tokens persisted before the first warm-up step; ascending): the tokens up
+    to t are bulk-appended untimed, then `warmup` steps, then `steps` timed
+    steps.  Returns one result per position."""
     import torch
 
     from paper_2608_28276_amd import pask
@@ -157,7 +161,9 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
     dev = torch.device("cuda:0")
     B, L, Hq, Hkv, D = cfg.batch, cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     T = cfg.gen_tokens
-    assert t_start + warmup + steps <= T, "not enough generated tokens for the requested steps"
+    positions = sorted(positions)
+    assert positions[0] >= 0 and positions[-1] + warmup + steps <= T, "not enough generated tokens for the steps"
+    assert all(b >= a + warmup + steps for a, b in zip(positions, positions[1:])), "timed ranges overlap"
     hi_pages, lo_pages = plan_pool_pages(cfg, P, tags, pol, ptags, online=states is not None)
     max_tok = int(P.max()) + T
     sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=cfg.n_layers, n_q_heads=Hq, n_kv_heads=Hkv,
@@ -187,14 +193,8 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
         fill_ev[layer][1].record(sptr)
         after_prompt.append(sess.counters()[:B, layer, :2].clone())
         del k, v
-        if t_start:
-            k = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-            v = torch.randn((B, t_start, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
-            sess.append(layer, tags_dev[:, :t_start].contiguous(), k, v,
-                        states=None if states is None else states_dev[:, :t_start].contiguous())
-            del k, v
     torch.cuda.synchronize()
-    log(f"prompt + {t_start} generated tokens persisted in {time.time() - t0:.1f} s")
+    log(f"prompts persisted in {time.time() - t0:.1f} s")
     # The prompt's bulk append per layer (plan + pack kernels): algorithmic bytes = K / V read
     # (bf16), tags read, the stored forms and index-list entries written.
     mH = 2 * Hkv * D * 2
@@ -244,49 +244,99 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, states=Non
             if events is not None:
                 events[layer][1].record(sptr)
 
-    for i in range(warmup):
-        step(t_start + i)
-    torch.cuda.synchronize()
-    cnt0 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
-    events = [[[HipEvent(), HipEvent()] for _ in range(L)] for _ in range(steps)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for i in range(steps):
-        step(t_start + warmup + i, events[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    cnt1 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
-    call_ms = np.array([[e[0].elapsed_ms(e[1]) for e in ev] for ev in events])   # [steps, L]
-    st, status, _ = sess.stats(batch=B)
-    if status != 0:
-        raise RuntimeError(f"device flags set: {st.device_flags:#x}")
-
-    # Algorithmic bytes of one attention launch, averaged over the timed ones:
-    # every persisted entry read once (counts grow linearly over the region,
-    # each launch sees its step's token), q read, o written.  The one-token
-    # append adds the step's token in its stored form and one list entry.
     W = int(pol.recent_window)
     kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL + np.minimum(c[..., 2], W) * mH   # stores + window
-    read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)          # per layer, summed over seqs
-    qo = 2 * 2 * B * Hq * D
-    attn_bytes = read + qo                                                 # [L]
-    new_tok = (kv_bytes(cnt1) - kv_bytes(cnt0)).sum(axis=0) / steps      # per layer per step
-    stored = ((cnt1[..., 0] + cnt1[..., 1]) - (cnt0[..., 0] + cnt0[..., 1])).sum(axis=0) / steps
-    if W:                                        # the token entering the window and the one leaving it
-        new_tok = new_tok + 2 * B * mH
-    append_bytes = new_tok + 4 * stored + 2 * B * Hkv * D * 2             # stored form + lists + k/v read
-    bytes_per_step = float((attn_bytes + append_bytes).sum())
-    avg_attn_s = float(call_ms.mean()) / 1e3
-    achieved = float(attn_bytes.mean()) / avg_attn_s / 1e9
-    tokens_per_s = B * steps / wall
-    res = dict(
-        tokens_per_s=tokens_per_s, ms_per_step=wall / steps * 1e3, achieved=achieved,
-        avg_call_us=avg_attn_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(attn_bytes.mean()),
-        c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
-        step_gbs=bytes_per_step / (wall / steps) / 1e9,
-        mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()), prompt_append=prompt_append,
-    )
-    return res
+    results = []
+    t = 0                                                # generated tokens persisted so far
+    for pos in positions:
+        if pos > t:                                      # untimed bulk append of tokens t..pos-1
+            for layer in range(L):
+                k = torch.randn((B, pos - t, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+                v = torch.randn((B, pos - t, Hkv, D), generator=g, device=dev, dtype=torch.bfloat16)
+                sess.append(layer, tags_dev[:, t:pos].contiguous(), k, v,
+                            states=None if states is None else states_dev[:, t:pos].contiguous())
+                del k, v
+            t = pos
+        for i in range(warmup):
+            step(t + i)
+        torch.cuda.synchronize()
+        cnt0 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
+        events = [[[HipEvent(), HipEvent()] for _ in range(L)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for i in range(steps):
+            step(t + warmup + i, events[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        t += warmup + steps
+        cnt1 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
+        call_ms = np.array([[e[0].elapsed_ms(e[1]) for e in ev] for ev in events])   # [steps, L]
+        st, status, _ = sess.stats(batch=B)
+        if status != 0:
+            raise RuntimeError(f"device flags set: {st.device_flags:#x}")
+
+        # Algorithmic bytes of one attention launch, averaged over the timed ones:
+        # every persisted entry read once (counts grow linearly over the region,
+        # each launch sees its step's token), q read, o written.  The one-token
+        # append adds the step's token in its stored form and one list entry.
+        read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)      # per layer, summed over seqs
+        qo = 2 * 2 * B * Hq * D
+        attn_bytes = read + qo                                             # [L]
+        new_tok = (kv_bytes(cnt1) - kv_bytes(cnt0)).sum(axis=0) / steps  # per layer per step
+        stored = ((cnt1[..., 0] + cnt1[..., 1]) - (cnt0[..., 0] + cnt0[..., 1])).sum(axis=0) / steps
+        if W:                                    # the token entering the window and the one leaving it
+            new_tok = new_tok + 2 * B * mH
+        append_bytes = new_tok + 4 * stored + 2 * B * Hkv * D * 2         # stored form + lists + k/v read
+        bytes_per_step = float((attn_bytes + append_bytes).sum())
+        avg_attn_s = float(call_ms.mean()) / 1e3
+        achieved = float(attn_bytes.mean()) / avg_attn_s / 1e9
+        res = dict(
+            t=pos, tokens_per_s=B * steps / wall, ms_per_step=wall / steps * 1e3, achieved=achieved,
+            avg_call_us=avg_attn_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(attn_bytes.mean()),
+            c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
+            step_gbs=bytes_per_step / (wall / steps) / 1e9,
+            mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()), prompt_append=prompt_append,
+        )
+        log(f"t={pos}: {res['tokens_per_s']:.0f} tokens/s, call {res['avg_call_us']:.1f} us, "
+            f"{achieved:.0f} GB/s algorithmic")
+        results.append(res)
+    return results
+
+
+def probe_leg(read_gib: float = 4.0, copy_gib: float = 2.0, reps: int = 5):
+    """On-device ceilings measured on the same box in the same run: the
+    streaming read and copy probes (paper_2608_28276_amd/csrc/probe.hip),
+    HIP events around `reps` back-to-back launches after a warm-up."""
+    import ctypes as C
+
+    import torch
+    lib = C.CDLL(os.path.join(ROOT, "paper_2608_28276_amd", "libpask_probe.so"))
+    lib.pask_probe_read.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int, C.c_void_p]
+    lib.pask_probe_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+    dev = torch.device("cuda:0")
+    sptr = torch.cuda.current_stream(dev).cuda_stream
+    nr, nc = int(read_gib * 2**30), int(copy_gib * 2**30)
+    x = torch.empty(nr, dtype=torch.uint8, device=dev).fill_(3)
+    outw = torch.empty(65536, dtype=torch.int32, device=dev)
+    y = torch.empty(nc, dtype=torch.uint8, device=dev)
+
+    def timed(fn):
+        if fn() != 0:
+            raise RuntimeError("probe launch failed")
+        e0, e1 = HipEvent(), HipEvent()
+        e0.record(sptr)
+        for _ in range(reps):
+            if fn() != 0:
+                raise RuntimeError("probe launch failed")
+        e1.record(sptr)
+        torch.cuda.synchronize()
+        return e0.elapsed_ms(e1) / 1e3 / reps
+
+    rd = timed(lambda: lib.pask_probe_read(x.data_ptr(), nr, outw.data_ptr(), 0, sptr))
+    cp = timed(lambda: lib.pask_probe_copy(x.data_ptr(), y.data_ptr(), nc, 0, sptr))
+    del x, y
+    return dict(read_gbs=round(nr / rd / 1e9, 1), copy_gbs=round(2 * nc / cp / 1e9, 1),
+                read_bytes=nr, copy_bytes=nc)
 
 
 def distortion_leg(cfg, P, tags, pol, steps: int, warmup: int, t_start: int, bucket):
@@ -431,18 +481,36 @@ def cpu_leg(cfg, P, tags, pol, t_start: int, n_seq: int, states=None, ptags=None
     kn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_k", 0))
     vn = bf16_normal((L, Hkv, D), sub_seed(cfg.seed, "gen_v", 0))
     scale = float(np.float32(1.0 / math.sqrt(D)))
-    info = threadpoolctl.threadpool_info()
-    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
-    t0 = time.perf_counter()
-    for b in seqs:
-        for layer in range(L):
-            oc.append(layer, b, tags[b, t_start:t_start + 1], bits(kn[layer][None]), bits(vn[layer][None]),
-                      states=st_of(b, t_start, t_start + 1))
-            oc.attend(layer, b, bits(q[layer]), scale)
-    el = time.perf_counter() - t0
-    return dict(value=len(seqs) / el, unit="tokens/s", cores=int(threads), kind="oracle",
+    # The oracle is a per-head loop of small products: timed with its BLAS pool
+    # held to one thread, it runs on one core (torch's own pool too).
+    torch_threads = torch.get_num_threads()
+    torch.set_num_threads(1)
+    try:
+        with threadpoolctl.threadpool_limits(1):
+            t0 = time.perf_counter()
+            for b in seqs:
+                for layer in range(L):
+                    oc.append(layer, b, tags[b, t_start:t_start + 1], bits(kn[layer][None]), bits(vn[layer][None]),
+                              states=st_of(b, t_start, t_start + 1))
+                    oc.attend(layer, b, bits(q[layer]), scale)
+            el = time.perf_counter() - t0
+    finally:
+        torch.set_num_threads(torch_threads)
+    return dict(value=len(seqs) / el, unit="tokens/s", cores=1, kind="oracle",
                 sample=f"{len(seqs)} sequences (prompts {', '.join(str(int(P[b])) for b in seqs)} + {t_start} "
-                       f"generated tokens) x 1 decode step x {L} layers, fp64 numpy, {el:.1f} s")
+                       f"generated tokens) x 1 decode step x {L} layers, fp64 numpy on one thread, {el:.1f} s",
+                threads=1, nproc=os.cpu_count(), cpu_model=cpu_model())
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def kernel_source_digest() -> str:
@@ -529,7 +597,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2, help="workload index (default: the B=64 serving batch)")
     ap.add_argument("--t-start", type=int, default=None,
-                    help="generated tokens persisted before timing (default: min(512, half the generation))")
+                    help="time only this decode position: generated tokens persisted before the warm-up "
+                         "(default: three positions, 0, min(512, half the generation) and the last steps; "
+                         "the line's value is the middle one)")
     ap.add_argument("--budget", type=float, default=None,
                     help="KV budget of the policy table (default: the workload's; 0.33 for the budget sweep)")
     ap.add_argument("--cpu-seqs", type=int, default=3, help="sequences in the oracle's timed sample")
@@ -541,6 +611,7 @@ def main():
     ap.add_argument("--distortion", type=str, default=None, metavar="TAG,GROUP,ACTION",
                     help="measure the attention-output distortion (Eq. 4) of one bucket instead "
                          "(ACTION 0 = DROP, 1 = RETAIN-LOW)")
+    ap.add_argument("--no-probe", action="store_true", help="skip the on-device read / copy probes")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -557,6 +628,9 @@ def main():
     t_default = min(512, cfg0.gen_tokens // 2)
     if args.t_start is None:
         args.t_start = t_default
+        positions = sorted({0, t_default, cfg0.gen_tokens - args.warmup - args.steps})
+    else:
+        positions = [args.t_start]
     cfg, P, tags, pol, ptags = build_workload(args.config, beta)
     pol.recent_window = args.window
     workload = (cfg.name + (f"_beta{beta:g}" if len(cfg.budgets) > 1 or beta not in cfg.budgets else "") +
@@ -590,9 +664,13 @@ def main():
                          "bytes_per_launch": round(d["call_bytes"]), "avg_launch_us": round(d["avg_call_us"], 2)},
             "cpu_baseline": None}), flush=True)
         return
-    g = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, args.t_start, states, ptags)
+    runs = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, positions, states, ptags)
+    g = next(r for r in runs if r["t"] == args.t_start)
     log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
         f"{g['achieved']:.0f} GB/s algorithmic")
+    probe = None if args.no_probe else probe_leg()
+    if probe:
+        log(f"probes: read {probe['read_gbs']} GB/s, copy {probe['copy_gbs']} GB/s")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_leg(cfg, P, tags, pol, args.t_start, args.cpu_seqs, states, ptags)
@@ -629,7 +707,14 @@ def main():
             "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(workload),
             "kernel": attn_kernels(cfg) + " (one pask_decode_attn call)",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
+            "read_probe_gbs": probe["read_gbs"] if probe else None,
+            "frac_of_read_probe": round(g["achieved"] / probe["read_gbs"], 4) if probe else None,
+            "copy_probe_gbs": probe["copy_gbs"] if probe else None,
         },
+        "positions": [dict(t=r["t"], tokens_per_s=round(r["tokens_per_s"], 1), ms_per_step=round(r["ms_per_step"], 4),
+                           avg_call_us=round(r["avg_call_us"], 2), bytes_per_call=round(r["per_call_bytes"]),
+                           achieved_gbs=round(r["achieved"], 1), frac=round(r["achieved"] / HBM_PEAK_GBS, 4))
+                      for r in runs],
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -23,6 +23,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpask.so")
 KERNEL_SOURCES = ("pask_append.hip", "pask_attn.hip")   # persisting entries; reading them
+# The benchmark's on-device bandwidth probes: a library of their own, outside the C ABI.
+PROBE_LIB = os.path.join(PKG, "libpask_probe.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -51,8 +53,11 @@ def build(verbose: bool = False) -> str:
         tmp_lib = os.path.join(tmp, "libpask.so")
         _run([HIPCC, *DEVICE, "-shared", "-fPIC", *objs, "-o", tmp_lib])
         shutil.move(tmp_lib, LIB)
+        tmp_probe = os.path.join(tmp, "libpask_probe.so")
+        _run([HIPCC, *COMMON, *DEVICE, "-shared", os.path.join(CSRC, "probe.hip"), "-o", tmp_probe])
+        shutil.move(tmp_probe, PROBE_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 
