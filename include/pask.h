@@ -290,7 +290,9 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
 
 /* Workspace bytes pask_decode_attn needs for `batch` sequences when no
  * sequence holds more than max_ctx_hint persisted entries (a larger count is
- * still correct, only less parallel): batch * n_kv_heads * S partial blocks
+ * still correct, only less parallel; a hint below 1 or above
+ * max_tokens_per_seq counts as max_tokens_per_seq; 0 for an invalid geometry
+ * or batch outside 1..max_batch): batch * n_kv_heads * S partial blocks
  * of max(G, 4) * (head_dim + 2) fp32, S = ceil(hint / 128) + 2, or for
  * batch * n_kv_heads <= 64 the larger of that and min(ceil(hint / 16) + 2,
  * 4096 / (batch * n_kv_heads)). */

@@ -472,8 +472,9 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
 }
 
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint) {
-  if (!valid_geom(geom) || batch < 1) return 0;
-  if (max_ctx_hint < 1) max_ctx_hint = geom->max_tokens_per_seq;
+  if (!valid_geom(geom) || batch < 1 || batch > geom->max_batch) return 0;
+  // no sequence holds more than max_tokens_per_seq entries: a larger hint sizes nothing more
+  if (max_ctx_hint < 1 || max_ctx_hint > geom->max_tokens_per_seq) max_ctx_hint = geom->max_tokens_per_seq;
   return (size_t)ws_layout(geom, batch, splits_for(max_ctx_hint, (int64_t)batch * geom->n_kv_heads)).total;
 }
 

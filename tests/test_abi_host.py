@@ -220,6 +220,8 @@ def _ws_want(g, batch, hint):
     # one page while the call holds at most 4096 partials: max(that, min(ceil(hint / 16) + 2,
     # 4096 // segments)).  Per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
     # o: blocks*G4*D*4, ml: blocks*G4*2*4 (each 256-aligned)
+    # a hint above max_tokens_per_seq counts as max_tokens_per_seq
+    hint = min(hint, g.max_tokens_per_seq)
     segs = batch * g.n_kv_heads
     splits = -(-hint // 128) + 2
     if segs <= 64:
@@ -234,6 +236,17 @@ def _ws_want(g, batch, hint):
 def test_workspace_bytes(batch, hint):
     g = geom(max_batch=64)
     assert pask.pask_workspace_bytes(g, batch, hint) == _ws_want(g, batch, hint)
+    g = geom(max_batch=64, max_tokens_per_seq=200000)
+    assert pask.pask_workspace_bytes(g, batch, hint) == _ws_want(g, batch, hint)
+
+
+def test_workspace_bytes_hint_and_batch_edges():
+    """A hint at the int32 limit sizes as max_tokens_per_seq (no overflow); a
+    batch outside 1..max_batch gets 0."""
+    g = geom(max_batch=64)
+    top = pask.pask_workspace_bytes(g, 64, g.max_tokens_per_seq)
+    assert pask.pask_workspace_bytes(g, 64, 2**31 - 1) == top == pask.pask_workspace_bytes(g, 64, 0)
+    assert pask.pask_workspace_bytes(g, 65, 512) == 0 and pask.pask_workspace_bytes(g, 0, 512) == 0
 
 
 def test_distortion_validation_before_any_hip_call():
