@@ -152,7 +152,7 @@ typedef struct pask_cache_layout {
                                 store 0 = HIGH, 1 = LOW                            */
   uint64_t index_list_off;   /* i32 [max_batch][n_layers][2][max_tokens_per_seq]:
                                 position of each slot of each store               */
-  uint64_t staging_off;      /* i32 [max_batch][max_tokens_per_seq]: append plan   */
+  uint64_t staging_off;      /* i32 [max_batch][staging_stride]: append plan       */
   uint64_t budget_off;       /* the online controller's tables (pask_budget_init)  */
   uint64_t ring_act_off;     /* u8 [max_batch][n_layers][W]: decided action | forced
                                 << 2 of the token in each recent-window slot       */
@@ -183,7 +183,8 @@ typedef struct pask_cache_layout {
   int32_t max_pages;         /* ceil(max_tokens_per_seq / 16)                      */
   int32_t counter_stride;    /* 8                                                  */
   int32_t ring_pages;        /* max_batch * n_layers * ceil(W / 16)                */
-  int32_t staging_stride;    /* i32 per sequence in the staging region             */
+  int32_t staging_stride;    /* i32 per sequence in the staging region:
+                                max_tokens_per_seq + recent_window + 4             */
 } pask_cache_layout;
 
 /* Accounting of what a cache holds (Eq. 1).  Entry = one (token, layer). */

@@ -50,7 +50,7 @@ bool layout_of(const pask_geom* g, pask_cache_layout* L) {
   L->max_pages = (int32_t)((T + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS);
   L->counter_stride = pask::kCounterStride;
   L->ring_pages = (int32_t)(B * NL * ((W + PASK_PAGE_TOKENS - 1) / PASK_PAGE_TOKENS));
-  L->staging_stride = (int32_t)(T + W + 2);
+  L->staging_stride = (int32_t)(T + W + 4);
   L->hi_page_bytes = H * 2 * PASK_PAGE_TOKENS * D * 2;
   L->lo_page_bytes = H * 2 * (PASK_PAGE_TOKENS * (D / 2) + PASK_PAGE_TOKENS * (D / PASK_QGROUP) * 2);
   uint64_t off = 0;

@@ -26,7 +26,7 @@
 namespace pask {
 namespace {
 
-constexpr int kPackTokens = 16;   // tokens per append_pack block
+constexpr int kPackTokens = 16;   // tokens per block of the recent-window pack and fill kernels
 
 // ---------------------------------------------------------------------------
 // reset
@@ -219,6 +219,11 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
   int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
   int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  if (threadIdx.x == 0) {                          // for the pack kernel: stores and position before the call
+    stg[cv.staging_stride - 4] = nst[0];
+    stg[cv.staging_stride - 3] = nst[1];
+    stg[cv.staging_stride - 2] = pos0;
+  }
   const bool keep_all = (a.flags & kKeepAll) != 0u;
   const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
   __syncthreads();
@@ -321,52 +326,34 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
 // RETAIN-HIGH copy and RETAIN-LOW quantise-and-pack of one token
 // ---------------------------------------------------------------------------
 
+// The scale of a RETAIN-LOW group from its absmax: s = fp16(absmax / 7) with
+// a correctly rounded fp32 division, saturated at 65504, rounded to nearest
+// even; returns its fp16 bits and s as fp32.
+__device__ __forceinline__ uint16_t quant_scale(float absmax, float& s) {
+  const _Float16 h = (_Float16)fminf(absmax / 7.0f, 65504.0f);
+  s = (float)h;
+  return __builtin_bit_cast(uint16_t, h);
+}
+// The code of x under scale s: clamp(rint(x / s), -7, 7), 0 when s == 0.
+__device__ __forceinline__ int quant_code(float x, float s) {
+  return s != 0.0f ? (int)fminf(fmaxf(rintf(x / s), -7.0f), 7.0f) : 0;
+}
+
 // Quantise 4 consecutive elements of a 32-element group held by 8 adjacent
-// lanes: s = fp16(absmax / 7) (correctly rounded division, saturated at 65504,
-// round-to-nearest-even conversion), q = clamp(rint(x / s), -7, 7).  Returns
-// the 4 codes as offset-binary nibbles q + 8 (element i in bits 4i..4i+3; the
-// pages hold codes in this form) and the scale bits.
+// lanes (quant_scale of the group's absmax, quant_code of each element).
+// Returns the 4 codes as offset-binary nibbles q + 8 (element i in bits
+// 4i..4i+3; the pages hold codes in this form) and the scale bits.
 __device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& packed, uint32_t& sbits) {
   float f[4] = {bf16_lo(x01), bf16_hi(x01), bf16_lo(x23), bf16_hi(x23)};
   float am = fmaxf(fmaxf(fabsf(f[0]), fabsf(f[1])), fmaxf(fabsf(f[2]), fabsf(f[3])));
   am = fmaxf(am, __shfl_xor(am, 1, 8));
   am = fmaxf(am, __shfl_xor(am, 2, 8));
   am = fmaxf(am, __shfl_xor(am, 4, 8));
-  const float s32 = fminf(am / 7.0f, 65504.0f);
-  const _Float16 h = (_Float16)s32;
-  const float s = (float)h;
-  sbits = (uint32_t)__builtin_bit_cast(uint16_t, h);
+  float s;
+  sbits = quant_scale(am, s);
   uint32_t p = 0u;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int q = 0;
-    if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
-    p |= (uint32_t)(q + 8) << (4 * i);
-  }
-  packed = p;
-}
-
-// The same rule for 8 consecutive elements of a group held by 4 adjacent
-// lanes (element i of x in bits 4i..4i+3 of `packed`, offset binary).
-__device__ __forceinline__ void quant8(const uint4& x, uint32_t& packed, uint32_t& sbits) {
-  const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
-                      bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
-  float am = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) am = fmaxf(am, fabsf(f[i]));
-  am = fmaxf(am, __shfl_xor(am, 1, 4));
-  am = fmaxf(am, __shfl_xor(am, 2, 4));
-  const float s32 = fminf(am / 7.0f, 65504.0f);
-  const _Float16 h = (_Float16)s32;
-  const float s = (float)h;
-  sbits = (uint32_t)__builtin_bit_cast(uint16_t, h);
-  uint32_t p = 0u;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    int q = 0;
-    if (s != 0.0f) q = (int)fminf(fmaxf(rintf(f[i] / s), -7.0f), 7.0f);
-    p |= (uint32_t)(q + 8) << (4 * i);
-  }
+  for (int i = 0; i < 4; ++i) p |= (uint32_t)(quant_code(f[i], s) + 8) << (4 * i);
   packed = p;
 }
 
@@ -445,163 +432,253 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
   }
 }
 
-// Bulk persist of kPackTokens tokens of sequence blockIdx.y, after the plan
-// kernel has slotted them (staging code = store << 30 | slot, or -1).
-//   1. One thread per token reads its code and page id; thread 0 marks the
-//      runs of 4 tokens that fill a whole slot group (4 consecutive slots of
-//      one store, the first a multiple of 4).
-//   2. Every thread loads its 16-byte chunk of every token's K / V row (chunk
-//      k: K when k < Hkv*D/8, else V; head, then 8-dim piece), all in flight
-//      together (non-temporal: read once).
-//   3. K chunks (bf16, or int4 quantised by groups of 4 adjacent lanes with
-//      quant8) and scales go to the pages directly.  V tiles interleave the 4
-//      slots of a group at 2-byte (bf16) or 1-byte (int4 codes) granularity:
-//      for a whole group the lane holding a V chunk holds it for all 4 tokens
-//      and writes 8-byte (bf16) or 4-byte (codes) pieces; other tokens' V goes
-//      element by element.
+// Bulk persist by destination page, after the plan kernel has slotted the
+// call's tokens: block (k, store, b) fills page k of the pages of sequence b's
+// store that this call's slots reach (slots n0..n1-1 of the store, n0 saved by
+// the plan kernel, n1 the store's count after it).  Each slot's source token
+// comes from the index list (position - p0), so every page is written whole
+// by one block, in the operand order of the attention kernel, with 16-byte
+// stores of consecutive addresses (1 KiB per wave and instruction).
+//   1. Every thread issues its loads at once (non-temporal: read once): the
+//      page's V rows (16 slots x Hkv x D bf16) in row order, and its K chunks
+//      (HIGH: one 16-byte chunk per page-order chunk; LOW: per KV head, the
+//      four 8-element chunks of a 32-element group of a slot, one lane each).
+//   2. V rows go to LDS ([slot][Hkv][D], rows padded by 16 bytes).
+//   3. HIGH: K chunks are stored as loaded; V chunks (4 slots x 2 dims x 8
+//      elements each) are gathered from LDS.  LOW: K groups are quantised in
+//      registers (absmax over the group's 4 lanes); V groups are gathered from
+//      LDS by 16 lanes (dims 32i + e and 32i + 16 + e) and quantised.
+// Slots of the page before n0 hold earlier entries and are left as they are
+// (a V piece that mixes them with new slots is written element by element);
+// slots from n1 on are not yet in use and may be written.
+constexpr int kPackThreads = 256;
+constexpr int kLdsRowPad = 16;                     // bytes after each staged V row (bank spread)
+
 template <int D>
-__global__ __launch_bounds__(256) void append_pack_kernel(AppendArgs a) {
+__global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendArgs a) {
   using PL = PageLayout<D>;
-  constexpr int kC = D / 8;                        // 16-byte chunks per head row
-  __shared__ int s_code[kPackTokens], s_page[kPackTokens];
-  __shared__ uint32_t s_runs;                      // bit jj: tokens jj..jj+3 fill a slot group
+  constexpr int NG = PL::NG;
+  constexpr int kRowChunks = D / 8;                // 16-byte chunks per head row
+  constexpr int kMaxChunks = kPage * 8 * kRowChunks;   // a page's K (or V) chunks at Hkv 8
+  constexpr int kIt = kMaxChunks / kPackThreads;
+  constexpr int kLdsRow = 8 * D * 2 + kLdsRowPad;
+  __shared__ __align__(16) uint8_t s_v[kPage * kLdsRow];
+  __shared__ int s_src[kPage];                     // token of each slot in this call, or -1
   const CacheView& cv = a.cv;
-  const int b = blockIdx.y;
+  const int b = blockIdx.z, st = blockIdx.y;
   const int H = cv.n_kv_heads;
-  uint32_t unused = 0;
-  const int n = clamp_n_new(a, b, unused);
-  const int j0 = (int)blockIdx.x * kPackTokens;
-  if (j0 >= n) return;                             // the whole block
-  const int nt = min(kPackTokens, n - j0);
-  if (threadIdx.x < kPackTokens) {
-    const int j = j0 + (int)threadIdx.x;
-    int code = -1, page = 0;
-    if (j < n) {
-      code = cv.staging[(size_t)b * cv.staging_stride + j];
-      if (code >= 0) page = block_table_of(cv, b, a.layer, code >> 30)[(code & 0x3FFFFFFF) / kPage];
+  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  const int n0 = stg[cv.staging_stride - 4 + st];
+  const int p0 = stg[cv.staging_stride - 2];
+  const int n1 = counters_of(cv, b, a.layer)[st];
+  const int pidx = n0 / kPage + (int)blockIdx.x;
+  const int tl0 = max(n0 - pidx * kPage, 0);       // first new slot of the page
+  const int th0 = min(n1 - pidx * kPage, kPage);   // past the last new slot
+  if (tl0 >= th0) return;                          // block-uniform: no new slot here
+  const int page = block_table_of(cv, b, a.layer, st)[pidx];
+  if (threadIdx.x < kPage) {
+    const int t = (int)threadIdx.x;
+    int j = -1;
+    if (t >= tl0 && t < th0) {
+      j = index_list_of(cv, b, a.layer, st)[pidx * kPage + t] - p0;
+      if (j < 0 || j >= a.max_new) j = -1;         // never outside the call's rows
     }
-    s_code[threadIdx.x] = code;
-    s_page[threadIdx.x] = page;
+    s_src[t] = j;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t runs = 0u;
-    for (int jj = 0; jj + 4 <= nt;) {
-      const int c0 = s_code[jj];
-      bool full = c0 >= 0 && (c0 & 3) == 0;        // slot % 4 == 0 (the store bit is above)
-      for (int r = 1; full && r < 4; ++r) full = s_code[jj + r] == c0 + r;
-      if (full) {
-        runs |= 1u << jj;
-        jj += 4;
-      } else {
-        ++jj;
+  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t row = (size_t)H * D;                // bf16 per K (or V) row of a token
+  const int n_chunks = kPage * H * kRowChunks;     // the page's V chunks (as many K chunks)
+  const uint16_t* vbase = a.v + (size_t)b * a.max_new * row;
+  const uint16_t* kbase = a.k + (size_t)b * a.max_new * row;
+  const bool is_hi = st == kHi;
+  // 1. loads
+  uint4 vx[kIt], kx[kIt];
+#pragma unroll
+  for (int it = 0; it < kIt; ++it) {
+    const int e = it * kPackThreads + tid;
+    vx[it] = make_uint4(0u, 0u, 0u, 0u);
+    kx[it] = make_uint4(0u, 0u, 0u, 0u);
+    if (e < n_chunks) {
+      const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+      const int j = s_src[t];
+      if (j >= 0) vx[it] = stream_load16(reinterpret_cast<const uint8_t*>(vbase + (size_t)j * row + col * 8));
+    }
+  }
+  if (is_hi) {
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+      const int e = it * kPackThreads + tid;       // page order: (g, i) = e / 64, q = lane / 16, t = lane % 16
+      if (e < n_chunks) {
+        const int gi = e >> 6, q = (e >> 4) & 3, t = e & 15;
+        const int g = gi / NG, i = gi % NG;
+        const int j = s_src[t];
+        if (j >= 0)
+          kx[it] = stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + g * D + (4 * i + q) * 8));
       }
     }
-    s_runs = runs;
+  } else {
+    // LOW K: wave w takes KV heads w, w + 4; lane (q, t) loads dims 32i + 8q..+8 of slot t
+    const int q = lane >> 4, t = lane & 15, j = s_src[t];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int g = wave + 4 * h2;
+#pragma unroll
+      for (int i = 0; i < NG; ++i)
+        if (g < H && j >= 0)
+          kx[h2 * NG + i] =
+              stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + g * D + (4 * i + q) * 8));
+    }
+  }
+  // 2. V rows into LDS
+#pragma unroll
+  for (int it = 0; it < kIt; ++it) {
+    const int e = it * kPackThreads + tid;
+    if (e < n_chunks) {
+      const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+      *reinterpret_cast<uint4*>(s_v + t * kLdsRow + col * 16) = vx[it];
+    }
   }
   __syncthreads();
-  const uint32_t runs = s_runs;
-  uint32_t covered = 0u;                           // tokens written by a whole-group piece
+  auto v_at = [&](int t, int g, int d) -> uint32_t {   // bf16 bits of V[t][g][d]
+    return *reinterpret_cast<const uint16_t*>(s_v + t * kLdsRow + (g * D + d) * 2);
+  };
+  if (is_hi) {
+    uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
+    // K chunks as loaded: chunk (g, i, q, t) at (i*64 + q*16 + t) * 16 of head slot (g + page) % H
 #pragma unroll
-  for (int jj = 0; jj < kPackTokens; ++jj)
-    if (runs >> jj & 1u) covered |= 0xFu << jj;
-  const size_t row = (size_t)H * D;
-  const int n_chunks = 2 * H * kC;                 // K and V chunks of one token (<= 256)
-  const int k = (int)threadIdx.x;
-  const bool active = k < n_chunks;                // whole 4-lane groups alike (H*kC is a multiple of 4)
-  const int kv = k / (H * kC), g = (k / kC) % H, c = k % kC;
-  const uint16_t* src = (kv ? a.v : a.k) + ((size_t)b * a.max_new + j0) * row + g * D + c * 8;
-  uint4 x[kPackTokens];
-  uint32_t packed[kPackTokens];                    // int4 codes of this lane's 8 elements, per LOW token
-#pragma unroll
-  for (int jj = 0; jj < kPackTokens; ++jj) {      // every token's chunk in flight together
-    x[jj] = active && jj < nt ? stream_load16(reinterpret_cast<const uint8_t*>(src + jj * row))
-                              : make_uint4(0u, 0u, 0u, 0u);
-    packed[jj] = 0u;
-  }
-  const int i = c / 4, q = c % 4;                  // int4: scale group i, dims 32i + 8q + 0..7
-#pragma unroll
-  for (int jj = 0; jj < kPackTokens; ++jj) {
-    const int code = s_code[jj];
-    if (jj >= nt || code < 0) continue;            // block-uniform
-    const int page = s_page[jj], t = (code & 0x3FFFFFFF) % kPage;
-    const bool grouped = covered >> jj & 1u;
-    if ((code >> 30) == kHi) {
-      if (!active) continue;
-      uint8_t* hb = cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % H) * PL::kHiHead;
-      if (kv == 0) {                               // dims 8c..8c+7 = 32i + 8q + 0..7
-        *reinterpret_cast<uint4*>(hb + ((c / 4) * 64 + (c % 4) * 16 + t) * 16) = x[jj];
-      } else if (!grouped) {                       // dims 16m + dd, dd = 8(c%2) + e
-        uint16_t* vt = reinterpret_cast<uint16_t*>(hb + PL::kHiV);
-        const int m = c / 2;
-        const uint32_t w[4] = {x[jj].x, x[jj].y, x[jj].z, x[jj].w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          vt[(((m >> 1) * 64 + (t / 4) * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4 + t % 4] =
-              (uint16_t)(w[e / 2] >> (16 * (e % 2)));
+    for (int it = 0; it < kIt; ++it) {
+      const int e = it * kPackThreads + tid;
+      if (e < n_chunks) {
+        const int gi = e >> 6, t = e & 15;
+        const int g = gi / NG, i = gi % NG;
+        if (s_src[t] >= 0)
+          *reinterpret_cast<uint4*>(pg + (size_t)((g + page) % H) * PL::kHiHead + (size_t)(i * 64 + (e & 63)) * 16) =
+              kx[it];
       }
-    } else {
-      uint32_t sbits = 0u;
-      quant8(x[jj], packed[jj], sbits);            // every lane: the shuffles need whole groups
-      const uint32_t partner = __shfl_xor(packed[jj], 2, 4);   // V: dims 16 higher (lanes q < 2)
-      if (!active) continue;
-      uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
-      if (kv == 0) {
-        *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * PL::NG + i) * 4) = k_word(packed[jj]);
-        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
-      } else {
-        // byte ((t/4*16 + dd)*(NM/2) + i)*4 + t%4 holds dims 32i + dd (low nibble) and
-        // 32i + 16 + dd (high nibble), dd = 8q + e for lanes q < 2
-        if (q < 2 && !grouped) {
+    }
+    // V chunk o = M*64 + T4*16 + e of a head: elements (slot 4*T4 + r, dim 16*(2M + h) + e), h-major
+    constexpr int kPerHead = 2 * D;                // 16-byte chunks of one head's V tile
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int dd = 8 * q + e;
-            hb[PL::kLoVC + (((t / 4) * 16 + dd) * (PL::NM / 2) + i) * 4 + t % 4] =
-                (uint8_t)(((packed[jj] >> (4 * e)) & 0xFu) | (((partner >> (4 * e)) & 0xFu) << 4));
-          }
+    for (int it = 0; it < kIt; ++it) {
+      const int c = it * kPackThreads + tid;
+      if (c < n_chunks) {
+        const int g = c / kPerHead, o = c % kPerHead;
+        const int M = o >> 6, T4 = (o >> 4) & 3, e = o & 15;
+        if (4 * T4 + 3 < tl0 || 4 * T4 >= th0) continue;   // no new slot in the group
+        uint32_t w[4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int r2 = 0; r2 < 2; ++r2)
+            w[2 * h + r2] = v_at(4 * T4 + 2 * r2, g, 16 * (2 * M + h) + e) |
+                            (v_at(4 * T4 + 2 * r2 + 1, g, 16 * (2 * M + h) + e) << 16);
+        uint8_t* dst = pg + (size_t)((g + page) % H) * PL::kHiHead + PL::kHiV + (size_t)o * 16;
+        if (4 * T4 >= tl0) {
+          *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else {                                   // the group holds earlier slots: new ones only
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (4 * T4 + r >= tl0 && 4 * T4 + r < th0)
+                reinterpret_cast<uint16_t*>(dst)[4 * h + r] = (uint16_t)(w[2 * h + r / 2] >> (16 * (r % 2)));
         }
-        if (q == 0) *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * PL::NG + i) * 2) = (uint16_t)sbits;
+      }
+    }
+    return;
+  }
+  uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
+  // LOW K: lane (q, t) of wave w quantises the chunks it loaded; the group's
+  // absmax is shared by the four lanes t, t + 16, t + 32, t + 48
+  {
+    const int q = lane >> 4, t = lane & 15;
+    const bool mine = s_src[t] >= 0;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int g = wave + 4 * h2;
+      if (g >= H) break;                           // wave-uniform
+      uint8_t* hb = pg + (size_t)((g + page) % H) * PL::kLoHead;
+      uint32_t words[NG];
+      uint16_t sc[NG];
+#pragma unroll
+      for (int i = 0; i < NG; ++i) {
+        const uint4 x = kx[h2 * NG + i];
+        const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
+                            bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
+        float am = 0.0f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) am = fmaxf(am, fabsf(f[u]));
+        am = fmaxf(am, __shfl_xor(am, 16));
+        am = fmaxf(am, __shfl_xor(am, 32));
+        float s;
+        sc[i] = quant_scale(am, s);
+        uint32_t packed = 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) packed |= (uint32_t)(quant_code(f[u], s) + 8) << (4 * u);
+        words[i] = k_word(packed);
+      }
+      if (mine) {
+        uint32_t* dst = reinterpret_cast<uint32_t*>(hb + (size_t)((q * 16 + t) * NG) * 4);
+        if constexpr (NG == 4) *reinterpret_cast<uint4*>(dst) = make_uint4(words[0], words[1], words[2], words[3]);
+        else *reinterpret_cast<uint2*>(dst) = make_uint2(words[0], words[1]);
+        if (q == 0) {
+          uint16_t* sd = reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (size_t)t * NG * 2);
+#pragma unroll
+          for (int i = 0; i < NG; ++i) sd[i] = sc[i];
+        }
       }
     }
   }
-  // Whole slot groups: tokens jj0..jj0+3 in slots 4u..4u+3 of one page.
+  // LOW V: lane (T4, e) of the wave holding KV head g quantises dims 32i + e
+  // and 32i + 16 + e of slots 4*T4 + r; a group's absmax over its 16 lanes
+  {
+    const int T4 = lane >> 4, e = lane & 15;
+    for (int g = wave; g < H; g += 4) {
+      uint8_t* hb = pg + (size_t)((g + page) % H) * PL::kLoHead;
+      uint32_t words[NG];
+      uint16_t sc[4][NG];
 #pragma unroll
-  for (int jj0 = 0; jj0 + 4 <= kPackTokens; ++jj0) {
-    if (!(runs >> jj0 & 1u)) continue;             // block-uniform
-    const int code = s_code[jj0], page = s_page[jj0], u = ((code & 0x3FFFFFFF) % kPage) / 4;
-    if ((code >> 30) == kHi) {
-      if (!active || kv == 0) continue;
-      // 8 bytes per (m, dd): the 4 slots' bf16 values, in slot order
-      uint16_t* vt = reinterpret_cast<uint16_t*>(cv.hi_pool + (size_t)page * cv.hi_page_bytes +
-                                                 (size_t)((g + page) % H) * PL::kHiHead + PL::kHiV);
-      const int m = c / 2;
-      const uint32_t w0[4] = {x[jj0].x, x[jj0].y, x[jj0].z, x[jj0].w};
-      const uint32_t w1[4] = {x[jj0 + 1].x, x[jj0 + 1].y, x[jj0 + 1].z, x[jj0 + 1].w};
-      const uint32_t w2[4] = {x[jj0 + 2].x, x[jj0 + 2].y, x[jj0 + 2].z, x[jj0 + 2].w};
-      const uint32_t w3[4] = {x[jj0 + 3].x, x[jj0 + 3].y, x[jj0 + 3].z, x[jj0 + 3].w};
+      for (int i = 0; i < NG; ++i) words[i] = 0u;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = 16 * (e % 2);
-        const uint32_t lo = ((w0[e / 2] >> sh) & 0xFFFFu) | (((w1[e / 2] >> sh) & 0xFFFFu) << 16);
-        const uint32_t hi = ((w2[e / 2] >> sh) & 0xFFFFu) | (((w3[e / 2] >> sh) & 0xFFFFu) << 16);
-        *reinterpret_cast<uint2*>(vt + (((m >> 1) * 64 + u * 16 + 8 * (c % 2) + e) * 2 + (m & 1)) * 4) =
-            make_uint2(lo, hi);
+      for (int r = 0; r < 4; ++r) {
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+          const float x0 = bf16_lo(v_at(4 * T4 + r, g, 32 * i + e));
+          const float x1 = bf16_lo(v_at(4 * T4 + r, g, 32 * i + 16 + e));
+          float am = fmaxf(fabsf(x0), fabsf(x1));
+          am = fmaxf(am, __shfl_xor(am, 1, 16));
+          am = fmaxf(am, __shfl_xor(am, 2, 16));
+          am = fmaxf(am, __shfl_xor(am, 4, 16));
+          am = fmaxf(am, __shfl_xor(am, 8, 16));
+          float s;
+          sc[r][i] = quant_scale(am, s);
+          const uint32_t byte = (uint32_t)(quant_code(x0, s) + 8) | ((uint32_t)(quant_code(x1, s) + 8) << 4);
+          words[i] |= byte << (8 * r);
+        }
       }
-    } else {
-      // 4 bytes per (dd, i): the 4 slots' code bytes, in slot order
-      uint32_t pt[4];
+      if (4 * T4 + 3 < tl0 || 4 * T4 >= th0) continue;   // no new slot in the group
+      uint8_t* dst = hb + PL::kLoVC + (size_t)((T4 * 16 + e) * NG) * 4;
+      if (4 * T4 >= tl0) {
+        if constexpr (NG == 4) *reinterpret_cast<uint4*>(dst) = make_uint4(words[0], words[1], words[2], words[3]);
+        else *reinterpret_cast<uint2*>(dst) = make_uint2(words[0], words[1]);
+      } else {                                     // the group holds earlier slots: new ones only
 #pragma unroll
-      for (int r = 0; r < 4; ++r) pt[r] = __shfl_xor(packed[jj0 + r], 2, 4);
-      if (!active || kv == 0 || q >= 2) continue;
-      uint8_t* vc = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead +
-                    PL::kLoVC;
+        for (int i = 0; i < NG; ++i)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint32_t word = 0u;
+          for (int r = 0; r < 4; ++r)
+            if (4 * T4 + r >= tl0 && 4 * T4 + r < th0) dst[4 * i + r] = (uint8_t)(words[i] >> (8 * r));
+      }
+      if (e < 4) {                                 // lane e writes the scales of slot 4*T4 + e
+        const int t = 4 * T4 + e;
+        if (t >= tl0 && t < th0) {
+          uint16_t* sd = reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (size_t)t * NG * 2);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          word |= (((packed[jj0 + r] >> (4 * e)) & 0xFu) | (((pt[r] >> (4 * e)) & 0xFu) << 4)) << (8 * r);
-        *reinterpret_cast<uint32_t*>(vc + ((u * 16 + 8 * q + e) * (PL::NM / 2) + i) * 4) = word;
+          for (int r = 0; r < 4; ++r)
+            if (r == e)
+#pragma unroll
+              for (int i = 0; i < NG; ++i) sd[i] = sc[r][i];
+        }
       }
     }
   }
@@ -1044,9 +1121,10 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
   }
   if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
   else append_plan_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
-  const dim3 grid((a.max_new + kPackTokens - 1) / kPackTokens, a.batch);
-  if (a.cv.head_dim == 64) append_pack_kernel<64><<<grid, dim3(256), 0, s>>>(a);
-  else append_pack_kernel<128><<<grid, dim3(256), 0, s>>>(a);
+  // pages of a store one sequence's slots of this call can reach: ceil(max_new / 16) + 1
+  const dim3 grid((a.max_new + kPage - 1) / kPage + 1, 2, a.batch);
+  if (a.cv.head_dim == 64) append_pack_page_kernel<64><<<grid, dim3(kPackThreads), 0, s>>>(a);
+  else append_pack_page_kernel<128><<<grid, dim3(kPackThreads), 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -77,7 +77,8 @@ struct CacheView {
   int32_t hi_base;        // first page of the HIGH store (= recent-window pages)
   int32_t window;         // W
   int32_t ring_pp;        // pages of one (sequence, layer) window: ceil(W / 16)
-  int32_t staging_stride; // max_tokens + W + 2 (the last two: the append's p0, n_fit)
+  int32_t staging_stride; // max_tokens + W + 4: the last four are the append's HIGH and LOW
+                          // store counts before it, its first position p0 and n_fit
   uint32_t hi_page_bytes, lo_page_bytes;
 };
 

@@ -169,8 +169,8 @@ def test_recent_window_geometry_and_layout():
     assert e.value.status == pask.PASK_E_SHAPE
     L0 = pask.pask_cache_layout_query(geom())
     L = pask.pask_cache_layout_query(geom(recent_window=20))
-    assert (L0.ring_pages, L0.staging_stride) == (0, 512 + 2)
-    assert (L.ring_pages, L.staging_stride) == (4 * 2 * 2, 512 + 20 + 2)
+    assert (L0.ring_pages, L0.staging_stride) == (0, 512 + 4)
+    assert (L.ring_pages, L.staging_stride) == (4 * 2 * 2, 512 + 20 + 4)
     assert L.lo_pool_off - L.hi_pool_off >= (16 + 64) * L.hi_page_bytes
     assert L.hi_pool_off - L.ring_act_off >= 4 * 2 * 20 and L.ring_act_off >= L.budget_off + 11232
     assert pask.pask_cache_bytes(geom(recent_window=513)) == 0       # W <= max_tokens_per_seq
