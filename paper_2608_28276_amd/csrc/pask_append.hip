@@ -185,17 +185,51 @@ __device__ __forceinline__ int clamp_n_new(const AppendArgs& a, int b, uint32_t&
   return n;
 }
 
-// kBudget: the tokens carry parser states and the online controller decides
-// (one thread walks each chunk's tokens in position order, the table in LDS).
+// Exclusive counts of N predicates over a block of kWaves waves in thread
+// order (a wavefront ballot and the popcount of the lanes below for each, plus
+// the per-wave totals in s_wave), and the block totals: two barriers for all
+// N.  Every thread of the block must call it.
+template <int N, int kWaves>
+__device__ __forceinline__ void block_counts(const bool (&pred)[N], int (*s_wave)[kWaves], int (&excl)[N],
+                                             int (&total)[N]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int below[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const unsigned long long mask = __ballot(pred[k]);
+    below[k] = __popcll(mask & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wave[k][wave] = __popcll(mask);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int cw = s_wave[k][w];
+      base += (w < wave) ? cw : 0;
+      tot += cw;
+    }
+    excl[k] = base + below[k];
+    total[k] = tot;
+  }
+  __syncthreads();
+}
+
+// One block of kPlanThreads threads per sequence walks the call's tokens in
+// chunks of kPlanThreads.  kBudget: the tokens carry parser states and the
+// online controller decides (one thread walks each chunk's tokens in position
+// order, the table in LDS).
+constexpr int kPlanThreads = 1024, kPlanWaves = kPlanThreads / 64;
 template <bool kBudget>
-__global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
+__global__ __launch_bounds__(kPlanThreads) void append_plan_kernel(AppendArgs a) {
   __shared__ uint8_t s_a0[64], s_amin[64];
-  __shared__ int s_wave[4];
+  __shared__ int s_wave[4][kPlanWaves];
   __shared__ unsigned s_page_base[2];
   __shared__ int s_granted[2];
   struct Empty {};
   __shared__ std::conditional_t<kBudget, BudgetTable, Empty> s_bud;
-  __shared__ uint8_t s_act[kBudget ? 256 : 1];
+  __shared__ uint8_t s_act[kBudget ? kPlanThreads : 1];
   const CacheView& cv = a.cv;
   const int b = blockIdx.x;
   load_table(a.tab, s_a0, s_amin);
@@ -208,7 +242,7 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   if constexpr (kBudget) {
     const uint4* src = reinterpret_cast<const uint4*>(cv.budget);
     uint4* dst = reinterpret_cast<uint4*>(&s_bud);
-    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += 256) dst[i] = src[i];
+    for (int i = threadIdx.x; i < (int)(sizeof(BudgetTable) / 16); i += kPlanThreads) dst[i] = src[i];
     __syncthreads();
     budget = s_bud.loaded == kBudgetLoaded;
     if (!budget && threadIdx.x == 0) flags |= PASK_FLAG_NO_BUDGET;
@@ -228,14 +262,17 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
   const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
   __syncthreads();
 
-  for (int c0 = 0; c0 < n; c0 += 256) {
+  // Every chunk's reads of the shared words (s_page_base, s_granted, s_act)
+  // come before the first barrier of the next chunk's counts, which every
+  // writer of the next chunk passes first: no barrier at the end of a chunk.
+  for (int c0 = 0; c0 < n; c0 += kPlanThreads) {
     const int j = c0 + (int)threadIdx.x;
     const bool valid = j < n;
     const int pos = pos0 + j;
     const bool fits = valid && pos < cv.max_tokens;
     if constexpr (kBudget) {
       if (budget && threadIdx.x == 0) {
-        const int j1 = min(min(n, c0 + 256), cv.max_tokens - pos0);
+        const int j1 = min(min(n, c0 + kPlanThreads), cv.max_tokens - pos0);
         const int group = (int)a.tab.group;
         for (int jj = c0; jj < j1; ++jj) {
           const size_t at = (size_t)b * a.max_new + jj;
@@ -259,15 +296,12 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
     if (valid && !fits) flags |= PASK_FLAG_SEQ_CAPACITY;
     const int st = act == kHigh ? kHi : kLo;
     const bool keep = fits && act != kDrop;
-    int tot_hi, tot_lo, np_hi, np_lo;
-    const int r_hi = block_exclusive_count(keep && st == kHi, s_wave, tot_hi);
-    const int r_lo = block_exclusive_count(keep && st == kLo, s_wave, tot_lo);
-    const int slot = keep ? nst[st] + (st == kHi ? r_hi : r_lo) : 0;
+    int rank[2], tot[2], prank[2], np[2];
+    block_counts<2, kPlanWaves>({keep && st == kHi, keep && st == kLo}, s_wave, rank, tot);
+    const int slot = keep ? nst[st] + rank[st] : 0;
     const bool new_page = keep && (slot % kPage) == 0;
-    const int pr_hi = block_exclusive_count(new_page && st == kHi, s_wave, np_hi);
-    const int pr_lo = block_exclusive_count(new_page && st == kLo, s_wave, np_lo);
+    block_counts<2, kPlanWaves>({new_page && st == kHi, new_page && st == kLo}, s_wave, prank, np);
     if (threadIdx.x == 0) {
-      const int np[2] = {np_hi, np_lo};
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
         unsigned base = 0u;
@@ -289,26 +323,23 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
       const int pidx = slot / kPage;
       stored = pidx < pages_before[st] + s_granted[st];
       if (stored) {
-        if (new_page) bt[st][pidx] = (int)(s_page_base[st] + (unsigned)(st == kHi ? pr_hi : pr_lo));
+        if (new_page) bt[st][pidx] = (int)(s_page_base[st] + (unsigned)prank[st]);
         il[st][slot] = pos;
       } else {
         flags |= st == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
       }
     }
     if (valid) stg[j] = stored ? ((st << 30) | slot) : -1;
-    int c_drop, c_forced, c_lost, c_fit;
-    block_exclusive_count(fits && act == kDrop, s_wave, c_drop);
-    block_exclusive_count(stored && forced, s_wave, c_forced);
-    block_exclusive_count(valid && !stored && !(fits && act == kDrop), s_wave, c_lost);
-    block_exclusive_count(fits, s_wave, c_fit);
-    const int tot[2] = {tot_hi, tot_lo};
+    int unused[4], c[4];
+    block_counts<4, kPlanWaves>({fits && act == kDrop, stored && forced, valid && !stored && !(fits && act == kDrop),
+                                 fits},
+                                s_wave, unused, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) nst[x] = min(nst[x] + tot[x], (pages_before[x] + s_granted[x]) * kPage);
-    n_drop += c_drop;
-    n_forced += c_forced;
-    n_lost += c_lost;
-    n_fit += c_fit;
-    __syncthreads();
+    n_drop += c[0];
+    n_forced += c[1];
+    n_lost += c[2];
+    n_fit += c[3];
   }
   if (threadIdx.x == 0) {
     cnt[kCntHi] = nst[0];
@@ -328,17 +359,13 @@ __global__ __launch_bounds__(256) void append_plan_kernel(AppendArgs a) {
 
 // The scale of a RETAIN-LOW group from its absmax: s = fp16(absmax / 7) with
 // a correctly rounded fp32 division, saturated at 65504, rounded to nearest
-// even; returns its fp16 bits and s as fp32.
-__device__ __forceinline__ uint16_t quant_scale(float absmax, float& s) {
+// even; returns its fp16 bits, s as fp32 and an approximation of 1 / s.
+__device__ __forceinline__ uint16_t quant_scale(float absmax, float& s, float& inv) {
   const _Float16 h = (_Float16)fminf(absmax / 7.0f, 65504.0f);
   s = (float)h;
+  inv = __builtin_amdgcn_rcpf(s);
   return __builtin_bit_cast(uint16_t, h);
 }
-// The code of x under scale s: clamp(rint(x / s), -7, 7), 0 when s == 0.
-__device__ __forceinline__ int quant_code(float x, float s) {
-  return s != 0.0f ? (int)fminf(fmaxf(rintf(x / s), -7.0f), 7.0f) : 0;
-}
-
 // Quantise 4 consecutive elements of a 32-element group held by 8 adjacent
 // lanes (quant_scale of the group's absmax, quant_code of each element).
 // Returns the 4 codes as offset-binary nibbles q + 8 (element i in bits
@@ -349,11 +376,11 @@ __device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& pac
   am = fmaxf(am, __shfl_xor(am, 1, 8));
   am = fmaxf(am, __shfl_xor(am, 2, 8));
   am = fmaxf(am, __shfl_xor(am, 4, 8));
-  float s;
-  sbits = quant_scale(am, s);
+  float s, inv;
+  sbits = quant_scale(am, s, inv);
   uint32_t p = 0u;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) p |= (uint32_t)(quant_code(f[i], s) + 8) << (4 * i);
+  for (int i = 0; i < 4; ++i) p |= (uint32_t)(quant_code(f[i], s, inv) + 8) << (4 * i);
   packed = p;
 }
 
@@ -452,6 +479,108 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
 // (a V piece that mixes them with new slots is written element by element);
 // slots from n1 on are not yet in use and may be written.
 constexpr int kPackThreads = 256;
+
+// The 8 codes of the bf16 elements of x (element u in bits 4u..4u+3, offset
+// binary) under scale s, inv ~ 1/s.  rint(x * inv) is the nearest integer of
+// x / s whenever x / s is not within 2^-12 of a half-integer: for a bf16 x
+// and an fp16 s no quotient other than an exact tie comes that close, and
+// x * inv is within 2^-19 of x / s.  Lanes holding an element near a tie take
+// the exact rule (quant_code) for their 8 elements.
+__device__ __forceinline__ uint32_t codes8(const uint4& x, float s, float inv) {
+  const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
+                      bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
+  uint32_t p = 0u;
+  bool near_tie = false;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float y = f[u] * inv;
+    const float c = rintf(y);
+    near_tie |= fabsf(y - c) > 0.49988f;
+    p |= (uint32_t)(fminf(fmaxf(c, -7.0f), 7.0f) + 8.0f) << (4 * u);
+  }
+  if (__ballot(near_tie)) {
+    if (near_tie) {
+      p = 0u;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) p |= (uint32_t)(quant_code(f[u], s, inv) + 8) << (4 * u);
+    }
+  }
+  return s != 0.0f ? p : 0x88888888u;
+}
+
+// The page image of a LOW page from the call's K and V rows (kx, vx: 16-byte
+// chunks in row order, chunk e of the page's rows at e = it * threads + tid,
+// so the four chunks of a 32-element group sit in four adjacent lanes):
+// every lane quantises its 8 elements (the group's absmax over the 4 lanes),
+// the codes and scales go to an LDS image of the page in its stored order,
+// which is then copied out with 16-byte stores (whole pages), or byte by byte
+// for the new slots only when the page holds earlier slots.
+template <int D, int kIt>
+__device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& cv, int page, int tl0, int th0,
+                                         const uint4 (&kx)[kIt], const uint4 (&vx)[kIt], int n_chunks,
+                                         uint8_t* s_img) {
+  using PL = PageLayout<D>;
+  constexpr int NG = PL::NG, kRowChunks = D / 8;
+  const int H = cv.n_kv_heads, tid = (int)threadIdx.x;
+#pragma unroll
+  for (int it = 0; it < kIt; ++it) {
+    const int e = it * kPackThreads + tid;
+    const bool valid = e < n_chunks;
+    const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+    const int g = col / kRowChunks, c = col % kRowChunks, i = c / 4, q = c % 4;
+#pragma unroll
+    for (int kv = 0; kv < 2; ++kv) {
+      const uint4 x = kv ? vx[it] : kx[it];
+      float am = 0.0f;
+      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.x)), fabsf(bf16_hi(x.x))));
+      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.y)), fabsf(bf16_hi(x.y))));
+      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.z)), fabsf(bf16_hi(x.z))));
+      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.w)), fabsf(bf16_hi(x.w))));
+      am = fmaxf(am, __shfl_xor(am, 1));           // the group's four lanes
+      am = fmaxf(am, __shfl_xor(am, 2));
+      float s, inv;
+      const uint16_t sbits = quant_scale(am, s, inv);
+      const uint32_t packed = codes8(x, s, inv);
+      uint8_t* hd = s_img + g * PL::kLoHead;
+      if (kv == 0) {
+        if (valid) {
+          *reinterpret_cast<uint32_t*>(hd + ((q * 16 + t) * NG + i) * 4) = k_word(packed);
+          if (q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoKS + (t * NG + i) * 2) = sbits;
+        }
+      } else {
+        // lanes q and q ^ 2 hold dims 32i + dd and 32i + 16 + dd: one byte per dd
+        const uint32_t partner = __shfl_xor(packed, 2);
+        if (valid && q < 2) {
+          uint8_t* vc = hd + PL::kLoVC + ((t / 4) * 16 * NG + i) * 4 + t % 4;
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            vc[(8 * q + u) * NG * 4] = (uint8_t)(((packed >> (4 * u)) & 0xFu) | (((partner >> (4 * u)) & 0xFu) << 4));
+        }
+        if (valid && q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoVS + (t * NG + i) * 2) = sbits;
+      }
+    }
+  }
+  __syncthreads();
+  uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
+  constexpr int kHeadChunks = PL::kLoHead / 16;
+  if (tl0 == 0) {                                  // no earlier slot: whole 16-byte pieces
+    for (int k = tid; k < H * kHeadChunks; k += kPackThreads) {
+      const int g = k / kHeadChunks, off = k % kHeadChunks;
+      *reinterpret_cast<uint4*>(pg + (size_t)((g + page) % H) * PL::kLoHead + off * 16) =
+          *reinterpret_cast<const uint4*>(s_img + g * PL::kLoHead + off * 16);
+    }
+    return;
+  }
+  for (int x = tid; x < H * PL::kLoHead; x += kPackThreads) {   // the new slots' bytes only
+    const int g = x / PL::kLoHead, y = x % PL::kLoHead;
+    int t;
+    if (y < PL::kLoKS) t = (y / 4 / NG) % 16;                             // K word (q*16 + t)*NG + i
+    else if (y < PL::kLoVC) t = (y - PL::kLoKS) / 2 / NG;                 // K scale t*NG + i
+    else if (y < PL::kLoVS) t = ((y - PL::kLoVC) / 4 / NG / 16) * 4 + (y - PL::kLoVC) % 4;   // V byte
+    else t = (y - PL::kLoVS) / 2 / NG;                                    // V scale
+    if (t >= tl0 && t < th0) pg[(size_t)((g + page) % H) * PL::kLoHead + y] = s_img[x];
+  }
+}
 constexpr int kLdsRowPad = 16;                     // bytes after each staged V row (bank spread)
 
 template <int D>
@@ -518,19 +647,21 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
       }
     }
   } else {
-    // LOW K: wave w takes KV heads w, w + 4; lane (q, t) loads dims 32i + 8q..+8 of slot t
-    const int q = lane >> 4, t = lane & 15, j = s_src[t];
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int g = wave + 4 * h2;
-#pragma unroll
-      for (int i = 0; i < NG; ++i)
-        if (g < H && j >= 0)
-          kx[h2 * NG + i] =
-              stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + g * D + (4 * i + q) * 8));
+    for (int it = 0; it < kIt; ++it) {             // LOW K: row order, like V
+      const int e = it * kPackThreads + tid;
+      if (e < n_chunks) {
+        const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+        const int j = s_src[t];
+        if (j >= 0) kx[it] = stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + col * 8));
+      }
     }
   }
-  // 2. V rows into LDS
+  if (!is_hi) {
+    low_page<D>(a, cv, page, tl0, th0, kx, vx, n_chunks, s_v);
+    return;
+  }
+  // 2. HIGH: V rows into LDS
 #pragma unroll
   for (int it = 0; it < kIt; ++it) {
     const int e = it * kPackThreads + tid;
@@ -543,7 +674,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
   auto v_at = [&](int t, int g, int d) -> uint32_t {   // bf16 bits of V[t][g][d]
     return *reinterpret_cast<const uint16_t*>(s_v + t * kLdsRow + (g * D + d) * 2);
   };
-  if (is_hi) {
+  {                                                // HIGH page
     uint8_t* pg = cv.hi_pool + (size_t)page * cv.hi_page_bytes;
     // K chunks as loaded: chunk (g, i, q, t) at (i*64 + q*16 + t) * 16 of head slot (g + page) % H
 #pragma unroll
@@ -583,101 +714,6 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
             for (int r = 0; r < 4; ++r)
               if (4 * T4 + r >= tl0 && 4 * T4 + r < th0)
                 reinterpret_cast<uint16_t*>(dst)[4 * h + r] = (uint16_t)(w[2 * h + r / 2] >> (16 * (r % 2)));
-        }
-      }
-    }
-    return;
-  }
-  uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
-  // LOW K: lane (q, t) of wave w quantises the chunks it loaded; the group's
-  // absmax is shared by the four lanes t, t + 16, t + 32, t + 48
-  {
-    const int q = lane >> 4, t = lane & 15;
-    const bool mine = s_src[t] >= 0;
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int g = wave + 4 * h2;
-      if (g >= H) break;                           // wave-uniform
-      uint8_t* hb = pg + (size_t)((g + page) % H) * PL::kLoHead;
-      uint32_t words[NG];
-      uint16_t sc[NG];
-#pragma unroll
-      for (int i = 0; i < NG; ++i) {
-        const uint4 x = kx[h2 * NG + i];
-        const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
-                            bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
-        float am = 0.0f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) am = fmaxf(am, fabsf(f[u]));
-        am = fmaxf(am, __shfl_xor(am, 16));
-        am = fmaxf(am, __shfl_xor(am, 32));
-        float s;
-        sc[i] = quant_scale(am, s);
-        uint32_t packed = 0u;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) packed |= (uint32_t)(quant_code(f[u], s) + 8) << (4 * u);
-        words[i] = k_word(packed);
-      }
-      if (mine) {
-        uint32_t* dst = reinterpret_cast<uint32_t*>(hb + (size_t)((q * 16 + t) * NG) * 4);
-        if constexpr (NG == 4) *reinterpret_cast<uint4*>(dst) = make_uint4(words[0], words[1], words[2], words[3]);
-        else *reinterpret_cast<uint2*>(dst) = make_uint2(words[0], words[1]);
-        if (q == 0) {
-          uint16_t* sd = reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (size_t)t * NG * 2);
-#pragma unroll
-          for (int i = 0; i < NG; ++i) sd[i] = sc[i];
-        }
-      }
-    }
-  }
-  // LOW V: lane (T4, e) of the wave holding KV head g quantises dims 32i + e
-  // and 32i + 16 + e of slots 4*T4 + r; a group's absmax over its 16 lanes
-  {
-    const int T4 = lane >> 4, e = lane & 15;
-    for (int g = wave; g < H; g += 4) {
-      uint8_t* hb = pg + (size_t)((g + page) % H) * PL::kLoHead;
-      uint32_t words[NG];
-      uint16_t sc[4][NG];
-#pragma unroll
-      for (int i = 0; i < NG; ++i) words[i] = 0u;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-#pragma unroll
-        for (int i = 0; i < NG; ++i) {
-          const float x0 = bf16_lo(v_at(4 * T4 + r, g, 32 * i + e));
-          const float x1 = bf16_lo(v_at(4 * T4 + r, g, 32 * i + 16 + e));
-          float am = fmaxf(fabsf(x0), fabsf(x1));
-          am = fmaxf(am, __shfl_xor(am, 1, 16));
-          am = fmaxf(am, __shfl_xor(am, 2, 16));
-          am = fmaxf(am, __shfl_xor(am, 4, 16));
-          am = fmaxf(am, __shfl_xor(am, 8, 16));
-          float s;
-          sc[r][i] = quant_scale(am, s);
-          const uint32_t byte = (uint32_t)(quant_code(x0, s) + 8) | ((uint32_t)(quant_code(x1, s) + 8) << 4);
-          words[i] |= byte << (8 * r);
-        }
-      }
-      if (4 * T4 + 3 < tl0 || 4 * T4 >= th0) continue;   // no new slot in the group
-      uint8_t* dst = hb + PL::kLoVC + (size_t)((T4 * 16 + e) * NG) * 4;
-      if (4 * T4 >= tl0) {
-        if constexpr (NG == 4) *reinterpret_cast<uint4*>(dst) = make_uint4(words[0], words[1], words[2], words[3]);
-        else *reinterpret_cast<uint2*>(dst) = make_uint2(words[0], words[1]);
-      } else {                                     // the group holds earlier slots: new ones only
-#pragma unroll
-        for (int i = 0; i < NG; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (4 * T4 + r >= tl0 && 4 * T4 + r < th0) dst[4 * i + r] = (uint8_t)(words[i] >> (8 * r));
-      }
-      if (e < 4) {                                 // lane e writes the scales of slot 4*T4 + e
-        const int t = 4 * T4 + e;
-        if (t >= tl0 && t < th0) {
-          uint16_t* sd = reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (size_t)t * NG * 2);
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (r == e)
-#pragma unroll
-              for (int i = 0; i < NG; ++i) sd[i] = sc[r][i];
         }
       }
     }
@@ -1119,8 +1155,8 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
     }
     return hipGetLastError();
   }
-  if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
-  else append_plan_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
+  if (a.states) append_plan_kernel<true><<<dim3(a.batch), dim3(kPlanThreads), 0, s>>>(a);
+  else append_plan_kernel<false><<<dim3(a.batch), dim3(kPlanThreads), 0, s>>>(a);
   // pages of a store one sequence's slots of this call can reach: ceil(max_new / 16) + 1
   const dim3 grid((a.max_new + kPage - 1) / kPage + 1, 2, a.batch);
   if (a.cv.head_dim == 64) append_pack_page_kernel<64><<<grid, dim3(kPackThreads), 0, s>>>(a);

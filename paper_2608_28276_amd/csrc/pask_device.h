@@ -42,6 +42,21 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne_dev(float f) {
 }
 
 
+// The RETAIN-LOW code of x under scale s: clamp(RNE(x / s), -7, 7), 0 when
+// s == 0, without a division.  c = rint(x * inv) is within one of RNE(x / s)
+// whenever inv is 1 / s to a few ulp (|x / s| < 8 here); the residual
+// e = x - c*s is exact (c*s has at most 15 significant bits and |e| < 2s), so
+// comparing it with s/2 moves c to the nearest integer of x / s, ties to
+// even.  Host-callable so that the rule can be checked exhaustively on the CPU.
+__host__ __device__ inline int quant_code(float x, float s, float inv) {
+  float c = rintf(x * inv);
+  const float e = fmaf(-c, s, x);
+  const float h = 0.5f * s;
+  const bool odd = ((int)c & 1) != 0;
+  c += (e > h || (e == h && odd)) ? 1.0f : ((e < -h || (e == -h && odd)) ? -1.0f : 0.0f);
+  return s != 0.0f ? (int)fminf(fmaxf(c, -7.0f), 7.0f) : 0;
+}
+
 // Data read once per call (pages in the attention, a bulk append's input
 // rows): non-temporal loads, so the streamed lines do not displace others in
 // the L2 and the last-level cache (the attention call on the 64-sequence

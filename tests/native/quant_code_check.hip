@@ -1,0 +1,68 @@
+// The division-free RETAIN-LOW code rule of the append kernels (quant_code in
+// pask_device.h), checked on the CPU against RNE(x / s) computed in fp64 (exact
+// here: a tie x / s = k + 1/2 is exact in fp64, and any other quotient lies at
+// least 2^-12 from a tie), clamped to [-7, 7].  Every positive fp16 scale s,
+// every bf16 x with s/8 <= |x| <= 9s (both signs), and an approximate
+// reciprocal 1/s moved by up to 4 ulp either way (the device takes it from
+// v_rcp_f32, accurate to 1 ulp); then every bf16 x below s/8 at the exact
+// reciprocal, and s = 0.
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "pask_device.h"
+
+static float bf16_value(uint32_t bits) {
+  const uint32_t w = bits << 16;
+  float f;
+  memcpy(&f, &w, 4);
+  return f;
+}
+
+static int want(float x, float s) {
+  if (s == 0.0f) return 0;
+  const double q = nearbyint((double)x / (double)s);
+  return (int)fmin(fmax(q, -7.0), 7.0);
+}
+
+int main() {
+  long n = 0, bad = 0;
+  for (uint32_t hs = 1; hs < 0x7C00; ++hs) {        // every positive finite fp16 scale
+    const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)hs);
+    for (int du = -4; du <= 4; ++du) {
+      float inv = 1.0f / s;
+      for (int k = 0; k < (du < 0 ? -du : du); ++k) inv = nextafterf(inv, du < 0 ? 0.0f : INFINITY);
+      for (uint32_t bx = 0; bx < 0x7F80; ++bx) {
+        const float x = bf16_value(bx);
+        if (x < s / 8) continue;
+        if (x > 9 * s) break;
+        for (int sg = 0; sg < 2; ++sg) {
+          const float xs = sg ? -x : x;
+          const int got = pask::quant_code(xs, s, inv);
+          ++n;
+          if (got != want(xs, s)) {
+            if (++bad <= 10) printf("mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, got, want(xs, s));
+          }
+        }
+      }
+      if (du == 0) {
+        for (uint32_t bx = 0; bx < 0x7F80; ++bx) {  // small x (codes 0 and +-1) at the exact reciprocal
+          const float x = bf16_value(bx);
+          if (x >= s / 8) break;
+          for (int sg = 0; sg < 2; ++sg) {
+            const float xs = sg ? -x : x;
+            ++n;
+            if (pask::quant_code(xs, s, inv) != want(xs, s) && ++bad <= 10) printf("mismatch (small): x=%a s=%a\n", xs, s);
+          }
+        }
+      }
+    }
+  }
+  for (uint32_t bx = 0; bx < 0x7F80; bx += 7) {      // s == 0: every code 0
+    ++n;
+    if (pask::quant_code(bf16_value(bx), 0.0f, INFINITY) != 0 && ++bad <= 10) printf("s = 0 gives a code\n");
+  }
+  printf("%s: %ld cases, %ld mismatches\n", bad ? "FAIL" : "ok", n, bad);
+  return bad ? 1 : 0;
+}
