@@ -82,9 +82,13 @@ enum {
   PASK_FLAG_BAD_COUNT = 1u << 4,        /* n_new[b] outside [0, max_new]       */
   PASK_FLAG_BAD_STATE = 1u << 5,        /* parser state >= n_states: decided
                                            with Gamma = 0, not critical        */
-  PASK_FLAG_NO_BUDGET = 1u << 6         /* states given but no pask_budget_init
+  PASK_FLAG_NO_BUDGET = 1u << 6,        /* states given but no pask_budget_init
                                            since the last init / reset: token
                                            decided by Eq. 10 alone             */
+  PASK_FLAG_WORKSPACE = 1u << 7         /* internal: an attention piece fell
+                                           outside the workspace's partials
+                                           (never expected); not written, the
+                                           call's outputs are undefined        */
 };
 
 /* ---- append flags -------------------------------------------------------- */

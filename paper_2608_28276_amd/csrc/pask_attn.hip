@@ -1,9 +1,9 @@
 // gfx950 kernels of the PASK hot path that read the cache.
 //
-//   attn         grouped-query flash-decode, stream-K: one single-wave block
-//                per resident wave slot, each streaming an equal contiguous
-//                range of the (sequence, KV head, page) list over the HIGH and
-//                LOW stores; q.k on bf16 MFMA (query heads as columns), int4
+//   attn         grouped-query flash-decode, stream-K: one worker wave per
+//                resident wave slot, each streaming a contiguous range of the
+//                (sequence, KV head, page) list over the HIGH and LOW stores
+//                (pask_plan.h); q.k on bf16 MFMA (query heads as columns), int4
 //                K codes widened exactly to bf16 in registers with the offset
 //                removed in the accumulator, the K scale applied per 32-dim
 //                group; p.v on bf16 MFMA for HIGH pages and on fp16 MFMA with
@@ -27,6 +27,7 @@
 #include <type_traits>
 
 #include "pask_device.h"
+#include "pask_plan.h"
 
 namespace pask {
 namespace {
@@ -36,17 +37,18 @@ namespace {
 // ---------------------------------------------------------------------------
 //
 // Stream-K: the work is the list of (sequence b, KV head g, page) triples,
-// HIGH pages of a (b, g) before its LOW pages, each page weighing 32 units
-// (PASK_WEIGHT_LO for a LOW page).  The grid holds one single-wave worker
-// per resident wave slot of the chip, and worker w takes the w-th of
-// contiguous unit ranges, so every worker starts at launch.  In calls with
-// more than 64 (b, g) segments, workers on the odd-numbered XCDs (blockIdx
-// odd) take 15/16 of an even one's range: their waves stream pages about 10%
-// slower, so with equal ranges the even XCDs idle through the last ~15 us of
-// the call.  A range crossing a (b, g)
-// boundary closes that segment with a partial block; every range is at least
-// what keeps every (b, g) within as many pieces as the workspace holds
-// partials.
+// HIGH and window pages of a (b, g) before its LOW pages, each page weighing
+// 32 units.  The grid holds one worker wave per resident wave slot of the
+// chip, and worker w takes the w-th of contiguous unit ranges, so every
+// worker starts at launch.  Calls with more than 64 (b, g) segments run four
+// workers per workgroup, and the workers of workgroups on the odd-numbered
+// XCDs (odd workgroup index: workgroups are dealt to the 8 XCDs in turn)
+// take PASK_ODD_WEIGHT/16 of an even one's range: their waves stream pages
+// about 10% slower, so with equal ranges the even XCDs idle through the last
+// ~15 us of the call.  Calls with at most 64 segments run single-wave
+// workgroups with equal ranges.  A range crossing a (b, g) boundary closes
+// that segment with a partial block; every range is at least what keeps every
+// (b, g) within as many pieces as the workspace holds partials.
 //
 // Per page (16 slots x all G query heads of KV head g), one wave:
 //   scores  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: rows = slots, columns
@@ -389,7 +391,6 @@ __device__ __forceinline__ void attend_pair(const Raw& xa, const Raw& xb, AttnSt
   page_values<D, G, kIsHi, kMaskedB>(xb, st, sb, nvb, q);
 }
 
-__device__ __forceinline__ int cdiv(int x, int y) { return (x + y - 1) / y; }
 // A value the whole wave holds alike, moved to a scalar register so the
 // compiler treats what depends on it as uniform.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
@@ -414,32 +415,6 @@ __device__ __forceinline__ int wave_inclusive_scan(int x) {
   return x;
 }
 
-// Pages of sequence b in the layer: the HIGH store, the recent window (HIGH
-// layout, min(n_pos, W) slots) and the LOW store, in that order, and their
-// length in work units: the stream-K decomposition weighs a HIGH or window
-// page kWeightHi units and a LOW page kWeightLo (PASK_WEIGHT_LO).
-constexpr int kWeightHi = 32;
-constexpr int kWeightLo = PASK_WEIGHT_LO;
-static_assert(kWeightLo >= 1 && kWeightLo <= kWeightHi, "LOW page weight out of range");
-struct SeqPages {
-  int n_hi, n_win, n_lo;   // slots of the HIGH store, the window, the LOW store
-  int np_hi, np_w, np;     // pages: HIGH store, + window (the HIGH-weight ones), all
-  int len;
-};
-__device__ __forceinline__ int len_of(int n_hi, int n_win, int n_lo) {
-  return kWeightHi * (cdiv(n_hi, kPage) + cdiv(n_win, kPage)) + kWeightLo * cdiv(n_lo, kPage);
-}
-__device__ __forceinline__ SeqPages make_pages(int n_hi, int n_win, int n_lo) {
-  SeqPages s;
-  s.n_hi = n_hi;
-  s.n_win = n_win;
-  s.n_lo = n_lo;
-  s.np_hi = cdiv(n_hi, kPage);
-  s.np_w = s.np_hi + cdiv(n_win, kPage);
-  s.np = s.np_w + cdiv(n_lo, kPage);
-  s.len = len_of(n_hi, n_win, n_lo);
-  return s;
-}
 __device__ __forceinline__ int window_slots(const AttnArgs& a, int n_pos) { return min(n_pos, a.cv.window); }
 
 // Store counts of sequence `lane` for the first 64 sequences, read once per
@@ -474,119 +449,38 @@ __device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f,
   const int len = len_of(c[kCntHi], window_slots(a, c[kCntPos]), c[kCntLo]);
   return b < limit ? len : 0;
 }
-// Unit offset of page j (HIGH-weight pages first, then LOW) inside its segment.
-__device__ __forceinline__ int page_start(const SeqPages& s, int j) {
-  return j < s.np_w ? kWeightHi * j : kWeightHi * s.np_w + kWeightLo * (j - s.np_w);
-}
-// First page whose unit offset is >= u (s.np when there is none).
-__device__ __forceinline__ int first_page_at(const SeqPages& s, int u) {
-  if (u <= kWeightHi * s.np_w) return cdiv(u, kWeightHi);
-  return s.np_w + min(s.np - s.np_w, cdiv(u - kWeightHi * s.np_w, kWeightLo));
-}
-
-// a / b for 0 <= a, 0 < b (wave-uniform): 32-bit division when both fit, as
-// they do for any call below 2^32 units; the 64-bit expansion otherwise.
-__device__ __forceinline__ long long udiv(long long a, long long b) {
-  if ((((unsigned long long)a | (unsigned long long)b) >> 32) == 0) return (long long)((uint32_t)a / (uint32_t)b);
-  return a / b;
-}
-
-// Stream-K decomposition of one attention call, computed identically by every
-// block of the attention and merge kernels.  The work list is the segments
-// (sequence b, KV head g) in that nesting order, each the pages of (b, g) laid
-// out in units; segment (b, g) starts at unit excl(b) * Hkv + g * len(b), where
-// excl(b) sums len over the sequences before b.  Block w takes the pages that
-// start in its contiguous unit range [start_of(w), start_of(w) + size_of(w)),
-// size_of(w) = weight(w) x step.  Every range is at least one HIGH page and
-// kWeightLo <= kWeightHi, so every block between the first and the last one
-// of a segment holds a page of it; every range is also large enough that no
-// segment is cut into more than `splits` pieces (the workspace bound).
+// The work split of a call (pask_plan.h) from its counts: every block of the
+// attention, merge and distortion kernels computes the same plan.
 constexpr int kWpb = PASK_ATTN_WPB;   // workers (waves) per workgroup of the weighted attention kernel
-struct StreamPlan {
-  long long total;   // units
-  int step;          // units per sixteenth of weight
-  // Block w runs on XCD w % 8.  A block on an odd XCD weighs `odd`
-  // sixteenths (PASK_ODD_WEIGHT, or 16 when the ranges are at their minimum
-  // size), one on an even XCD 16: eight consecutive blocks weigh octet().
-  int odd;
-  // Workers w run in workgroup w / kWpb on XCD (w / kWpb) % 8.
-  __device__ __forceinline__ int octet() const { return kWpb * (4 * 16 + 4 * odd); }   // 8 workgroups
-  __device__ __forceinline__ int weight(int w) const { return ((w / kWpb) & 1) ? odd : 16; }
-  __device__ __forceinline__ long long weight_before(int w) const {   // of workers 0..w-1
-    const int wg = w / kWpb, j = wg & 7;
-    return (long long)(wg >> 3) * octet() + kWpb * ((j + 1) / 2 * 16 + (j / 2) * odd) + (w % kWpb) * weight(w);
-  }
-  __device__ __forceinline__ long long start_of(int w) const {
-    return odd == 16 ? (long long)w * (16 * step) : weight_before(w) * step;
-  }
-  __device__ __forceinline__ int size_of(int w) const { return weight(w) * step; }
-  // Block whose range holds unit u.
-  __device__ __forceinline__ long long block_of(long long u) const {
-    if (odd == 16) return udiv(u, 16 * step);
-    const long long wu = udiv(u, step);            // sixteenths of weight before u
-    const long long o = udiv(wu, octet());
-    int r = (int)(wu - o * octet()), j = 0;
-    while (r >= kWpb * weight(j * kWpb)) {
-      r -= kWpb * weight(j * kWpb);
-      ++j;
-    }
-    return o * 8 * kWpb + j * kWpb + r / weight(j * kWpb);
-  }
-};
+using WeightedPlan = StreamPlan<kWpb>;
 constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
 // Calls with few segments: workers of 4 pages (8 and 2 measured slower at
 // one Qwen3-4B-shaped sequence of 2.5k entries: fewer workers, or more
 // pieces to merge).
 constexpr int kSmallMinPages = 4;
-static_assert(PASK_ODD_WEIGHT >= 1 && PASK_ODD_WEIGHT <= 16, "odd-XCD block weight out of range");
+static_assert(PASK_ODD_WEIGHT >= 1 && PASK_ODD_WEIGHT <= 16, "odd-XCD worker weight out of range");
 
-__device__ __forceinline__ StreamPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
-  int total = 0, mx = 0;
+__device__ __forceinline__ void call_totals(const AttnArgs& a, const FirstCounts& f, long long& total, int& mx) {
+  int t = 0, m = 0;
   for (int c0 = 0; c0 < a.batch; c0 += 64) {
     const int len = lane_len(a, f, c0, a.batch);
-    total += uni(wave_sum(len));
-    mx = max(mx, uni(wave_max(len)));
+    t += uni(wave_sum(len));
+    m = max(m, uni(wave_max(len)));
   }
-  StreamPlan pl;
-  pl.total = (long long)total * a.cv.n_kv_heads;
-  const long long lo = max(kWeightHi * a.min_pages, cdiv(mx, a.splits - 1));
-  // Weighted ranges while every range stays above the minimum size; a call
-  // whose ranges are at the minimum (a few sequences: latency-bound) splits
-  // evenly, so no worker takes more than the minimum.
-  pl.odd = PASK_ODD_WEIGHT;
-  long long step = udiv(pl.total + pl.weight_before(n_blocks) - 1, pl.weight_before(n_blocks));
-  if (step * PASK_ODD_WEIGHT < lo) {
-    pl.odd = 16;
-    step = max(udiv(pl.total + pl.weight_before(n_blocks) - 1, pl.weight_before(n_blocks)), (lo + 15) / 16);
-  }
-  pl.step = (int)min(step, (long long)(INT_MAX / 16));
-  return pl;
+  total = (long long)t * a.cv.n_kv_heads;
+  mx = m;
 }
-
-// The same decomposition with equal ranges of U units, for calls with at
-// most kSmallSegments segments: their workers hold a few pages each and the
-// call is bound by latency, where the weighted plan's extra arithmetic before
-// the first page load measured 0.5-0.9 us slower per call at batch 1.
-struct EvenPlan {
-  long long total;   // units
-  int U;             // units per block
-  __device__ __forceinline__ long long start_of(int w) const { return (long long)w * U; }
-  __device__ __forceinline__ int size_of(int) const { return U; }
-  __device__ __forceinline__ long long block_of(long long u) const { return u / U; }
-};
+__device__ __forceinline__ WeightedPlan stream_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
+  long long total;
+  int mx;
+  call_totals(a, f, total, mx);
+  return stream_plan_of<kWpb>(total, mx, a.splits, a.min_pages, n_blocks, PASK_ODD_WEIGHT);
+}
 __device__ __forceinline__ EvenPlan even_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
-  int total = 0, mx = 0;
-  for (int c0 = 0; c0 < a.batch; c0 += 64) {
-    const int len = lane_len(a, f, c0, a.batch);
-    total += uni(wave_sum(len));
-    mx = max(mx, uni(wave_max(len)));
-  }
-  EvenPlan pl;
-  pl.total = (long long)total * a.cv.n_kv_heads;
-  const long long even = (pl.total + n_blocks - 1) / n_blocks;
-  pl.U = max(kWeightHi * a.min_pages, (int)min(even, (long long)INT_MAX));
-  pl.U = max(pl.U, cdiv(mx, a.splits - 1));
-  return pl;
+  long long total;
+  int mx;
+  call_totals(a, f, total, mx);
+  return even_plan_of(total, mx, a.splits, a.min_pages, n_blocks);
 }
 template <typename Plan>
 __device__ __forceinline__ Plan make_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {
@@ -753,6 +647,10 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   constexpr int G4 = G > 4 ? G : 4;
   const float l_n = head_sum(st.l);              // head n, over all slots
   const int slot = (int)(w - plan.block_of(seg0));   // < a.splits by the choice of range sizes
+  if (slot < 0 || slot >= a.splits) {            // never expected: report it, write nothing
+    if ((threadIdx.x & 63) == 0) atomicOr(a.cv.status, (uint32_t)PASK_FLAG_WORKSPACE);
+    return;
+  }
   const size_t blk = ((size_t)b * H + g) * a.splits + slot;
   if (4 * q < G4) {
     float* o = a.ws_o + blk * (G4 * D);
@@ -764,11 +662,12 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
   if (q == 0 && n < G4) *reinterpret_cast<float2*>(a.ws_ml + (blk * G4 + n) * 2) = make_float2(st.m, l_n);
 }
 
-// One single-wave workgroup per stream-K worker w; kWeighted: the per-XCD
-// weighted ranges (StreamPlan), else equal ranges (EvenPlan).
+// kWeighted: workgroups of kWpb worker waves with the per-XCD weighted
+// ranges (StreamPlan); else one single-wave workgroup per worker with equal
+// ranges (EvenPlan).
 template <int D, int G, bool kWeighted>
 __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(AttnArgs a) {
-  using Plan = typename std::conditional<kWeighted, StreamPlan, EvenPlan>::type;
+  using Plan = typename std::conditional<kWeighted, WeightedPlan, EvenPlan>::type;
   constexpr int kWaves = kWeighted ? kWpb : 1;   // workers per workgroup
   const int lane = threadIdx.x & 63;
   const int w = uni(blockIdx.x * kWaves + (int)(threadIdx.x >> 6));
@@ -778,7 +677,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
   const Plan plan = make_plan<Plan>(a, f, a.attn_blocks);
   const long long start = plan.start_of(w);
   if (start >= plan.total) return;
-  const long long end = min(plan.total, start + plan.size_of(w));
+  const long long end = plan.end_of(w);
   int b, excl;
   locate(a, f, start, b, excl);
   if (b < 0) return;
@@ -862,9 +761,8 @@ struct PieceMerge {
 // Pieces of segment (b, g) in the stream-K decomposition (sp: pages of b,
 // excl: units of the sequences before b; sp.np > 0).
 template <typename Plan>
-__device__ __forceinline__ int n_pieces(const Plan& plan, const SeqPages& sp, int excl, int g, int H) {
-  const long long seg0 = (long long)excl * H + (long long)g * sp.len;
-  return (int)(plan.block_of(seg0 + page_start(sp, sp.np - 1)) - plan.block_of(seg0)) + 1;
+__device__ __forceinline__ int pieces_of(const Plan& plan, const SeqPages& sp, int excl, int g, int H) {
+  return n_pieces(plan, sp, (long long)excl * H + (long long)g * sp.len);
 }
 // Units of the sequences before b (wave-uniform).
 __device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts& f, int b) {
@@ -901,8 +799,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
     if (a.lse && t < G) a.lse[row0 + t] = -INFINITY;
     return;
   }
-  const StreamPlan plan = stream_plan(a, f, a.attn_blocks);
-  const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
+  const WeightedPlan plan = stream_plan(a, f, a.attn_blocks);
+  const int nparts = pieces_of(plan, sp, units_before(a, f, b), g, H);
   pm.init();
   for (int p0 = 0; p0 < nparts; p0 += PieceMerge<D, G>::kBatch) {
     if (p0 > 0) pm.load(a, blk0, t, q, p0, nparts - 1);
@@ -953,7 +851,7 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
     return;
   }
   const EvenPlan plan = even_plan(a, f, a.attn_blocks);
-  const int nparts = n_pieces(plan, sp, units_before(a, f, b), g, H);
+  const int nparts = pieces_of(plan, sp, units_before(a, f, b), g, H);
   pm.init();
   for (int p0 = 0; p0 < nparts; p0 += 4 * kB) {
     const int first = p0 + j;
@@ -995,12 +893,12 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
 // loaded before either is merged, so their latencies overlap; 0 for an
 // empty history.
 template <int D, int G>
-__device__ __forceinline__ void merged_pair(const AttnArgs& ref, const StreamPlan& pr, const SeqPages& sr, int er,
-                                            const AttnArgs& itv, const StreamPlan& pi, const SeqPages& si, int ei,
+__device__ __forceinline__ void merged_pair(const AttnArgs& ref, const WeightedPlan& pr, const SeqPages& sr, int er,
+                                            const AttnArgs& itv, const WeightedPlan& pi, const SeqPages& si, int ei,
                                             int b, int g, int t, int q, float (&or_)[4], float (&oi)[4]) {
   constexpr int kB = 4;                          // pieces per batch and cache: both in flight, no spills
   const int H = ref.cv.n_kv_heads;
-  const int nr = sr.np ? n_pieces(pr, sr, er, g, H) : 0, ni = si.np ? n_pieces(pi, si, ei, g, H) : 0;
+  const int nr = sr.np ? pieces_of(pr, sr, er, g, H) : 0, ni = si.np ? pieces_of(pi, si, ei, g, H) : 0;
   const size_t blk0 = ((size_t)b * H + g);
   PieceMerge<D, G, kB> mr, mi;
   mr.init();
@@ -1049,7 +947,7 @@ __global__ __launch_bounds__(512) void distortion_kernel(AttnArgs ref, AttnArgs 
   const int H = ref.cv.n_kv_heads;
   const int q = t / (NM * 16);
   const FirstCounts fr = first_counts(ref), fi = first_counts(itv);
-  const StreamPlan pr = stream_plan(ref, fr, ref.attn_blocks), pi = stream_plan(itv, fi, itv.attn_blocks);
+  const WeightedPlan pr = stream_plan(ref, fr, ref.attn_blocks), pi = stream_plan(itv, fi, itv.attn_blocks);
   const SeqPages sr = seq_pages(ref, fr, b), si = seq_pages(itv, fi, b);
   const int er = units_before(ref, fr, b), ei = units_before(itv, fi, b);
   float worst = 0.0f;

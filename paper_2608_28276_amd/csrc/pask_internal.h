@@ -17,19 +17,15 @@ enum Counter { kCntHi = 0, kCntLo = 1, kCntPos = 2, kCntDrop = 3, kCntForced = 4
 constexpr int kCounterStride = 8;
 constexpr int kPage = 16;          // tokens per page
 constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW vector
-// Units a LOW page weighs in the attention kernel's work split; a HIGH page
-// weighs 32.  Bytes alone would give 9, but with the memory system saturated
-// a page iteration costs about the same time whatever its size, and equal
-// weights measure fastest.
-#ifndef PASK_WEIGHT_LO
-#define PASK_WEIGHT_LO 32
-#endif
 // Range an attention worker on an odd-numbered XCD takes, in sixteenths of
 // an even-XCD worker's: measured per-XCD finish times show the odd XCDs
 // streaming pages about 10% slower (two boxes, every call).  With four
 // workers per workgroup 15 and 14 tie on the batch-64 Qwen3-4B call, 15 is
 // 2% faster on the int4-heavy prompt-side call and 0.4% slower on the
-// Qwen3-32B-shaped one; 13 is slower on all.
+// Qwen3-32B-shaped one; 13 is slower on all.  Equal ranges (16) measured
+// 1.8% slower on the batch-64 call (202.6 against 198.9 us, interleaved in
+// one process), and so did ranges left to chunks taken at run time from a
+// counter (2/16 of the work: 208.7 us; 4/16: 218.0 us).
 #ifndef PASK_ODD_WEIGHT
 #define PASK_ODD_WEIGHT 15
 #endif

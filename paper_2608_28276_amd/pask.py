@@ -33,6 +33,7 @@ PASK_FLAG_SEQ_CAPACITY = 1 << 3
 PASK_FLAG_BAD_COUNT = 1 << 4
 PASK_FLAG_BAD_STATE = 1 << 5
 PASK_FLAG_NO_BUDGET = 1 << 6
+PASK_FLAG_WORKSPACE = 1 << 7
 PASK_APPEND_KEEP_ALL = 1 << 0
 
 PASK_MAX_TAGS, PASK_MAX_GROUPS, PASK_MAX_LAYERS, PASK_MAX_STATES = 64, 16, 128, 64
