@@ -147,11 +147,14 @@ def plan_pool_pages(cfg, P, tags, pol, ptags, online: bool):
     return hi + L * B, lo + L * B                                            # + one spare page per store
 
 
-def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, ptags=None):
+def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, ptags=None, graph=False):
     """Times the decode step at each position t of `positions` (generated
     tokens persisted before the first warm-up step; ascending): the tokens up
     to t are bulk-appended untimed, then `warmup` steps, then `steps` timed
-    steps.  Returns one result per position."""
+    steps.  With `graph`, `steps` more steps follow, each a replay of one HIP
+    graph holding the whole step (every layer's append and attention
+    launches), the step's tags copied into the graph's input buffer first.
+    Returns one result per position."""
     import torch
 
     from paper_2608_28276_amd import pask
@@ -162,8 +165,9 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
     B, L, Hq, Hkv, D = cfg.batch, cfg.layers_resident, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     T = cfg.gen_tokens
     positions = sorted(positions)
-    assert positions[0] >= 0 and positions[-1] + warmup + steps <= T, "not enough generated tokens for the steps"
-    assert all(b >= a + warmup + steps for a, b in zip(positions, positions[1:])), "timed ranges overlap"
+    per_pos = warmup + steps * (2 if graph else 1)
+    assert positions[0] >= 0 and positions[-1] + per_pos <= T, "not enough generated tokens for the steps"
+    assert all(b >= a + per_pos for a, b in zip(positions, positions[1:])), "timed ranges overlap"
     hi_pages, lo_pages = plan_pool_pages(cfg, P, tags, pol, ptags, online=states is not None)
     max_tok = int(P.max()) + T
     sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=cfg.n_layers, n_q_heads=Hq, n_kv_heads=Hkv,
@@ -225,24 +229,50 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
     import ctypes as C
     pol_ref, cache_ref = C.byref(pol_c), C.byref(cache_c)
 
-    def step(t, events=None):
+    def step(t, events=None, stream=None, tp=None, sp=None):
         # One decode step: per layer, persist the step's token (one-token append
         # kernel), then the attention kernel over the layer's persisted history.
-        tp = tags_t[t].data_ptr()
-        sp = None if states_t is None else states_t[t].data_ptr()
+        sptr_ = sptr if stream is None else stream
+        if tp is None:
+            tp = tags_t[t].data_ptr()
+            sp = None if states_t is None else states_t[t].data_ptr()
         for layer in range(L):
             st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, sp, kp[layer], vp[layer], 0,
-                                    sptr)
+                                    sptr_)
             if st != 0:
                 raise pask.PaskError(st, "pask_kv_append")
             if events is not None:
-                events[layer][0].record(sptr)
+                events[layer][0].record(sptr_)
             st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, None, None, None,
-                                      None, C.c_float(scale), hint, ws, ws_bytes, sptr)
+                                      None, C.c_float(scale), hint, ws, ws_bytes, sptr_)
             if st != 0:
                 raise pask.PaskError(st, "pask_decode_attn")
             if events is not None:
-                events[layer][1].record(sptr)
+                events[layer][1].record(sptr_)
+
+    def graph_steps(t0):
+        """`steps` decode steps from t0 as replays of one captured step."""
+        tags_cur = torch.empty(B, dtype=torch.uint8, device=dev)
+        states_cur = None if states_t is None else torch.empty(B, dtype=torch.uint8, device=dev)
+        tags_cur.copy_(tags_t[t0])
+        if states_cur is not None:
+            states_cur.copy_(states_t[t0])
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            cap = torch.cuda.current_stream(dev).cuda_stream
+            step(None, stream=cap, tp=tags_cur.data_ptr(),
+                 sp=None if states_cur is None else states_cur.data_ptr())
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for i in range(steps):
+            tags_cur.copy_(tags_t[t0 + i])
+            if states_cur is not None:
+                states_cur.copy_(states_t[t0 + i])
+            gr.replay()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        del gr
+        return wall
 
     W = int(pol.recent_window)
     kv_bytes = lambda c: c[..., 0] * mH + c[..., 1] * mL + np.minimum(c[..., 2], W) * mH   # stores + window
@@ -270,6 +300,13 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
         wall = time.perf_counter() - w0
         t += warmup + steps
         cnt1 = sess.counters()[:B, :L].cpu().numpy().astype(np.int64)
+        graph_res = None
+        if graph:
+            gwall = graph_steps(t)
+            t += steps
+            graph_res = dict(tokens_per_s=round(B * steps / gwall, 1), ms_per_step=round(gwall / steps * 1e3, 4),
+                             us_per_layer=round(gwall / steps / L * 1e6, 2))
+            log(f"t={t - steps}: HIP graph of the step: {graph_res}")
         call_ms = np.array([[e[0].elapsed_ms(e[1]) for e in ev] for ev in events])   # [steps, L]
         st, status, _ = sess.stats(batch=B)
         if status != 0:
@@ -296,6 +333,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
             c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
             step_gbs=bytes_per_step / (wall / steps) / 1e9,
             mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()), prompt_append=prompt_append,
+            graph=graph_res,
         )
         log(f"t={pos}: {res['tokens_per_s']:.0f} tokens/s, call {res['avg_call_us']:.1f} us, "
             f"{achieved:.0f} GB/s algorithmic")
@@ -612,6 +650,8 @@ def main():
                     help="measure the attention-output distortion (Eq. 4) of one bucket instead "
                          "(ACTION 0 = DROP, 1 = RETAIN-LOW)")
     ap.add_argument("--no-probe", action="store_true", help="skip the on-device read / copy probes")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step as replays of one HIP graph (after the eager steps; one position)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (counter calibration)")
     args = ap.parse_args()
@@ -626,10 +666,11 @@ def main():
     cfg0 = CONFIGS[args.config]
     beta = args.budget if args.budget is not None else (cfg0.budgets[0] if len(cfg0.budgets) == 1 else 0.33)
     t_default = min(512, cfg0.gen_tokens // 2)
-    if args.t_start is None:
+    if args.t_start is None and not args.graph:
         args.t_start = t_default
         positions = sorted({0, t_default, cfg0.gen_tokens - args.warmup - args.steps})
     else:
+        args.t_start = t_default if args.t_start is None else args.t_start
         positions = [args.t_start]
     cfg, P, tags, pol, ptags = build_workload(args.config, beta)
     pol.recent_window = args.window
@@ -664,7 +705,7 @@ def main():
                          "bytes_per_launch": round(d["call_bytes"]), "avg_launch_us": round(d["avg_call_us"], 2)},
             "cpu_baseline": None}), flush=True)
         return
-    runs = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, positions, states, ptags)
+    runs = gpu_leg(cfg, P, tags, pol, args.steps, args.warmup, positions, states, ptags, graph=args.graph)
     g = next(r for r in runs if r["t"] == args.t_start)
     log(f"gpu: {g['tokens_per_s']:.0f} tokens/s, {g['ms_per_step']:.2f} ms/step, call {g['avg_call_us']:.1f} us, "
         f"{g['achieved']:.0f} GB/s algorithmic")
@@ -711,6 +752,7 @@ def main():
             "frac_of_read_probe": round(g["achieved"] / probe["read_gbs"], 4) if probe else None,
             "copy_probe_gbs": probe["copy_gbs"] if probe else None,
         },
+        "graph": g["graph"],
         "positions": [dict(t=r["t"], tokens_per_s=round(r["tokens_per_s"], 1), ms_per_step=round(r["ms_per_step"], 4),
                            avg_call_us=round(r["avg_call_us"], 2), bytes_per_call=round(r["per_call_bytes"]),
                            achieved_gbs=round(r["achieved"], 1), frac=round(r["achieved"] / HBM_PEAK_GBS, 4))
