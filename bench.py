@@ -102,6 +102,7 @@ class HipEvent:
             hip.hipEventDestroy.argtypes = [C.c_void_p]
             HipEvent._hip = hip
         self._e = C.c_void_p()
+        self._lib = HipEvent._hip      # kept for __del__, which may run after module teardown
         if HipEvent._hip.hipEventCreateWithFlags(C.byref(self._e), self.DISABLE_SYSTEM_FENCE) != 0:
             raise RuntimeError("hipEventCreateWithFlags failed")
 
@@ -118,8 +119,9 @@ class HipEvent:
         return ms.value
 
     def __del__(self):
-        if HipEvent._hip is not None and self._e:
-            HipEvent._hip.hipEventDestroy(self._e)
+        lib = getattr(self, "_lib", None)
+        if lib is not None and self._e:
+            lib.hipEventDestroy(self._e)
 
 
 def plan_pool_pages(cfg, P, tags, pol, ptags, online: bool):

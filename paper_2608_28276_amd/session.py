@@ -18,7 +18,8 @@ class PaskSession:
 
     def __init__(self, policy_blob: bytes, *, max_batch: int, n_layers: int, n_q_heads: int, n_kv_heads: int,
                  head_dim: int, max_tokens_per_seq: int, hi_pages: int, lo_pages: int,
-                 max_ctx_hint: int | None = None, device: str = "cuda:0", extra_bytes: int = 0):
+                 max_ctx_hint: int | None = None, device: str = "cuda:0", extra_bytes: int = 0,
+                 prefill: int | None = None):
         self.device = torch.device(device)
         # the recent window W is the table's (blob header word at byte 24)
         self.window = struct.unpack_from("<I", bytes(policy_blob[:28]), 24)[0] if len(policy_blob) >= 28 else 0
@@ -32,12 +33,19 @@ class PaskSession:
             raise pask.PaskError(pask.PASK_E_SHAPE, "pask_cache_bytes")
         self.layout = pask.pask_cache_layout_query(self.geom)
         # extra_bytes: room after the cache for out-of-bounds canaries in tests.
+        # prefill: a byte written over the whole buffer and the workspace before
+        # pask_cache_init (tests: no result may depend on bytes the library has
+        # not written).
         self.buf = torch.empty(self.nbytes + extra_bytes, dtype=torch.uint8, device=self.device)
+        if prefill is not None:
+            self.buf.fill_(prefill)
         self.cache = pask.pask_cache()
         pask.pask_cache_init(self.cache, self.geom, self.buf, self.nbytes, self.stream)
         self.max_ctx_hint = max_ctx_hint or max_tokens_per_seq
         self.ws_bytes = pask.pask_workspace_bytes(self.geom, max_batch, self.max_ctx_hint)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        if prefill is not None:
+            self.ws.fill_(prefill)
         self.softmax_scale = float(torch.tensor(1.0 / math.sqrt(head_dim), dtype=torch.float32))
 
     @property

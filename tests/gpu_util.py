@@ -59,7 +59,7 @@ class Scenario:
 
     def __init__(self, pol, *, B, L, Hq, Hkv, D, prompt_lens, gen_tags, seed, prompt_tags=None,
                  max_ctx_hint=None, hi_pages=None, lo_pages=None, extra_bytes=0, outliers=0, gen_states=None,
-                 expect_flags=0, q_scale=1.0, v_scale=1.0):
+                 expect_flags=0, q_scale=1.0, v_scale=1.0, prefill=None):
         from paper_2608_28276_amd.session import PaskSession
         self.pol, self.B, self.L, self.Hq, self.Hkv, self.D = pol, B, L, Hq, Hkv, D
         self.P = np.asarray(prompt_lens, dtype=np.int64)
@@ -78,7 +78,8 @@ class Scenario:
             lo_pages = L * pages((self.P if prompt_tags is not None else np.zeros(B, np.int64)) + self.T)
         self.sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=L, n_q_heads=Hq, n_kv_heads=Hkv,
                                 head_dim=D, max_tokens_per_seq=self.max_tok, hi_pages=hi_pages,
-                                lo_pages=lo_pages, max_ctx_hint=max_ctx_hint, extra_bytes=extra_bytes)
+                                lo_pages=lo_pages, max_ctx_hint=max_ctx_hint, extra_bytes=extra_bytes,
+                                prefill=prefill)
         self.oc = oracle.OracleCache(policy_dict(pol), Hkv, D)
         self.scale = self.sess.softmax_scale
         self.outliers = outliers
