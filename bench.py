@@ -556,12 +556,13 @@ def cpu_model() -> str:
 def kernel_source_digest() -> str:
     """Digest of the attention kernels' code (the kernels the traffic
     counters measure): pask_internal.h (their tuning constants), pask_device.h,
-    then pask_attn.hip, each with its // comments, trailing blanks and empty
-    lines removed, so that a change of comments alone keeps the counters valid."""
+    pask_plan.h (the work split), then pask_attn.hip, each with its //
+    comments, trailing blanks and empty lines removed, so that a change of
+    comments alone keeps the counters valid."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for name in ("pask_internal.h", "pask_device.h", "pask_attn.hip"):
+    for name in ("pask_internal.h", "pask_device.h", "pask_plan.h", "pask_attn.hip"):
         text = open(os.path.join(ROOT, "paper_2608_28276_amd", "csrc", name)).read()
         code = [re.sub(r"//.*$", "", line).rstrip() for line in text.splitlines()]
         h.update("\n".join(line for line in code if line).encode())

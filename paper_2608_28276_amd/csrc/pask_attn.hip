@@ -454,10 +454,11 @@ __device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f,
 constexpr int kWpb = PASK_ATTN_WPB;   // workers (waves) per workgroup of the weighted attention kernel
 using WeightedPlan = StreamPlan<kWpb>;
 constexpr int kMinPagesPerBlock = kUnitTokens / kPage;   // 8 pages: the workspace's piece size
-// Calls with few segments: workers of 4 pages (8 and 2 measured slower at
-// one Qwen3-4B-shaped sequence of 2.5k entries: fewer workers, or more
-// pieces to merge).
+// Calls with few segments: workers of at least 4 pages (8 and 12 measured
+// slower at one Qwen3-4B-shaped sequence of 2.3k entries, 2 slower too), and
+// of at least 1/PASK_SMALL_PIECES of the longest segment.
 constexpr int kSmallMinPages = 4;
+static_assert(PASK_SMALL_PIECES >= 1, "pieces per segment");
 static_assert(PASK_ODD_WEIGHT >= 1 && PASK_ODD_WEIGHT <= 16, "odd-XCD worker weight out of range");
 
 __device__ __forceinline__ void call_totals(const AttnArgs& a, const FirstCounts& f, long long& total, int& mx) {
@@ -480,7 +481,7 @@ __device__ __forceinline__ EvenPlan even_plan(const AttnArgs& a, const FirstCoun
   long long total;
   int mx;
   call_totals(a, f, total, mx);
-  return even_plan_of(total, mx, a.splits, a.min_pages, n_blocks);
+  return even_plan_of(total, mx, min(a.splits, PASK_SMALL_PIECES + 1), a.min_pages, n_blocks);
 }
 template <typename Plan>
 __device__ __forceinline__ Plan make_plan(const AttnArgs& a, const FirstCounts& f, int n_blocks) {

@@ -35,6 +35,19 @@ constexpr int kQGroup = 32;        // elements per fp16 scale of a RETAIN-LOW ve
 #ifndef PASK_ATTN_WPB
 #define PASK_ATTN_WPB 4
 #endif
+// Calls with at most 64 (sequence, KV head) segments take ranges of at least
+// 1/PASK_SMALL_PIECES of the longest segment, so no segment is cut into more
+// than PASK_SMALL_PIECES + 1 pieces (the ranges grow instead).  Interleaved in one
+// process, per call at Qwen3-4B geometry with prompts U{1024..8192} against
+// no cap (pieces of 4 pages): 2 sequences 25.0 -> 20.7 us, 3: 26.5 -> 21.2,
+// 4: 30.2 -> 25.4, 6: 33.5 -> 29.4, 8: 38.3 -> 36.9, one sequence 17.5 ->
+// 16.1 us and one 2.3k-entry sequence unchanged (13.8 / 13.9 us); caps of 16,
+// 24 and 48 were each slower somewhere.  Fewer, longer workers carry less of
+// the per-worker fixed cost (plan, q loads, block tables, partial rows) and
+// leave fewer partials to merge.
+#ifndef PASK_SMALL_PIECES
+#define PASK_SMALL_PIECES 32
+#endif
 #ifndef PASK_UNIT_TOKENS
 #define PASK_UNIT_TOKENS 128
 #endif

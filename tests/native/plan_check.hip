@@ -161,6 +161,9 @@ int main(int argc, char** argv) {
     } else {
       const EvenPlan p = even_plan_of(c.total, c.mx, splits, 4, n);
       bad |= check(c, p, (int)((c.total + p.U - 1) / p.U), splits, "even");
+      const int capped = std::min(splits, 33);     // the attention's ranges of >= 1/32 of the longest segment
+      const EvenPlan pc = even_plan_of(c.total, c.mx, capped, 4, n);
+      bad |= check(c, pc, (int)((pc.total + pc.U - 1) / pc.U), capped, "even, ranges >= 1/32 of the longest segment");
     }
   }
   printf("%s: %lld calls\n", bad ? "FAIL" : "ok", calls);
