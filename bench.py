@@ -201,13 +201,15 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
         del k, v
     torch.cuda.synchronize()
     log(f"prompts persisted in {time.time() - t0:.1f} s")
-    # The prompt's bulk append per layer (plan + pack kernels): algorithmic bytes = K / V read
-    # (bf16), tags read, the stored forms and index-list entries written.
+    # The prompt's bulk append per layer (plan + pack kernels): algorithmic bytes = the K / V rows
+    # of the persisted tokens read (bf16; a released token's row is never read), tags read, the
+    # stored forms and index-list entries written.
     mH = 2 * Hkv * D * 2
     mL = 2 * Hkv * (D // 2 + 2 * (D // 32))
     n_prompt = int(P.sum())
     ap = torch.stack(after_prompt).cpu().numpy().astype(np.int64)        # [L, B, 2]: n_hi, n_lo
-    pa_bytes = (n_prompt * (mH + (1 if ptags is not None else 0)) + ap[..., 0].sum(1) * (mH + 4)
+    kept = ap[..., 0].sum(1) + ap[..., 1].sum(1)                          # [L]
+    pa_bytes = (kept * mH + n_prompt * (1 if ptags is not None else 0) + ap[..., 0].sum(1) * (mH + 4)
                 + ap[..., 1].sum(1) * (mL + 4))                          # [L]
     pa_ms = np.array([e0.elapsed_ms(e1) for e0, e1 in fill_ev])
     prompt_append = dict(tokens_per_layer=n_prompt, us_per_layer=round(float(pa_ms.mean()) * 1e3, 1),
