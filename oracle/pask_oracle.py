@@ -470,7 +470,8 @@ def group_costs(group_of_layer, n_groups: int, n_kv_heads: int, head_dim: int) -
 
 def initial_budget(beta_q: int, t_max: int, m) -> int:
     """R_0 = beta * T_max * sum_c m(H, c) bytes, beta = beta_q / 65536, rounded
-    down (the paper gives no R_0; this build's reading)."""
+    down (the paper gives no R_0: the budget fraction of the bytes of T_max
+    tokens kept HIGH in every layer is the reading taken here)."""
     full = int(np.asarray(m)[:, HIGH].sum())
     return (int(beta_q) * int(t_max) * full) // 65536
 
