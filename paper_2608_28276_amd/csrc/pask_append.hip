@@ -11,9 +11,11 @@
 //   append_pack  copy RETAIN-HIGH K/V (bf16) or quantise-and-pack RETAIN-LOW
 //                K/V (int4, one fp16 scale per 32 elements) into the pages.
 //   append_step  both of the above for one token per sequence (decode).
-//   window       the protected recent window (Section 3.1) variants of the
-//                three, and the online budget controller (Alg. 2) in the plan
-//                and step kernels.
+//   window       the protected recent window (Section 3.1): its plan, step
+//                and fill kernels (the bulk pack is append_pack, reading the
+//                entries that leave the window from their ring slots), and
+//                the online budget controller (Alg. 2) in the plan and step
+//                kernels.
 #include <hip/hip_runtime.h>
 
 #include <limits.h>
@@ -26,7 +28,7 @@
 namespace pask {
 namespace {
 
-constexpr int kPackTokens = 16;   // tokens per block of the recent-window pack and fill kernels
+constexpr int kPackTokens = 16;   // tokens per block of the recent-window fill kernel
 
 // ---------------------------------------------------------------------------
 // reset
@@ -463,7 +465,9 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
 // call's tokens: block (k, store, b) fills page k of the pages of sequence b's
 // store that this call's slots reach (slots n0..n1-1 of the store, n0 saved by
 // the plan kernel, n1 the store's count after it).  Each slot's source token
-// comes from the index list (position - p0), so every page is written whole
+// comes from the index list: row position - p0 of the call's input, or, with a
+// recent window, for an entry from before the call that leaves the window
+// now, its ring slot (position mod W).  So every page is written whole
 // by one block, in the operand order of the attention kernel, with 16-byte
 // stores of consecutive addresses (1 KiB per wave and instruction).
 //   1. Every thread issues its loads at once (non-temporal: read once): the
@@ -581,6 +585,32 @@ __device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& c
     if (t >= tl0 && t < th0) pg[(size_t)((g + page) % H) * PL::kLoHead + y] = s_img[x];
   }
 }
+// A window entry that leaves the recent window in a bulk append: its bf16 K
+// and V sit in its window slot ws = pos mod W, slot ws % 16 of a HIGH-layout
+// page of the (sequence, layer)'s window ring.  ring_head: KV head g of that
+// page; ring_k_chunk / ring_v_chunk: the 16-byte chunk c (dims 8c .. 8c + 7)
+// of slot t, as a row of the call's input holds it.
+template <int D>
+__device__ __forceinline__ const uint8_t* ring_head(const CacheView& cv, int b, int layer, int ws, int g) {
+  const int page = (b * cv.n_layers + layer) * cv.ring_pp + ws / kPage;
+  return cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % cv.n_kv_heads) * PageLayout<D>::kHiHead;
+}
+__device__ __forceinline__ uint4 ring_k_chunk(const uint8_t* head, int t, int c) {   // d = 32i + 8q + j, c = 4i + q
+  return *reinterpret_cast<const uint4*>(head + ((c / 4) * 64 + (c % 4) * 16 + t) * 16);
+}
+template <int D>
+__device__ __forceinline__ uint4 ring_v_chunk(const uint8_t* head, int t, int c) {
+  const uint16_t* v = reinterpret_cast<const uint16_t*>(head + PageLayout<D>::kHiV);
+  auto at = [&](int d) -> uint32_t {             // element (t, d = 16m + e) of the V tile
+    const int m = d / 16, e = d % 16;
+    return v[(((m >> 1) * 64 + (t / 4) * 16 + e) * 2 + (m & 1)) * 4 + t % 4];
+  };
+  uint32_t w[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) w[u] = at(8 * c + 2 * u) | (at(8 * c + 2 * u + 1) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 constexpr int kLdsRowPad = 16;                     // bytes after each staged V row (bank spread)
 
 template <int D>
@@ -592,7 +622,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
   constexpr int kIt = kMaxChunks / kPackThreads;
   constexpr int kLdsRow = 8 * D * 2 + kLdsRowPad;
   __shared__ __align__(16) uint8_t s_v[kPage * kLdsRow];
-  __shared__ int s_src[kPage];                     // token of each slot in this call, or -1
+  __shared__ int s_src[kPage];                     // per slot: input row, -2 - ring slot, or -1 (no new entry)
   const CacheView& cv = a.cv;
   const int b = blockIdx.z, st = blockIdx.y;
   const int H = cv.n_kv_heads;
@@ -609,8 +639,10 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
     const int t = (int)threadIdx.x;
     int j = -1;
     if (t >= tl0 && t < th0) {
-      j = index_list_of(cv, b, a.layer, st)[pidx * kPage + t] - p0;
-      if (j < 0 || j >= a.max_new) j = -1;         // never outside the call's rows
+      const int pos = index_list_of(cv, b, a.layer, st)[pidx * kPage + t];
+      const int r = pos - p0;
+      if (r >= 0 && r < a.max_new) j = r;          // row r of the call's input
+      else if (r < 0 && r >= -cv.window) j = -2 - pos % cv.window;   // leaving the window: its ring slot
     }
     s_src[t] = j;
   }
@@ -632,6 +664,9 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
       const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
       const int j = s_src[t];
       if (j >= 0) vx[it] = stream_load16(reinterpret_cast<const uint8_t*>(vbase + (size_t)j * row + col * 8));
+      else if (j <= -2)
+        vx[it] = ring_v_chunk<D>(ring_head<D>(cv, b, a.layer, -2 - j, col / kRowChunks), (-2 - j) % kPage,
+                                 col % kRowChunks);
     }
   }
   if (is_hi) {
@@ -644,6 +679,8 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
         const int j = s_src[t];
         if (j >= 0)
           kx[it] = stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + g * D + (4 * i + q) * 8));
+        else if (j <= -2)
+          kx[it] = ring_k_chunk(ring_head<D>(cv, b, a.layer, -2 - j, g), (-2 - j) % kPage, 4 * i + q);
       }
     }
   } else {
@@ -654,6 +691,9 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
         const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
         const int j = s_src[t];
         if (j >= 0) kx[it] = stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + col * 8));
+        else if (j <= -2)
+          kx[it] = ring_k_chunk(ring_head<D>(cv, b, a.layer, -2 - j, col / kRowChunks), (-2 - j) % kPage,
+                                col % kRowChunks);
       }
     }
   }
@@ -683,7 +723,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
       if (e < n_chunks) {
         const int gi = e >> 6, t = e & 15;
         const int g = gi / NG, i = gi % NG;
-        if (s_src[t] >= 0)
+        if (s_src[t] != -1)                        // a new entry (input row or ring slot)
           *reinterpret_cast<uint4*>(pg + (size_t)((g + page) % H) * PL::kHiHead + (size_t)(i * 64 + (e & 63)) * 16) =
               kx[it];
       }
@@ -863,8 +903,9 @@ __device__ __forceinline__ void read_hi_token(const CacheView& cv, int page, int
 // decisions go to ring_act (after every read of ring_act in the chunk: the
 // W positions of the window after the call have distinct slots, so no slot
 // still in the window is overwritten).  staging[x] gets the store code of x
-// or -1; the sequence's last two staging words keep p0 and n_fit for the
-// pack and window-fill kernels.
+// or -1; the sequence's last four staging words keep the stores' counts
+// before the call, p0 and n_fit for the pack (append_pack_page_kernel, which
+// reads a leaving window entry from its ring slot) and window-fill kernels.
 template <bool kBudget>
 __global__ __launch_bounds__(256) void append_plan_window_kernel(AppendArgs a) {
   __shared__ uint8_t s_a0[64], s_amin[64];
@@ -904,6 +945,10 @@ __global__ __launch_bounds__(256) void append_plan_window_kernel(AppendArgs a) {
   int32_t* bt[2] = {block_table_of(cv, b, a.layer, kHi), block_table_of(cv, b, a.layer, kLo)};
   int32_t* il[2] = {index_list_of(cv, b, a.layer, kHi), index_list_of(cv, b, a.layer, kLo)};
   int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
+  if (threadIdx.x == 0) {                          // for the pack kernel: the stores' counts before the call
+    stg[cv.staging_stride - 4] = nst[0];
+    stg[cv.staging_stride - 3] = nst[1];
+  }
   const bool keep_all = (a.flags & kKeepAll) != 0u;
   const unsigned pool[2] = {(unsigned)cv.hi_pages, (unsigned)cv.lo_pages};
   __syncthreads();
@@ -1008,43 +1053,6 @@ __global__ __launch_bounds__(256) void append_plan_window_kernel(AppendArgs a) {
   if (flags) atomicOr(cv.status, flags);
 }
 
-// Persist the entries the plan marked (x < n_out): from the window (read
-// into LDS first) or from the call's input rows.
-template <int D>
-__global__ __launch_bounds__(256) void append_pack_window_kernel(AppendArgs a) {
-  __shared__ __align__(16) uint16_t s_kv[2][8 * D];   // one window token's K and V rows (Hkv <= 8)
-  const CacheView& cv = a.cv;
-  const int b = blockIdx.y;
-  const int W = cv.window;
-  const int32_t* stg = cv.staging + (size_t)b * cv.staging_stride;
-  const int p0 = stg[cv.staging_stride - 2], n_fit = stg[cv.staging_stride - 1];
-  const int e0 = max(0, p0 - W), nr = p0 - e0;
-  const int n_out = max(e0, p0 + n_fit - W) - e0;
-  const size_t row = (size_t)cv.n_kv_heads * D;
-  for (int xx = 0; xx < kPackTokens; ++xx) {
-    const int x = (int)blockIdx.x * kPackTokens + xx;
-    if (x >= n_out) break;
-    const int code = stg[x];
-    if (code < 0) continue;
-    const int st = code >> 30, slot = code & 0x3FFFFFFF;
-    const int page = block_table_of(cv, b, a.layer, st)[slot / kPage];
-    const uint16_t *kin, *vin;
-    if (x < nr) {
-      const int ws = (e0 + x) % W;
-      read_hi_token<D>(cv, ring_page(cv, b, a.layer, ws / kPage), ws % kPage, s_kv[0], s_kv[1]);
-      __syncthreads();
-      kin = s_kv[0];
-      vin = s_kv[1];
-    } else {
-      kin = a.k + ((size_t)b * a.max_new + (x - nr)) * row;
-      vin = a.v + ((size_t)b * a.max_new + (x - nr)) * row;
-    }
-    if (st == kHi) write_hi<D>(cv, page, slot % kPage, kin, vin);
-    else write_lo<D>(cv, page, slot % kPage, kin, vin);
-    __syncthreads();                                 // s_kv is reused by the next entry
-  }
-}
-
 // The new tokens that stay in the window (the last min(n_fit, W) of the
 // call) into their window slots; after the pack kernel has read the slots
 // they replace.
@@ -1144,13 +1152,14 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
   if (a.cv.window > 0) {
     if (a.states) append_plan_window_kernel<true><<<dim3(a.batch), dim3(256), 0, s>>>(a);
     else append_plan_window_kernel<false><<<dim3(a.batch), dim3(256), 0, s>>>(a);
-    const dim3 gp((a.max_new + a.cv.window + kPackTokens - 1) / kPackTokens, a.batch);
+    // pages of a store this call's leaving entries (at most max_new + W) can reach
+    const dim3 gp((a.max_new + a.cv.window + kPage - 1) / kPage + 1, 2, a.batch);
     const dim3 gf((std::min(a.max_new, a.cv.window) + kPackTokens - 1) / kPackTokens, a.batch);
     if (a.cv.head_dim == 64) {
-      append_pack_window_kernel<64><<<gp, dim3(256), 0, s>>>(a);
+      append_pack_page_kernel<64><<<gp, dim3(kPackThreads), 0, s>>>(a);
       append_window_fill_kernel<64><<<gf, dim3(256), 0, s>>>(a);
     } else {
-      append_pack_window_kernel<128><<<gp, dim3(256), 0, s>>>(a);
+      append_pack_page_kernel<128><<<gp, dim3(kPackThreads), 0, s>>>(a);
       append_window_fill_kernel<128><<<gf, dim3(256), 0, s>>>(a);
     }
     return hipGetLastError();
