@@ -67,18 +67,6 @@ __device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
   const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
   return make_uint4(x[0], x[1], x[2], x[3]);
 }
-// A 16-byte piece of a page a bulk append writes once (read only by later
-// attention calls): non-temporal, so the stream does not displace other lines.
-#ifndef PASK_NT_STORES
-#define PASK_NT_STORES 1
-#endif
-__device__ __forceinline__ void stream_store16(uint8_t* p, const uint4& v) {
-#if PASK_NT_STORES
-  __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
-#else
-  *reinterpret_cast<uint4*>(p) = v;
-#endif
-}
 
 // Page layout, per KV head, chosen so that the MFMA operands of the attention
 // kernel arrive by fully coalesced loads: load instruction i of lane l = 16q + n
