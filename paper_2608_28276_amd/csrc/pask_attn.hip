@@ -13,8 +13,9 @@
 //   attn_merge   per (sequence, KV head): combine the partials of its pieces
 //                (max, sum, values) into bf16 outputs; zero for empty histories.
 //                Calls with few (sequence, KV head) segments cut them into
-//                pieces of 4 pages and spread each segment's merge over
-//                several single-wave blocks (attn_merge_sliced).
+//                pieces of at least 4 pages and 1/32 of the longest segment
+//                and spread each segment's merge over several single-wave
+//                blocks (attn_merge_sliced).
 //   distortion   the attention-output distortion of Eq. 4: the partials of a
 //                reference and an intervened cache merged in fp32, the squared
 //                distance of the outputs maximised over query heads.
