@@ -5,7 +5,9 @@
 // every bf16 x with s/8 <= |x| <= 9s (both signs), and an approximate
 // reciprocal 1/s moved by up to 4 ulp either way (the device takes it from
 // v_rcp_f32, accurate to 1 ulp); then every bf16 x below s/8 at the exact
-// reciprocal, and s = 0.
+// reciprocal, and s = 0.  Over the same x, s and reciprocals: the bulk pack's
+// fast path (rint(x * 1/s) unless within kNearTie of a tie) gives the exact
+// code wherever it does not defer to quant_code.
 #include <math.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -26,6 +28,9 @@ static int want(float x, float s) {
   return (int)fmin(fmax(q, -7.0), 7.0);
 }
 
+// The near-tie threshold of the bulk pack's fast path (codes8).
+constexpr float kNearTie = 0.49988f;
+
 int main() {
   long n = 0, bad = 0;
   for (uint32_t hs = 1; hs < 0x7C00; ++hs) {        // every positive finite fp16 scale
@@ -43,6 +48,16 @@ int main() {
           ++n;
           if (got != want(xs, s)) {
             if (++bad <= 10) printf("mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, got, want(xs, s));
+          }
+          // The bulk pack's fast path (codes8 in pask_append.hip): rint(x * inv)
+          // clamped, unless |x * inv - rint(x * inv)| > kNearTie sends the lane to
+          // quant_code.  Wherever it keeps the fast code, that code must be the
+          // exact one.
+          const float y = xs * inv, c = rintf(y);
+          if (!(fabsf(y - c) > kNearTie)) {
+            const int fast = (int)fminf(fmaxf(c, -7.0f), 7.0f);
+            if (fast != want(xs, s) && ++bad <= 10)
+              printf("fast-path mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, fast, want(xs, s));
           }
         }
       }
