@@ -842,7 +842,10 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
   const size_t blk0 = (size_t)seg * a.splits;
   PieceMerge<D, G, kSlicedBatch> pm;
   constexpr int kB = kSlicedBatch;
-  pm.load(a, blk0, t, q, j, a.splits - 1, 4);    // before the piece count is known
+  // Before the piece count is known: slots up to the most a segment can have
+  // (the ranges' 1/PASK_SMALL_PIECES floor), not the workspace's last, so the
+  // loads past the count re-read one slot instead of stale partials.
+  pm.load(a, blk0, t, q, j, min(a.splits, PASK_SMALL_PIECES + 1) - 1, 4);
   const FirstCounts f = first_counts(a);
   const SeqPages sp = seq_pages(a, f, b);
   if (sp.np == 0) {
