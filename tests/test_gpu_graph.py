@@ -24,11 +24,15 @@ def _gpu():
     import paper_2608_28276_amd.pask  # noqa: F401  (fails loudly when libpask.so is missing)
 
 
-@pytest.mark.parametrize("B,Hq,Hkv,D", [(1, 32, 8, 128), (12, 32, 8, 128), (3, 8, 2, 64)])
-def test_graph_replays_match_eager_steps(B, Hq, Hkv, D):
+@pytest.mark.parametrize("B,Hq,Hkv,D,noalloc", [(1, 32, 8, 128, False), (12, 32, 8, 128, False), (3, 8, 2, 64, False),
+                                                 (12, 32, 8, 128, True), (1, 32, 8, 128, True)])
+def test_graph_replays_match_eager_steps(B, Hq, Hkv, D, noalloc):
+    """noalloc: the captured calls are pask_decode_attn_noalloc (no workspace
+    argument: the callers it is for include code under graph capture), the
+    eager twin's attention-only calls too."""
     from paper_2608_28276_amd.session import PaskSession
     from workload.policy import pack_blob
-    say(f"case: HIP graph of the decode step, B={B} Hq={Hq} Hkv={Hkv} D={D}")
+    say(f"case: HIP graph of the decode step, B={B} Hq={Hq} Hkv={Hkv} D={D} noalloc={noalloc}")
     L, T, R = 2, 30, 5
     rng = np.random.default_rng(B + D)
     P = rng.integers(40, 900, size=B)
@@ -65,9 +69,13 @@ def test_graph_replays_match_eager_steps(B, Hq, Hkv, D):
 
     def calls():
         for layer in range(L):
-            sess.decode(layer, q_cur[layer], out[layer], lse[layer], tags_cur, k_cur[layer], v_cur[layer])
+            fn = sess.decode_noalloc if noalloc else sess.decode
+            fn(layer, q_cur[layer], out[layer], lse[layer], tags_cur, k_cur[layer], v_cur[layer])
 
     load(T - R)
+    if noalloc:                                              # the scratch's address is taken before capture
+        o = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
+        eager.sess.decode_noalloc(0, eager.q(0, T - R).to(dev), o)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):                            # recorded, not run
@@ -86,7 +94,8 @@ def test_graph_replays_match_eager_steps(B, Hq, Hkv, D):
         for layer in range(L):
             o = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
             l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-            eager.sess.decode(layer, eager.q(layer, t).to(dev), o, l)   # attention only: same history
+            attn = eager.sess.decode_noalloc if noalloc else eager.sess.decode
+            attn(layer, eager.q(layer, t).to(dev), o, l)             # attention only: same history
             want_o.append(o)
             want_l.append(l)
         torch.cuda.synchronize()
