@@ -45,6 +45,14 @@
  *     attention that must see it).  Distinct caches may run concurrently.
  *   - Device-side anomalies do not fail a launch: they set sticky bits in the
  *     cache's status word (PASK_FLAG_*), reported by pask_cache_stats.
+ *   - Debug mode: with the environment variable PASK_DEBUG set to anything
+ *     but "" or "0" when the library is first used, every entry point that
+ *     launches kernels waits for its stream before returning, returns
+ *     PASK_E_HIP if a launch or a kernel failed, and writes to stderr the
+ *     entry point with the HIP error, or with the cache's status flags when
+ *     they differ from the last ones written.  Return codes are otherwise
+ *     unchanged (flags are still reported by pask_cache_stats), and calls on
+ *     a stream being captured into a graph are not checked.
  */
 #ifndef PASK_H
 #define PASK_H

@@ -3,9 +3,12 @@
 // before the first HIP call of an entry point.
 #include <math.h>
 #include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <vector>
 
 #include <hip/hip_runtime_api.h>
@@ -107,6 +110,54 @@ CacheView view_of(const pask_cache* c) {
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// PASK_DEBUG set to anything but "" or "0" when the library is first used
+// turns on a check after every entry point that launches kernels: it waits for
+// the stream, turns a launch or execution error into PASK_E_HIP, and writes to
+// stderr the entry point with the HIP error, or with the cache's device status
+// flags when they differ from the last ones reported.  A failure is then named
+// by the call that caused it, not by a later synchronisation.  Calls on a
+// stream that is being captured into a graph are not checked.  Off by default:
+// each check costs a host round trip.
+bool debug_on() {
+  static const bool on = [] {
+    const char* e = getenv("PASK_DEBUG");
+    return e && e[0] && strcmp(e, "0") != 0;
+  }();
+  return on;
+}
+
+int debug_check(const char* where, int st, const pask_cache* const* caches, int n_caches, hipStream_t stream) {
+  if (st != PASK_OK || !debug_on()) return st;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e == hipSuccess && cs != hipStreamCaptureStatusNone) return st;
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) {
+    fprintf(stderr, "pask: %s: %s\n", where, hipGetErrorString(e));
+    return PASK_E_HIP;
+  }
+  static std::atomic<uint32_t> reported{0};
+  for (int i = 0; i < n_caches; ++i) {
+    pask_cache_layout L;
+    layout_of(&caches[i]->geom, &L);
+    uint32_t word = 0;
+    const uint8_t* status = static_cast<const uint8_t*>(caches[i]->base) + L.status_off;
+    if (hipMemcpyAsync(&word, status, sizeof(word), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess) {
+      fprintf(stderr, "pask: %s: status word not readable\n", where);
+      return PASK_E_HIP;
+    }
+    if (word != 0 && reported.exchange(word) != word)
+      fprintf(stderr, "pask: %s: device status flags 0x%x\n", where, word);
+  }
+  return st;
+}
+
+int debug_check(const char* where, int st, const pask_cache* cache, hipStream_t stream) {
+  return debug_check(where, st, &cache, 1, stream);
+}
 
 int check_cache(const pask_cache* c) {
   if (!c || !c->base) return PASK_E_ARG;
@@ -265,7 +316,9 @@ int decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int
   a.batch = batch;
   a.n_q_heads = g.n_q_heads;
   a.splits = splits;
-  return pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+  return debug_check(use_scratch ? "pask_decode_attn_noalloc" : "pask_decode_attn",
+                     pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP,
+                     cache, stream);
 }
 
 }  // namespace
@@ -383,7 +436,9 @@ int pask_cache_reset(pask_cache* cache, hipStream_t stream) {
   const int st = check_cache(cache);
   if (st != PASK_OK) return st;
   const CacheView v = view_of(cache);
-  return pask::launch_reset(v, cache->geom.max_batch, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+  return debug_check("pask_cache_reset",
+                     pask::launch_reset(v, cache->geom.max_batch, stream) == hipSuccess ? PASK_OK : PASK_E_HIP, cache,
+                     stream);
 }
 
 int pask_cache_init(pask_cache* cache, const pask_geom* geom, void* base, size_t bytes, hipStream_t stream) {
@@ -428,7 +483,8 @@ int pask_kv_append(const pask_policy* policy, pask_cache* cache, int32_t layer, 
   a.batch = batch;
   a.max_new = max_new;
   a.flags = flags;
-  return pask::launch_append(a, stream) == hipSuccess ? PASK_OK : PASK_E_HIP;
+  return debug_check("pask_kv_append", pask::launch_append(a, stream) == hipSuccess ? PASK_OK : PASK_E_HIP, cache,
+                     stream);
 }
 
 int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch, int32_t t_max,
@@ -468,7 +524,7 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
   const bool launched = pask::launch_budget_init(v, batch, (int64_t)r0, stream) == hipSuccess;
   // `t` lives on this frame: the copy must be done before returning.
   const bool synced = hipStreamSynchronize(stream) == hipSuccess;
-  return launched && synced ? PASK_OK : PASK_E_HIP;
+  return debug_check("pask_budget_init", launched && synced ? PASK_OK : PASK_E_HIP, cache, stream);
 }
 
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint) {
@@ -533,9 +589,12 @@ int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer,
     a[i].n_q_heads = g.n_q_heads;
     a[i].splits = splits;
   }
-  return pask::launch_distortion(a[0], a[1], g.n_q_heads / g.n_kv_heads, in_s_dev, dist_dev, stream) == hipSuccess
-             ? PASK_OK
-             : PASK_E_HIP;
+  const int launched =
+      pask::launch_distortion(a[0], a[1], g.n_q_heads / g.n_kv_heads, in_s_dev, dist_dev, stream) == hipSuccess
+          ? PASK_OK
+          : PASK_E_HIP;
+  const pask_cache* both[2] = {ref, intervened};
+  return debug_check("pask_attn_distortion", launched, both, 2, stream);
 }
 
 int pask_cache_stats(const pask_policy* policy, const pask_cache* cache, int32_t batch, pask_stats* out,

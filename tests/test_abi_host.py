@@ -381,3 +381,17 @@ def test_status_strings():
     assert pask.pask_status_string(0) == "ok"
     assert "policy" in pask.pask_status_string(pask.PASK_E_POLICY)
     assert pask.pask_status_string(-99) == "unknown status"
+
+
+def test_debug_mode_keeps_the_validation_codes():
+    """PASK_DEBUG=1 adds checks after launches only: every argument check
+    still returns its code before any HIP call (the library reads the
+    variable once, hence a process of its own)."""
+    import subprocess
+    import sys
+    env = dict(os.environ, PASK_DEBUG="1")
+    p = subprocess.run([sys.executable, "-m", "pytest", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
+                        os.path.join(ROOT, "tests", "test_abi_host.py"), "-k", "validation_before_any_hip_call"],
+                       cwd=ROOT, env=env, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, timeout=300)
+    assert p.returncode == 0, p.stdout[-3000:]
+    assert re.search(r"\b3 passed\b", p.stdout), p.stdout[-1000:]
