@@ -234,21 +234,20 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
     pol_ref, cache_ref = C.byref(pol_c), C.byref(cache_c)
 
     def step(t, events=None, stream=None, tp=None, sp=None):
-        # One decode step: per layer, persist the step's token (one-token append
-        # kernel), then the attention kernel over the layer's persisted history.
+        # One decode step: per layer, one pask_decode_attn call that persists the
+        # step's token and attends the layer's history including it (the
+        # attention and merge kernels persist the token themselves for at most
+        # 64 sequences without a recent window or parser states; otherwise the
+        # one-token append kernel runs first, inside the same call).
         sptr_ = sptr if stream is None else stream
         if tp is None:
             tp = tags_t[t].data_ptr()
             sp = None if states_t is None else states_t[t].data_ptr()
         for layer in range(L):
-            st = lib.pask_kv_append(pol_ref, cache_ref, layer, B, None, 1, tp, sp, kp[layer], vp[layer], 0,
-                                    sptr_)
-            if st != 0:
-                raise pask.PaskError(st, "pask_kv_append")
             if events is not None:
                 events[layer][0].record(sptr_)
-            st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, None, None, None,
-                                      None, C.c_float(scale), hint, ws, ws_bytes, sptr_)
+            st = lib.pask_decode_attn(pol_ref, cache_ref, layer, B, qp[layer], op[layer], None, tp, sp, kp[layer],
+                                      vp[layer], C.c_float(scale), hint, ws, ws_bytes, sptr_)
             if st != 0:
                 raise pask.PaskError(st, "pask_decode_attn")
             if events is not None:
@@ -316,10 +315,11 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
         if status != 0:
             raise RuntimeError(f"device flags set: {st.device_flags:#x}")
 
-        # Algorithmic bytes of one attention launch, averaged over the timed ones:
-        # every persisted entry read once (counts grow linearly over the region,
-        # each launch sees its step's token), q read, o written.  The one-token
-        # append adds the step's token in its stored form and one list entry.
+        # Algorithmic bytes of one call, averaged over the timed ones: every
+        # persisted entry read once (counts grow linearly over the region, each
+        # call sees its step's token), q read, o written; and the append of the
+        # step's token: its K and V rows read, its stored form and one list
+        # entry written.
         read = 0.5 * (kv_bytes(cnt0) + kv_bytes(cnt1)).sum(axis=0)      # per layer, summed over seqs
         qo = 2 * 2 * B * Hq * D
         attn_bytes = read + qo                                             # [L]
@@ -328,12 +328,13 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
         if W:                                    # the token entering the window and the one leaving it
             new_tok = new_tok + 2 * B * mH
         append_bytes = new_tok + 4 * stored + 2 * B * Hkv * D * 2         # stored form + lists + k/v read
-        bytes_per_step = float((attn_bytes + append_bytes).sum())
-        avg_attn_s = float(call_ms.mean()) / 1e3
-        achieved = float(attn_bytes.mean()) / avg_attn_s / 1e9
+        call_bytes = attn_bytes + append_bytes                             # [L]
+        bytes_per_step = float(call_bytes.sum())
+        avg_call_s = float(call_ms.mean()) / 1e3
+        achieved = float(call_bytes.mean()) / avg_call_s / 1e9
         res = dict(
             t=pos, tokens_per_s=B * steps / wall, ms_per_step=wall / steps * 1e3, achieved=achieved,
-            avg_call_us=avg_attn_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(attn_bytes.mean()),
+            avg_call_us=avg_call_s * 1e6, bytes_per_step=bytes_per_step, per_call_bytes=float(call_bytes.mean()),
             c_kv_governed=st.c_kv_governed, c_kv_all=st.c_kv_all,
             step_gbs=bytes_per_step / (wall / steps) / 1e9,
             mean_entries=float((cnt1[..., 0] + cnt1[..., 1]).mean()), prompt_append=prompt_append,
@@ -571,14 +572,21 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def attn_kernels(cfg) -> str:
-    """The kernels of one pask_decode_attn call: calls with at most 64
-    (sequence, KV head) segments use the equal-range attention and the
-    sliced merge, larger ones the per-XCD weighted attention and the merge."""
+def attn_kernels(cfg, window: int = 0, controller: bool = False) -> str:
+    """The kernels of one pask_decode_attn call with its step's token: calls
+    with at most 64 (sequence, KV head) segments use the equal-range attention
+    and the sliced merge, larger ones the per-XCD weighted attention and the
+    merge; the one-token append kernel comes first when the call cannot
+    persist the token in those (more than 64 sequences, a recent window or
+    parser states)."""
     D, G = cfg.head_dim, cfg.group_size
     if cfg.batch * cfg.n_kv_heads <= 64:
-        return f"attn_kernel<{D}, {G}, false> + attn_merge_sliced_kernel<{D}, {G}>"
-    return f"attn_kernel<{D}, {G}, true> + attn_merge_kernel<{D}, {G}>"
+        k = f"attn_kernel<{D}, {G}, false> + attn_merge_sliced_kernel<{D}, {G}>"
+    else:
+        k = f"attn_kernel<{D}, {G}, true> + attn_merge_kernel<{D}, {G}>"
+    if cfg.batch > 64 or window or controller:
+        k = f"append_step{'_window' if window else ''}_kernel<{D}> + " + k
+    return k
 
 
 def prompt_desc(cfg) -> str:
@@ -751,7 +759,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(g["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(g["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic_record(workload),
-            "kernel": attn_kernels(cfg) + " (one pask_decode_attn call)",
+            "kernel": attn_kernels(cfg, args.window, bool(args.controller)) + " (one pask_decode_attn call)",
             "bytes_per_launch": round(g["per_call_bytes"]), "avg_launch_us": round(g["avg_call_us"], 2),
             "read_probe_gbs": probe["read_gbs"] if probe else None,
             "frac_of_read_probe": round(g["achieved"] / probe["read_gbs"], 4) if probe else None,

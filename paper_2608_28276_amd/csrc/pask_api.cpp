@@ -236,19 +236,21 @@ int splits_for(int32_t max_ctx_hint, int64_t segments) {
 
 
 struct WsLayout {
-  uint64_t o_off, ml_off, total;
+  uint64_t o_off, ml_off, seq_off, total;
 };
 
 // Partials of the attention pieces: per (sequence, KV head, piece) a block of
 // G4 = max(G, 4) query-head rows of head_dim fp32 values, and G4 (max, sum)
-// pairs.
+// pairs; then 8 int32 per sequence for a call that persists its step's
+// entries (the counts its attention planned with and each entry's outcome).
 WsLayout ws_layout(const pask_geom* g, int32_t batch, int splits) {
   WsLayout w;
   const uint64_t group = (uint64_t)std::max(4, g->n_q_heads / g->n_kv_heads);
   const uint64_t blocks = (uint64_t)batch * g->n_kv_heads * splits;
   w.o_off = 0;
   w.ml_off = align_up(blocks * group * g->head_dim * 4, kAlignSmall);
-  w.total = align_up(w.ml_off + blocks * group * 2 * 4, kAlignSmall);
+  w.seq_off = align_up(w.ml_off + blocks * group * 2 * 4, kAlignSmall);
+  w.total = align_up(w.seq_off + (uint64_t)batch * 8 * 4, kAlignSmall);
   return w;
 }
 
@@ -289,7 +291,11 @@ int decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int
     return PASK_E_HIP;
   }
 
-  if (tags_new_dev) {
+  // The step's entries are persisted by the attention call itself (no
+  // one-token append kernel) for at most kFusedMaxBatch sequences without a
+  // recent window or parser states; otherwise by the append kernel first.
+  const bool fused = tags_new_dev && !states_new_dev && g.recent_window == 0 && batch <= pask::kFusedMaxBatch;
+  if (tags_new_dev && !fused) {
     pask::AppendArgs a;
     a.cv = view_of(cache);
     a.tab = column_of(policy, layer);
@@ -316,6 +322,11 @@ int decode_attn(const pask_policy* policy, pask_cache* cache, int32_t layer, int
   a.batch = batch;
   a.n_q_heads = g.n_q_heads;
   a.splits = splits;
+  a.tags_new = fused ? tags_new_dev : nullptr;
+  a.k_new = fused ? static_cast<const uint16_t*>(k_new_dev) : nullptr;
+  a.v_new = fused ? static_cast<const uint16_t*>(v_new_dev) : nullptr;
+  a.ws_seq = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(ws_dev) + w.seq_off);
+  a.tab = column_of(policy, layer);
   return debug_check(use_scratch ? "pask_decode_attn_noalloc" : "pask_decode_attn",
                      pask::launch_attention(a, g.n_q_heads / g.n_kv_heads, stream) == hipSuccess ? PASK_OK : PASK_E_HIP,
                      cache, stream);
@@ -588,6 +599,10 @@ int pask_attn_distortion(pask_cache* ref, pask_cache* intervened, int32_t layer,
     a[i].batch = batch;
     a[i].n_q_heads = g.n_q_heads;
     a[i].splits = splits;
+    a[i].tags_new = nullptr;
+    a[i].k_new = a[i].v_new = nullptr;
+    a[i].ws_seq = reinterpret_cast<int32_t*>(base + w.seq_off);
+    a[i].tab = pask::TableColumn{};
   }
   const int launched =
       pask::launch_distortion(a[0], a[1], g.n_q_heads / g.n_kv_heads, in_s_dev, dist_dev, stream) == hipSuccess

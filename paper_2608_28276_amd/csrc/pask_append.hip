@@ -60,22 +60,6 @@ __global__ void budget_init_kernel(CacheView cv, int32_t batch, int64_t r0) {
 // decisions and slotting
 // ---------------------------------------------------------------------------
 
-// Action of one token (Eq. 10): the higher of the selected action and the
-// floor of its (tag, group) bucket.  Sinks, keep-all tokens and tags outside
-// the table are RETAIN-HIGH (the latter also flagged).
-__device__ __forceinline__ int decide(const uint8_t* s_a0, const uint8_t* s_amin, uint32_t n_tags,
-                                      uint32_t n_sink, bool keep_all, int tag, int pos,
-                                      bool& forced, bool& bad) {
-  bad = (uint32_t)tag >= n_tags;
-  if (keep_all || (uint32_t)pos < n_sink || bad) {
-    forced = true;
-    return kHigh;
-  }
-  forced = false;
-  const int a0 = s_a0[tag], am = s_amin[tag];
-  return a0 > am ? a0 : am;
-}
-
 // The online controller for one token (Alg. 2 after the lookup; Eq. 9-10):
 // the token's actions in every group start at max(a0, a-) (Eq. 10); while
 // their bytes exceed B = max(0, R - Gamma(s)), the group above its floor whose
@@ -368,46 +352,6 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan_kernel(AppendArgs a)
 // RETAIN-HIGH copy and RETAIN-LOW quantise-and-pack of one token
 // ---------------------------------------------------------------------------
 
-// The scale of a RETAIN-LOW group from its absmax: s = fp16(absmax / 7) with
-// a correctly rounded fp32 division, saturated at 65504, rounded to nearest
-// even; returns its fp16 bits, s as fp32 and an approximation of 1 / s.
-__device__ __forceinline__ uint16_t quant_scale(float absmax, float& s, float& inv) {
-  const _Float16 h = (_Float16)fminf(absmax / 7.0f, 65504.0f);
-  s = (float)h;
-  inv = __builtin_amdgcn_rcpf(s);
-  return __builtin_bit_cast(uint16_t, h);
-}
-// Quantise 4 consecutive elements of a 32-element group held by 8 adjacent
-// lanes (quant_scale of the group's absmax, quant_code of each element).
-// Returns the 4 codes as offset-binary nibbles q + 8 (element i in bits
-// 4i..4i+3; the pages hold codes in this form) and the scale bits.
-__device__ __forceinline__ void quant4(uint32_t x01, uint32_t x23, uint32_t& packed, uint32_t& sbits) {
-  float f[4] = {bf16_lo(x01), bf16_hi(x01), bf16_lo(x23), bf16_hi(x23)};
-  float am = fmaxf(fmaxf(fabsf(f[0]), fabsf(f[1])), fmaxf(fabsf(f[2]), fabsf(f[3])));
-  am = fmaxf(am, __shfl_xor(am, 1, 8));
-  am = fmaxf(am, __shfl_xor(am, 2, 8));
-  am = fmaxf(am, __shfl_xor(am, 4, 8));
-  float s, inv;
-  sbits = quant_scale(am, s, inv);
-  uint32_t p = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) p |= (uint32_t)(quant_code(f[i], s, inv) + 8) << (4 * i);
-  packed = p;
-}
-
-// Nibbles 0..3 of p moved to the low nibbles of bytes 0..3.
-__device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t p) {
-  p &= 0xFFFFu;
-  p = (p | (p << 8)) & 0x00FF00FFu;
-  return (p | (p << 4)) & 0x0F0F0F0Fu;
-}
-// A K word in page order from 8 codes in element order: element e (< 4) in
-// the low nibble of byte e, element 4 + e in its high nibble.
-__device__ __forceinline__ uint32_t k_word(uint32_t packed) {
-  return nibbles_to_bytes(packed) | (nibbles_to_bytes(packed >> 16) << 4);
-}
-
-
 template <int D>
 __device__ __forceinline__ void write_hi(const CacheView& cv, int page, int t, const uint16_t* kin,
                                          const uint16_t* vin) {
@@ -493,33 +437,6 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
 // slots from n1 on are not yet in use and may be written.
 constexpr int kPackThreads = 256;
 
-// The 8 codes of the bf16 elements of x (element u in bits 4u..4u+3, offset
-// binary) under scale s, inv ~ 1/s.  rint(x * inv) is the nearest integer of
-// x / s whenever x / s is not within 2^-12 of a half-integer: for a bf16 x
-// and an fp16 s no quotient other than an exact tie comes that close, and
-// x * inv is within 2^-19 of x / s.  Lanes holding an element near a tie take
-// the exact rule (quant_code) for their 8 elements.
-__device__ __forceinline__ uint32_t codes8(const uint4& x, float s, float inv) {
-  const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
-                      bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
-  uint32_t p = 0u;
-  bool near_tie = false;
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const float y = f[u] * inv;
-    const float c = rintf(y);
-    near_tie |= fabsf(y - c) > 0.49988f;
-    p |= (uint32_t)(fminf(fmaxf(c, -7.0f), 7.0f) + 8.0f) << (4 * u);
-  }
-  if (__ballot(near_tie)) {
-    if (near_tie) {
-      p = 0u;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) p |= (uint32_t)(quant_code(f[u], s, inv) + 8) << (4 * u);
-    }
-  }
-  return s != 0.0f ? p : 0x88888888u;
-}
 
 // The page image of a LOW page from the call's K and V rows (kx, vx: 16-byte
 // chunks in row order, chunk e of the page's rows at e = it * threads + tid,

@@ -423,6 +423,7 @@ __device__ __forceinline__ int window_slots(const AttnArgs& a, int n_pos) { retu
 // the next sequence take them from registers instead of memory.
 struct FirstCounts {
   int n_hi, n_lo, n_win;   // 0 past the batch
+  int n_x;                 // 1 when the call persists and attends an entry of the sequence
 };
 __device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
   const int lane = threadIdx.x & 63;
@@ -432,20 +433,127 @@ __device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
   f.n_hi = lane < a.batch ? hi : 0;
   f.n_lo = lane < a.batch ? lo : 0;
   f.n_win = lane < a.batch ? window_slots(a, pos) : 0;
+  f.n_x = 0;
   return f;
 }
+
+// ---------------------------------------------------------------------------
+// the step's new entry, persisted by the attention call itself
+// ---------------------------------------------------------------------------
+// Outcome of the one-token append of a sequence.  word: action (bits 0-1),
+// stored (bit 2), forced (3), opens a page (4), past the sequence capacity
+// (5), status flags (bits 8 on); page: the page granted when the entry opens
+// one, else -1.
+struct EntryRecord {
+  int word, slot, page, pos;
+};
+constexpr int kEntStored = 4, kEntForced = 8, kEntOpens = 16, kEntCapacity = 32;
+
+// The one-token append's rules (decide, then the next slot of the entry's
+// store, a new page when that slot opens one), with the pages a call opens
+// granted in sequence order from the pool cursors rather than by atomics, so
+// that every worker computes the same outcome for every sequence from the
+// cache as it stands when the call starts.  Lane b < batch takes sequence b
+// (n_hi, n_lo, pos: its counters); s_a0 / s_amin: Lambda's column.
+__device__ __forceinline__ EntryRecord predict_entry(const AttnArgs& a, const uint8_t* s_a0, const uint8_t* s_amin,
+                                                     int n_hi, int n_lo, int pos) {
+  const CacheView& cv = a.cv;
+  const int lane = threadIdx.x & 63;
+  const bool live = lane < a.batch;
+  const int tag = live ? (int)a.tags_new[lane] : 0;
+  uint32_t flags = 0u;
+  bool forced = false, bad = false, opens = false, stored = false;
+  int act = kDrop, store = kHi, slot = 0, page = -1;
+  const bool cap = pos >= cv.max_tokens;
+  if (cap) {
+    flags |= PASK_FLAG_SEQ_CAPACITY;
+  } else {
+    act = decide(s_a0, s_amin, a.tab.n_tags, a.tab.n_sink, false, tag, pos, forced, bad);
+    if (bad) flags |= PASK_FLAG_BAD_TAG;
+    if (act != kDrop) {
+      store = act == kHigh ? kHi : kLo;
+      slot = store == kHi ? n_hi : n_lo;
+      opens = slot % kPage == 0;
+      stored = !opens;
+    }
+  }
+  const unsigned long long open_hi = __ballot(live && opens && store == kHi);
+  const unsigned long long open_lo = __ballot(live && opens && store == kLo);
+  if (live && opens) {
+    const unsigned long long m = store == kHi ? open_hi : open_lo;
+    const uint32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    const uint32_t pid = cv.status[2 + store] + before;
+    const uint32_t pool = store == kHi ? (uint32_t)cv.hi_pages : (uint32_t)cv.lo_pages;
+    if (pid < pool) {
+      page = (int)pid;
+      stored = true;
+    } else {
+      flags |= store == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
+    }
+  }
+  EntryRecord r;
+  r.word = act | (stored ? kEntStored : 0) | (forced ? kEntForced : 0) | (opens ? kEntOpens : 0) |
+           (cap ? kEntCapacity : 0) | (int)(flags << 8);
+  r.slot = slot;
+  r.page = page;
+  r.pos = pos;
+  return r;
+}
+
+// First counts of a call that persists its step's entry (at most 64
+// sequences, no recent window): the stores as they stand, plus the entry of
+// each sequence that gets stored (n_x), whose outcome goes to s_ent[lane].
+__device__ __forceinline__ FirstCounts first_counts_entry(const AttnArgs& a, const uint8_t* s_a0,
+                                                          const uint8_t* s_amin, EntryRecord* s_ent) {
+  const int lane = threadIdx.x & 63;
+  const int32_t* c = counters_of(a.cv, lane < a.batch ? lane : 0, a.layer);
+  const int hi = c[kCntHi], lo = c[kCntLo], pos = c[kCntPos];
+  FirstCounts f;
+  f.n_hi = lane < a.batch ? hi : 0;
+  f.n_lo = lane < a.batch ? lo : 0;
+  f.n_win = 0;
+  const EntryRecord r = predict_entry(a, s_a0, s_amin, hi, lo, pos);
+  f.n_x = lane < a.batch && (r.word & kEntStored) ? 1 : 0;
+  s_ent[lane] = r;
+  return f;
+}
+// The merge kernels of such a call take the counts the attention kernel
+// planned with from the workspace (the counters change under them: the
+// merge kernel also enters the entries).
+__device__ __forceinline__ FirstCounts planned_counts(const AttnArgs& a) {
+  if (!a.tags_new) return first_counts(a);
+  const int lane = threadIdx.x & 63;
+  const int4 r = lane < a.batch ? *reinterpret_cast<const int4*>(a.ws_seq + lane * 8) : make_int4(0, 0, 0, 0);
+  FirstCounts f;
+  f.n_hi = r.x;
+  f.n_win = r.y;
+  f.n_lo = r.z;
+  f.n_x = r.w;
+  return f;
+}
+
 // Pages of sequence b (wave-uniform, < batch).
 __device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const FirstCounts& f, int b) {
   if (b < 64)
     return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_win, b),
-                      __builtin_amdgcn_readlane(f.n_lo, b));
+                      __builtin_amdgcn_readlane(f.n_lo, b), __builtin_amdgcn_readlane(f.n_x, b));
+  const int32_t* c = counters_of(a.cv, b, a.layer);
+  return make_pages(uni(c[kCntHi]), uni(window_slots(a, c[kCntPos])), uni(c[kCntLo]));
+}
+// The same from a wave's copy of the first counts in LDS (lane b's counts at
+// c[b]), so that the walk over sequences keeps no registers for them.
+__device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const int4* c64, int b) {
+  if (b < 64) {
+    const int4 c = c64[b];
+    return make_pages(uni(c.x), uni(c.y), uni(c.z), uni(c.w));
+  }
   const int32_t* c = counters_of(a.cv, b, a.layer);
   return make_pages(uni(c[kCntHi]), uni(window_slots(a, c[kCntPos])), uni(c[kCntLo]));
 }
 // Length in units of sequence c0 + lane (c0 wave-uniform; 0 past `limit`).
 __device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f, int c0, int limit) {
   const int b = c0 + (int)(threadIdx.x & 63);
-  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_win, f.n_lo) : 0;
+  if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_win, f.n_lo, f.n_x) : 0;
   const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
   const int len = len_of(c[kCntHi], window_slots(a, c[kCntPos]), c[kCntLo]);
   return b < limit ? len : 0;
@@ -598,14 +706,163 @@ __device__ __forceinline__ void run_pages(const uint8_t* pool, size_t page_bytes
   }
 }
 
+// The step's entry's K and V rows, fetched at the start of its segment as
+// D/64 words per lane (the rows' 4D bytes spread over the wave: lane l holds
+// words l D/64 .. of [K; V]), so that only D/64 registers stay live while the
+// pages stream; read back by lane shuffles.
+template <int D>
+struct EntryRows {
+  static constexpr int kW = D / 64;            // words per lane
+  uint32_t w[kW];
+  // Word j (< D) of [K; V] (two bf16 per word), for any lane's j.
+  __device__ __forceinline__ uint32_t word(int j) const {
+    if constexpr (kW == 1) {
+      return (uint32_t)__shfl((int)w[0], j);
+    } else {
+      const uint32_t a0 = (uint32_t)__shfl((int)w[0], j / kW), a1 = (uint32_t)__shfl((int)w[1], j / kW);
+      return (j % kW) ? a1 : a0;
+    }
+  }
+  // bf16 bits of element e (< 2D) of [K; V].
+  __device__ __forceinline__ uint32_t elem(int e) const { return (word(e >> 1) >> (16 * (e & 1))) & 0xFFFFu; }
+};
+
+// The step's entry of (b, g), stored per record r: KV head g of it is
+// written into slot r.slot of its page, exactly as the one-token append
+// writes it (bf16 for HIGH; for LOW the same codes and scales: the group's
+// absmax, quant_scale, and the code rule, here through codes8, which is
+// quant_code wherever it counts).  A LOW entry's operands, as slot 0 of a
+// page in the attention's layout, are left in x.
+template <int D>
+__device__ __forceinline__ void prepare_entry(const AttnArgs& a, int b, int g, const EntryRecord& r, int q, int n,
+                                              LoRaw<D>& x, const EntryRows<D>& rows) {
+  using PL = PageLayout<D>;
+  const CacheView& cv = a.cv;
+  const int H = cv.n_kv_heads, lane = threadIdx.x & 63;
+  const int act = r.word & 3;
+  const int store = act == kHigh ? kHi : kLo;
+  const int t = r.slot % kPage, qq = t / 4, jj = t % 4;
+  const int page = r.page >= 0 ? r.page : block_table_of(cv, b, a.layer, store)[r.slot / kPage];
+  if (act == kHigh) {
+    uint8_t* hd = cv.hi_pool + (size_t)page * cv.hi_page_bytes + (size_t)((g + page) % H) * PL::kHiHead;
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {           // K chunk (i, q) of the slot: dims 32i + 8q .. +8
+      const int w0 = 16 * i + 4 * q;
+      const uint4 c = make_uint4(rows.word(w0), rows.word(w0 + 1), rows.word(w0 + 2), rows.word(w0 + 3));
+      if (n == t) *reinterpret_cast<uint4*>(hd + (size_t)(i * 64 + q * 16 + t) * 16) = c;
+    }
+    uint16_t* vd = reinterpret_cast<uint16_t*>(hd + PL::kHiV);
+#pragma unroll
+    for (int k = 0; k < D / 64; ++k) {           // V dim d = 16m + dd
+      const int d = lane + 64 * k, m = d / 16, dd = d % 16;
+      vd[(((m >> 1) * 64 + qq * 16 + dd) * 2 + (m & 1)) * 4 + jj] = (uint16_t)rows.elem(D + d);
+    }
+    return;
+  }
+  uint8_t* hb = cv.lo_pool + (size_t)page * cv.lo_page_bytes + (size_t)((g + page) % H) * PL::kLoHead;
+  constexpr int NG = PL::NG;
+  uint32_t sk[NG], sv[NG];
+#pragma unroll
+  for (int i = 0; i < NG; ++i) {                 // K group i: lane (q, n) holds elements 8q .. 8q + 7
+    const int w0 = 16 * i + 4 * q;
+    const uint4 w = make_uint4(rows.word(w0), rows.word(w0 + 1), rows.word(w0 + 2), rows.word(w0 + 3));
+    const float f[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                        bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
+    float am = fabsf(f[0]);
+#pragma unroll
+    for (int u = 1; u < 8; ++u) am = fmaxf(am, fabsf(f[u]));
+    am = fmaxf(am, __shfl_xor(am, 16));          // the group's absmax over its four lanes
+    am = fmaxf(am, __shfl_xor(am, 32));
+    float sc, inv;
+    sk[i] = quant_scale(am, sc, inv);
+    const uint32_t kw = k_word(codes8(w, sc, inv));
+    if (n == t) *reinterpret_cast<uint32_t*>(hb + ((q * 16 + t) * NG + i) * 4) = kw;
+    x.kc[i] = n == 0 ? kw : 0x88888888u;         // other slots: code 0 (masked)
+  }
+#pragma unroll
+  for (int i = 0; i < NG; ++i) {                 // V group i: lane (q, n) holds dims n, n + 16
+    const float v0 = __uint_as_float(rows.elem(D + 32 * i + n) << 16);
+    const float v1 = __uint_as_float(rows.elem(D + 32 * i + 16 + n) << 16);
+    float am = fmaxf(fabsf(v0), fabsf(v1));
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) am = fmaxf(am, __shfl_xor(am, off));
+    float sc, inv;
+    sv[i] = quant_scale(am, sc, inv);
+    const uint32_t byte = (uint32_t)(quant_code(v0, sc, inv) + 8) | ((uint32_t)(quant_code(v1, sc, inv) + 8) << 4);
+    if (q == 0) hb[PL::kLoVC + ((qq * 16 + n) * (PL::NM / 2) + i) * 4 + jj] = (uint8_t)byte;
+    x.vc[i] = q == 0 ? (0x88888800u | byte) : 0x88888888u;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < NG; ++i) {
+      *reinterpret_cast<uint16_t*>(hb + PL::kLoKS + (t * NG + i) * 2) = (uint16_t)sk[i];
+      *reinterpret_cast<uint16_t*>(hb + PL::kLoVS + (t * NG + i) * 2) = (uint16_t)sv[i];
+    }
+  }
+  // The row's scale words as load_lo hands them out: lane n < KW holds K word
+  // n, KW <= n < 2 KW V word n - KW; word w holds halves 2w, 2w + 1 of the
+  // row's [4 slots][NG] scales, and only slot 0 of row 0 is the entry.
+  constexpr int KW = 2 * NG;
+  const bool is_v = n >= KW && n < 2 * KW;
+  const int wd = n < KW ? n : (is_v ? n - KW : 0);
+  uint32_t lo16 = 0u, hi16 = 0u;
+#pragma unroll
+  for (int i = 0; i < NG; ++i) {
+    const uint32_t v = is_v ? sv[i] : sk[i];
+    if (2 * wd == i) lo16 = v;
+    if (2 * wd + 1 == i) hi16 = v;
+  }
+  x.sc = q == 0 ? (lo16 | (hi16 << 16)) : 0u;
+}
+
+// The entry attended as a page holding just that slot (slot 0): HIGH from
+// its bf16 rows, LOW from the operands prepare_entry made; `offsets`
+// computes the LOW code offsets of q.
+template <int D, int G, typename Offsets>
+__device__ __forceinline__ void attend_entry(const AttnArgs& a, const EntryRecord& r, AttnState<D, G>& st, int q,
+                                             int n, Offsets offsets, const LoRaw<D>& xl, const EntryRows<D>& rows) {
+  using PL = PageLayout<D>;
+  if ((r.word & 3) == kHigh) {
+    HiRaw<D> x;
+#pragma unroll
+    for (int i = 0; i < PL::NG; ++i) {           // K dims 32i + 8q .. +8 of slot 0: lanes (q, 0)
+      const int w0 = 16 * i + 4 * q;
+      const uint4 w = make_uint4(rows.word(w0), rows.word(w0 + 1), rows.word(w0 + 2), rows.word(w0 + 3));
+      x.k[4 * i] = n == 0 ? w.x : 0u;
+      x.k[4 * i + 1] = n == 0 ? w.y : 0u;
+      x.k[4 * i + 2] = n == 0 ? w.z : 0u;
+      x.k[4 * i + 3] = n == 0 ? w.w : 0u;
+    }
+#pragma unroll
+    for (int m = 0; m < PL::NM; ++m) {           // V dim 16m + n of slot 0: lanes (0, n)
+      const uint32_t e = rows.elem(D + 16 * m + n);
+      x.v[2 * m] = q == 0 ? e : 0u;
+      x.v[2 * m + 1] = 0u;
+    }
+    attend_page<D, G, true, true>(x, st, 1, a.scale_log2, q);
+    return;
+  }
+  offsets();
+  attend_page<D, G, false, true>(xl, st, 1, a.scale_log2, q);
+}
+
 // Pages [j0, j1) of (b, g) (HIGH store, recent window, LOW store): this
 // piece's partial of (b, g), combined with the others by attn_merge.
 template <int D, int G, typename Plan>
 __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, int g, int j0, int j1, const SeqPages& sp,
-                                               long long seg0, const Plan& plan, int q, int n) {
+                                               long long seg0, const Plan& plan, int q, int n,
+                                               const EntryRecord* ent) {
   using PL = PageLayout<D>;
   const CacheView& cv = a.cv;
   const int H = cv.n_kv_heads;
+  EntryRows<D> rows;                               // the step's entry, attended last: its rows now
+  if (j1 > sp.np_l) {
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(
+        ((threadIdx.x & 63) < 32 ? a.k_new : a.v_new) + ((size_t)b * H + g) * D);
+    const int l = threadIdx.x & 31;                // [K; V]: lanes 0-31 K, 32-63 V
+#pragma unroll
+    for (int k = 0; k < EntryRows<D>::kW; ++k) rows.w[k] = src[l * EntryRows<D>::kW + k];
+  }
   const size_t bh0 = (size_t)b * a.n_q_heads + (size_t)g * G;
   AttnState<D, G> st;
   // Columns n >= G repeat head G-1 (finite scores; their results are unused).
@@ -637,10 +894,16 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int w, int b, 
     run_pages<D, G, true, true>(cv.hi_pool, cv.hi_page_bytes, PL::kHiHead, H, nullptr,
                                 (b * cv.n_layers + a.layer) * cv.ring_pp, max(j0, sp.np_hi) - sp.np_hi,
                                 min(j1, sp.np_w) - sp.np_hi, sp.n_win, g, st, a.scale_log2, q, n);
-  if (j1 > sp.np_w)
+  const int l0 = max(j0, sp.np_w), l1 = min(j1, sp.np_l);   // the LOW store's pages of the range
+  if (l0 < l1)
     run_pages<D, G, false>(cv.lo_pool, cv.lo_page_bytes, PL::kLoHead, H, block_table_of(cv, b, a.layer, kLo), 0,
-                           max(j0, sp.np_w) - sp.np_w, j1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n,
-                           code_offsets);
+                           l0 - sp.np_w, l1 - sp.np_w, sp.n_lo, g, st, a.scale_log2, q, n, code_offsets);
+  if (j1 > sp.np_l) {                            // the step's entry (only when the call persists it)
+    const EntryRecord er = ent[b];
+    LoRaw<D> xl;
+    prepare_entry<D>(a, b, g, er, q, n, xl, rows);
+    attend_entry<D, G>(a, er, st, q, n, code_offsets, xl, rows);
+  }
   // Partial of piece `slot` of (b, g): rows of G4 = max(G, 4) query heads,
   // stored as float4s of 4 heads at one dim (index ((q*NM + k)*16 + n)*4 + r
   // for head 4q + r, dim 16k + n): each store instruction writes 256
@@ -675,7 +938,27 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
   const int w = uni(blockIdx.x * kWaves + (int)(threadIdx.x >> 6));
   const int q = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
-  const FirstCounts f = first_counts(a);
+  // A call that persists its step's entry: Lambda's column and every
+  // sequence's entry outcome, one copy per wave (no barrier).
+  __shared__ uint8_t s_tab[kWaves][128];
+  __shared__ EntryRecord s_ent[kWaves][64];
+  const int wv = (int)(threadIdx.x >> 6);
+  FirstCounts f;
+  if (a.tags_new) {
+    s_tab[wv][lane] = a.tab.a0[lane];
+    s_tab[wv][64 + lane] = a.tab.amin[lane];
+    f = first_counts_entry(a, &s_tab[wv][0], &s_tab[wv][64], &s_ent[wv][0]);
+    if (w == 0 && lane < a.batch) {              // the merge kernel's copy
+      int4* rec = reinterpret_cast<int4*>(a.ws_seq + lane * 8);
+      const EntryRecord r = s_ent[wv][lane];
+      rec[0] = make_int4(f.n_hi, f.n_win, f.n_lo, f.n_x);
+      rec[1] = make_int4(r.word, r.slot, r.page, r.pos);
+    }
+  } else {
+    f = first_counts(a);
+  }
+  __shared__ int4 s_cnt[kWaves][64];
+  s_cnt[wv][lane] = make_int4(f.n_hi, f.n_win, f.n_lo, f.n_x);
   const Plan plan = make_plan<Plan>(a, f, a.attn_blocks);
   const long long start = plan.start_of(w);
   if (start >= plan.total) return;
@@ -683,7 +966,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
   int b, excl;
   locate(a, f, start, b, excl);
   if (b < 0) return;
-  SeqPages sp = seq_pages(a, f, b);
+  SeqPages sp = seq_pages(a, &s_cnt[wv][0], b);
   const long long rel = start - (long long)excl * H;
   int g = (int)udiv(rel, sp.len);
   int j0 = first_page_at(sp, (int)(rel - (long long)g * sp.len));
@@ -691,7 +974,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
     const long long seg0 = (long long)excl * H + (long long)g * sp.len;
     if (seg0 >= end) return;
     const int j1 = end - seg0 >= sp.len ? sp.np : first_page_at(sp, (int)(end - seg0));
-    if (j0 < j1) attend_segment<D, G, Plan>(a, w, b, g, j0, j1, sp, seg0, plan, q, n);
+    if (j0 < j1) attend_segment<D, G, Plan>(a, w, b, g, j0, j1, sp, seg0, plan, q, n, &s_ent[wv][0]);
     if (j1 < sp.np) return;
     j0 = 0;
     if (++g == H) {                              // next sequence that holds any page
@@ -699,7 +982,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
       excl += sp.len;
       do {
         if (++b >= a.batch) return;
-        sp = seq_pages(a, f, b);
+        sp = seq_pages(a, &s_cnt[wv][0], b);
       } while (sp.len == 0);
     }
   }
@@ -773,6 +1056,49 @@ __device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts
   return excl;
 }
 
+// The step's entries of a call that persists them, entered into the cache
+// after the attention kernel has planned, written and attended them (one
+// wave, lane b = sequence b): counters, index lists, the block table entry
+// of an opened page, the pool cursors (one page per opening entry, granted or
+// not, as the one-token append counts them) and the status flags.
+__device__ __forceinline__ void enter_entries(const AttnArgs& a) {
+  const CacheView& cv = a.cv;
+  const int lane = threadIdx.x & 63;
+  const bool live = lane < a.batch;
+  const int4 r = live ? *reinterpret_cast<const int4*>(a.ws_seq + lane * 8 + 4) : make_int4(0, 0, 0, 0);
+  const int word = r.x, slot = r.y, page = r.z, pos = r.w;
+  const int act = word & 3, store = act == kHigh ? kHi : kLo;
+  const bool opens = (word & kEntOpens) != 0;
+  if (live) {
+    int32_t* cnt = counters_of(cv, lane, a.layer);
+    if (word & kEntCapacity) {
+      cnt[kCntLost] += 1;
+    } else {
+      if (act == kDrop) {
+        cnt[kCntDrop] += 1;
+      } else if (!(word & kEntStored)) {         // no page left in its pool
+        cnt[kCntLost] += 1;
+      } else {
+        if (opens) block_table_of(cv, lane, a.layer, store)[slot / kPage] = page;
+        index_list_of(cv, lane, a.layer, store)[slot] = pos;
+        cnt[store] = slot + 1;
+        if (word & kEntForced) cnt[kCntForced] += 1;
+      }
+      cnt[kCntPos] = pos + 1;
+    }
+  }
+  const unsigned long long open_hi = __ballot(live && opens && store == kHi);
+  const unsigned long long open_lo = __ballot(live && opens && store == kLo);
+  uint32_t flags = live ? (uint32_t)word >> 8 : 0u;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) flags |= (uint32_t)__shfl_xor((int)flags, off);
+  if (lane == 0) {
+    if (open_hi) atomicAdd(&cv.status[2], (unsigned)__popcll(open_hi));
+    if (open_lo) atomicAdd(&cv.status[3], (unsigned)__popcll(open_lo));
+    if (flags) atomicOr(cv.status, flags);
+  }
+}
+
 // One (sequence, KV head): combine the partials of its pieces (one or more)
 // into the bf16 outputs and log-sum-exps of its G query heads; zero output
 // and -inf for an empty history.  Thread t merges float4 position t of the
@@ -785,6 +1111,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   __shared__ __align__(16) uint16_t s_out[G][D];
   const int t = threadIdx.x;
   const int H = a.cv.n_kv_heads;
+  if (a.tags_new && blockIdx.x == gridDim.x - 1) {   // the extra block: the step's entries
+    if (t < 64) enter_entries(a);
+    return;
+  }
   const int b = uni(blockIdx.x / H), g = uni(blockIdx.x % H);
   const size_t row0 = (size_t)b * a.n_q_heads + (size_t)g * G;   // first query head row
   const size_t blk0 = ((size_t)b * H + g) * a.splits;
@@ -794,7 +1124,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {   // merg
   // below `splits` are in bounds; those past the count are skipped), so their
   // latency overlaps that of the counters the count comes from.
   pm.load(a, blk0, t, q, 0, a.splits - 1);
-  const FirstCounts f = first_counts(a);
+  const FirstCounts f = planned_counts(a);
   const SeqPages sp = seq_pages(a, f, b);
   if (sp.np == 0) {
     for (int i = t; i < G * D; i += merge_threads<D, G>()) a.out[row0 * D + i] = 0;
@@ -835,6 +1165,10 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
   constexpr int NM = D / 16, X = merge_threads<D, G>() / 16;
   const int lane = threadIdx.x, j = lane >> 4, n = lane & 15;
   const int H = a.cv.n_kv_heads;
+  if (a.tags_new && blockIdx.x == gridDim.x - 1) {   // the extra block: the step's entries
+    enter_entries(a);
+    return;
+  }
   const int seg = uni(blockIdx.x / X), x = uni(blockIdx.x % X);
   const int b = seg / H, g = seg % H;
   const int q = x / NM, k = x % NM, t = 16 * x + n;
@@ -846,7 +1180,7 @@ __global__ __launch_bounds__(64) void attn_merge_sliced_kernel(AttnArgs a) {
   // (the ranges' 1/PASK_SMALL_PIECES floor), not the workspace's last, so the
   // loads past the count re-read one slot instead of stale partials.
   pm.load(a, blk0, t, q, j, min(a.splits, PASK_SMALL_PIECES + 1) - 1, 4);
-  const FirstCounts f = first_counts(a);
+  const FirstCounts f = planned_counts(a);
   const SeqPages sp = seq_pages(a, f, b);
   if (sp.np == 0) {
 #pragma unroll
@@ -1035,6 +1369,8 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
   AttnArgs a = args;
   const int segs = a.batch * a.cv.n_kv_heads;
   const bool small = segs <= kSmallSegments;
+  if (a.tags_new && (a.batch > kFusedMaxBatch || a.cv.window != 0 || a.ws_seq == nullptr)) return hipErrorInvalidValue;
+  const int extra = a.tags_new ? 1 : 0;           // the merge block that enters the step's entries
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
     a.attn_blocks = small ? attn_grid<DD, GG, false>() : attn_grid<DD, GG, true>(); \
@@ -1042,10 +1378,10 @@ hipError_t launch_attention(const AttnArgs& args, int group_size, hipStream_t s)
     a.min_pages = small ? kSmallMinPages : kMinPagesPerBlock;                    \
     if (small) {                                                                 \
       attn_kernel<DD, GG, false><<<dim3(a.attn_blocks), dim3(64), 0, s>>>(a);    \
-      attn_merge_sliced_kernel<DD, GG><<<dim3(segs * (merge_threads<DD, GG>() / 16)), dim3(64), 0, s>>>(a); \
+      attn_merge_sliced_kernel<DD, GG><<<dim3(segs * (merge_threads<DD, GG>() / 16) + extra), dim3(64), 0, s>>>(a); \
     } else {                                                                     \
       attn_kernel<DD, GG, true><<<dim3(a.attn_blocks / kWpb), dim3(64 * kWpb), 0, s>>>(a); \
-      attn_merge_kernel<DD, GG><<<dim3(segs), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
+      attn_merge_kernel<DD, GG><<<dim3(segs + extra), dim3(merge_threads<DD, GG>()), 0, s>>>(a); \
     }                                                                            \
     return hipGetLastError();                                                    \
   }
@@ -1063,6 +1399,7 @@ hipError_t launch_distortion(const AttnArgs& ref_args, const AttnArgs& itv_args,
 #define PASK_CASE(DD, GG)                                                        \
   if (D == DD && group_size == GG) {                                             \
     ref.attn_blocks = itv.attn_blocks = attn_grid<DD, GG, true>();               \
+    ref.tags_new = itv.tags_new = nullptr;                                       \
     ref.min_pages = itv.min_pages = kMinPagesPerBlock;                           \
     if (ref.attn_blocks <= 0) return hipErrorInvalidDeviceFunction;              \
     attn_kernel<DD, GG, true><<<dim3(ref.attn_blocks / kWpb), block, 0, s>>>(ref); \

@@ -119,6 +119,16 @@ struct AttnArgs {
   float* lse;               // [batch][Hq] or null
   float* ws_o;              // [batch][Hkv][splits][G4 * D], G4 = max(G, 4) heads
   float* ws_ml;             // [batch][Hkv][splits][G4][2]  (max, sum) in log2 units
+  // The step's new entry, persisted by the call itself (kFusedMaxBatch
+  // sequences at most, no recent window, no parser states): the attention
+  // kernel decides it, writes it into its page and attends it; the merge
+  // kernel enters it in the counters, lists and block tables.  Null when the
+  // call persists nothing or the one-token append kernel ran before it.
+  const uint8_t* tags_new;  // [batch]
+  const uint16_t* k_new;    // bf16 bits [batch][Hkv][D]
+  const uint16_t* v_new;
+  int32_t* ws_seq;          // [batch][8]: the merge's page counts and the entry's outcome
+  TableColumn tab;          // Lambda's column of the layer (with tags_new)
   float scale_log2;         // softmax_scale * log2(e)
   int32_t layer, batch, n_q_heads, splits;   // splits: partials per (b, g) the workspace holds
   int32_t attn_blocks;      // stream-K workers (waves) of the attention kernel, set at launch
@@ -131,6 +141,9 @@ struct AttnArgs {
 // several thread groups at once.
 constexpr int kSmallSegments = 64;
 constexpr int kSmallPartials = 4096;
+// Calls that persist their step's entry themselves: every worker decides the
+// entries of all sequences, one per lane of its wave.
+constexpr int kFusedMaxBatch = 64;
 
 // The library-owned scratch of pask_decode_attn_noalloc: a device array of
 // kScratchBytes in pask_attn.hip, one copy per GPU.  scratch_workspace gives

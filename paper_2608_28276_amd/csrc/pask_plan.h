@@ -21,28 +21,42 @@ __host__ __device__ __forceinline__ long long udiv(long long a, long long b) {
 }
 
 // Pages of one sequence in a layer: the HIGH store, the recent window (HIGH
-// layout, min(n_pos, W) slots) and the LOW store, in that order.  Every page
-// weighs kUnit work units (with the memory system saturated a page iteration
-// costs about the same time whatever its size; weighting LOW pages by their
-// bytes measured slower), so every page starts at a multiple of kUnit.
+// layout, min(n_pos, W) slots), the LOW store and, when the call itself
+// persists the step's entry, one page holding just that entry (n_x = 1), in
+// that order.  Every page weighs kUnit work units (with the memory system
+// saturated a page iteration costs about the same time whatever its size;
+// weighting LOW pages by their bytes measured slower), so every page starts
+// at a multiple of kUnit.
 constexpr int kUnit = 32;
+// The page of the step's own entry weighs four pages: the worker that writes
+// and attends it does more than stream a page (its K / V rows are quantised,
+// stored and attended from registers).  Interleaved in one process against a
+// weight of one page: one Qwen3-4B-shaped sequence 13.3 / 13.3 us per call,
+// four sequences 28.1 against 29.3, the batch-64 call 203.5 against 204.8
+// (two pages: 13.3, 28.9, 203.7).
+#ifndef PASK_ENTRY_UNITS
+#define PASK_ENTRY_UNITS 128
+#endif
+constexpr int kEntryUnits = PASK_ENTRY_UNITS;
 struct SeqPages {
   int n_hi, n_win, n_lo;   // slots of the HIGH store, the window, the LOW store
-  int np_hi, np_w, np;     // pages: HIGH store, + window (HIGH layout), all
+  int np_hi, np_w, np_l;   // pages: HIGH store, + window (HIGH layout), + LOW store
+  int np;                  // all pages: np_l + n_x
   int len;                 // units
 };
-__host__ __device__ __forceinline__ int len_of(int n_hi, int n_win, int n_lo) {
-  return kUnit * (cdiv(n_hi, 16) + cdiv(n_win, 16) + cdiv(n_lo, 16));
+__host__ __device__ __forceinline__ int len_of(int n_hi, int n_win, int n_lo, int n_x = 0) {
+  return kUnit * (cdiv(n_hi, 16) + cdiv(n_win, 16) + cdiv(n_lo, 16)) + kEntryUnits * n_x;
 }
-__host__ __device__ __forceinline__ SeqPages make_pages(int n_hi, int n_win, int n_lo) {
+__host__ __device__ __forceinline__ SeqPages make_pages(int n_hi, int n_win, int n_lo, int n_x = 0) {
   SeqPages s;
   s.n_hi = n_hi;
   s.n_win = n_win;
   s.n_lo = n_lo;
   s.np_hi = cdiv(n_hi, 16);
   s.np_w = s.np_hi + cdiv(n_win, 16);
-  s.np = s.np_w + cdiv(n_lo, 16);
-  s.len = len_of(n_hi, n_win, n_lo);
+  s.np_l = s.np_w + cdiv(n_lo, 16);
+  s.np = s.np_l + n_x;
+  s.len = len_of(n_hi, n_win, n_lo, n_x);
   return s;
 }
 // Unit offset of page j inside its segment.

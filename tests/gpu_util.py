@@ -147,9 +147,12 @@ class Scenario:
                 self.oc.append(layer, b, self.gen_tags[b, t0:t1], bits16(k[b]), bits16(v[b]),
                                states=None if st is None else st[b])
 
-    def decode_step(self, t, layers=None, check=True, seqs=None):
-        """Fused append of token t + attention, on every layer; compare."""
+    def decode_step(self, t, layers=None, check=True, seqs=None, noalloc=False):
+        """Fused append of token t + attention, on every layer; compare.  The
+        outputs and log-sum-exps of the last call per layer stay in
+        self.last[layer]; noalloc: through pask_decode_attn_noalloc."""
         worst = 0.0
+        self.last = getattr(self, "last", {})
         for layer in (range(self.L) if layers is None else layers):
             k, v = self.gen_kv(layer, t, t + 1)
             q = self.q(layer, t)
@@ -158,8 +161,10 @@ class Scenario:
             tg = torch.as_tensor(np.ascontiguousarray(self.gen_tags[:, t]), device=self.dev)
             st = self._states(t, t + 1)
             sd = None if st is None else torch.as_tensor(np.ascontiguousarray(st[:, 0]), device=self.dev)
-            self.sess.decode(layer, q.to(self.dev), out, lse, tg, k[:, 0].contiguous().to(self.dev),
-                             v[:, 0].contiguous().to(self.dev), states_new=sd)
+            call = self.sess.decode_noalloc if noalloc else self.sess.decode
+            call(layer, q.to(self.dev), out, lse, tg, k[:, 0].contiguous().to(self.dev),
+                 v[:, 0].contiguous().to(self.dev), states_new=sd)
+            self.last[layer] = (out, lse)
             for b in range(self.B):
                 self.oc.append(layer, b, self.gen_tags[b, t:t + 1], bits16(k[b]), bits16(v[b]),
                                states=None if st is None else st[b])

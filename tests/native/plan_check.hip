@@ -134,11 +134,11 @@ int main(int argc, char** argv) {
       const int shape = rnd(6);
       int hi = shape == 0 ? 0 : rnd(shape == 1 ? 40 : 9000), win = rnd(3) ? 0 : rnd(70), lo = rnd(2) ? rnd(3000) : 0;
       if (shape == 5) hi = 20000 + rnd(20000);
-      SeqPages s = make_pages(hi, win, lo);
+      SeqPages s = make_pages(hi, win, lo, rnd(3) == 0 ? 1 : 0);   // with or without the step's own entry
       c.excl.push_back(acc);
       acc += s.len;
       c.seqs.push_back(s);
-      mx_tok = std::max(mx_tok, hi + win + lo);
+      mx_tok = std::max(mx_tok, hi + win + lo + 1);
     }
     c.total = acc * c.H;
     c.mx = 0;

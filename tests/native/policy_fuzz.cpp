@@ -47,6 +47,18 @@ extern "C" hipError_t hipStreamSynchronize(hipStream_t) {
   pask::never("hipStreamSynchronize");
   return hipSuccess;
 }
+extern "C" hipError_t hipStreamIsCapturing(hipStream_t, hipStreamCaptureStatus*) {
+  pask::never("hipStreamIsCapturing");
+  return hipSuccess;
+}
+extern "C" hipError_t hipGetLastError(void) {
+  pask::never("hipGetLastError");
+  return hipSuccess;
+}
+extern "C" const char* hipGetErrorString(hipError_t) {
+  pask::never("hipGetErrorString");
+  return "";
+}
 
 namespace {
 

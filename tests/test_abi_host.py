@@ -219,7 +219,7 @@ def _ws_want(g, batch, hint):
     # splits = ceil(hint / 128) + 2; with at most 64 (sequence, KV head) segments, pieces down to
     # one page while the call holds at most 4096 partials: max(that, min(ceil(hint / 16) + 2,
     # 4096 // segments)).  Per (sequence, KV head, piece) a block of G4 = max(G, 4) rows:
-    # o: blocks*G4*D*4, ml: blocks*G4*2*4 (each 256-aligned)
+    # o: blocks*G4*D*4, ml: blocks*G4*2*4, then 8 int32 per sequence (each 256-aligned)
     # a hint above max_tokens_per_seq counts as max_tokens_per_seq
     hint = min(hint, g.max_tokens_per_seq)
     segs = batch * g.n_kv_heads
@@ -229,7 +229,8 @@ def _ws_want(g, batch, hint):
     G4 = max(4, g.n_q_heads // g.n_kv_heads)
     blocks = segs * splits
     want = ((blocks * G4 * g.head_dim * 4 + 255) // 256) * 256
-    return ((want + blocks * G4 * 8 + 255) // 256) * 256
+    want = ((want + blocks * G4 * 8 + 255) // 256) * 256
+    return ((want + batch * 32 + 255) // 256) * 256
 
 
 @pytest.mark.parametrize("batch,hint", [(4, 512), (8, 512), (9, 512), (1, 100000), (32, 100000), (64, 9000)])

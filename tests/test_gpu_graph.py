@@ -3,8 +3,8 @@ attention calls (pask_decode_attn with a token to persist) recorded once and
 replayed step after step, the step's inputs copied into the graph's buffers
 before each replay, with eager work and synchronisations between replays.
 Every replay's outputs and log-sum-exps must equal, bit for bit, those of the
-same calls made eagerly on a second cache fed the same inputs (which is
-itself compared with the CPU oracle), and the caches' final states must
+same calls made eagerly on a second cache fed the same inputs (which are
+themselves compared with the CPU oracle), and the caches' final states must
 agree."""
 
 import numpy as np
@@ -29,7 +29,7 @@ def _gpu():
 def test_graph_replays_match_eager_steps(B, Hq, Hkv, D, noalloc):
     """noalloc: the captured calls are pask_decode_attn_noalloc (no workspace
     argument: the callers it is for include code under graph capture), the
-    eager twin's attention-only calls too."""
+    eager twin's calls too."""
     from paper_2608_28276_amd.session import PaskSession
     from workload.policy import pack_blob
     say(f"case: HIP graph of the decode step, B={B} Hq={Hq} Hkv={Hkv} D={D} noalloc={noalloc}")
@@ -87,17 +87,10 @@ def test_graph_replays_match_eager_steps(B, Hq, Hkv, D, noalloc):
         graph.replay()
         torch.cuda.synchronize()
         got_o, got_l = out.clone(), lse.clone()
-        want_o, want_l = [], []
-        for layer in range(L):                               # the eager twin (oracle-checked)
-            eager.decode_step(t, layers=[layer], check=True)
-        # the eager twin's outputs for the same step, recomputed through the same calls
-        for layer in range(L):
-            o = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
-            l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-            attn = eager.sess.decode_noalloc if noalloc else eager.sess.decode
-            attn(layer, eager.q(layer, t).to(dev), o, l)             # attention only: same history
-            want_o.append(o)
-            want_l.append(l)
+        for layer in range(L):                               # the same calls, eagerly (oracle-checked)
+            eager.decode_step(t, layers=[layer], check=True, noalloc=noalloc)
+        want_o = [eager.last[layer][0] for layer in range(L)]
+        want_l = [eager.last[layer][1] for layer in range(L)]
         torch.cuda.synchronize()
         for layer in range(L):
             assert torch.equal(got_o[layer], want_o[layer]), f"replay {r} layer {layer}: outputs differ"

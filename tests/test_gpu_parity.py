@@ -243,6 +243,74 @@ def test_flags_bad_tag_capacity_and_pool_exhaustion():
     assert (canary == 0xA5).all()
 
 
+def test_call_persisting_its_tokens_flags_and_page_order():
+    """A decode call that persists each sequence's token itself (at most 64
+    sequences, no window, no parser states): the pages one call opens are
+    granted in sequence order, so the first opener takes the last page of a
+    pool and the later ones are lost and flagged; a tag outside the table is
+    kept HIGH (forced) and flagged; a sequence at its capacity loses the token.
+    Counters, cursors and flags follow these rules exactly, the stored entries
+    match the oracle bit for bit, and each sequence's attention matches the
+    oracle over what was stored (zeros and -inf for a sequence with nothing)."""
+    say("case: one call persisting its tokens: flags and page order")
+    from paper_2608_28276_amd import pask
+    from paper_2608_28276_amd.session import PaskSession
+    from workload.policy import pack_blob
+    from workload.tensors import bf16_normal
+    from tests.gpu_util import bf16_f64, policy_dict
+    pol = uniform_policy(6, 1, 1, oracle.LOW)
+    P = [32, 5, 16, 0, 16]                               # HIGH pages 2 + 1 + 1 + 0 + 1 = the whole HIGH pool
+    B, Hq, Hkv, D = len(P), 8, 2, 64
+    sess = PaskSession(pack_blob(pol), max_batch=B, n_layers=1, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D,
+                       max_tokens_per_seq=32, hi_pages=5, lo_pages=1)
+    dev = sess.device
+    oc = oracle.OracleCache(policy_dict(pol), Hkv, D)
+    k = bf16_normal((B, 32, Hkv, D), 71)
+    v = bf16_normal((B, 32, Hkv, D), 72)
+    sess.append(0, None, k.to(dev), v.to(dev), n_new=torch.as_tensor(P, dtype=torch.int32, device=dev), keep_all=True)
+    for b, p in enumerate(P):
+        oc.append(0, b, np.zeros(p, np.uint8), bits16(k[b, :p]), bits16(v[b, :p]), keep_all=True)
+    tags = np.array([0, 200, 0, 0, 200], np.uint8)
+    kn, vn = bf16_normal((B, Hkv, D), 73), bf16_normal((B, Hkv, D), 74)
+    q = bf16_normal((B, Hq, D), 75)
+    out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    sess.decode(0, q.to(dev), out, lse, torch.as_tensor(tags, device=dev), kn.to(dev), vn.to(dev))
+    torch.cuda.synchronize()
+    cnt = sess.counters()[:B, 0].cpu().numpy()
+    sw = sess.status_words().cpu().numpy().astype(np.uint32)
+    #            hi  lo  pos drop forced lost      (the kept-all prompt tokens count as forced)
+    want = [(32, 0, 32, 0, 32, 1),                       # at capacity: lost
+            (6, 0, 6, 0, 6, 0),                          # tag 200: HIGH, forced, slot 5 of its page
+            (16, 1, 17, 0, 16, 0),                       # LOW, opens the LOW pool's only page
+            (0, 0, 1, 0, 0, 1),                          # LOW, opens a page: none left, lost
+            (16, 0, 17, 0, 16, 1)]                       # tag 200: HIGH, opens a page: none left, lost
+    for b in range(B):
+        assert tuple(int(x) for x in cnt[b, :6]) == want[b], (b, cnt[b, :6], want[b])
+    assert sw[2] == 5 + 1 and sw[3] == 0 + 2, sw         # one page per opener, granted or not
+    assert sw[0] == (pask.PASK_FLAG_SEQ_CAPACITY | pask.PASK_FLAG_BAD_TAG | pask.PASK_FLAG_LO_POOL_EXHAUSTED |
+                     pask.PASK_FLAG_HI_POOL_EXHAUSTED), hex(sw[0])
+    for b in (1, 2):                                     # the stored tokens
+        oc.append(0, b, tags[b:b + 1], bits16(kn[b:b + 1]), bits16(vn[b:b + 1]))
+    il = sess.index_lists().cpu().numpy()
+    assert il[1, 0, 0, 5] == 5 and il[2, 0, 1, 0] == 16
+    for b in (1, 2):
+        gk, gv = sess.gather_store(b, 0, 0)
+        ok, ov = oc.hi_entries(b, 0)
+        assert (gk == ok).all() and (gv == ov).all(), ("HIGH store", b)
+    lo = oc.lo_entries(2, 0)
+    glo = sess.gather_store(2, 0, 1)
+    assert all(np.array_equal(x, y) for x, y in zip(glo, lo)), "LOW store of sequence 2"
+    o = bf16_f64(out)
+    l_gpu = lse.cpu().double().numpy()
+    for b in range(B):
+        o_ref, lse_ref = oc.attend(0, b, bits16(q[b]), sess.softmax_scale)
+        if P[b] == 0:                                    # nothing stored: zeros, -inf
+            assert (o[b] == 0).all() and np.isneginf(l_gpu[b]).all()
+            continue
+        assert_attn_close(o[b], o_ref, f"sequence {b}")
+
+
 def test_stats_ckv_matches_oracle_counts():
     say("case: stats")
     pol = make_policy(6, 2, 4, 0.33, seed=16)

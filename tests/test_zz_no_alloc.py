@@ -65,15 +65,20 @@ def test_noalloc_matches_workspace_entry_point_two_calls():
     say("call 1: no-alloc matches the workspace entry point and the oracle")
 
     # Call 2, smaller: 5 sequences x 2 KV heads (few segments: the sliced
-    # merge path), the step's token appended by the same call (fused).  The
-    # scratch still holds call 1's partials.  Both entry points then use the
-    # same pieces, so their outputs agree bit for bit.
+    # merge path), the step's token persisted by the same call, on two caches
+    # in the same state: one through the no-alloc entry point, the other
+    # through pask_decode_attn.  The scratch still holds call 1's partials.
+    # Both entry points then use the same pieces, so their outputs and the
+    # caches they leave agree bit for bit.
     say("case: no-alloc attention, second call with a smaller input (fused append)")
     pol2 = make_policy(6, 2, 2, 0.33, seed=42)
     tags2 = np.stack([function_call_tags(8, 500 + b) for b in range(5)])
-    sc2 = Scenario(pol2, B=5, L=2, Hq=8, Hkv=2, D=64, prompt_lens=[3, 40, 170, 0, 333], gen_tags=tags2, seed=42)
-    sc2.fill_prompt()
-    sc2.append_steps(0, 7)
+    twins = [Scenario(pol2, B=5, L=2, Hq=8, Hkv=2, D=64, prompt_lens=[3, 40, 170, 0, 333], gen_tags=tags2, seed=42)
+             for _ in range(2)]
+    for x in twins:
+        x.fill_prompt()
+        x.append_steps(0, 7)
+    sc2, sc2w = twins
     for layer in range(2):
         k, v = sc2.gen_kv(layer, 7, 8)
         q2 = sc2.q(layer, 7)
@@ -81,11 +86,12 @@ def test_noalloc_matches_workspace_entry_point_two_calls():
         o_na, l_na = _outs(sc2, 5)
         o_ws, l_ws = _outs(sc2, 5)
         tg = torch.as_tensor(np.ascontiguousarray(sc2.gen_tags[:, 7]), device=sc2.dev)
-        sc2.sess.decode_noalloc(layer, q2d, o_na, l_na, tg, k[:, 0].contiguous().to(sc2.dev),
-                                v[:, 0].contiguous().to(sc2.dev))
-        for b in range(5):
-            sc2.oc.append(layer, b, sc2.gen_tags[b, 7:8], bits16(k[b]), bits16(v[b]))
-        sc2.sess.decode(layer, q2d, o_ws, l_ws)               # no append: the same history
+        kd, vd = k[:, 0].contiguous().to(sc2.dev), v[:, 0].contiguous().to(sc2.dev)
+        sc2.sess.decode_noalloc(layer, q2d, o_na, l_na, tg, kd, vd)
+        sc2w.sess.decode(layer, q2d, o_ws, l_ws, tg, kd, vd)
+        for x in twins:
+            for b in range(5):
+                x.oc.append(layer, b, x.gen_tags[b, 7:8], bits16(k[b]), bits16(v[b]))
         torch.cuda.synchronize()
         assert torch.equal(o_na, o_ws), f"call 2 layer {layer}: outputs differ from the workspace entry point"
         assert torch.equal(l_na, l_ws), f"call 2 layer {layer}: lse differs from the workspace entry point"
@@ -93,5 +99,6 @@ def test_noalloc_matches_workspace_entry_point_two_calls():
         for b in range(5):
             o_ref, _ = sc2.oc.attend(layer, b, bits16(q2[b]), sc2.scale)
             assert_attn_close(on[b], o_ref, f"call 2: no-alloc vs oracle, layer {layer} seq {b}")
-    sc2.check_state()
+    for x in twins:
+        x.check_state()
     say("call 2: no-alloc equals the workspace entry point bit for bit and matches the oracle")
