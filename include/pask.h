@@ -308,7 +308,7 @@ int pask_budget_init(const pask_policy* policy, pask_cache* cache, int32_t batch
  * or batch outside 1..max_batch): batch * n_kv_heads * S partial blocks
  * of max(G, 4) * (head_dim + 2) fp32, S = ceil(hint / 128) + 2, or for
  * batch * n_kv_heads <= 64 the larger of that and min(ceil(hint / 16) + 2,
- * 4096 / (batch * n_kv_heads)). */
+ * 4096 / (batch * n_kv_heads)); plus 32 bytes per sequence. */
 size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ctx_hint);
 
 /* One decode step of one layer: the Persist step of Alg. 2 for the token just
@@ -325,6 +325,13 @@ size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ct
  *   lse_dev[b][h] = natural-log sum-exp of the scaled scores (fp32; nullable)
  * The history is the persisted entries plus the recent window (bf16).  A
  * sequence with no visible entry gives out = 0 and lse = -inf.
+ * With a new token, at most 64 sequences, no recent window and no parser
+ * states, the attention kernels persist the tokens themselves (one launch
+ * fewer): the pages the call opens are then granted in sequence order (where
+ * a pool runs out, the lower sequences get its last pages), where the
+ * one-token append of pask_kv_append grants them in the order its blocks
+ * reach the pool.  Decisions, stored entries, counters and flags follow the
+ * same rules either way.
  * ws_dev: device workspace of at least pask_workspace_bytes(geom, batch,
  * max_ctx_hint) bytes, 256-byte aligned.
  *
