@@ -215,9 +215,11 @@ class DeviceRun:
         assert status == 0 and st.device_flags == 0, f"device flags {st.device_flags:#x}"
         say(f"counters and lists of {self.B} sequences x {len(self.layers)} layers bit-exact")
 
-    def check_stores(self):
-        """Stored bits, codes and scales of the sampled pairs."""
-        for (b, layer) in self.sample:
+    def check_stores(self, pairs=None):
+        """Stored bits, codes and scales of the sampled pairs (or of `pairs`,
+        a subset of them)."""
+        pairs = self.sample if pairs is None else list(pairs)
+        for (b, layer) in pairs:
             gk, gv = self.sess.gather_store(b, layer, 0)
             ok, ov = self.oc.hi_entries(b, layer)
             assert (gk == ok).all() and (gv == ov).all(), ("HIGH bf16 copies", layer, b)
@@ -225,7 +227,7 @@ class DeviceRun:
             okc, oks, ovc, ovs = self.oc.lo_entries(b, layer)
             assert (kc == okc).all() and (vc == ovc).all(), ("LOW codes", layer, b)
             assert (ks == oks).all() and (vs == ovs).all(), ("LOW scales", layer, b)
-        for (b, layer) in self.sample:
+        for (b, layer) in pairs:
             c = self.oc.counts(b, layer)
             e = self.exp[(b, int(self.gol[layer]))]
             assert (c["hi"], c["lo"], c["R"]) == (e["hi"].size, e["lo"].size, e["R"]), ("oracle replay", b, layer)
@@ -234,4 +236,4 @@ class DeviceRun:
                 sl = self.oc.sl(b, layer)
                 assert (wpos == sl.w_pos).all() and (wk == sl.w_k).all() and (wv == sl.w_v).all(), \
                     ("window", b, layer)
-        say(f"stores of {len(self.sample)} sampled pairs bit-exact")
+        say(f"stores of {len(pairs)} sampled pairs bit-exact")

@@ -58,26 +58,30 @@ def test_qwen3_4b_one_sequence_every_step():
 def test_qwen3_4b_batch64_bench_launch():
     """The timed workload in the launch configuration the bench times: 64
     sequences, prompts U{1024..8192} kept HIGH, 512 generated tokens
-    bulk-appended, then decode steps of one-token appends and attention over
-    all 36 layers with the bench's workspace hint.  Every counter and list of
-    all 64 sequences x 36 layers bit-exact; stores and attention of all 64
-    sequences in layer 27 and of 7 sequences x the first layer of each
-    group."""
+    bulk-appended, then decode steps over all 36 layers, each one
+    pask_decode_attn call that persists the step's token (the attention and
+    merge kernels do it themselves at this batch) with the bench's workspace
+    hint.  Every counter and list of all 64 sequences x 36 layers bit-exact;
+    attention of all 64 sequences in the first layer of each group at two
+    steps; stores of all 64 sequences in layer 27 and of 7 sequences x the
+    first layer of each group."""
     from bench import build_workload
     from tests.fullsize_util import DeviceRun
     cfg, P, tags, pol, _ = build_workload(2)
     say(f"case: {cfg.name}")
-    sample = sorted({(b, l) for b in (0, 9, 21, 33, 42, 50, 63) for l in (0, 9, 18, 27)} |
+    layers = (0, 9, 18, 27)
+    sample = sorted({(b, l) for b in range(cfg.batch) for l in layers})
+    stores = sorted({(b, l) for b in (0, 9, 21, 33, 42, 50, 63) for l in layers} |
                     {(b, 27) for b in range(cfg.batch)})
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=range(cfg.n_layers), Hq=cfg.n_q_heads,
                     Hkv=cfg.n_kv_heads, D=cfg.head_dim, P=P, prompt_tags=None, gen_tags=tags, sample=sample,
                     seed=cfg.seed, n_bulk=512, n_steps=3)
     run.fill()
-    run.step(check=True)
-    run.step(check=False)
-    run.step(check=True)
+    run.step(check=True, fused=True)
+    run.step(check=False, fused=True)
+    run.step(check=True, fused=True)
     run.check_lists()
-    run.check_stores()
+    run.check_stores(stores)
 
 
 @pytest.mark.parametrize("beta", [0.25, 0.33, 0.5, 1.0])
