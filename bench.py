@@ -237,7 +237,7 @@ def gpu_leg(cfg, P, tags, pol, steps: int, warmup: int, positions, states=None, 
         # One decode step: per layer, one pask_decode_attn call that persists the
         # step's token and attends the layer's history including it (the
         # attention and merge kernels persist the token themselves for at most
-        # 64 sequences without a recent window or parser states; otherwise the
+        # 256 sequences without a recent window or parser states; otherwise the
         # one-token append kernel runs first, inside the same call).
         sptr_ = sptr if stream is None else stream
         if tp is None:
@@ -577,14 +577,14 @@ def attn_kernels(cfg, window: int = 0, controller: bool = False) -> str:
     with at most 64 (sequence, KV head) segments use the equal-range attention
     and the sliced merge, larger ones the per-XCD weighted attention and the
     merge; the one-token append kernel comes first when the call cannot
-    persist the token in those (more than 64 sequences, a recent window or
+    persist the token in those (more than 256 sequences, a recent window or
     parser states)."""
     D, G = cfg.head_dim, cfg.group_size
     if cfg.batch * cfg.n_kv_heads <= 64:
         k = f"attn_kernel<{D}, {G}, false> + attn_merge_sliced_kernel<{D}, {G}>"
     else:
         k = f"attn_kernel<{D}, {G}, true> + attn_merge_kernel<{D}, {G}>"
-    if cfg.batch > 64 or window or controller:
+    if cfg.batch > 256 or window or controller:
         k = f"append_step{'_window' if window else ''}_kernel<{D}> + " + k
     return k
 

@@ -325,7 +325,7 @@ size_t pask_workspace_bytes(const pask_geom* geom, int32_t batch, int32_t max_ct
  *   lse_dev[b][h] = natural-log sum-exp of the scaled scores (fp32; nullable)
  * The history is the persisted entries plus the recent window (bf16).  A
  * sequence with no visible entry gives out = 0 and lse = -inf.
- * With a new token, at most 64 sequences, no recent window and no parser
+ * With a new token, at most 256 sequences, no recent window and no parser
  * states, the attention kernels persist the tokens themselves (one launch
  * fewer): the pages the call opens are then granted in sequence order (where
  * a pool runs out, the lower sequences get its last pages), where the

@@ -421,9 +421,14 @@ __device__ __forceinline__ int window_slots(const AttnArgs& a, int n_pos) { retu
 // Store counts of sequence `lane` for the first 64 sequences, read once per
 // block: the plan, the search for a block's first sequence and the walk to
 // the next sequence take them from registers instead of memory.
+// A call that persists its step's entries plans with counts that differ
+// from the counters: those of every sequence (n_hi, n_win, n_lo, n_x as four
+// ints) are then at more[b * stride], for the sequences beyond the first 64.
 struct FirstCounts {
   int n_hi, n_lo, n_win;   // 0 past the batch
   int n_x;                 // 1 when the call persists and attends an entry of the sequence
+  const int32_t* more;     // null: the counters
+  int stride;
 };
 __device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
   const int lane = threadIdx.x & 63;
@@ -434,6 +439,8 @@ __device__ __forceinline__ FirstCounts first_counts(const AttnArgs& a) {
   f.n_lo = lane < a.batch ? lo : 0;
   f.n_win = lane < a.batch ? window_slots(a, pos) : 0;
   f.n_x = 0;
+  f.more = nullptr;
+  f.stride = 0;
   return f;
 }
 
@@ -453,14 +460,16 @@ constexpr int kEntStored = 4, kEntForced = 8, kEntOpens = 16, kEntCapacity = 32;
 // store, a new page when that slot opens one), with the pages a call opens
 // granted in sequence order from the pool cursors rather than by atomics, so
 // that every worker computes the same outcome for every sequence from the
-// cache as it stands when the call starts.  Lane b < batch takes sequence b
-// (n_hi, n_lo, pos: its counters); s_a0 / s_amin: Lambda's column.
+// cache as it stands when the call starts.  Lane l takes sequence b = c0 + l
+// of a chunk of 64 (n_hi, n_lo, pos: its counters; opened_*: the pages the
+// sequences of earlier chunks open, advanced past this chunk's); s_a0 /
+// s_amin: Lambda's column.
 __device__ __forceinline__ EntryRecord predict_entry(const AttnArgs& a, const uint8_t* s_a0, const uint8_t* s_amin,
-                                                     int n_hi, int n_lo, int pos) {
+                                                     int b, int n_hi, int n_lo, int pos, uint32_t& opened_hi,
+                                                     uint32_t& opened_lo) {
   const CacheView& cv = a.cv;
-  const int lane = threadIdx.x & 63;
-  const bool live = lane < a.batch;
-  const int tag = live ? (int)a.tags_new[lane] : 0;
+  const bool live = b < a.batch;
+  const int tag = live ? (int)a.tags_new[b] : 0;
   uint32_t flags = 0u;
   bool forced = false, bad = false, opens = false, stored = false;
   int act = kDrop, store = kHi, slot = 0, page = -1;
@@ -481,7 +490,8 @@ __device__ __forceinline__ EntryRecord predict_entry(const AttnArgs& a, const ui
   const unsigned long long open_lo = __ballot(live && opens && store == kLo);
   if (live && opens) {
     const unsigned long long m = store == kHi ? open_hi : open_lo;
-    const uint32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    const uint32_t before = (store == kHi ? opened_hi : opened_lo) +
+                            __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
     const uint32_t pid = cv.status[2 + store] + before;
     const uint32_t pool = store == kHi ? (uint32_t)cv.hi_pages : (uint32_t)cv.lo_pages;
     if (pid < pool) {
@@ -491,6 +501,8 @@ __device__ __forceinline__ EntryRecord predict_entry(const AttnArgs& a, const ui
       flags |= store == kHi ? PASK_FLAG_HI_POOL_EXHAUSTED : PASK_FLAG_LO_POOL_EXHAUSTED;
     }
   }
+  opened_hi += (uint32_t)__popcll(open_hi);       // the lower sequences' page openings, in later chunks
+  opened_lo += (uint32_t)__popcll(open_lo);
   EntryRecord r;
   r.word = act | (stored ? kEntStored : 0) | (forced ? kEntForced : 0) | (opens ? kEntOpens : 0) |
            (cap ? kEntCapacity : 0) | (int)(flags << 8);
@@ -500,21 +512,37 @@ __device__ __forceinline__ EntryRecord predict_entry(const AttnArgs& a, const ui
   return r;
 }
 
-// First counts of a call that persists its step's entry (at most 64
-// sequences, no recent window): the stores as they stand, plus the entry of
-// each sequence that gets stored (n_x), whose outcome goes to s_ent[lane].
+// First counts of a call that persists its step's entries (at most
+// kFusedMaxBatch sequences, no recent window): the stores as they stand, plus
+// the entry of each sequence that gets stored (n_x).  Every sequence's counts
+// go to cnt[b] and its entry's outcome to ent[b]; the first 64 also stay in
+// registers.
+template <int kSeq>                                // the sequences ent and cnt hold (>= batch)
 __device__ __forceinline__ FirstCounts first_counts_entry(const AttnArgs& a, const uint8_t* s_a0,
-                                                          const uint8_t* s_amin, EntryRecord* s_ent) {
+                                                          const uint8_t* s_amin, EntryRecord* ent, int4* cnt) {
   const int lane = threadIdx.x & 63;
-  const int32_t* c = counters_of(a.cv, lane < a.batch ? lane : 0, a.layer);
-  const int hi = c[kCntHi], lo = c[kCntLo], pos = c[kCntPos];
+  uint32_t opened_hi = 0u, opened_lo = 0u;
   FirstCounts f;
-  f.n_hi = lane < a.batch ? hi : 0;
-  f.n_lo = lane < a.batch ? lo : 0;
-  f.n_win = 0;
-  const EntryRecord r = predict_entry(a, s_a0, s_amin, hi, lo, pos);
-  f.n_x = lane < a.batch && (r.word & kEntStored) ? 1 : 0;
-  s_ent[lane] = r;
+#pragma unroll
+  for (int c0 = 0; c0 < kSeq; c0 += 64) {
+    if (c0 > 0 && c0 >= a.batch) break;
+    const int b = c0 + lane;
+    const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
+    const int hi = c[kCntHi], lo = c[kCntLo], pos = c[kCntPos];
+    const EntryRecord r = predict_entry(a, s_a0, s_amin, b, hi, lo, pos, opened_hi, opened_lo);
+    const bool live = b < a.batch;
+    const int4 k = live ? make_int4(hi, 0, lo, (r.word & kEntStored) ? 1 : 0) : make_int4(0, 0, 0, 0);
+    ent[b] = r;
+    cnt[b] = k;
+    if (c0 == 0) {
+      f.n_hi = k.x;
+      f.n_win = 0;
+      f.n_lo = k.z;
+      f.n_x = k.w;
+    }
+  }
+  f.more = reinterpret_cast<const int32_t*>(cnt);
+  f.stride = 4;
   return f;
 }
 // The merge kernels of such a call take the counts the attention kernel
@@ -529,6 +557,8 @@ __device__ __forceinline__ FirstCounts planned_counts(const AttnArgs& a) {
   f.n_win = r.y;
   f.n_lo = r.z;
   f.n_x = r.w;
+  f.more = a.ws_seq;
+  f.stride = 8;
   return f;
 }
 
@@ -537,14 +567,18 @@ __device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const FirstCoun
   if (b < 64)
     return make_pages(__builtin_amdgcn_readlane(f.n_hi, b), __builtin_amdgcn_readlane(f.n_win, b),
                       __builtin_amdgcn_readlane(f.n_lo, b), __builtin_amdgcn_readlane(f.n_x, b));
+  if (f.more) {
+    const int4 c = *reinterpret_cast<const int4*>(f.more + (size_t)b * f.stride);
+    return make_pages(uni(c.x), uni(c.y), uni(c.z), uni(c.w));
+  }
   const int32_t* c = counters_of(a.cv, b, a.layer);
   return make_pages(uni(c[kCntHi]), uni(window_slots(a, c[kCntPos])), uni(c[kCntLo]));
 }
-// The same from a wave's copy of the first counts in LDS (lane b's counts at
-// c[b]), so that the walk over sequences keeps no registers for them.
-__device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const int4* c64, int b) {
-  if (b < 64) {
-    const int4 c = c64[b];
+// The same from a wave's copy of the counts in LDS (sequence b's at c[b] for
+// b < n_lds), so that the walk over sequences keeps no registers for them.
+__device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const int4* c_lds, int n_lds, int b) {
+  if (b < n_lds) {
+    const int4 c = c_lds[b];
     return make_pages(uni(c.x), uni(c.y), uni(c.z), uni(c.w));
   }
   const int32_t* c = counters_of(a.cv, b, a.layer);
@@ -554,6 +588,10 @@ __device__ __forceinline__ SeqPages seq_pages(const AttnArgs& a, const int4* c64
 __device__ __forceinline__ int lane_len(const AttnArgs& a, const FirstCounts& f, int c0, int limit) {
   const int b = c0 + (int)(threadIdx.x & 63);
   if (c0 == 0) return b < limit ? len_of(f.n_hi, f.n_win, f.n_lo, f.n_x) : 0;
+  if (f.more) {
+    const int4 r = b < limit ? *reinterpret_cast<const int4*>(f.more + (size_t)b * f.stride) : make_int4(0, 0, 0, 0);
+    return len_of(r.x, r.y, r.z, r.w);
+  }
   const int32_t* c = counters_of(a.cv, b < a.batch ? b : 0, a.layer);
   const int len = len_of(c[kCntHi], window_slots(a, c[kCntPos]), c[kCntLo]);
   return b < limit ? len : 0;
@@ -940,25 +978,29 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
   const int H = a.cv.n_kv_heads;
   // A call that persists its step's entry: Lambda's column and every
   // sequence's entry outcome, one copy per wave (no barrier).
+  constexpr int kSeq = kWeighted ? kFusedMaxBatch : 64;   // the equal-range plan takes at most 64 segments
   __shared__ uint8_t s_tab[kWaves][128];
-  __shared__ EntryRecord s_ent[kWaves][64];
+  __shared__ EntryRecord s_ent[kWaves][kSeq];
+  __shared__ int4 s_cnt[kWaves][kSeq];
   const int wv = (int)(threadIdx.x >> 6);
   FirstCounts f;
   if (a.tags_new) {
     s_tab[wv][lane] = a.tab.a0[lane];
     s_tab[wv][64 + lane] = a.tab.amin[lane];
-    f = first_counts_entry(a, &s_tab[wv][0], &s_tab[wv][64], &s_ent[wv][0]);
-    if (w == 0 && lane < a.batch) {              // the merge kernel's copy
-      int4* rec = reinterpret_cast<int4*>(a.ws_seq + lane * 8);
-      const EntryRecord r = s_ent[wv][lane];
-      rec[0] = make_int4(f.n_hi, f.n_win, f.n_lo, f.n_x);
-      rec[1] = make_int4(r.word, r.slot, r.page, r.pos);
+    f = first_counts_entry<kSeq>(a, &s_tab[wv][0], &s_tab[wv][64], &s_ent[wv][0], &s_cnt[wv][0]);
+    if (w == 0) {                                // the merge kernel's copy
+      for (int b = lane; b < a.batch; b += 64) {
+        int4* rec = reinterpret_cast<int4*>(a.ws_seq + b * 8);
+        const EntryRecord r = s_ent[wv][b];
+        rec[0] = s_cnt[wv][b];
+        rec[1] = make_int4(r.word, r.slot, r.page, r.pos);
+      }
     }
   } else {
     f = first_counts(a);
+    s_cnt[wv][lane] = make_int4(f.n_hi, f.n_win, f.n_lo, 0);
   }
-  __shared__ int4 s_cnt[kWaves][64];
-  s_cnt[wv][lane] = make_int4(f.n_hi, f.n_win, f.n_lo, f.n_x);
+  const int n_lds = a.tags_new ? a.batch : 64;   // sequences whose counts the wave holds in LDS
   const Plan plan = make_plan<Plan>(a, f, a.attn_blocks);
   const long long start = plan.start_of(w);
   if (start >= plan.total) return;
@@ -966,7 +1008,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
   int b, excl;
   locate(a, f, start, b, excl);
   if (b < 0) return;
-  SeqPages sp = seq_pages(a, &s_cnt[wv][0], b);
+  SeqPages sp = seq_pages(a, &s_cnt[wv][0], n_lds, b);
   const long long rel = start - (long long)excl * H;
   int g = (int)udiv(rel, sp.len);
   int j0 = first_page_at(sp, (int)(rel - (long long)g * sp.len));
@@ -982,7 +1024,7 @@ __global__ __launch_bounds__(64 * (kWeighted ? kWpb : 1), 2) void attn_kernel(At
       excl += sp.len;
       do {
         if (++b >= a.batch) return;
-        sp = seq_pages(a, &s_cnt[wv][0], b);
+        sp = seq_pages(a, &s_cnt[wv][0], n_lds, b);
       } while (sp.len == 0);
     }
   }
@@ -1064,37 +1106,41 @@ __device__ __forceinline__ int units_before(const AttnArgs& a, const FirstCounts
 __device__ __forceinline__ void enter_entries(const AttnArgs& a) {
   const CacheView& cv = a.cv;
   const int lane = threadIdx.x & 63;
-  const bool live = lane < a.batch;
-  const int4 r = live ? *reinterpret_cast<const int4*>(a.ws_seq + lane * 8 + 4) : make_int4(0, 0, 0, 0);
-  const int word = r.x, slot = r.y, page = r.z, pos = r.w;
-  const int act = word & 3, store = act == kHigh ? kHi : kLo;
-  const bool opens = (word & kEntOpens) != 0;
-  if (live) {
-    int32_t* cnt = counters_of(cv, lane, a.layer);
-    if (word & kEntCapacity) {
-      cnt[kCntLost] += 1;
-    } else {
-      if (act == kDrop) {
-        cnt[kCntDrop] += 1;
-      } else if (!(word & kEntStored)) {         // no page left in its pool
+  uint32_t flags = 0u, opened_hi = 0u, opened_lo = 0u;
+  for (int c0 = 0; c0 < a.batch; c0 += 64) {
+    const int b = c0 + lane;
+    const bool live = b < a.batch;
+    const int4 r = live ? *reinterpret_cast<const int4*>(a.ws_seq + b * 8 + 4) : make_int4(0, 0, 0, 0);
+    const int word = r.x, slot = r.y, page = r.z, pos = r.w;
+    const int act = word & 3, store = act == kHigh ? kHi : kLo;
+    const bool opens = (word & kEntOpens) != 0;
+    if (live) {
+      int32_t* cnt = counters_of(cv, b, a.layer);
+      if (word & kEntCapacity) {
         cnt[kCntLost] += 1;
       } else {
-        if (opens) block_table_of(cv, lane, a.layer, store)[slot / kPage] = page;
-        index_list_of(cv, lane, a.layer, store)[slot] = pos;
-        cnt[store] = slot + 1;
-        if (word & kEntForced) cnt[kCntForced] += 1;
+        if (act == kDrop) {
+          cnt[kCntDrop] += 1;
+        } else if (!(word & kEntStored)) {       // no page left in its pool
+          cnt[kCntLost] += 1;
+        } else {
+          if (opens) block_table_of(cv, b, a.layer, store)[slot / kPage] = page;
+          index_list_of(cv, b, a.layer, store)[slot] = pos;
+          cnt[store] = slot + 1;
+          if (word & kEntForced) cnt[kCntForced] += 1;
+        }
+        cnt[kCntPos] = pos + 1;
       }
-      cnt[kCntPos] = pos + 1;
+      flags |= (uint32_t)word >> 8;
     }
+    opened_hi += (uint32_t)__popcll(__ballot(live && opens && store == kHi));
+    opened_lo += (uint32_t)__popcll(__ballot(live && opens && store == kLo));
   }
-  const unsigned long long open_hi = __ballot(live && opens && store == kHi);
-  const unsigned long long open_lo = __ballot(live && opens && store == kLo);
-  uint32_t flags = live ? (uint32_t)word >> 8 : 0u;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) flags |= (uint32_t)__shfl_xor((int)flags, off);
   if (lane == 0) {
-    if (open_hi) atomicAdd(&cv.status[2], (unsigned)__popcll(open_hi));
-    if (open_lo) atomicAdd(&cv.status[3], (unsigned)__popcll(open_lo));
+    if (opened_hi) atomicAdd(&cv.status[2], opened_hi);
+    if (opened_lo) atomicAdd(&cv.status[3], opened_lo);
     if (flags) atomicOr(cv.status, flags);
   }
 }

@@ -142,8 +142,9 @@ struct AttnArgs {
 constexpr int kSmallSegments = 64;
 constexpr int kSmallPartials = 4096;
 // Calls that persist their step's entry themselves: every worker decides the
-// entries of all sequences, one per lane of its wave.
-constexpr int kFusedMaxBatch = 64;
+// entries of all sequences, 64 at a time (one per lane of its wave), and
+// keeps their counts and outcomes in LDS.
+constexpr int kFusedMaxBatch = 256;
 
 // The library-owned scratch of pask_decode_attn_noalloc: a device array of
 // kScratchBytes in pask_attn.hip, one copy per GPU.  scratch_workspace gives
