@@ -438,66 +438,214 @@ __device__ __forceinline__ void write_lo(const CacheView& cv, int page, int t, c
 constexpr int kPackThreads = 256;
 
 
+// The offset-binary codes q + 8 of the 8 bf16 elements of x under scale s
+// (inv ~ 1 / s), the rule of quant_code, with code u in the low byte of b[u]
+// (bits 4..7 zero, the bits above unspecified).  y = RN(x * inv + 1.5 * 2^23
+// + 8) lies in [2^23, 2^24), where floats are spaced by 1, so its low byte is
+// rint(x * inv) + 8 once clamped to [1, 15]; r = x * inv - (y - M) is the
+// part rounded away.  As in codes8, x * inv rounds like x / s unless x / s
+// lies within 2^-12 of a half-integer, so a lane whose largest |r| comes
+// within 1.2e-4 of 1/2 takes quant_code for its 8 elements.  s = 0 (an
+// all-zero group) takes inv = 0: every code 8, as quant_code gives.  About
+// two thirds of the vector instructions of codes8 + k_word, which the bulk
+// pack of RETAIN-LOW pages, bound by its vector ALU, spends most of its time
+// on.
+__device__ __forceinline__ void code_bytes8(const uint4& x, float s, float inv, uint32_t (&b)[8]) {
+  const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
+                      bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
+  constexpr float M = 12582920.0f;                 // 1.5 * 2^23 + 8
+  const float iv = s != 0.0f ? inv : 0.0f;
+  float worst = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float y = fmaf(f[u], iv, M);
+    worst = fmaxf(worst, fabsf(fmaf(f[u], iv, M - y)));
+    b[u] = __float_as_uint(__builtin_amdgcn_fmed3f(y, M - 7.0f, M + 7.0f));
+  }
+  const bool near_tie = worst > 0.49988f;
+  if (__ballot(near_tie)) {
+    if (near_tie) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) b[u] = (uint32_t)(quant_code(f[u], s, inv) + 8);
+    }
+  }
+}
+// Low bytes of w0..w3 as bytes 0..3 of one word.
+__device__ __forceinline__ uint32_t low_bytes4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  return __builtin_amdgcn_perm(w1, w0, 0x0c0c0400u) | __builtin_amdgcn_perm(w3, w2, 0x04000c0cu);
+}
+
+// The largest |element| of the 8 bf16 in x, as the bits of its bf16 magnitude
+// (the order of non-negative floats is that of their bits): packed 16-bit
+// integer maxima of the sign-cleared words.
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t abs_max_bits8(const uint4& x) {
+  const uint32_t m = 0x7FFF7FFFu;
+  const u16x2_t a = __builtin_bit_cast(u16x2_t, x.x & m), b = __builtin_bit_cast(u16x2_t, x.y & m);
+  const u16x2_t c = __builtin_bit_cast(u16x2_t, x.z & m), d = __builtin_bit_cast(u16x2_t, x.w & m);
+  const u16x2_t r = __builtin_elementwise_max(__builtin_elementwise_max(a, b), __builtin_elementwise_max(c, d));
+  return r.x > r.y ? (uint32_t)r.x : (uint32_t)r.y;
+}
+
+// quant_scale of a bf16 absmax, dividing only where s is an fp16 subnormal:
+// from 7 * 2^-14 up, the product with RN(1/7) rounds to the same fp16 as the
+// correctly rounded quotient (an exact quotient of a bf16 by 7 has at most 8
+// significant bits, an inexact one never comes within 2^-15 of an fp16
+// midpoint); below it an exact quotient can be a midpoint between fp16
+// subnormals, which the product may miss.  Equal to quant_scale for every
+// bf16 absmax (checked over all of them on the CPU).
+__device__ __forceinline__ uint16_t quant_scale_bf16(float absmax, float& s, float& inv) {
+  float q = absmax * (1.0f / 7.0f);
+  const bool small = absmax < 7.0f * 0x1p-14f;
+  if (__ballot(small)) {
+    if (small) {
+      float a = absmax;
+      asm volatile("" : "+v"(a));                  // no code: keeps the division on this rare branch
+      q = a / 7.0f;
+    }
+  }
+  const _Float16 h = (_Float16)fminf(q, 65504.0f);
+  s = (float)h;
+  inv = __builtin_amdgcn_rcpf(s);
+  return __builtin_bit_cast(uint16_t, h);
+}
+
+// Lane l's 32-bit value from lane l ^ 1 / l ^ 2 of its group of four (quad
+// DPP: a vector move, no LDS round trip).
+__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true);   // quad_perm [1, 0, 3, 2]
+}
+__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true);   // quad_perm [2, 3, 0, 1]
+}
+
+// Row t and column col (of H * D / 8) of the page's 16-byte input chunks
+// e = it * kPackThreads + tid, it = 0, 1, ...: one division per thread, then
+// carried from one it to the next.
+struct ChunkWalk {
+  int t, col, R, dt, dc;
+  __device__ __forceinline__ explicit ChunkWalk(int r) : R(r) {
+    t = (int)threadIdx.x / R;
+    col = (int)threadIdx.x - t * R;
+    dt = kPackThreads / R;
+    dc = kPackThreads - dt * R;
+  }
+  __device__ __forceinline__ void next() {
+    t += dt;
+    col += dc;
+    if (col >= R) {
+      col -= R;
+      ++t;
+    }
+  }
+};
+
+// The LDS image of a LOW page keeps each 16-byte piece of a head's K and V
+// code regions at its stored index XOR a key of (image head g, quarter q of
+// the 32-element group the piece's codes come from).  In stored order the
+// lanes of one store instruction (4 heads x 4 quarters x 4 groups for K, 4 x
+// 2 x 4 for V, one slot) fall in 4 / 8 of the 32 LDS banks; with the keys the
+// K words spread over all 32 (two lanes a bank) and the V bytes over 32.  The
+// XOR keeps q (and the slot quad of V) in place, so the copy-out finds each
+// piece from its stored index.
+template <int D>
+struct LowImage {
+  using PL = PageLayout<D>;
+  static constexpr int NG = PL::NG;
+  static constexpr int kKMask = (4 * NG < 8 ? 4 * NG : 8) - 1;   // K pieces per quarter: 4 NG
+  static constexpr int kVMask = (2 * NG < 8 ? 2 * NG : 8) - 1;   // V pieces per quarter of a slot quad: 2 NG
+  __device__ __forceinline__ static int k_key(int g, int q) { return (g * 4 + q) & kKMask; }
+  __device__ __forceinline__ static int v_key(int g, int q) { return (g * 2 + q) & kVMask; }
+  // Image index of stored 16-byte piece p of image head g.
+  __device__ __forceinline__ static int piece(int g, int p) {
+    if (p < PL::kLoKS / 16) return p ^ k_key(g, p / (4 * NG));
+    if (p >= PL::kLoVC / 16 && p < PL::kLoVS / 16) {
+      const int r = p - PL::kLoVC / 16;
+      return PL::kLoVC / 16 + (r ^ v_key(g, (r % (4 * NG)) / (2 * NG)));
+    }
+    return p;
+  }
+};
+
 // The page image of a LOW page from the call's K and V rows (kx, vx: 16-byte
 // chunks in row order, chunk e of the page's rows at e = it * threads + tid,
 // so the four chunks of a 32-element group sit in four adjacent lanes):
 // every lane quantises its 8 elements (the group's absmax over the 4 lanes),
-// the codes and scales go to an LDS image of the page in its stored order,
-// which is then copied out with 16-byte stores (whole pages), or byte by byte
-// for the new slots only when the page holds earlier slots.
+// the codes and scales go to the LDS image of the page (LowImage), which is
+// then copied out in stored order with 16-byte stores (whole pages), or byte
+// by byte for the new slots only when the page holds earlier slots.
 template <int D, int kIt>
 __device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& cv, int page, int tl0, int th0,
                                          const uint4 (&kx)[kIt], const uint4 (&vx)[kIt], int n_chunks,
                                          uint8_t* s_img) {
   using PL = PageLayout<D>;
+  using Img = LowImage<D>;
   constexpr int NG = PL::NG, kRowChunks = D / 8;
   const int H = cv.n_kv_heads, tid = (int)threadIdx.x;
+  ChunkWalk w(H * kRowChunks);
 #pragma unroll
-  for (int it = 0; it < kIt; ++it) {
+  for (int it = 0; it < kIt; ++it, w.next()) {
     const int e = it * kPackThreads + tid;
     const bool valid = e < n_chunks;
-    const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
-    const int g = col / kRowChunks, c = col % kRowChunks, i = c / 4, q = c % 4;
+    const uint32_t t = (uint32_t)w.t, col = (uint32_t)w.col;
+    const uint32_t g = col / kRowChunks, c = col % kRowChunks, i = c / 4, q = c % 4;
+    uint8_t* hd = s_img + g * PL::kLoHead;
 #pragma unroll
     for (int kv = 0; kv < 2; ++kv) {
       const uint4 x = kv ? vx[it] : kx[it];
-      float am = 0.0f;
-      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.x)), fabsf(bf16_hi(x.x))));
-      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.y)), fabsf(bf16_hi(x.y))));
-      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.z)), fabsf(bf16_hi(x.z))));
-      am = fmaxf(am, fmaxf(fabsf(bf16_lo(x.w)), fabsf(bf16_hi(x.w))));
-      am = fmaxf(am, __shfl_xor(am, 1));           // the group's four lanes
-      am = fmaxf(am, __shfl_xor(am, 2));
+      uint32_t mb = abs_max_bits8(x);
+      mb = max(mb, quad_xor1(mb));                 // the group's four lanes
+      mb = max(mb, quad_xor2(mb));
       float s, inv;
-      const uint16_t sbits = quant_scale(am, s, inv);
-      const uint32_t packed = codes8(x, s, inv);
-      uint8_t* hd = s_img + g * PL::kLoHead;
+      const uint16_t sbits = quant_scale_bf16(__uint_as_float(mb << 16), s, inv);
+      uint32_t cb[8];
+      code_bytes8(x, s, inv, cb);
       if (kv == 0) {
         if (valid) {
-          *reinterpret_cast<uint32_t*>(hd + ((q * 16 + t) * NG + i) * 4) = k_word(packed);
-          if (q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoKS + (t * NG + i) * 2) = sbits;
+          // byte e: element e in the low nibble, element 4 + e in the high one
+          const uint32_t o = ((q * 16u + t) * NG + i) * 4u;
+          *reinterpret_cast<uint32_t*>(hd + (((o >> 4) ^ (uint32_t)Img::k_key(g, q)) << 4) + (o & 15u)) =
+              low_bytes4((cb[4] << 4) | cb[0], (cb[5] << 4) | cb[1], (cb[6] << 4) | cb[2], (cb[7] << 4) | cb[3]);
+          if (q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoKS + (t * NG + i) * 2u) = sbits;
         }
       } else {
         // lanes q and q ^ 2 hold dims 32i + dd and 32i + 16 + dd: one byte per dd
-        const uint32_t partner = __shfl_xor(packed, 2);
+        const uint32_t lo = low_bytes4(cb[0], cb[1], cb[2], cb[3]), hi = low_bytes4(cb[4], cb[5], cb[6], cb[7]);
+        const uint32_t blo = lo | (quad_xor2(lo) << 4), bhi = hi | (quad_xor2(hi) << 4);
         if (valid && q < 2) {
-          uint8_t* vc = hd + PL::kLoVC + ((t / 4) * 16 * NG + i) * 4 + t % 4;
+          const uint32_t key = (uint32_t)Img::v_key(g, q);
+          if constexpr (NG == 4) {
+            // byte dd = 8q + u sits in piece (t / 4) * 16 + 8q + (u ^ key).  The
+            // image is 128-byte aligned and every other term of the offset is a
+            // multiple of 128 or below 16, so bits 4..6 of vo are the key and
+            // piece 8q + (u ^ key) is at vo ^ (u << 4).
+            static_assert(PL::kLoHead % 128 == 0 && PL::kLoVC % 128 == 0, "V offsets of the LOW image");
+            const uint32_t vo = g * PL::kLoHead + PL::kLoVC + ((t / 4u) * 16u + 8u * q) * 16u + 4u * i + t % 4u +
+                                key * 16u;
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
-            vc[(8 * q + u) * NG * 4] = (uint8_t)(((packed >> (4 * u)) & 0xFu) | (((partner >> (4 * u)) & 0xFu) << 4));
+            for (int u = 0; u < 8; ++u) s_img[vo ^ (uint32_t)(u << 4)] = (uint8_t)((u < 4 ? blo : bhi) >> (8 * (u % 4)));
+          } else {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const uint32_t b = ((t / 4u) * 16u * NG + i) * 4u + t % 4u + (8u * q + u) * NG * 4u;
+              hd[PL::kLoVC + (((b >> 4) ^ key) << 4) + (b & 15u)] = (uint8_t)((u < 4 ? blo : bhi) >> (8 * (u % 4)));
+            }
+          }
         }
-        if (valid && q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoVS + (t * NG + i) * 2) = sbits;
+        if (valid && q == 0) *reinterpret_cast<uint16_t*>(hd + PL::kLoVS + (t * NG + i) * 2u) = sbits;
       }
     }
   }
   __syncthreads();
   uint8_t* pg = cv.lo_pool + (size_t)page * cv.lo_page_bytes;
   constexpr int kHeadChunks = PL::kLoHead / 16;
+  const int pm = page % H;                         // image head g is stored at (g + page) % H
   if (tl0 == 0) {                                  // no earlier slot: whole 16-byte pieces
     for (int k = tid; k < H * kHeadChunks; k += kPackThreads) {
       const int g = k / kHeadChunks, off = k % kHeadChunks;
-      stream_store16(pg + (size_t)((g + page) % H) * PL::kLoHead + off * 16,
-                     *reinterpret_cast<const uint4*>(s_img + g * PL::kLoHead + off * 16));
+      const int hg = g + pm < H ? g + pm : g + pm - H;
+      stream_store16(pg + (size_t)hg * PL::kLoHead + off * 16,
+                     *reinterpret_cast<const uint4*>(s_img + g * PL::kLoHead + Img::piece(g, off) * 16));
     }
     return;
   }
@@ -508,7 +656,9 @@ __device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& c
     else if (y < PL::kLoVC) t = (y - PL::kLoKS) / 2 / NG;                 // K scale t*NG + i
     else if (y < PL::kLoVS) t = ((y - PL::kLoVC) / 4 / NG / 16) * 4 + (y - PL::kLoVC) % 4;   // V byte
     else t = (y - PL::kLoVS) / 2 / NG;                                    // V scale
-    if (t >= tl0 && t < th0) pg[(size_t)((g + page) % H) * PL::kLoHead + y] = s_img[x];
+    const int hg = g + pm < H ? g + pm : g + pm - H;
+    if (t >= tl0 && t < th0)
+      pg[(size_t)hg * PL::kLoHead + y] = s_img[g * PL::kLoHead + Img::piece(g, y >> 4) * 16 + (y & 15)];
   }
 }
 // A window entry that leaves the recent window in a bulk append: its bf16 K
@@ -547,7 +697,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
   constexpr int kMaxChunks = kPage * 8 * kRowChunks;   // a page's K (or V) chunks at Hkv 8
   constexpr int kIt = kMaxChunks / kPackThreads;
   constexpr int kLdsRow = 8 * D * 2 + kLdsRowPad;
-  __shared__ __align__(16) uint8_t s_v[kPage * kLdsRow];
+  __shared__ __align__(128) uint8_t s_v[kPage * kLdsRow];   // 128: the LOW image's V offsets (low_page)
   __shared__ int s_src[kPage];                     // per slot: input row, -2 - ring slot, or -1 (no new entry)
   const CacheView& cv = a.cv;
   const int b = blockIdx.z, st = blockIdx.y;
@@ -581,13 +731,14 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
   const bool is_hi = st == kHi;
   // 1. loads
   uint4 vx[kIt], kx[kIt];
+  ChunkWalk w0(H * kRowChunks);
 #pragma unroll
-  for (int it = 0; it < kIt; ++it) {
+  for (int it = 0; it < kIt; ++it, w0.next()) {
     const int e = it * kPackThreads + tid;
     vx[it] = make_uint4(0u, 0u, 0u, 0u);
     kx[it] = make_uint4(0u, 0u, 0u, 0u);
     if (e < n_chunks) {
-      const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+      const int t = w0.t, col = w0.col;
       const int j = s_src[t];
       if (j >= 0) vx[it] = stream_load16(reinterpret_cast<const uint8_t*>(vbase + (size_t)j * row + col * 8));
       else if (j <= -2)
@@ -610,11 +761,12 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
       }
     }
   } else {
+    ChunkWalk w(H * kRowChunks);
 #pragma unroll
-    for (int it = 0; it < kIt; ++it) {             // LOW K: row order, like V
+    for (int it = 0; it < kIt; ++it, w.next()) {   // LOW K: row order, like V
       const int e = it * kPackThreads + tid;
       if (e < n_chunks) {
-        const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+        const int t = w.t, col = w.col;
         const int j = s_src[t];
         if (j >= 0) kx[it] = stream_load16(reinterpret_cast<const uint8_t*>(kbase + (size_t)j * row + col * 8));
         else if (j <= -2)
@@ -628,11 +780,12 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
     return;
   }
   // 2. HIGH: V rows into LDS
+  ChunkWalk w1(H * kRowChunks);
 #pragma unroll
-  for (int it = 0; it < kIt; ++it) {
+  for (int it = 0; it < kIt; ++it, w1.next()) {
     const int e = it * kPackThreads + tid;
     if (e < n_chunks) {
-      const int t = e / (H * kRowChunks), col = e % (H * kRowChunks);
+      const int t = w1.t, col = w1.col;
       *reinterpret_cast<uint4*>(s_v + t * kLdsRow + col * 16) = vx[it];
     }
   }

@@ -5,9 +5,13 @@
 // every bf16 x with s/8 <= |x| <= 9s (both signs), and an approximate
 // reciprocal 1/s moved by up to 4 ulp either way (the device takes it from
 // v_rcp_f32, accurate to 1 ulp); then every bf16 x below s/8 at the exact
-// reciprocal, and s = 0.  Over the same x, s and reciprocals: the bulk pack's
-// fast path (rint(x * 1/s) unless within kNearTie of a tie) gives the exact
-// code wherever it does not defer to quant_code.
+// reciprocal, and s = 0.  Over the same x, s and reciprocals, the two fast
+// paths give the exact code wherever they do not defer to quant_code: codes8
+// (the decode call's entry: rint(x * 1/s) unless within kNearTie of a tie) and
+// code_bytes8 (the bulk pack: the low byte of RN(x * 1/s + 1.5 * 2^23 + 8)
+// clamped to 1..15, unless the part rounded away is within kNearTie of 1/2).
+// Last, the bulk pack's division-free scale against fp16(absmax / 7) for
+// every bf16 absmax.
 #include <math.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -28,8 +32,20 @@ static int want(float x, float s) {
   return (int)fmin(fmax(q, -7.0), 7.0);
 }
 
-// The near-tie threshold of the bulk pack's fast path (codes8).
+// The near-tie threshold of both fast paths.
 constexpr float kNearTie = 0.49988f;
+constexpr float kM = 12582920.0f;                    // 1.5 * 2^23 + 8
+
+// code_bytes8's fast code of x, or 100 when it defers to quant_code; its low
+// byte must hold the code + 8 with bits 4..7 zero (else -100).
+static int fast_byte_code(float x, float inv) {
+  const float y = fmaf(x, inv, kM);
+  if (fabsf(fmaf(x, inv, kM - y)) > kNearTie) return 100;
+  const float yc = fminf(fmaxf(y, kM - 7.0f), kM + 7.0f);
+  uint32_t bits;
+  memcpy(&bits, &yc, 4);
+  return (bits & 0xF0u) ? -100 : (int)(bits & 0xFFu) - 8;
+}
 
 int main() {
   long n = 0, bad = 0;
@@ -49,16 +65,18 @@ int main() {
           if (got != want(xs, s)) {
             if (++bad <= 10) printf("mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, got, want(xs, s));
           }
-          // The bulk pack's fast path (codes8 in pask_append.hip): rint(x * inv)
-          // clamped, unless |x * inv - rint(x * inv)| > kNearTie sends the lane to
-          // quant_code.  Wherever it keeps the fast code, that code must be the
-          // exact one.
+          // codes8: rint(x * inv) clamped, unless |x * inv - rint(x * inv)| >
+          // kNearTie sends the lane to quant_code.  Wherever a fast path keeps
+          // its code, that code must be the exact one.
           const float y = xs * inv, c = rintf(y);
           if (!(fabsf(y - c) > kNearTie)) {
             const int fast = (int)fminf(fmaxf(c, -7.0f), 7.0f);
             if (fast != want(xs, s) && ++bad <= 10)
               printf("fast-path mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, fast, want(xs, s));
           }
+          const int fb = fast_byte_code(xs, inv);
+          if (fb != 100 && fb != want(xs, s) && ++bad <= 10)
+            printf("byte fast-path mismatch: x=%a s=%a inv=%a got %d want %d\n", xs, s, inv, fb, want(xs, s));
         }
       }
       if (du == 0) {
@@ -69,6 +87,8 @@ int main() {
             const float xs = sg ? -x : x;
             ++n;
             if (pask::quant_code(xs, s, inv) != want(xs, s) && ++bad <= 10) printf("mismatch (small): x=%a s=%a\n", xs, s);
+            const int fb = fast_byte_code(xs, inv);
+            if (fb != 100 && fb != want(xs, s) && ++bad <= 10) printf("byte fast-path mismatch (small): x=%a s=%a\n", xs, s);
           }
         }
       }
@@ -77,6 +97,19 @@ int main() {
   for (uint32_t bx = 0; bx < 0x7F80; bx += 7) {      // s == 0: every code 0
     ++n;
     if (pask::quant_code(bf16_value(bx), 0.0f, INFINITY) != 0 && ++bad <= 10) printf("s = 0 gives a code\n");
+    if (fast_byte_code(bf16_value(bx), 0.0f) != 0 && ++bad <= 10) printf("s = 0 (inv taken as 0) gives a byte code\n");
+  }
+  // The bulk pack's scale (quant_scale_bf16 in pask_append.hip): absmax times
+  // RN(1/7), divided instead below 7 * 2^-14, rounds to the fp16 of the
+  // correctly rounded absmax / 7 (quant_scale) for every finite bf16 absmax.
+  for (uint32_t bx = 0; bx < 0x7F80; ++bx) {
+    const float am = bf16_value(bx);
+    float q = am * (1.0f / 7.0f);
+    if (am < 7.0f * 0x1p-14f) q = am / 7.0f;
+    const _Float16 want_s = (_Float16)fminf(am / 7.0f, 65504.0f), got_s = (_Float16)fminf(q, 65504.0f);
+    ++n;
+    if (__builtin_bit_cast(uint16_t, want_s) != __builtin_bit_cast(uint16_t, got_s) && ++bad <= 10)
+      printf("scale mismatch: absmax=%a\n", am);
   }
   printf("%s: %ld cases, %ld mismatches\n", bad ? "FAIL" : "ok", n, bad);
   return bad ? 1 : 0;
