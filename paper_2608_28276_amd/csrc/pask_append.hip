@@ -442,29 +442,29 @@ constexpr int kPackThreads = 256;
 // (inv ~ 1 / s), the rule of quant_code, with code u in the low byte of b[u]
 // (bits 4..7 zero, the bits above unspecified).  y = RN(x * inv + 1.5 * 2^23
 // + 8) lies in [2^23, 2^24), where floats are spaced by 1, so its low byte is
-// rint(x * inv) + 8 once clamped to [1, 15]; r = x * inv - (y - M) is the
-// part rounded away.  As in codes8, x * inv rounds like x / s unless x / s
-// lies within 2^-12 of a half-integer, so a lane whose largest |r| comes
-// within 1.2e-4 of 1/2 takes quant_code for its 8 elements.  s = 0 (an
-// all-zero group) takes inv = 0: every code 8, as quant_code gives.  About
-// two thirds of the vector instructions of codes8 + k_word, which the bulk
-// pack of RETAIN-LOW pages, bound by its vector ALU, spends most of its time
-// on.
-__device__ __forceinline__ void code_bytes8(const uint4& x, float s, float inv, uint32_t (&b)[8]) {
+// rint(x * inv) + 8; r = x * inv - (y - M) is the part rounded away.  As in
+// codes8, x * inv rounds like x / s unless x / s lies within 2^-12 of a
+// half-integer, so a lane whose largest |r| comes within 1.2e-4 of 1/2 takes
+// quant_code for its 8 elements.  plain: s is a normal, unsaturated fp16
+// scale of the group's absmax (quant_scale_bf16), so |x / s| <= 7 (1 + 2^-11)
+// for every element of the group and the code needs no clamp; a lane without
+// it (s subnormal or zero, or saturated at 65504) takes quant_code too.  About
+// half the vector instructions of codes8 + k_word, which the bulk pack of
+// RETAIN-LOW pages, bound by its vector ALU, spends most of its time on.
+__device__ __forceinline__ void code_bytes8(const uint4& x, float s, float inv, bool plain, uint32_t (&b)[8]) {
   const float f[8] = {bf16_lo(x.x), bf16_hi(x.x), bf16_lo(x.y), bf16_hi(x.y),
                       bf16_lo(x.z), bf16_hi(x.z), bf16_lo(x.w), bf16_hi(x.w)};
   constexpr float M = 12582920.0f;                 // 1.5 * 2^23 + 8
-  const float iv = s != 0.0f ? inv : 0.0f;
   float worst = 0.0f;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
-    const float y = fmaf(f[u], iv, M);
-    worst = fmaxf(worst, fabsf(fmaf(f[u], iv, M - y)));
-    b[u] = __float_as_uint(__builtin_amdgcn_fmed3f(y, M - 7.0f, M + 7.0f));
+    const float y = fmaf(f[u], inv, M);
+    worst = fmaxf(worst, fabsf(fmaf(f[u], inv, M - y)));
+    b[u] = __float_as_uint(y);
   }
-  const bool near_tie = worst > 0.49988f;
-  if (__ballot(near_tie)) {
-    if (near_tie) {
+  const bool exact = !plain || worst > 0.49988f;
+  if (__ballot(exact)) {
+    if (exact) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) b[u] = (uint32_t)(quant_code(f[u], s, inv) + 8);
     }
@@ -493,8 +493,9 @@ __device__ __forceinline__ uint32_t abs_max_bits8(const uint4& x) {
 // significant bits, an inexact one never comes within 2^-15 of an fp16
 // midpoint); below it an exact quotient can be a midpoint between fp16
 // subnormals, which the product may miss.  Equal to quant_scale for every
-// bf16 absmax (checked over all of them on the CPU).
-__device__ __forceinline__ uint16_t quant_scale_bf16(float absmax, float& s, float& inv) {
+// bf16 absmax (checked over all of them on the CPU).  plain: s is a normal
+// fp16 and not saturated (7 * 2^-14 <= absmax <= 7 * 65504).
+__device__ __forceinline__ uint16_t quant_scale_bf16(float absmax, float& s, float& inv, bool& plain) {
   float q = absmax * (1.0f / 7.0f);
   const bool small = absmax < 7.0f * 0x1p-14f;
   if (__ballot(small)) {
@@ -504,6 +505,7 @@ __device__ __forceinline__ uint16_t quant_scale_bf16(float absmax, float& s, flo
       q = a / 7.0f;
     }
   }
+  plain = !small && absmax <= 7.0f * 65504.0f;
   const _Float16 h = (_Float16)fminf(q, 65504.0f);
   s = (float)h;
   inv = __builtin_amdgcn_rcpf(s);
@@ -597,9 +599,10 @@ __device__ __forceinline__ void low_page(const AppendArgs& a, const CacheView& c
       mb = max(mb, quad_xor1(mb));                 // the group's four lanes
       mb = max(mb, quad_xor2(mb));
       float s, inv;
-      const uint16_t sbits = quant_scale_bf16(__uint_as_float(mb << 16), s, inv);
+      bool plain;
+      const uint16_t sbits = quant_scale_bf16(__uint_as_float(mb << 16), s, inv, plain);
       uint32_t cb[8];
-      code_bytes8(x, s, inv, cb);
+      code_bytes8(x, s, inv, plain, cb);
       if (kv == 0) {
         if (valid) {
           // byte e: element e in the low nibble, element 4 + e in the high one
@@ -723,7 +726,7 @@ __global__ __launch_bounds__(kPackThreads) void append_pack_page_kernel(AppendAr
     s_src[t] = j;
   }
   __syncthreads();
-  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = (int)threadIdx.x;
   const size_t row = (size_t)H * D;                // bf16 per K (or V) row of a token
   const int n_chunks = kPage * H * kRowChunks;     // the page's V chunks (as many K chunks)
   const uint16_t* vbase = a.v + (size_t)b * a.max_new * row;
