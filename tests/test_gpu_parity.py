@@ -91,10 +91,14 @@ def test_quantiser_exhaustive_absmax_on_gpu():
 
 
 @pytest.mark.parametrize("Hq,Hkv,D", [(8, 8, 64), (16, 8, 64), (8, 2, 64), (16, 2, 64),
-                                      (8, 8, 128), (16, 8, 128), (32, 8, 128), (64, 8, 128)])
+                                      (8, 8, 128), (16, 8, 128), (32, 8, 128), (64, 8, 128),
+                                      (1, 1, 64), (6, 3, 64), (12, 3, 128), (40, 5, 128), (7, 7, 128)])
 def test_geometries_mixed_policy(Hq, Hkv, D):
-    """Every supported (group size, head_dim) pair; ragged prompts (not page
-    multiples), a batch of 5, mixed HIGH / LOW / DROP decode tokens."""
+    """Every supported (group size, head_dim) pair, and KV head counts that
+    are not powers of two (a page's chunk rows then do not divide the pack's
+    256 threads; the head rotation of the pages wraps at 3, 5, 7); ragged
+    prompts (not page multiples), a batch of 5, mixed HIGH / LOW / DROP decode
+    tokens."""
     say(f"case: geometry Hq={Hq} Hkv={Hkv} D={D}")
     pol = make_policy(6, 2, 4, 0.33, seed=Hq * 100 + D)
     P = [1, 15, 17, 33, 300]
