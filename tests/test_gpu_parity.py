@@ -113,6 +113,24 @@ def test_geometries_mixed_policy(Hq, Hkv, D):
     sc.check_state()
 
 
+@pytest.mark.parametrize("B", [256, 260])
+def test_decode_batch_around_single_call_limit(B):
+    """Up to 256 sequences a decode call with new tokens persists them in its
+    own attention and merge kernels; above, it runs the one-token append
+    kernel first.  Both sides of the limit: ragged short prompts (some empty),
+    mixed HIGH / LOW / DROP tokens, three steps, every sequence compared."""
+    say(f"case: decode batch {B}")
+    pol = make_policy(6, 2, 2, 0.33, seed=900 + B)
+    P = [(7 * b) % 45 for b in range(B)]
+    T = 3
+    tags = np.stack([function_call_tags(T, 1000 + b) for b in range(B)])
+    sc = Scenario(pol, B=B, L=2, Hq=8, Hkv=2, D=64, prompt_lens=P, gen_tags=tags, seed=B)
+    sc.fill_prompt()
+    for t in range(T):
+        sc.decode_step(t)
+    sc.check_state()
+
+
 @pytest.mark.parametrize("B", [8, 9])
 def test_segment_count_boundary(B):
     """8 sequences x 8 KV heads = 64 segments take the few-segment path
