@@ -52,7 +52,7 @@ def replay_changes(pol, tags, states, t_max, Hkv, D):
     return dem, pro, R
 
 
-@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 64), (32, 8, 128)])
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 64), (32, 8, 128), (20, 5, 64)])
 def test_controller_bulk_step_and_fused(Hq, Hkv, D):
     """3 sequences, 4 layers in 2 groups, 3 sinks; prompts of 0 / 37 / 300
     tokens kept HIGH (they bypass the controller), then 600 generated tokens

@@ -31,7 +31,8 @@ def _windowed(pol, W):
     return pol
 
 
-@pytest.mark.parametrize("Hq,Hkv,D,W", [(8, 2, 64, 16), (8, 2, 64, 37), (32, 8, 128, 16), (64, 8, 128, 53)])
+@pytest.mark.parametrize("Hq,Hkv,D,W", [(8, 2, 64, 16), (8, 2, 64, 37), (32, 8, 128, 16), (64, 8, 128, 53),
+                                        (12, 3, 128, 24)])
 def test_window_bulk_step_and_fused(Hq, Hkv, D, W):
     """3 sequences, 4 layers in 2 groups, 3 sinks, prompts of 0 / 37 / 300
     tokens kept HIGH (they pass through the window too), then 900 generated
