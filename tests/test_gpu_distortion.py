@@ -42,7 +42,7 @@ def _bits(t):
 
 
 @pytest.mark.parametrize("action", [oracle.DROP, oracle.LOW])
-@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 64), (32, 8, 128), (16, 2, 128)])
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 2, 64), (32, 8, 128), (16, 2, 128), (24, 3, 128)])
 def test_distortion_matches_oracle(Hq, Hkv, D, action):
     from paper_2608_28276_amd import pask
     from paper_2608_28276_amd.session import PaskSession
