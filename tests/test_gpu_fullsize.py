@@ -124,7 +124,7 @@ def test_qwen3_32b_attention_batch256_one_layer_group():
     8 KV heads (group 8), head_dim 128; two layers of the resident group, 256
     generated tokens bulk-appended, then two fused decode steps.  Every
     counter and list bit-exact; stores and attention of 6 sequences x 2
-    layers."""
+    layers and of 10 more sequences in the first layer."""
     from tests.fullsize_util import DeviceRun
     cfg = CONFIGS[4]
     say(f"case: {cfg.name}")
@@ -133,6 +133,7 @@ def test_qwen3_32b_attention_batch256_one_layer_group():
     pol = _calls_policy(cfg)
     layers = (0, 5)
     sample = [(b, l) for b in (0, 63, 64, 130, 200, 255) for l in layers]
+    sample += [(b, layers[0]) for b in (17, 40, 90, 101, 150, 170, 190, 222, 240, 250)]
     run = DeviceRun(pol, n_layers=cfg.n_layers, layers=layers, Hq=cfg.n_q_heads, Hkv=cfg.n_kv_heads,
                     D=cfg.head_dim, P=P, prompt_tags=None, gen_tags=tags, sample=sample, seed=cfg.seed,
                     n_bulk=256, n_steps=2)
